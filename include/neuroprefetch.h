@@ -1,0 +1,237 @@
+/*
+ * neuroprefetch.h -- C ABI of the per-token decode hot path of NeuroPrefetcher
+ * ("Storage-Aware Sparse LLM Inference via Delta Prefetching", arXiv 2608.22643),
+ * built for one AMD Instinct MI355X (gfx950).
+ *
+ * One decode token runs five steps (paper Sec. 3.1, "System Overview"; Sec. 3.4,
+ * "Predictive Delta Prefetching"; Sec. 3.5, "I/O Path"):
+ *
+ *   np_predict     score the MLP neurons of every downstream layer in one pass
+ *   np_select      top-k of the scores -> one fixed-size active set per layer
+ *   np_delta       active set vs. the GPU-resident row buffer -> incoming rows,
+ *                  evicted slots, hits; updates the slot map (Sec. 3.4, eqs. 2-3)
+ *   np_stage_rows  incoming neuron records, storage tier -> their device slots
+ *   np_sparse_mlp  ReLU-gated MLP over the resident active rows of one layer
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - extern "C"; plain pointers and sizes only.  All memory is owned by the
+ *    caller; no call allocates or frees device or host memory.  The staging
+ *    path keeps two HIP events and a small worker-thread pool per process,
+ *    created on first use (see np_stage_rows).
+ *  - "device" pointers point into memory of the current HIP device.  Device
+ *    pointers must be 16-byte aligned.  Every call is asynchronous on the HIP
+ *    stream it is given (0 = the null stream) unless stated otherwise.
+ *  - Host-side argument validation runs first; when it fails nothing is
+ *    enqueued and the call returns NP_ERR_INVALID_ARG or NP_ERR_CAPACITY.
+ *    np_last_error() then gives a detail string (thread-local).
+ *  - A failing HIP runtime call returns NP_ERR_HIP.  Data errors that only the
+ *    device can see (a NaN score, an active row that is not resident, a slot
+ *    map that disagrees with its inverse) set bits in a sticky error word in
+ *    the device workspace; read it with np_device_error().
+ *  - Calls that share a workspace or a state must not run concurrently.
+ *
+ * Shapes and layouts (np_shape)
+ * -----------------------------
+ *  L' = layers (downstream layers, i.e. layers 1..N-1 of an N-layer model),
+ *  d  = d_model, F = d_ffn (MLP intermediate size), r = predictor rank,
+ *  k  = active rows per layer, C = resident slots per layer.
+ *  w  = wdtype (MLP records and predictor factors), a = adtype (h, x, y).
+ *  Requirements: 1 <= k <= C <= F <= 65535, 1 <= L', r >= 1;
+ *  d and r multiples of 8 for 16-bit types and of 4 for fp32; d <= 16384.
+ *
+ *  Neuron record (Sec. 3.5, neuron-centric layout): row n of gate, row n of up
+ *  and row n of down^T (down transposed offline so all three share one shape),
+ *  3*d elements of type w, contiguous, no padding.  Storage tier:
+ *  [L'][F][3d] (record n of layer l at ((l*F)+n)*3d).  Device resident
+ *  buffer: [L'][C][3d] (slot s of layer l at ((l*C)+s)*3d).
+ */
+#ifndef NEUROPREFETCH_H
+#define NEUROPREFETCH_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum np_status {
+  NP_OK = 0,
+  NP_ERR_INVALID_ARG = 1, /* null/misaligned pointer, bad size or dtype */
+  NP_ERR_CAPACITY = 2,    /* k > C, staging buffer smaller than one record, ... */
+  NP_ERR_HIP = 3,         /* a HIP runtime call failed; detail in np_last_error() */
+  NP_ERR_UNSUPPORTED = 4, /* valid request this build does not implement */
+  NP_ERR_STATE = 5        /* state marked invalid by an earlier staging failure */
+} np_status;
+
+typedef enum np_dtype { NP_F32 = 0, NP_F16 = 1, NP_BF16 = 2 } np_dtype;
+
+/* Device error word bits (sticky, OR-ed; see np_device_error). */
+#define NP_DEVERR_NAN_SCORE    0x1  /* np_select saw a NaN score */
+#define NP_DEVERR_NOT_RESIDENT 0x2  /* np_sparse_mlp got a slot outside [0, C) */
+#define NP_DEVERR_STATE        0x4  /* np_delta found slot_of / neuron_of inconsistent */
+#define NP_DEVERR_SPIN_LIMIT   0x8  /* a bounded in-kernel wait gave up */
+
+typedef struct np_shape {
+  int32_t layers;   /* L' */
+  int32_t d_model;  /* d */
+  int32_t d_ffn;    /* F */
+  int32_t rank;     /* r */
+  int32_t k;        /* active rows per layer */
+  int32_t capacity; /* C: resident slots per layer */
+  int32_t wdtype;   /* np_dtype of MLP records and predictor factors */
+  int32_t adtype;   /* np_dtype of activations h, x, y */
+} np_shape;
+
+/* Residency state of every downstream layer, device memory, int32.
+ * slot_of   [L'][F]: the slot map S of Sec. 3.4; slot of neuron n or -1.
+ * neuron_of [L'][C]: inverse map; neuron held by slot s or -1.
+ * last_used [L'][F]: last token at which neuron n was active, -1 if never
+ *                    (drives least-recently-used eviction when C > k). */
+typedef struct np_state {
+  int32_t* slot_of;
+  int32_t* neuron_of;
+  int32_t* last_used;
+} np_state;
+
+/* Outputs of np_delta, device memory.  Each list is [L'][k] int32 (row l
+ * holds layer l's list; only the first counts[l][.] entries are defined).
+ * counts [L'][4] = { n_in, n_hit, n_ev, n_free_used = n_in - n_ev }. */
+typedef struct np_delta_out {
+  int32_t* in_ids;       /* incoming neurons, ascending */
+  int32_t* in_slots;     /* slot given to in_ids[j], ascending */
+  int32_t* ev_ids;       /* evicted neurons, ascending */
+  int32_t* ev_slots;     /* the slot ev_ids[j] held before eviction */
+  int32_t* hit_ids;      /* active neurons already resident, ascending */
+  int32_t* active_slots; /* slot of active_ids[j] after the update, k per layer */
+  int32_t* counts;
+} np_delta_out;
+
+/* Host copy of the parts of np_delta_out that staging needs ([L'][4] and
+ * [L'][k] int32, any host memory; pinned makes the device->host copy async). */
+typedef struct np_stage_plan {
+  const int32_t* counts;
+  const int32_t* in_ids;
+  const int32_t* in_slots;
+} np_stage_plan;
+
+/* Text of a status code; never NULL. */
+const char* np_status_str(int32_t status);
+
+/* Detail of the last failing call on this thread ("" if none). */
+const char* np_last_error(void);
+
+/* Validates a shape (the requirements listed above).  Host only. */
+np_status np_shape_check(const np_shape* shape);
+
+/* Bytes of device workspace ("dev_ws") the calls below need for this shape.
+ * One workspace serves all calls of one decode stream.  Host only. */
+np_status np_workspace_size(const np_shape* shape, size_t* dev_ws_bytes);
+
+/* Cold start (Sec. 3.1 last paragraph; Sec. 3.4 "the first token has no
+ * previous active set"): sets every entry of slot_of, neuron_of and last_used
+ * to -1 with a fill kernel on `stream`, and clears the device error word and
+ * the workspace counters.  After it, np_delta on the next token gives every
+ * active neuron a slot (slots 0..k-1 in ascending neuron order). */
+np_status np_state_reset(const np_shape* shape, const np_state* state,
+                         void* dev_ws, hipStream_t stream);
+
+/* Activity predictor (Sec. 3.1 step 2, Sec. 3.3 role: one pass after layer 0
+ * scores every downstream layer).  Low-rank form per downstream layer l:
+ *     z_l = A_l h          (r values, fp32, kept in dev_ws)
+ *     scores[l] = B_l z_l  (F values, fp32)
+ * h [d] of type a; A [L'][r][d] and B [L'][F][r] of type w, row-major;
+ * scores [L'][F] fp32; all device.  Two kernels on `stream`. */
+np_status np_predict(const np_shape* shape, const void* h, const void* A,
+                     const void* B, float* scores, void* dev_ws,
+                     hipStream_t stream);
+
+/* Fixed-size active sets (Sec. 3.4: every active set has the same size).
+ * For each layer: the k neurons with the largest score; a tie at the k-th
+ * score goes to the smaller neuron id; -0.0 equals +0.0; a NaN sets
+ * NP_DEVERR_NAN_SCORE (its neuron is then treated as the smallest score).
+ * scores [L'][F] fp32 device -> mask [L'][ceil(F/32)] uint32 (bit n%32 of
+ * word n/32, LSB first, pad bits 0) and active_ids [L'][k] int32 ascending.
+ * One workgroup per layer on `stream`. */
+np_status np_select(const np_shape* shape, const float* scores, uint32_t* mask,
+                    int32_t* active_ids, void* dev_ws, hipStream_t stream);
+
+/* Delta against the resident set (Sec. 3.4, eqs. 2-3 and the slot-map
+ * paragraph), for token index `token` >= 0:
+ *   hits H = active neurons with slot_of >= 0; incoming I = the rest;
+ *   free slots Fr = slots with neuron_of == -1 (ascending);
+ *   if |I| > |Fr|, the m = |I|-|Fr| victims are the resident, non-active
+ *   neurons with the smallest (last_used, id); their slots join the pool;
+ *   the pool (ascending) is paired with I (ascending); last_used := token for
+ *   every active neuron.  With C == k this is exactly D_in = A_t \ A_{t-1},
+ *   D_out = A_{t-1} \ A_t.
+ * active_ids [L'][k] ascending (np_select output), device.  `state` is read
+ * and updated in place; `out` lists are written.  One workgroup per layer. */
+np_status np_delta(const np_shape* shape, int32_t token,
+                   const int32_t* active_ids, const np_state* state,
+                   const np_delta_out* out, void* dev_ws, hipStream_t stream);
+
+/* Staging through pinned host memory and hipMemcpyAsync (Sec. 3.5: incoming
+ * ids sorted and coalesced into contiguous ranges, one token-level batch for
+ * all layers, staging capacity-bounded with chunked submit-and-scatter).
+ * For layers [layer_begin, layer_end):
+ *   resident[l][in_slots[l][j]] <- storage[l][in_ids[l][j]],  j < counts[l][0].
+ * plan: host copy of np_delta's counts/in_ids/in_slots (read synchronously).
+ * host_storage: [L'][F][3d] records, pinned host memory (hipHostMalloc).
+ * dev_resident: [L'][C][3d] device.  host_staging / staging_bytes: pinned
+ * host area, used as two halves (double buffer).  dev_landing /
+ * landing_bytes: device area that receives each chunk before the scatter
+ * kernel moves its records into their slots.  A chunk holds at most
+ * min(staging_bytes/2, landing_bytes) / (3d*sizeof(w) + 4) records.
+ * `side`: stream that runs the copies and the scatter kernels.
+ * wait_before (nullable): `side` waits on it before the first write into
+ * dev_resident (orders the write after the previous token's MLP reads).
+ * layer_ready (nullable, [L'] events): event l is recorded on `side` once
+ * layer l's rows are in place.  The host blocks only to reuse a staging half
+ * whose previous copy has not finished.  Returns NP_ERR_CAPACITY if the
+ * staging or landing area is smaller than one chunk of one record. */
+np_status np_stage_rows(const np_shape* shape, const np_stage_plan* plan,
+                        int32_t layer_begin, int32_t layer_end,
+                        const void* host_storage, void* dev_resident,
+                        void* host_staging, size_t staging_bytes,
+                        void* dev_landing, size_t landing_bytes,
+                        hipStream_t side, hipEvent_t wait_before,
+                        hipEvent_t* layer_ready);
+
+/* Staging without a host round trip: one kernel per call copies, for layers
+ * [layer_begin, layer_end), resident[l][in_slots[l][j]] <- storage[l][in_ids[l][j]]
+ * reading counts/in_ids/in_slots straight from np_delta's device output.
+ * `storage` is [L'][F][3d] in device memory (a storage tier kept in HBM) or in
+ * pinned host memory mapped into the device address space (the kernel then
+ * reads it over the host link, as the paper's mapped staging does, Sec. 3.5).
+ * Asynchronous on `stream`; no host synchronisation. */
+np_status np_stage_gather(const np_shape* shape, const np_delta_out* out,
+                          int32_t layer_begin, int32_t layer_end,
+                          const void* storage, void* dev_resident,
+                          hipStream_t stream);
+
+/* Sparse MLP of one downstream layer over its resident active rows
+ * (Sec. 3.4: the slot map locates each active row; row order is irrelevant;
+ * Sec. 3.3: the down projection's output stays dense):
+ *     g_j = gate_j . x,  u_j = up_j . x,  y = sum_j max(g_j, 0) * u_j * downT_j
+ * where row j is slot active_slots[j] (j < n_active) of layer `layer` of
+ * dev_resident.  x [d] and y [d] of type a, device; accumulation in fp32 and
+ * one rounding of y to type a.  A slot outside [0, C) sets
+ * NP_DEVERR_NOT_RESIDENT and is skipped.  One kernel on `stream`; call it once
+ * per layer, in layer order.  n_active = 0 gives y = 0. */
+np_status np_sparse_mlp(const np_shape* shape, int32_t layer, const void* x,
+                        const void* dev_resident, const int32_t* active_slots,
+                        int32_t n_active, void* y, void* dev_ws,
+                        hipStream_t stream);
+
+/* Waits for `stream`, then returns the sticky device error word in *code
+ * (0 = none; NP_DEVERR_* bits otherwise).  Synchronous. */
+np_status np_device_error(const void* dev_ws, hipStream_t stream, int32_t* code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NEUROPREFETCH_H */

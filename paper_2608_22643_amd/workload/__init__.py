@@ -1,0 +1,271 @@
+"""Seeded synthetic workloads for the NeuroPrefetcher decode path.
+
+Inputs only: neuron records, predictor factors, hidden states and the
+configuration registry.  Nothing here computes any step of the method; the
+HIP path and the CPU oracle both read what this module writes.
+
+Workload recipe (stand-in for decoding WikiText-2 with a 7B model, which the
+paper measures in its evaluation setup):
+  * MLP records ~ N(0, 0.02^2), layer-major [L'][F][3d] (gate | up | down^T);
+  * predictor factors A_l ~ N(0, 1/d) [r x d], B_l ~ N(0, 1/r) [F x r], so the
+    scores have roughly unit variance;
+  * hidden states h_t = rho h_{t-1} + sqrt(1-rho^2) e_t (AR(1), float64, then
+    rounded once to the activation type), rho chosen so that consecutive
+    top-k sets overlap by the persistence target (82-85% in the paper's
+    abstract and delta-reuse measurements);
+  * a dyadic variant whose values are small multiples of powers of two, so
+    every sum on the path is exact in fp32 in any order.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+from dataclasses import dataclass, field, replace
+from functools import lru_cache
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "npgen.c")
+_LIB_PATH = os.path.join(_HERE, "libnpgen.so")
+
+DTYPE_CODES = {"f32": 0, "f16": 1, "bf16": 2}
+ITEMSIZE = {"f32": 4, "f16": 2, "bf16": 2}
+STORAGE_NP = {"f32": np.float32, "f16": np.uint16, "bf16": np.uint16}
+
+TENSOR_PRED_A = 4
+TENSOR_PRED_B = 5
+
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    if force or not os.path.exists(_LIB_PATH) or (
+        os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)
+    ):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _gen():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        L = ctypes.CDLL(_LIB_PATH)
+        vp, i32, i64, u64, u32, f64 = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                                       ctypes.c_uint64, ctypes.c_uint32, ctypes.c_double)
+        L.npg_fill_records.argtypes = [i32, u64, i64, i64, i64, i64, i32, f64, i64, vp, i32]
+        L.npg_fill_matrix.argtypes = [i32, u64, u32, i64, i64, i64, i64, i32, f64, i64, vp, i32]
+        L.npg_hidden.argtypes = [i32, u64, i64, i64, f64, i32, i64, vp, vp]
+        L.npg_encode.argtypes = [i32, vp, i64, vp]
+        L.npg_stream.argtypes = [u64, u32, u32]
+        L.npg_stream.restype = u64
+        L.npg_draw.argtypes = [u64, u64]
+        L.npg_draw.restype = u64
+        L.npg_normal.argtypes = [u64, u64]
+        L.npg_normal.restype = f64
+        L.npg_f16.argtypes = [f64]
+        L.npg_f16.restype = ctypes.c_uint16
+        L.npg_bf16.argtypes = [f64]
+        L.npg_bf16.restype = ctypes.c_uint16
+        _lib = L
+    return _lib
+
+
+def _threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+# --------------------------------------------------------------------------
+# persistence of consecutive top-k sets under an AR(1) hidden state
+# --------------------------------------------------------------------------
+
+def persistence_closed_form(rho: float, p: float) -> float:
+    """Expected |A_t & A_{t-1}| / k when each score is a unit Gaussian with
+    token-to-token correlation rho and the top fraction p is kept:
+    P(X > q, Y > q) / p with q = Phi^{-1}(1 - p)."""
+    from scipy.stats import multivariate_normal, norm
+
+    q = norm.ppf(1.0 - p)
+    both = multivariate_normal(mean=[0.0, 0.0], cov=[[1.0, rho], [rho, 1.0]]).cdf([-q, -q])
+    return float(both / p)
+
+
+@lru_cache(maxsize=None)
+def rho_for_persistence(p: float, target: float) -> float:
+    from scipy.optimize import brentq
+
+    return float(brentq(lambda r: persistence_closed_form(r, p) - target, 0.0, 0.99999,
+                        xtol=1e-7))
+
+
+# --------------------------------------------------------------------------
+# configurations
+# --------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class Config:
+    name: str
+    layers: int          # L': downstream layers scored by one predictor pass
+    d_model: int
+    d_ffn: int
+    rank: int
+    active_frac: float
+    resident_frac: float
+    wdtype: str
+    adtype: str
+    tokens: int
+    persistence: float | None = None   # target overlap; None -> use rho as given
+    rho_given: float | None = None
+    seed: int = 0
+    weight_std: float = 0.02
+    dyadic: bool = False
+    dyadic_w_range: int = 3             # MLP weights m * 2^-6, m in {-R..R}
+    dyadic_h_range: int = 4             # h integers in {-R..R}
+    dyadic_redraw: float = 0.1          # per-token redraw rate of h coordinates
+    k_override: int | None = None
+    c_override: int | None = None
+    extra: dict = field(default_factory=dict, compare=False, hash=False)
+
+    @property
+    def k(self) -> int:
+        return self.k_override if self.k_override is not None else int(
+            math.floor(self.active_frac * self.d_ffn + 1e-9))
+
+    @property
+    def capacity(self) -> int:
+        return self.c_override if self.c_override is not None else int(
+            math.floor(self.resident_frac * self.d_ffn + 1e-9))
+
+    @property
+    def rho(self) -> float:
+        if self.rho_given is not None:
+            return self.rho_given
+        return rho_for_persistence(self.k / self.d_ffn, self.persistence)
+
+    @property
+    def record_bytes(self) -> int:
+        return 3 * self.d_model * ITEMSIZE[self.wdtype]
+
+    @property
+    def storage_bytes(self) -> int:
+        return self.layers * self.d_ffn * self.record_bytes
+
+    @property
+    def resident_bytes(self) -> int:
+        return self.layers * self.capacity * self.record_bytes
+
+    def with_(self, **kw) -> "Config":
+        return replace(self, **kw)
+
+
+CONFIGS = {
+    # 4 layers (3 downstream), fp32, rho 0.95 as given, 10% active, 50% resident
+    "tiny": Config("tiny", 3, 256, 1024, 32, 0.10, 0.50, "f32", "f32", 16, rho_given=0.95),
+    # 32 layers (31 downstream), fp16, 15% active, 50% resident, 83.5% persistence
+    "7b": Config("7b", 31, 4096, 11008, 416, 0.15, 0.50, "f16", "f16", 256, persistence=0.835),
+    # 40 layers, fp16, 12% active, 40% resident
+    "13b": Config("13b", 39, 5120, 13824, 512, 0.12, 0.40, "f16", "f16", 256, persistence=0.835),
+    # 80 layers, bf16, 10% active, 35% resident, 85% persistence
+    "70b": Config("70b", 79, 8192, 28672, 768, 0.10, 0.35, "bf16", "bf16", 128, persistence=0.85),
+    # dyadic-exact variants (test only)
+    "dyadic_tiny": Config("dyadic_tiny", 3, 256, 1024, 32, 0.10, 0.50, "f32", "f32", 16,
+                          rho_given=0.0, dyadic=True, dyadic_w_range=3, dyadic_h_range=4),
+    "dyadic_7b": Config("dyadic_7b", 31, 4096, 11008, 416, 0.15, 0.50, "f16", "f16", 8,
+                        rho_given=0.0, dyadic=True, dyadic_w_range=3, dyadic_h_range=1),
+}
+
+
+def sweep_configs() -> list[Config]:
+    """One-factor-at-a-time sweep around 7B (15% active, 83.5% persistence,
+    50% resident)."""
+    base = CONFIGS["7b"]
+    out = []
+    for a in (0.05, 0.15, 0.30):
+        out.append(base.with_(name=f"7b_act{int(a*100)}", active_frac=a))
+    for p in (0.70, 0.82, 0.85, 0.95):
+        out.append(base.with_(name=f"7b_pers{int(p*100)}", persistence=p))
+    for r in (0.25, 0.50, 0.75):
+        out.append(base.with_(name=f"7b_res{int(r*100)}", resident_frac=r))
+    return out
+
+
+def get(name: str) -> Config:
+    if name in CONFIGS:
+        return CONFIGS[name]
+    for c in sweep_configs():
+        if c.name == name:
+            return c
+    raise KeyError(name)
+
+
+# --------------------------------------------------------------------------
+# generators
+# --------------------------------------------------------------------------
+
+def fill_storage(cfg: Config, dst_ptr: int, layer0: int = 0, layers: int | None = None,
+                 nthreads: int | None = None) -> None:
+    """Write records of layers [layer0, layer0+layers) to raw memory at dst_ptr
+    ([layers][F][3d] of cfg.wdtype)."""
+    layers = cfg.layers - layer0 if layers is None else layers
+    if cfg.dyadic:
+        dy, scale, mr = 1, 2.0 ** -6, cfg.dyadic_w_range
+    else:
+        dy, scale, mr = 0, cfg.weight_std, 0
+    _gen().npg_fill_records(DTYPE_CODES[cfg.wdtype], cfg.seed, layer0, layers, cfg.d_ffn,
+                            cfg.d_model, dy, scale, mr, dst_ptr, nthreads or _threads())
+
+
+def storage(cfg: Config, layer0: int = 0, layers: int | None = None) -> np.ndarray:
+    """Records as a numpy array [layers][F][3d] of storage bits."""
+    layers = cfg.layers - layer0 if layers is None else layers
+    out = np.empty((layers, cfg.d_ffn, 3 * cfg.d_model), dtype=STORAGE_NP[cfg.wdtype])
+    fill_storage(cfg, out.ctypes.data, layer0, layers)
+    return out
+
+
+def predictor(cfg: Config) -> tuple[np.ndarray, np.ndarray]:
+    """A [L'][r][d] ~ N(0, 1/d) and B [L'][F][r] ~ N(0, 1/r) (storage bits);
+    dyadic: entries m * 2^-3 with m in {-1, 0, 1}."""
+    L, d, F, r = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.rank
+    A = np.empty((L, r, d), dtype=STORAGE_NP[cfg.wdtype])
+    B = np.empty((L, F, r), dtype=STORAGE_NP[cfg.wdtype])
+    g = _gen()
+    if cfg.dyadic:
+        sa = sb = (1, 2.0 ** -3, 1)
+    else:
+        sa, sb = (0, 1.0 / math.sqrt(d), 0), (0, 1.0 / math.sqrt(r), 0)
+    g.npg_fill_matrix(DTYPE_CODES[cfg.wdtype], cfg.seed, TENSOR_PRED_A, 0, L, r, d,
+                      sa[0], sa[1], sa[2], A.ctypes.data, _threads())
+    g.npg_fill_matrix(DTYPE_CODES[cfg.wdtype], cfg.seed, TENSOR_PRED_B, 0, L, F, r,
+                      sb[0], sb[1], sb[2], B.ctypes.data, _threads())
+    return A, B
+
+
+def hidden(cfg: Config, tokens: int | None = None, want_f64: bool = False):
+    """h_0..h_{T-1} as [T][d] storage bits of cfg.adtype (and the float64
+    AR(1) state when want_f64)."""
+    T = cfg.tokens if tokens is None else tokens
+    out = np.empty((T, cfg.d_model), dtype=STORAGE_NP[cfg.adtype])
+    f64 = np.empty((T, cfg.d_model), dtype=np.float64)
+    if cfg.dyadic:
+        _gen().npg_hidden(DTYPE_CODES[cfg.adtype], cfg.seed, T, cfg.d_model, cfg.dyadic_redraw,
+                          1, cfg.dyadic_h_range, out.ctypes.data, f64.ctypes.data)
+    else:
+        _gen().npg_hidden(DTYPE_CODES[cfg.adtype], cfg.seed, T, cfg.d_model, cfg.rho, 0, 0,
+                          out.ctypes.data, f64.ctypes.data)
+    return (out, f64) if want_f64 else out
+
+
+def encode(dtype: str, values) -> np.ndarray:
+    """float64 values -> storage bits (the generator's own encoder)."""
+    v = np.ascontiguousarray(np.asarray(values, dtype=np.float64))
+    out = np.empty(v.shape, dtype=STORAGE_NP[dtype])
+    _gen().npg_encode(DTYPE_CODES[dtype], v.ctypes.data, v.size, out.ctypes.data)
+    return out

@@ -1,0 +1,287 @@
+/*
+ * npgen.c -- seeded synthetic inputs for the NeuroPrefetcher decode path.
+ *
+ * This file generates inputs only: MLP neuron records, predictor factors and
+ * the hidden-state sequence.  It holds none of the method's arithmetic; both
+ * the HIP path and the CPU oracle consume what it writes.
+ *
+ * Random numbers come from a counter-based generator: value i of the stream
+ * (seed, tensor, layer) is the i-th output of SplitMix64 (Steele, Lea and
+ * Flood, "Fast splittable pseudorandom number generators", OOPSLA 2014)
+ * started from a state derived from (seed, tensor, layer).  Any element can
+ * therefore be generated independently, in any order and on any thread.
+ * Normal variates use the Box-Muller transform on two consecutive draws.
+ *
+ * Floating-point encodings (fp16 = IEEE binary16, bf16 = the top half of
+ * binary32) round to nearest, ties to even, from a double.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <string.h>
+
+#define NPG_F32 0
+#define NPG_F16 1
+#define NPG_BF16 2
+
+static const uint64_t GOLDEN = 0x9E3779B97F4A7C15ULL;
+
+static inline uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+uint64_t npg_stream(uint64_t seed, uint32_t tensor, uint32_t layer) {
+  uint64_t s = mix64(seed + GOLDEN * ((uint64_t)tensor + 1));
+  return mix64(s + GOLDEN * ((uint64_t)layer + 1));
+}
+
+/* i-th SplitMix64 output of a generator whose state starts at `stream`. */
+uint64_t npg_draw(uint64_t stream, uint64_t i) {
+  return mix64(stream + GOLDEN * (i + 1));
+}
+
+/* Uniform on the open interval (0, 1): 53 random bits, centred in their cell. */
+static inline double unit_open(uint64_t x) {
+  return ((double)(x >> 11) + 0.5) * (1.0 / 9007199254740992.0);
+}
+
+double npg_normal(uint64_t stream, uint64_t i) {
+  double u1 = unit_open(npg_draw(stream, 2 * i));
+  double u2 = unit_open(npg_draw(stream, 2 * i + 1));
+  return sqrt(-2.0 * log(u1)) * cos(6.283185307179586476925 * u2);
+}
+
+/* Integer uniform on {-m, ..., m}. */
+int64_t npg_int(uint64_t stream, uint64_t i, int64_t m) {
+  uint64_t span = (uint64_t)(2 * m + 1);
+  return (int64_t)((npg_draw(stream, i) >> 11) % span) - m;
+}
+
+/* ---- encodings: double -> storage bits, round to nearest even ---------- */
+
+static inline uint32_t f32_bits(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  return u;
+}
+
+/* binary32 -> bfloat16: keep the top 16 bits, rounding the low 16 to
+ * nearest, ties to even.  NaN stays NaN (quiet bit forced). */
+static uint16_t bf16_from_f32(float f) {
+  uint32_t u = f32_bits(f);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu))
+    return (uint16_t)((u >> 16) | 0x0040u);
+  uint32_t lsb = (u >> 16) & 1u;
+  u += 0x7FFFu + lsb;
+  return (uint16_t)(u >> 16);
+}
+
+/* double -> bfloat16 with one rounding: the double is first cut to binary32
+ * with round-to-odd (sticky bit), which makes the later rounding to 8
+ * significand bits equal to direct rounding of the double. */
+uint16_t npg_bf16(double v) {
+  float f = (float)v; /* round to nearest even */
+  if (isfinite(v) && (double)f != v) {
+    /* redo as round-to-odd: truncate toward zero, then set the last bit */
+    uint32_t u = f32_bits(f);
+    double back = (double)f;
+    if (fabs(back) > fabs(v)) u -= 1; /* step back toward zero */
+    u |= 1u;
+    memcpy(&f, &u, 4);
+  }
+  return bf16_from_f32(f);
+}
+
+/* double -> IEEE binary16, round to nearest even, overflow to infinity. */
+uint16_t npg_f16(double v) {
+  uint16_t sign = signbit(v) ? 0x8000u : 0;
+  double a = fabs(v);
+  if (isnan(v)) return 0x7E00u;
+  if (a >= 65520.0) return sign | 0x7C00u; /* at or above max + half ulp */
+  if (a < ldexp(1.0, -14)) {
+    /* subnormal range: units of 2^-24 */
+    double q = a * 16777216.0; /* a / 2^-24, exact */
+    double fl = floor(q);
+    double rem = q - fl;
+    uint32_t m = (uint32_t)fl;
+    if (rem > 0.5 || (rem == 0.5 && (m & 1u))) m += 1;
+    return sign | (uint16_t)m; /* m == 1024 becomes the smallest normal */
+  }
+  int e;
+  double fr = frexp(a, &e); /* a = fr * 2^e, fr in [0.5, 1) */
+  int exp16 = e - 1 + 15;   /* biased exponent of a = 1.xxx * 2^(e-1) */
+  double q = ldexp(fr, 11); /* 1.xxx * 2^10: 11 significant bits */
+  double fl = floor(q);
+  double rem = q - fl;
+  uint32_t m = (uint32_t)fl;
+  if (rem > 0.5 || (rem == 0.5 && (m & 1u))) m += 1;
+  if (m == 2048) { m = 1024; exp16 += 1; }
+  if (exp16 >= 31) return sign | 0x7C00u;
+  return sign | (uint16_t)((exp16 << 10) | (m - 1024));
+}
+
+static inline void put(int dtype, void* out, size_t i, double v) {
+  if (dtype == NPG_F32) {
+    ((float*)out)[i] = (float)v;
+  } else if (dtype == NPG_F16) {
+    ((uint16_t*)out)[i] = npg_f16(v);
+  } else {
+    ((uint16_t*)out)[i] = npg_bf16(v);
+  }
+}
+
+/* ---- threaded fill ------------------------------------------------------ */
+
+enum { KIND_RECORDS = 0, KIND_MATRIX = 1 };
+
+typedef struct {
+  int kind, dtype, dyadic;
+  uint64_t seed;
+  uint32_t tensor;
+  int64_t layer0, layers, rows, cols;
+  double scale;    /* std (gaussian) or power-of-two unit (dyadic) */
+  int64_t mrange;  /* dyadic integer range */
+  void* out;
+  int64_t row_begin, row_end; /* rows over the flattened [layers][rows] */
+} fill_job;
+
+/* Records: element c of the gate, up or down^T row of neuron n in layer l is
+ * drawn from stream (seed, tensor 1/2/3, l) at index n*d + c. */
+static void* fill_worker(void* p) {
+  fill_job* j = (fill_job*)p;
+  for (int64_t rr = j->row_begin; rr < j->row_end; ++rr) {
+    int64_t l = j->layer0 + rr / j->rows;
+    int64_t n = rr % j->rows;
+    if (j->kind == KIND_RECORDS) {
+      int64_t d = j->cols;
+      for (int part = 0; part < 3; ++part) {
+        uint64_t st = npg_stream(j->seed, (uint32_t)(1 + part), (uint32_t)l);
+        size_t base = (size_t)rr * 3 * d + (size_t)part * d;
+        for (int64_t c = 0; c < d; ++c) {
+          uint64_t idx = (uint64_t)(n * d + c);
+          double v = j->dyadic ? (double)npg_int(st, idx, j->mrange) * j->scale
+                               : npg_normal(st, idx) * j->scale;
+          put(j->dtype, j->out, base + (size_t)c, v);
+        }
+      }
+    } else {
+      uint64_t st = npg_stream(j->seed, j->tensor, (uint32_t)l);
+      size_t base = (size_t)rr * j->cols;
+      for (int64_t c = 0; c < j->cols; ++c) {
+        uint64_t idx = (uint64_t)(n * j->cols + c);
+        double v = j->dyadic ? (double)npg_int(st, idx, j->mrange) * j->scale
+                             : npg_normal(st, idx) * j->scale;
+        put(j->dtype, j->out, base + (size_t)c, v);
+      }
+    }
+  }
+  return NULL;
+}
+
+static int run_fill(fill_job proto, int nthreads) {
+  int64_t total = proto.layers * proto.rows;
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > 256) nthreads = 256;
+  if (total < nthreads) nthreads = total > 0 ? (int)total : 1;
+  pthread_t th[256];
+  fill_job jobs[256];
+  int started = 0;
+  for (int t = 0; t < nthreads; ++t) {
+    jobs[t] = proto;
+    jobs[t].row_begin = total * t / nthreads;
+    jobs[t].row_end = total * (t + 1) / nthreads;
+    if (t == nthreads - 1) {
+      fill_worker(&jobs[t]);
+    } else if (pthread_create(&th[t], NULL, fill_worker, &jobs[t]) == 0) {
+      ++started;
+    } else {
+      fill_worker(&jobs[t]);
+      th[t] = 0;
+    }
+  }
+  for (int t = 0; t < nthreads - 1; ++t)
+    if (th[t]) pthread_join(th[t], NULL);
+  (void)started;
+  return 0;
+}
+
+/* MLP neuron records of layers [layer0, layer0+layers), written to `out`
+ * as [layers][F][3d].  Gaussian N(0, std^2), or dyadic m * unit with m
+ * uniform on {-mrange..mrange} when dyadic != 0. */
+int npg_fill_records(int dtype, uint64_t seed, int64_t layer0, int64_t layers,
+                     int64_t F, int64_t d, int dyadic, double std_or_unit,
+                     int64_t mrange, void* out, int nthreads) {
+  fill_job j;
+  memset(&j, 0, sizeof j);
+  j.kind = KIND_RECORDS;
+  j.dtype = dtype;
+  j.dyadic = dyadic;
+  j.seed = seed;
+  j.layer0 = layer0;
+  j.layers = layers;
+  j.rows = F;
+  j.cols = d;
+  j.scale = std_or_unit;
+  j.mrange = mrange;
+  j.out = out;
+  return run_fill(j, nthreads);
+}
+
+/* A [layers][rows][cols] matrix stack for tensor id `tensor` (4 = predictor
+ * A, 5 = predictor B), element (l, i, c) from stream (seed, tensor, l) at
+ * index i*cols + c. */
+int npg_fill_matrix(int dtype, uint64_t seed, uint32_t tensor, int64_t layer0,
+                    int64_t layers, int64_t rows, int64_t cols, int dyadic,
+                    double std_or_unit, int64_t mrange, void* out,
+                    int nthreads) {
+  fill_job j;
+  memset(&j, 0, sizeof j);
+  j.kind = KIND_MATRIX;
+  j.dtype = dtype;
+  j.dyadic = dyadic;
+  j.seed = seed;
+  j.tensor = tensor;
+  j.layer0 = layer0;
+  j.layers = layers;
+  j.rows = rows;
+  j.cols = cols;
+  j.scale = std_or_unit;
+  j.mrange = mrange;
+  j.out = out;
+  return run_fill(j, nthreads);
+}
+
+/* Hidden states h_0..h_{T-1}, [T][d], encoded as `dtype`.
+ * Gaussian: h_0 = e_0, h_t = rho*h_{t-1} + sqrt(1-rho^2)*e_t with
+ * e_t[c] = N(0,1) from stream (seed, 6, t) at index c; kept in double.
+ * Dyadic (dyadic != 0): h_0[c] uniform on {-mrange..mrange}; afterwards each
+ * coordinate is redrawn with probability `rho` (read as a redraw rate) and
+ * kept otherwise. */
+int npg_hidden(int dtype, uint64_t seed, int64_t T, int64_t d, double rho,
+               int dyadic, int64_t mrange, void* out, double* out_f64) {
+  double prev_scale = rho, fresh_scale = sqrt(1.0 - rho * rho);
+  for (int64_t c = 0; c < d; ++c) {
+    double h = 0.0;
+    for (int64_t t = 0; t < T; ++t) {
+      uint64_t st = npg_stream(seed, 6, (uint32_t)t);
+      if (dyadic) {
+        uint64_t st_pick = npg_stream(seed, 7, (uint32_t)t);
+        double r = unit_open(npg_draw(st_pick, (uint64_t)c));
+        if (t == 0 || r < rho) h = (double)npg_int(st, (uint64_t)c, mrange);
+      } else {
+        double e = npg_normal(st, (uint64_t)c);
+        h = (t == 0) ? e : prev_scale * h + fresh_scale * e;
+      }
+      put(dtype, out, (size_t)(t * d + c), h);
+      if (out_f64) out_f64[t * d + c] = h;
+    }
+  }
+  return 0;
+}
+
+/* Encode an array of doubles (tests use this to build small inputs). */
+void npg_encode(int dtype, const double* in, int64_t n, void* out) {
+  for (int64_t i = 0; i < n; ++i) put(dtype, out, (size_t)i, in[i]);
+}
