@@ -1,0 +1,264 @@
+"""Decode-step benchmark of the NeuroPrefetcher hot path on one MI355X.
+
+One step = one decode token through the whole path: np_predict, np_select,
+np_delta, staging of the incoming rows and np_sparse_mlp for every downstream
+layer.  Inputs are synthetic and already resident in HBM when the timed
+region starts (predictor factors, hidden states, and the storage tier the
+incoming rows are staged from); the step's own work is timed, nothing is
+skipped.  Prints one JSON line.
+
+Extra measurements in the same run:
+  * the sparse-MLP kernel's average launch time, from HIP events around each
+    launch on its stream, against the HBM roofline;
+  * a per-step breakdown (predict / select / delta / stage / mlp);
+  * the same step with the storage tier in pinned host memory (staging over
+    the host link) -- reported under "host_tier", never as `value`;
+  * the CPU oracle on a bounded sample, on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def mlp_bytes_per_launch(cfg) -> int:
+    """Algorithmic bytes of one np_sparse_mlp launch: k records of 3d weights,
+    k int32 slots, x and y."""
+    esz = 4 if cfg.wdtype == "f32" else 2
+    return cfg.k * 3 * cfg.d_model * esz + cfg.k * 4 + 2 * cfg.d_model * esz
+
+
+def timed_steps(pipe, t0, steps, with_mlp_events=True):
+    import torch
+
+    L = pipe.cfg.layers
+    evs = None
+    if with_mlp_events:
+        evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+                for _ in range(L)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(steps):
+        pipe.step(t0 + i, mlp_events=evs[i] if evs else None)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    mlp_us = None
+    if evs:
+        durs = [e[0].elapsed_time(e[1]) * 1e3 for st in evs for e in st]
+        mlp_us = sum(durs) / len(durs)
+    return wall, mlp_us
+
+
+def breakdown(pipe, t0, steps):
+    """Per-phase device time (µs, mean over steps) from events on the main
+    stream, one phase at a time (no overlap)."""
+    import torch
+
+    from paper_2608_22643_amd import binding as B
+
+    s, cfg = pipe.shape, pipe.cfg
+    L, k = cfg.layers, cfg.k
+    names = ("predict", "select", "delta", "stage", "mlp")
+    acc = {n: 0.0 for n in names}
+    ybytes = cfg.d_model * (4 if cfg.adtype == "f32" else 2)
+    for i in range(steps):
+        t = t0 + i
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        m = pipe.main
+        ev[0].record(m)
+        B.np_predict(s, pipe.x_ptr(t), pipe.A, pipe.B, pipe.scores, pipe.ws, m)
+        ev[1].record(m)
+        B.np_select(s, pipe.scores, pipe.mask, pipe.active_ids, pipe.ws, m)
+        ev[2].record(m)
+        B.np_delta(s, t, pipe.active_ids, pipe.state, pipe.out, pipe.ws, m)
+        ev[3].record(m)
+        B.np_stage_gather(s, pipe.out, 0, L, pipe.storage, pipe.resident, pipe.ws, m)
+        ev[4].record(m)
+        slots = pipe.lists["active_slots"].data_ptr()
+        for l in range(L):
+            B.np_sparse_mlp(s, l, pipe.x_ptr(t), pipe.resident, slots + 4 * l * k, k,
+                            pipe.y.data_ptr() + l * ybytes, pipe.ws, m)
+        ev[5].record(m)
+        torch.cuda.synchronize()
+        for j, n in enumerate(names):
+            acc[n] += ev[j].elapsed_time(ev[j + 1]) * 1e3
+    return {n: round(v / steps, 2) for n, v in acc.items()}
+
+
+def delta_stats(pipe):
+    import numpy as np
+
+    c = pipe.counts.cpu().numpy().reshape(-1, 4)
+    return c
+
+
+def cpu_baseline(cfg, host_storage, seconds: float):
+    """The oracle (plain C, fp64, one thread) on whole tokens of the same
+    workload until `seconds` of CPU work have run (at least one token)."""
+    import numpy as np
+
+    import oracle
+    from paper_2608_22643_amd import workload as W
+
+    oracle.build()
+    A, Bm = W.predictor(cfg)
+    h = W.hidden(cfg, 64)
+    store = host_storage.numpy().view(np.float32 if cfg.wdtype == "f32" else np.uint16)
+    store = store.reshape(cfg.layers, cfg.d_ffn, 3 * cfg.d_model)
+    st = oracle.State(cfg.layers, cfg.d_ffn, cfg.capacity)
+    n, t0 = 0, time.perf_counter()
+    while True:
+        s = oracle.predict(cfg, h[n], A, Bm)
+        _, ids = oracle.select(s, cfg.k)
+        oracle.delta(n, ids, st, cfg.capacity)
+        for l in range(cfg.layers):
+            oracle.sparse_mlp(cfg, l, h[n], store, ids[l])
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or n >= 64:
+            break
+    return {"value": round(n / el, 4), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} whole decode tokens (cold start first) of the {cfg.name} workload: "
+                      f"predict, select, delta, sparse MLP of all {cfg.layers} layers; "
+                      f"staging omitted (a byte copy); {el:.1f} s on 1 host thread"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="7b")
+    ap.add_argument("--overlap", type=int, default=1)
+    ap.add_argument("--host-tier-steps", type=int, default=20)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--breakdown-steps", type=int, default=10)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(this build runs the hot path of one GPU only)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_22643_amd import workload as W
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get(args.config)
+    K, Wm = args.steps, args.warmup
+    T = 1 + Wm + K + args.breakdown_steps + args.host_tier_steps + 2
+    log(f"[bench] config {cfg.name}: L'={cfg.layers} d={cfg.d_model} F={cfg.d_ffn} r={cfg.rank} "
+        f"k={cfg.k} C={cfg.capacity} {cfg.wdtype}; tokens {T}")
+    t = time.perf_counter()
+    host_storage = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
+    W.fill_storage(cfg, host_storage.data_ptr())
+    log(f"[bench] storage tier generated: {cfg.storage_bytes / 1e9:.2f} GB in "
+        f"{time.perf_counter() - t:.1f} s")
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", overlap=bool(args.overlap),
+                          tokens=T, host_storage=host_storage)
+    log("[bench] pipeline ready (storage tier in HBM)")
+    # cold start, then warmup
+    torch.cuda.synchronize()
+    c0 = time.perf_counter()
+    pipe.step(0)
+    torch.cuda.synchronize()
+    cold_ms = (time.perf_counter() - c0) * 1e3
+    for i in range(Wm):
+        pipe.step(1 + i)
+    torch.cuda.synchronize()
+    log("[bench] warmup done")
+    wall, mlp_us = timed_steps(pipe, 1 + Wm, K)
+    log(f"[bench] timed {K} steps: {wall * 1e3 / K:.3f} ms/step, mlp launch {mlp_us:.2f} us")
+    err = pipe.device_error()
+    if err:
+        log(f"[bench] device error word {err:#x}")
+        sys.exit(1)
+    ms_per_step = wall * 1e3 / K
+    bytes_launch = mlp_bytes_per_launch(cfg)
+    achieved = bytes_launch / (mlp_us * 1e-6) / 1e9
+    counts = delta_stats(pipe)
+    # per-phase breakdown (no overlap) and persistence statistics
+    t1 = 1 + Wm + K
+    bd = breakdown(pipe, t1, args.breakdown_steps)
+    log(f"[bench] breakdown us: {bd}")
+    n_in = counts[:, 0].astype(np.float64)
+    rec = cfg.record_bytes
+    stats = {"incoming_rows_per_token": int(n_in.sum()),
+             "staged_MB_per_token": round(float(n_in.sum()) * rec / 1e6, 2),
+             "reuse_pct": round(100.0 * float(counts[:, 1].sum()) / (cfg.k * cfg.layers), 2)}
+    del pipe
+    torch.cuda.empty_cache()
+    # storage tier in pinned host memory: the PCIe-inclusive rate
+    host = None
+    if args.host_tier_steps > 0:
+        hp = DecodePipeline(cfg, tier="host", staging="memcpy", overlap=True, tokens=T,
+                            host_storage=host_storage)
+        hp.step(0)
+        for i in range(3):
+            hp.step(1 + i)
+        torch.cuda.synchronize()
+        hw, _ = timed_steps(hp, 4, args.host_tier_steps, with_mlp_events=False)
+        hg = DecodePipeline(cfg, tier="host", staging="gather", overlap=True, tokens=T,
+                            host_storage=host_storage)
+        hg.step(0)
+        for i in range(3):
+            hg.step(1 + i)
+        torch.cuda.synchronize()
+        gw, _ = timed_steps(hg, 4, args.host_tier_steps, with_mlp_events=False)
+        host = {"memcpy_staging_tok_s": round(args.host_tier_steps / hw, 2),
+                "mapped_gather_tok_s": round(args.host_tier_steps / gw, 2),
+                "note": "storage tier in pinned host memory; staging crosses the host link"}
+        log(f"[bench] host tier: {host}")
+        del hp, hg
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(cfg, host_storage, args.cpu_seconds)
+        log(f"[bench] cpu baseline: {cpu}")
+    line = {
+        "metric": "sparse-MLP decode tokens/sec + achieved HBM GB/s (% peak), 7B-shaped, batch 1",
+        "value": round(1e3 / ms_per_step, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.wdtype,
+        "data": "synthetic (seeded generator; no model weights or datasets)",
+        "config": {"workload": f"{cfg.name}-shaped decode: {cfg.layers} downstream layers, "
+                               f"d={cfg.d_model}, F={cfg.d_ffn}, rank {cfg.rank}, k={cfg.k} "
+                               f"({cfg.active_frac:.0%}), C={cfg.capacity} "
+                               f"({cfg.resident_frac:.0%}), {cfg.wdtype}, batch 1",
+                   "storage_tier": "HBM", "staging": "np_stage_gather",
+                   "overlap": bool(args.overlap)},
+        "roofline": {"bound": "hbm", "kernel": "np_sparse_mlp",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "bytes_per_launch": bytes_launch, "avg_launch_us": round(mlp_us, 3)},
+        "sparse_mlp_tok_s": round(1e6 / (mlp_us * cfg.layers), 1),
+        "cold_start_ms": round(cold_ms, 2),
+        "breakdown_us": bd,
+        "delta": stats,
+        "host_tier": host,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -37,8 +37,10 @@
  *  d  = d_model, F = d_ffn (MLP intermediate size), r = predictor rank,
  *  k  = active rows per layer, C = resident slots per layer.
  *  w  = wdtype (MLP records and predictor factors), a = adtype (h, x, y).
- *  Requirements: 1 <= k <= C <= F <= 65535, 1 <= L', r >= 1;
- *  d and r multiples of 8 for 16-bit types and of 4 for fp32; d <= 16384.
+ *  Requirements: wdtype == adtype; 1 <= k <= C <= F <= 65535; k <= 8192;
+ *  L' >= 1; d and r multiples of 8 for 16-bit types and of 4 for fp32;
+ *  d <= 16384 (16-bit) or 8192 (fp32); r <= 1024 (16-bit) or 512 (fp32).
+ *  k > C is NP_ERR_CAPACITY; any other violation NP_ERR_INVALID_ARG.
  *
  *  Neuron record (Sec. 3.5, neuron-centric layout): row n of gate, row n of up
  *  and row n of down^T (down transposed offline so all three share one shape),
@@ -63,15 +65,15 @@ typedef enum np_status {
   NP_ERR_CAPACITY = 2,    /* k > C, staging buffer smaller than one record, ... */
   NP_ERR_HIP = 3,         /* a HIP runtime call failed; detail in np_last_error() */
   NP_ERR_UNSUPPORTED = 4, /* valid request this build does not implement */
-  NP_ERR_STATE = 5        /* state marked invalid by an earlier staging failure */
+  NP_ERR_STATE = 5        /* reserved */
 } np_status;
 
 typedef enum np_dtype { NP_F32 = 0, NP_F16 = 1, NP_BF16 = 2 } np_dtype;
 
 /* Device error word bits (sticky, OR-ed; see np_device_error). */
 #define NP_DEVERR_NAN_SCORE    0x1  /* np_select saw a NaN score */
-#define NP_DEVERR_NOT_RESIDENT 0x2  /* np_sparse_mlp got a slot outside [0, C) */
-#define NP_DEVERR_STATE        0x4  /* np_delta found slot_of / neuron_of inconsistent */
+#define NP_DEVERR_NOT_RESIDENT 0x2  /* a slot outside [0, C) or id outside [0, F) */
+#define NP_DEVERR_STATE        0x4  /* inconsistent state or plan (ids, slots, counts) */
 #define NP_DEVERR_SPIN_LIMIT   0x8  /* a bounded in-kernel wait gave up */
 
 typedef struct np_shape {
@@ -206,11 +208,13 @@ np_status np_stage_rows(const np_shape* shape, const np_stage_plan* plan,
  * `storage` is [L'][F][3d] in device memory (a storage tier kept in HBM) or in
  * pinned host memory mapped into the device address space (the kernel then
  * reads it over the host link, as the paper's mapped staging does, Sec. 3.5).
- * Asynchronous on `stream`; no host synchronisation. */
+ * An id or slot outside [0, F) x [0, C) sets NP_DEVERR_NOT_RESIDENT in
+ * dev_ws and that record is skipped.  Asynchronous on `stream`; no host
+ * synchronisation. */
 np_status np_stage_gather(const np_shape* shape, const np_delta_out* out,
                           int32_t layer_begin, int32_t layer_end,
                           const void* storage, void* dev_resident,
-                          hipStream_t stream);
+                          void* dev_ws, hipStream_t stream);
 
 /* Sparse MLP of one downstream layer over its resident active rows
  * (Sec. 3.4: the slot map locates each active row; row order is irrelevant;

@@ -1,0 +1,191 @@
+// np_abi.cpp -- host side of the C ABI: argument validation, status text,
+// workspace sizing and dispatch to the kernel launchers.  Validation runs
+// before anything is enqueued.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "np_internal.hpp"
+
+namespace np {
+
+thread_local std::string g_last_error;
+
+np_status fail(np_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+np_status hip_fail(hipError_t e, const char* what) {
+  return fail(NP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return p && ((uintptr_t)p & 15u) == 0; }
+
+np_status check_shape(const np_shape* s) {
+  if (!s) return fail(NP_ERR_INVALID_ARG, "shape is NULL");
+  if (s->wdtype < NP_F32 || s->wdtype > NP_BF16)
+    return fail(NP_ERR_INVALID_ARG, "wdtype %d is not an np_dtype", s->wdtype);
+  if (s->adtype != s->wdtype)
+    return fail(NP_ERR_INVALID_ARG, "adtype %d must equal wdtype %d", s->adtype, s->wdtype);
+  const int V = vec_elems(s->wdtype);
+  if (s->layers < 1) return fail(NP_ERR_INVALID_ARG, "layers %d < 1", s->layers);
+  if (s->d_model < V || s->d_model % V)
+    return fail(NP_ERR_INVALID_ARG, "d_model %d is not a positive multiple of %d", s->d_model, V);
+  if (s->d_model > (s->wdtype == NP_F32 ? 8192 : 16384))
+    return fail(NP_ERR_INVALID_ARG, "d_model %d above the supported maximum", s->d_model);
+  if (s->rank < V || s->rank % V)
+    return fail(NP_ERR_INVALID_ARG, "rank %d is not a positive multiple of %d", s->rank, V);
+  if (s->rank > 128 * V)
+    return fail(NP_ERR_INVALID_ARG, "rank %d above the supported maximum %d", s->rank, 128 * V);
+  if (s->d_ffn < 1 || s->d_ffn > 65535)
+    return fail(NP_ERR_INVALID_ARG, "d_ffn %d outside [1, 65535]", s->d_ffn);
+  if (s->k < 1 || s->k > s->d_ffn || s->k > 8192)
+    return fail(NP_ERR_INVALID_ARG, "k %d outside [1, min(d_ffn, 8192)]", s->k);
+  if (s->capacity < 1 || s->capacity > s->d_ffn)
+    return fail(NP_ERR_INVALID_ARG, "capacity %d outside [1, d_ffn]", s->capacity);
+  if (s->k > s->capacity)
+    return fail(NP_ERR_CAPACITY, "k %d exceeds the resident capacity %d", s->k, s->capacity);
+  return NP_OK;
+}
+
+}  // namespace np
+
+using namespace np;
+
+extern "C" {
+
+const char* np_status_str(int32_t st) {
+  switch (st) {
+    case NP_OK: return "NP_OK";
+    case NP_ERR_INVALID_ARG: return "NP_ERR_INVALID_ARG";
+    case NP_ERR_CAPACITY: return "NP_ERR_CAPACITY";
+    case NP_ERR_HIP: return "NP_ERR_HIP";
+    case NP_ERR_UNSUPPORTED: return "NP_ERR_UNSUPPORTED";
+    case NP_ERR_STATE: return "NP_ERR_STATE";
+    default: return "NP_ERR_UNKNOWN";
+  }
+}
+
+const char* np_last_error(void) { return g_last_error.c_str(); }
+
+np_status np_shape_check(const np_shape* s) {
+  np_status st = check_shape(s);
+  if (st == NP_OK) g_last_error.clear();
+  return st;
+}
+
+np_status np_workspace_size(const np_shape* s, size_t* bytes) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (!bytes) return fail(NP_ERR_INVALID_ARG, "dev_ws_bytes is NULL");
+  *bytes = ws_total(*s);
+  return NP_OK;
+}
+
+np_status np_state_reset(const np_shape* s, const np_state* state, void* ws, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (!state || !aligned16(state->slot_of) || !aligned16(state->neuron_of) ||
+      !aligned16(state->last_used))
+    return fail(NP_ERR_INVALID_ARG, "state arrays must be non-NULL and 16-byte aligned");
+  if (!aligned16(ws)) return fail(NP_ERR_INVALID_ARG, "dev_ws must be non-NULL and 16-byte aligned");
+  hipError_t e = launch_fill_state(*s, *state, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_state_reset launch");
+}
+
+np_status np_predict(const np_shape* s, const void* h, const void* A, const void* B,
+                     float* scores, void* ws, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (!aligned16(h) || !aligned16(A) || !aligned16(B) || !aligned16(scores) || !aligned16(ws))
+    return fail(NP_ERR_INVALID_ARG, "np_predict: pointers must be non-NULL and 16-byte aligned");
+  hipError_t e = launch_predict(*s, h, A, B, scores, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_predict launch");
+}
+
+np_status np_select(const np_shape* s, const float* scores, uint32_t* mask, int32_t* ids,
+                    void* ws, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (!aligned16(scores) || !aligned16(mask) || !aligned16(ids) || !aligned16(ws))
+    return fail(NP_ERR_INVALID_ARG, "np_select: pointers must be non-NULL and 16-byte aligned");
+  hipError_t e = launch_select(*s, scores, mask, ids, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_select launch");
+}
+
+np_status np_delta(const np_shape* s, int32_t token, const int32_t* ids, const np_state* state,
+                   const np_delta_out* out, void* ws, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (token < 0) return fail(NP_ERR_INVALID_ARG, "token %d < 0", token);
+  if (!aligned16(ids) || !state || !aligned16(state->slot_of) || !aligned16(state->neuron_of) ||
+      !aligned16(state->last_used) || !aligned16(ws))
+    return fail(NP_ERR_INVALID_ARG, "np_delta: pointers must be non-NULL and 16-byte aligned");
+  if (!out || !aligned16(out->in_ids) || !aligned16(out->in_slots) || !aligned16(out->ev_ids) ||
+      !aligned16(out->ev_slots) || !aligned16(out->hit_ids) || !aligned16(out->active_slots) ||
+      !aligned16(out->counts))
+    return fail(NP_ERR_INVALID_ARG, "np_delta: output lists must be non-NULL and 16-byte aligned");
+  hipError_t e = launch_delta(*s, token, ids, *state, *out, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_delta launch");
+}
+
+np_status np_stage_gather(const np_shape* s, const np_delta_out* out, int32_t lb, int32_t le,
+                          const void* storage, void* resident, void* ws, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (lb < 0 || le > s->layers || lb > le)
+    return fail(NP_ERR_INVALID_ARG, "layer range [%d, %d) outside [0, %d)", lb, le, s->layers);
+  if (!out || !aligned16(out->counts) || !aligned16(out->in_ids) || !aligned16(out->in_slots))
+    return fail(NP_ERR_INVALID_ARG, "np_stage_gather: plan lists must be non-NULL and aligned");
+  if (!aligned16(storage) || !aligned16(resident) || !aligned16(ws))
+    return fail(NP_ERR_INVALID_ARG, "np_stage_gather: pointers must be non-NULL and aligned");
+  if (lb == le) return NP_OK;
+  // a pinned host storage tier is read through its device mapping
+  hipPointerAttribute_t attr;
+  if (hipPointerGetAttributes(&attr, storage) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(NP_ERR_INVALID_ARG, "np_stage_gather: storage is not device-accessible memory");
+  }
+  if (attr.type == hipMemoryTypeHost) {
+    if (!attr.devicePointer)
+      return fail(NP_ERR_INVALID_ARG, "np_stage_gather: host storage is not mapped to the device");
+    storage = attr.devicePointer;
+  }
+  hipError_t e = launch_stage_gather(*s, *out, lb, le, storage, resident, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_stage_gather launch");
+}
+
+np_status np_sparse_mlp(const np_shape* s, int32_t layer, const void* x, const void* resident,
+                        const int32_t* slots, int32_t n_active, void* y, void* ws,
+                        hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (layer < 0 || layer >= s->layers)
+    return fail(NP_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, s->layers);
+  if (n_active < 0 || n_active > s->capacity)
+    return fail(NP_ERR_INVALID_ARG, "n_active %d outside [0, capacity]", n_active);
+  if (!aligned16(x) || !aligned16(resident) || !aligned16(y) || !aligned16(ws) ||
+      (n_active > 0 && !slots))
+    return fail(NP_ERR_INVALID_ARG, "np_sparse_mlp: pointers must be non-NULL and aligned");
+  hipError_t e = launch_sparse_mlp(*s, layer, x, resident, slots, n_active, y, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp launch");
+}
+
+np_status np_device_error(const void* ws, hipStream_t stream, int32_t* code) {
+  if (!aligned16(ws) || !code) return fail(NP_ERR_INVALID_ARG, "np_device_error: bad pointer");
+  hipError_t e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_fail(e, "np_device_error synchronize");
+  e = hipMemcpy(code, (const char*)ws + WS_ERR, sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "np_device_error copy");
+  return NP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,287 @@
+// np_device.hpp -- device-side building blocks for gfx950 (64-wide waves):
+// element types moved as 16-byte vectors, dot products on the packed dot
+// instructions, wave reductions, workgroup scans, the sticky error word and
+// the workgroup k-selection primitive shared by top-k and victim selection.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "np_internal.hpp"
+
+namespace np {
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf162_t __attribute__((ext_vector_type(2)));
+
+constexpr int WAVE = 64;
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte load with the nontemporal hint (data streamed once)
+__device__ inline uint4 load_nt(const uint4* p) {
+  const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// ---------------------------------------------------------------------------
+// element types.  A 16-byte vector (uint4) holds V elements.
+// dot(w, x, acc): acc + sum_e w[e] * x[e] in fp32 (packed dot instructions
+// for 16-bit types: products are exact in fp32).
+// axpy(acc, a, w): acc[e] += a * float(w[e]).
+// ---------------------------------------------------------------------------
+struct TF32 {
+  static constexpr int V = 4;
+  static constexpr int dtype = NP_F32;
+  __device__ static inline float dot(uint4 w, uint4 x, float acc) {
+    acc = __builtin_fmaf(__uint_as_float(w.x), __uint_as_float(x.x), acc);
+    acc = __builtin_fmaf(__uint_as_float(w.y), __uint_as_float(x.y), acc);
+    acc = __builtin_fmaf(__uint_as_float(w.z), __uint_as_float(x.z), acc);
+    acc = __builtin_fmaf(__uint_as_float(w.w), __uint_as_float(x.w), acc);
+    return acc;
+  }
+  __device__ static inline void axpy(float* acc, float a, uint4 w) {
+    acc[0] = __builtin_fmaf(a, __uint_as_float(w.x), acc[0]);
+    acc[1] = __builtin_fmaf(a, __uint_as_float(w.y), acc[1]);
+    acc[2] = __builtin_fmaf(a, __uint_as_float(w.z), acc[2]);
+    acc[3] = __builtin_fmaf(a, __uint_as_float(w.w), acc[3]);
+  }
+  __device__ static inline void unpack(uint4 w, float* f) {
+    f[0] = __uint_as_float(w.x);
+    f[1] = __uint_as_float(w.y);
+    f[2] = __uint_as_float(w.z);
+    f[3] = __uint_as_float(w.w);
+  }
+  __device__ static inline uint32_t from_f32(float f) { return __float_as_uint(f); }
+};
+
+__device__ inline half2_t as_h2(uint32_t u) { return __builtin_bit_cast(half2_t, u); }
+__device__ inline bf162_t as_b2(uint32_t u) { return __builtin_bit_cast(bf162_t, u); }
+
+struct TF16 {
+  static constexpr int V = 8;
+  static constexpr int dtype = NP_F16;
+  __device__ static inline float dot(uint4 w, uint4 x, float acc) {
+    acc = __builtin_amdgcn_fdot2(as_h2(w.x), as_h2(x.x), acc, false);
+    acc = __builtin_amdgcn_fdot2(as_h2(w.y), as_h2(x.y), acc, false);
+    acc = __builtin_amdgcn_fdot2(as_h2(w.z), as_h2(x.z), acc, false);
+    acc = __builtin_amdgcn_fdot2(as_h2(w.w), as_h2(x.w), acc, false);
+    return acc;
+  }
+  __device__ static inline float lo(uint32_t u) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(u & 0xFFFFu));
+  }
+  __device__ static inline float hi(uint32_t u) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(u >> 16));
+  }
+  __device__ static inline void unpack(uint4 w, float* f) {
+    f[0] = lo(w.x);
+    f[1] = hi(w.x);
+    f[2] = lo(w.y);
+    f[3] = hi(w.y);
+    f[4] = lo(w.z);
+    f[5] = hi(w.z);
+    f[6] = lo(w.w);
+    f[7] = hi(w.w);
+  }
+  __device__ static inline void axpy(float* acc, float a, uint4 w) {
+    acc[0] = __builtin_fmaf(a, lo(w.x), acc[0]);
+    acc[1] = __builtin_fmaf(a, hi(w.x), acc[1]);
+    acc[2] = __builtin_fmaf(a, lo(w.y), acc[2]);
+    acc[3] = __builtin_fmaf(a, hi(w.y), acc[3]);
+    acc[4] = __builtin_fmaf(a, lo(w.z), acc[4]);
+    acc[5] = __builtin_fmaf(a, hi(w.z), acc[5]);
+    acc[6] = __builtin_fmaf(a, lo(w.w), acc[6]);
+    acc[7] = __builtin_fmaf(a, hi(w.w), acc[7]);
+  }
+  // fp32 -> binary16, round to nearest even (the hardware conversion)
+  __device__ static inline uint32_t from_f32(float f) {
+    return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
+  }
+};
+
+struct TBF16 {
+  static constexpr int V = 8;
+  static constexpr int dtype = NP_BF16;
+  __device__ static inline float dot(uint4 w, uint4 x, float acc) {
+    acc = __builtin_amdgcn_fdot2_f32_bf16(as_b2(w.x), as_b2(x.x), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(as_b2(w.y), as_b2(x.y), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(as_b2(w.z), as_b2(x.z), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(as_b2(w.w), as_b2(x.w), acc, false);
+    return acc;
+  }
+  // bf16 -> fp32 is exact: the bf16 bits are the top half of the fp32 bits
+  __device__ static inline float lo(uint32_t u) { return __uint_as_float(u << 16); }
+  __device__ static inline float hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+  __device__ static inline void unpack(uint4 w, float* f) {
+    f[0] = lo(w.x);
+    f[1] = hi(w.x);
+    f[2] = lo(w.y);
+    f[3] = hi(w.y);
+    f[4] = lo(w.z);
+    f[5] = hi(w.z);
+    f[6] = lo(w.w);
+    f[7] = hi(w.w);
+  }
+  __device__ static inline void axpy(float* acc, float a, uint4 w) {
+    acc[0] = __builtin_fmaf(a, lo(w.x), acc[0]);
+    acc[1] = __builtin_fmaf(a, hi(w.x), acc[1]);
+    acc[2] = __builtin_fmaf(a, lo(w.y), acc[2]);
+    acc[3] = __builtin_fmaf(a, hi(w.y), acc[3]);
+    acc[4] = __builtin_fmaf(a, lo(w.z), acc[4]);
+    acc[5] = __builtin_fmaf(a, hi(w.z), acc[5]);
+    acc[6] = __builtin_fmaf(a, lo(w.w), acc[6]);
+    acc[7] = __builtin_fmaf(a, hi(w.w), acc[7]);
+  }
+  // fp32 -> bfloat16, round to nearest even; NaN stays a quiet NaN
+  __device__ static inline uint32_t from_f32(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (u >> 16) | 0x40u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// wave / workgroup reductions and scans
+// ---------------------------------------------------------------------------
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, WAVE);
+  return v;
+}
+
+// Sum over aligned groups of G lanes (G a power of two <= 64); every lane of
+// the group receives the group sum.  Fixed order: deterministic.
+template <int G>
+__device__ inline float group_sum(float v) {
+#pragma unroll
+  for (int off = G / 2; off >= 1; off >>= 1) v += __shfl_xor(v, off, WAVE);
+  return v;
+}
+
+__device__ inline uint32_t wave_incl_scan(uint32_t v) {
+  const int lane = threadIdx.x & (WAVE - 1);
+#pragma unroll
+  for (int off = 1; off < WAVE; off <<= 1) {
+    uint32_t y = __shfl_up(v, off, WAVE);
+    if (lane >= off) v += y;
+  }
+  return v;
+}
+
+// Exclusive prefix sum over the NT threads of a workgroup, in thread order.
+// lds must hold NT/64 + 1 uint32.  Returns the exclusive value; *total gets
+// the sum.  Contains barriers: every thread must call it.
+template <int NT>
+__device__ inline uint32_t block_excl_scan(uint32_t v, uint32_t* lds, uint32_t* total) {
+  constexpr int NW = NT / WAVE;
+  const int lane = threadIdx.x & (WAVE - 1), w = threadIdx.x / WAVE;
+  uint32_t incl = wave_incl_scan(v);
+  if (lane == WAVE - 1) lds[w] = incl;
+  __syncthreads();
+  if (w == 0) {
+    uint32_t t = lane < NW ? lds[lane] : 0u;
+    uint32_t ti = wave_incl_scan(t);
+    if (lane < NW) lds[lane] = ti - t;
+    if (lane == NW - 1) lds[NW] = ti;
+  }
+  __syncthreads();
+  uint32_t res = lds[w] + incl - v;
+  *total = lds[NW];
+  __syncthreads();
+  return res;
+}
+
+// ---------------------------------------------------------------------------
+// sticky device error word
+// ---------------------------------------------------------------------------
+__device__ inline void raise_error(void* ws, int bits) {
+  atomicOr((int*)((char*)ws + WS_ERR), bits);
+}
+
+// ---------------------------------------------------------------------------
+// k-selection over one workgroup (NT threads).  Each thread owns WPT
+// consecutive 32-id words (thread t: words t*WPT .. t*WPT+WPT-1), and key[w][b]
+// is the 32-bit unsigned key of id 32*(t*WPT+w)+b.  Selects the `kk` largest
+// keys; ties at the kk-th key go to the smaller ids.  On return sel[w] holds
+// the selected bits of each owned word.  Radix select from the top in three
+// passes (12 + 10 + 10 bits) on an LDS histogram, then an ordered scan of the
+// ties.  hist: 4096 uint32 of LDS; scan: NT/64 + 1 uint32; res: 2 uint32.
+// ---------------------------------------------------------------------------
+template <int NT, int WPT>
+__device__ inline void block_select_largest(const uint32_t (&key)[WPT][32], uint32_t kk,
+                                            uint32_t (&sel)[WPT], uint32_t* hist,
+                                            uint32_t* scan, uint32_t* res) {
+  const int tid = threadIdx.x;
+  uint32_t prefix = 0, pmask = 0, rem = kk;
+#pragma unroll
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+    const int nbits = pass == 0 ? 12 : 10;
+    const uint32_t nb = 1u << nbits;
+    for (uint32_t i = tid; i < nb; i += NT) hist[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < WPT; ++w) {
+#pragma unroll
+      for (int b = 0; b < 32; ++b) {
+        uint32_t kv = key[w][b];
+        if ((kv & pmask) == prefix) atomicAdd(&hist[(kv >> shift) & (nb - 1)], 1u);
+      }
+    }
+    __syncthreads();
+    // thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top
+    const uint32_t bpt = nb / NT;  // 4 or 1 (nb >= NT)
+    const uint32_t hi_bin = nb - (uint32_t)tid * bpt;  // exclusive
+    uint32_t local = 0;
+    for (uint32_t i = 0; i < bpt; ++i) local += hist[hi_bin - 1 - i];
+    uint32_t tot;
+    uint32_t above = block_excl_scan<NT>(local, scan, &tot);
+    if (above < rem && above + local >= rem) {
+      uint32_t c = above;
+      for (uint32_t i = 0; i < bpt; ++i) {
+        uint32_t bin = hi_bin - 1 - i;
+        if (c + hist[bin] >= rem) {
+          res[0] = bin;
+          res[1] = rem - c;
+          break;
+        }
+        c += hist[bin];
+      }
+    }
+    __syncthreads();
+    prefix |= res[0] << shift;
+    pmask |= (nb - 1) << shift;
+    rem = res[1];
+    __syncthreads();
+  }
+  // prefix is the kk-th largest key; take all larger keys and the first `rem`
+  // equal keys in id order.
+  uint32_t eqm[WPT], neq = 0;
+#pragma unroll
+  for (int w = 0; w < WPT; ++w) {
+    uint32_t gt = 0, eq = 0;
+#pragma unroll
+    for (int b = 0; b < 32; ++b) {
+      gt |= (key[w][b] > prefix ? 1u : 0u) << b;
+      eq |= (key[w][b] == prefix ? 1u : 0u) << b;
+    }
+    sel[w] = gt;
+    eqm[w] = eq;
+    neq += __builtin_popcount(eq);
+  }
+  uint32_t tot;
+  uint32_t before = block_excl_scan<NT>(neq, scan, &tot);
+#pragma unroll
+  for (int w = 0; w < WPT; ++w) {
+    uint32_t e = eqm[w];
+    while (e && before < rem) {
+      uint32_t low = e & (0u - e);
+      sel[w] |= low;
+      e ^= low;
+      ++before;
+    }
+  }
+}
+
+}  // namespace np

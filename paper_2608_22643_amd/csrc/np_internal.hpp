@@ -1,0 +1,67 @@
+// np_internal.hpp -- definitions shared by the HIP kernels and the host side
+// of libneuroprefetch (workspace layout, launch helpers, device utilities).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/neuroprefetch.h"
+
+namespace np {
+
+// ---------------------------------------------------------------------------
+// Device workspace layout (dev_ws).  Offsets are multiples of 256 bytes.
+//   [0, 4096)            control block
+//       +0    int32  sticky error word (NP_DEVERR_* bits)
+//       +256  uint32 sparse-MLP arrival counter
+//       +512  uint32 sparse-MLP reducer-done counter
+//   [4096, +L'*r*4)      predictor intermediate z, fp32 [L'][r]
+//   [.., +MLP_MAX_WG*d*4) sparse-MLP per-workgroup partial sums, fp32
+// ---------------------------------------------------------------------------
+constexpr size_t WS_ERR = 0;
+constexpr size_t WS_MLP_ARRIVE = 256;
+constexpr size_t WS_MLP_DONE = 512;
+constexpr size_t WS_CTRL_BYTES = 4096;
+constexpr int MLP_MAX_WG = 512;
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline size_t ws_z_offset() { return WS_CTRL_BYTES; }
+inline size_t ws_partials_offset(const np_shape& s) {
+  return align256(ws_z_offset() + (size_t)s.layers * s.rank * 4);
+}
+inline size_t ws_total(const np_shape& s) {
+  return align256(ws_partials_offset(s) + (size_t)MLP_MAX_WG * s.d_model * 4);
+}
+
+inline int dtype_size(int dt) { return dt == NP_F32 ? 4 : 2; }
+// elements per 16-byte vector
+inline int vec_elems(int dt) { return 16 / dtype_size(dt); }
+
+// ---------------------------------------------------------------------------
+// launchers (defined in the .hip files; return hipError_t of the launch)
+// ---------------------------------------------------------------------------
+hipError_t launch_fill_state(const np_shape& s, const np_state& st, void* ws, hipStream_t stream);
+hipError_t launch_predict(const np_shape& s, const void* h, const void* A, const void* B,
+                          float* scores, void* ws, hipStream_t stream);
+hipError_t launch_select(const np_shape& s, const float* scores, uint32_t* mask,
+                         int32_t* active_ids, void* ws, hipStream_t stream);
+hipError_t launch_delta(const np_shape& s, int32_t token, const int32_t* active_ids,
+                        const np_state& st, const np_delta_out& out, void* ws,
+                        hipStream_t stream);
+hipError_t launch_stage_gather(const np_shape& s, const np_delta_out& out, int layer_begin,
+                               int layer_end, const void* storage, void* resident, void* ws,
+                               hipStream_t stream);
+hipError_t launch_stage_scatter(const np_shape& s, const void* landing, int n_records,
+                                void* resident, hipStream_t stream);
+hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const void* resident,
+                             const int32_t* active_slots, int n_active, void* y, void* ws,
+                             hipStream_t stream);
+
+// host-side helpers shared by the ABI files (np_abi.cpp)
+np_status fail(np_status st, const char* fmt, ...);
+np_status hip_fail(hipError_t e, const char* what);
+bool aligned16(const void* p);
+np_status check_shape(const np_shape* s);
+
+}  // namespace np

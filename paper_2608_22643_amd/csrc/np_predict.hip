@@ -1,0 +1,142 @@
+// np_predict.hip -- low-rank activity predictor for all downstream layers
+// (the one predictor pass after layer 0, Sec. 3.1 step 2 / Sec. 3.3):
+//   z_l = A_l h        (r values per layer, fp32, kept in the workspace)
+//   scores_l = B_l z_l (F values per layer, fp32)
+// Both steps are batch-1 matrix-vector products: one weight element read per
+// multiply-add, so they are bound by HBM bandwidth.  Weight rows are streamed
+// with 16-byte loads that cover whole contiguous 1 KiB spans per wave
+// instruction; there is no data reuse for matrix cores to exploit.
+#include "np_device.hpp"
+
+namespace np {
+
+// Stage 1: one wave per row of the stacked [L'*r][d] matrix A.  Lane i reads
+// vectors i, i+64, ... of the row; UNROLL loads are issued before any math.
+template <class T, int UNROLL>
+__global__ __launch_bounds__(256) void predict_z_kernel(const uint4* __restrict__ A,
+                                                        const uint4* __restrict__ h,
+                                                        float* __restrict__ z, int rows,
+                                                        int nv) {
+  const int lane = threadIdx.x & (WAVE - 1);
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const uint4* a = A + (size_t)row * nv;
+  float acc = 0.f;
+  for (int base = lane; base < nv; base += WAVE * UNROLL) {
+    uint4 wv[UNROLL], xv[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      const int v = base + WAVE * u;
+      if (v < nv) {
+        wv[u] = load_nt(a + v);
+        xv[u] = h[v];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      if (base + WAVE * u < nv) acc = T::dot(wv[u], xv[u], acc);
+    }
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) z[row] = acc;
+}
+
+// Stage 2: scores[l][n] = B_l[n] . z_l.  A row of B is r elements (nvr
+// vectors).  Groups of 16 lanes own one row each (4 rows per wave
+// instruction, 256 contiguous bytes per group); each wave covers RG row
+// groups (4*RG rows); a workgroup of 4 waves covers 16*RG rows of one layer.
+// Lane g of a group reads vectors g, g+16, ... of its row (ZPL of them) and
+// keeps the matching z values in registers.
+template <class T, int ZPL, int RG>
+__global__ __launch_bounds__(256) void predict_scores_kernel(const uint4* __restrict__ B,
+                                                             const float* __restrict__ z,
+                                                             float* __restrict__ scores,
+                                                             int F, int r, int nvr) {
+  constexpr int V = T::V;
+  const int lane = threadIdx.x & (WAVE - 1);
+  const int wave = threadIdx.x >> 6;
+  const int g = lane & 15;
+  const int l = blockIdx.y;
+  const float* zl = z + (size_t)l * r;
+  float zr[ZPL][V];
+#pragma unroll
+  for (int i = 0; i < ZPL; ++i) {
+    const int v = g + 16 * i;
+#pragma unroll
+    for (int e = 0; e < V; ++e) zr[i][e] = (v < nvr) ? zl[v * V + e] : 0.f;
+  }
+  const int row0 = (blockIdx.x * 4 + wave) * (4 * RG) + (lane >> 4);
+  uint4 wv[RG][ZPL];
+#pragma unroll
+  for (int q = 0; q < RG; ++q) {
+    const int n = row0 + 4 * q;
+    const uint4* brow = B + ((size_t)l * F + n) * nvr;
+#pragma unroll
+    for (int i = 0; i < ZPL; ++i) {
+      const int v = g + 16 * i;
+      if (n < F && v < nvr) wv[q][i] = load_nt(brow + v);
+      else wv[q][i] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < RG; ++q) {
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < ZPL; ++i) {
+      float wf[V];
+      T::unpack(wv[q][i], wf);
+#pragma unroll
+      for (int e = 0; e < V; ++e) acc = __builtin_fmaf(wf[e], zr[i][e], acc);
+    }
+    acc = group_sum<16>(acc);
+    const int n = row0 + 4 * q;
+    if (g == 0 && n < F) scores[(size_t)l * F + n] = acc;
+  }
+}
+
+template <class T>
+static hipError_t predict_t(const np_shape& s, const void* h, const void* A, const void* B,
+                            float* scores, void* ws, hipStream_t stream) {
+  constexpr int V = T::V;
+  const int nv = s.d_model / V;
+  const int rows = s.layers * s.rank;
+  float* z = (float*)((char*)ws + ws_z_offset());
+  hipLaunchKernelGGL((predict_z_kernel<T, 8>), dim3((rows + 3) / 4), dim3(256), 0, stream,
+                     (const uint4*)A, (const uint4*)h, z, rows, nv);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int nvr = s.rank / V;
+  const int zpl = (nvr + 15) / 16;
+  constexpr int RG = 4;
+  dim3 grid((s.d_ffn + 16 * RG - 1) / (16 * RG), s.layers);
+#define NP_SCORES_CASE(Z)                                                                     \
+  case Z:                                                                                     \
+    hipLaunchKernelGGL((predict_scores_kernel<T, Z, RG>), grid, dim3(256), 0, stream,         \
+                       (const uint4*)B, (const float*)z, scores, s.d_ffn, s.rank, nvr);       \
+    break;
+  switch (zpl) {
+    NP_SCORES_CASE(1)
+    NP_SCORES_CASE(2)
+    NP_SCORES_CASE(3)
+    NP_SCORES_CASE(4)
+    NP_SCORES_CASE(5)
+    NP_SCORES_CASE(6)
+    NP_SCORES_CASE(7)
+    NP_SCORES_CASE(8)
+    default:
+      return hipErrorInvalidValue;  // rank beyond 128 vectors: rejected by validation
+  }
+#undef NP_SCORES_CASE
+  return hipGetLastError();
+}
+
+hipError_t launch_predict(const np_shape& s, const void* h, const void* A, const void* B,
+                          float* scores, void* ws, hipStream_t stream) {
+  switch (s.wdtype) {
+    case NP_F32: return predict_t<TF32>(s, h, A, B, scores, ws, stream);
+    case NP_F16: return predict_t<TF16>(s, h, A, B, scores, ws, stream);
+    default: return predict_t<TBF16>(s, h, A, B, scores, ws, stream);
+  }
+}
+
+}  // namespace np

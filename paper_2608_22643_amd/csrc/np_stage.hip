@@ -1,0 +1,97 @@
+// np_stage.hip -- moving incoming neuron records into their resident slots
+// (Sec. 3.5: a record holds the gate, up and down^T rows of one neuron, so a
+// single contiguous copy of 3d elements places all three; the scatter writes
+// each record into the slot the delta assigned).  Pure data movement: HBM or
+// host-link bound.  One workgroup copies one whole record per iteration with
+// 16-byte vectors, all loads of a record issued before its stores.
+#include "np_device.hpp"
+
+namespace np {
+
+constexpr int STAGE_NT = 256;
+constexpr int STAGE_UNROLL = 8;
+
+__device__ inline void copy_record(uint4* __restrict__ dst, const uint4* __restrict__ src,
+                                   int rec_vecs) {
+  for (int v0 = threadIdx.x; v0 < rec_vecs; v0 += STAGE_NT * STAGE_UNROLL) {
+    uint4 t[STAGE_UNROLL];
+#pragma unroll
+    for (int u = 0; u < STAGE_UNROLL; ++u) {
+      const int v = v0 + u * STAGE_NT;
+      if (v < rec_vecs) t[u] = load_nt(src + v);
+    }
+#pragma unroll
+    for (int u = 0; u < STAGE_UNROLL; ++u) {
+      const int v = v0 + u * STAGE_NT;
+      if (v < rec_vecs) dst[v] = t[u];
+    }
+  }
+}
+
+// Gather: the plan is np_delta's device output.  Records of layers
+// [lb, le) are numbered layer by layer; workgroup b copies records
+// b, b + gridDim.x, ...  Entries outside [0, F) x [0, C) raise
+// NP_DEVERR_NOT_RESIDENT and are skipped.
+__global__ __launch_bounds__(STAGE_NT) void stage_gather_kernel(
+    const int32_t* __restrict__ counts, const int32_t* __restrict__ in_ids,
+    const int32_t* __restrict__ in_slots, int k, int F, int C, int lb, int le,
+    const uint4* __restrict__ storage, uint4* __restrict__ resident, int rec_vecs, void* ws) {
+  const int G = gridDim.x, bid = blockIdx.x;
+  int base = 0;
+  for (int l = lb; l < le; ++l) {
+    int n = counts[(size_t)l * 4];
+    if (n < 0 || n > k) {  // not a count np_delta can produce
+      if (threadIdx.x == 0 && bid == 0) raise_error(ws, NP_DEVERR_STATE);
+      n = n < 0 ? 0 : k;
+    }
+    int j = ((bid - base) % G + G) % G;
+    for (; j < n; j += G) {
+      const int id = in_ids[(size_t)l * k + j];
+      const int slot = in_slots[(size_t)l * k + j];
+      if (id < 0 || id >= F || slot < 0 || slot >= C) {
+        if (threadIdx.x == 0) raise_error(ws, NP_DEVERR_NOT_RESIDENT);
+        continue;
+      }
+      copy_record(resident + ((size_t)l * C + slot) * rec_vecs,
+                  storage + ((size_t)l * F + id) * rec_vecs, rec_vecs);
+    }
+    base += n;
+  }
+}
+
+// Scatter: a landing chunk holds n records followed by n int32 destination
+// rows (row = layer * C + slot, checked on the host when the chunk is packed).
+__global__ __launch_bounds__(STAGE_NT) void stage_scatter_kernel(const uint4* __restrict__ landing,
+                                                                 int n, int rec_vecs,
+                                                                 uint4* __restrict__ resident) {
+  const int32_t* dst_rows = (const int32_t*)(landing + (size_t)n * rec_vecs);
+  for (int r = blockIdx.x; r < n; r += gridDim.x) {
+    const int row = dst_rows[r];
+    copy_record(resident + (size_t)row * rec_vecs, landing + (size_t)r * rec_vecs, rec_vecs);
+  }
+}
+
+hipError_t launch_stage_gather(const np_shape& s, const np_delta_out& out, int lb, int le,
+                               const void* storage, void* resident, void* ws,
+                               hipStream_t stream) {
+  const int rec_vecs = 3 * s.d_model * dtype_size(s.wdtype) / 16;
+  int grid = 128 * (le - lb);
+  if (grid > 2048) grid = 2048;
+  if (grid < 64) grid = 64;
+  hipLaunchKernelGGL(stage_gather_kernel, dim3(grid), dim3(STAGE_NT), 0, stream, out.counts,
+                     out.in_ids, out.in_slots, s.k, s.d_ffn, s.capacity, lb, le,
+                     (const uint4*)storage, (uint4*)resident, rec_vecs, ws);
+  return hipGetLastError();
+}
+
+hipError_t launch_stage_scatter(const np_shape& s, const void* landing, int n_records,
+                                void* resident, hipStream_t stream) {
+  const int rec_vecs = 3 * s.d_model * dtype_size(s.wdtype) / 16;
+  int grid = n_records < 1024 ? n_records : 1024;
+  if (grid < 1) return hipSuccess;
+  hipLaunchKernelGGL(stage_scatter_kernel, dim3(grid), dim3(STAGE_NT), 0, stream,
+                     (const uint4*)landing, n_records, rec_vecs, (uint4*)resident);
+  return hipGetLastError();
+}
+
+}  // namespace np

@@ -1,0 +1,186 @@
+"""Per-token decode loop over the C ABI (the runtime around the kernels).
+
+DecodePipeline owns the device buffers of one configuration (torch
+allocations: PyTorch supplies memory and streams only) and runs one decode
+token per step():
+
+    np_predict -> np_select -> np_delta -> staging -> np_sparse_mlp x L'
+
+Staging modes:
+  "gather"  np_stage_gather straight from np_delta's device lists; the storage
+            tier is device memory ("device" tier) or mapped pinned host memory
+            ("host" tier, read over the host link by the kernel).  No host
+            synchronisation anywhere in the step.
+  "memcpy"  np_stage_rows: the incoming lists are copied to pinned host
+            memory, the host packs coalesced records into pinned staging and
+            each chunk goes over with hipMemcpyAsync on a side stream, then a
+            scatter kernel places the records.  Needs the "host" tier.
+
+With overlap=True staging runs on a side stream and layer l's MLP waits only
+for layer l's rows (a per-layer event), so staging later layers overlaps the
+MLP of earlier ones.  The side stream waits for np_delta of the same token,
+which itself follows the previous token's MLP on the main stream, so a victim
+slot is never overwritten while the previous token still reads it.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import binding as B
+from . import workload as W
+
+TORCH_DT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+
+
+def _i32(n, device):
+    return torch.empty(n, dtype=torch.int32, device=device)
+
+
+class DecodePipeline:
+    def __init__(self, cfg: W.Config, device: str = "cuda:0", tier: str = "device",
+                 staging: str = "gather", overlap: bool = False, tokens: int | None = None,
+                 staging_mib: int = 64, landing_mib: int = 32,
+                 host_storage: torch.Tensor | None = None):
+        if staging == "memcpy" and tier != "host":
+            raise ValueError("memcpy staging reads a pinned host storage tier")
+        self.cfg, self.device, self.tier, self.staging, self.overlap = cfg, device, tier, staging, overlap
+        torch.cuda.set_device(device)
+        L, d, F, r, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.rank, cfg.k, cfg.capacity
+        self.shape = B.make_shape(L, d, F, r, k, C, cfg.wdtype, cfg.adtype)
+        B.np_shape_check(self.shape)
+        self.T = cfg.tokens if tokens is None else tokens
+        dev = torch.device(device)
+        # inputs resident in HBM: predictor factors and hidden states
+        A, Bm = W.predictor(cfg)
+        self.A = torch.from_numpy(A.view(np.uint8)).to(dev)
+        self.B = torch.from_numpy(Bm.view(np.uint8)).to(dev)
+        h = W.hidden(cfg, self.T)
+        self.h = torch.from_numpy(h.view(np.uint8).reshape(self.T, -1)).to(dev)
+        self.row_bytes = d * W.ITEMSIZE[cfg.adtype]
+        # storage tier (host_storage: an already generated pinned copy to reuse)
+        if host_storage is not None:
+            assert host_storage.numel() == cfg.storage_bytes and host_storage.is_pinned()
+        if tier == "host":
+            if host_storage is not None:
+                self.storage = host_storage
+            else:
+                self.storage = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
+                W.fill_storage(cfg, self.storage.data_ptr())
+        else:
+            self.storage = torch.empty(cfg.storage_bytes, dtype=torch.uint8, device=dev)
+            if host_storage is not None:
+                self.storage.copy_(host_storage)
+            else:
+                layer_bytes = F * cfg.record_bytes
+                buf = torch.empty(layer_bytes, dtype=torch.uint8, pin_memory=True)
+                for l in range(L):
+                    W.fill_storage(cfg, buf.data_ptr(), l, 1)
+                    self.storage[l * layer_bytes:(l + 1) * layer_bytes].copy_(buf)
+                torch.cuda.synchronize()
+                del buf
+            torch.cuda.synchronize()
+        self.resident = torch.empty(cfg.resident_bytes, dtype=torch.uint8, device=dev)
+        # residency state and step outputs
+        self.slot_of, self.neuron_of, self.last_used = _i32(L * F, dev), _i32(L * C, dev), _i32(L * F, dev)
+        self.state = B.np_state(self.slot_of.data_ptr(), self.neuron_of.data_ptr(),
+                                self.last_used.data_ptr())
+        self.lists = {n: _i32(L * k, dev) for n in
+                      ("in_ids", "in_slots", "ev_ids", "ev_slots", "hit_ids", "active_slots")}
+        self.counts = _i32(L * 4, dev)
+        self.out = B.np_delta_out(*[self.lists[n].data_ptr() for n in
+                                    ("in_ids", "in_slots", "ev_ids", "ev_slots", "hit_ids",
+                                     "active_slots")], self.counts.data_ptr())
+        self.scores = torch.empty(L * F, dtype=torch.float32, device=dev)
+        self.words = (F + 31) // 32
+        self.mask = _i32(L * self.words, dev)
+        self.active_ids = _i32(L * k, dev)
+        self.y = torch.empty(L * d, dtype=TORCH_DT[cfg.adtype], device=dev)
+        self.ws = torch.zeros(B.np_workspace_size(self.shape), dtype=torch.uint8, device=dev)
+        self.main = torch.cuda.Stream(device=dev)
+        self.side = torch.cuda.Stream(device=dev) if overlap else self.main
+        self.ev_delta = torch.cuda.Event()
+        self.layer_ready = [torch.cuda.Event() for _ in range(L)] if overlap else None
+        if staging == "memcpy":
+            self.plan_counts = torch.empty(L * 4, dtype=torch.int32, pin_memory=True)
+            self.plan_ids = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
+            self.plan_slots = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
+            self.plan = B.np_stage_plan(self.plan_counts.data_ptr(), self.plan_ids.data_ptr(),
+                                        self.plan_slots.data_ptr())
+            self.staging_buf = torch.empty(staging_mib << 20, dtype=torch.uint8, pin_memory=True)
+            self.landing = torch.empty(landing_mib << 20, dtype=torch.uint8, device=dev)
+            self.ev_plan = torch.cuda.Event()
+            # events handed to the library must exist: record them once
+            for e in (self.layer_ready or []):
+                e.record(self.side)
+            self.ev_delta.record(self.main)
+            torch.cuda.synchronize()
+        self.reset()
+
+    # ------------------------------------------------------------------
+    def reset(self) -> None:
+        """Cold start: every slot map entry -1 (the next token loads its
+        whole active set)."""
+        B.np_state_reset(self.shape, self.state, self.ws, self.main)
+        self.main.synchronize()
+
+    def x_ptr(self, t: int) -> int:
+        return self.h.data_ptr() + t * self.row_bytes
+
+    def step(self, t: int, mlp_events=None) -> None:
+        """Enqueue one decode token (index t of the hidden-state sequence).
+        mlp_events: optional list of (start, end) torch events per layer,
+        recorded around each np_sparse_mlp on the main stream."""
+        s, cfg = self.shape, self.cfg
+        L, k = cfg.layers, cfg.k
+        main = self.main
+        B.np_predict(s, self.x_ptr(t), self.A, self.B, self.scores, self.ws, main)
+        B.np_select(s, self.scores, self.mask, self.active_ids, self.ws, main)
+        B.np_delta(s, t, self.active_ids, self.state, self.out, self.ws, main)
+        if self.staging == "gather":
+            if self.overlap:
+                self.ev_delta.record(main)
+                self.side.wait_event(self.ev_delta)
+                for l in range(L):
+                    B.np_stage_gather(s, self.out, l, l + 1, self.storage, self.resident,
+                                      self.ws, self.side)
+                    self.layer_ready[l].record(self.side)
+            else:
+                B.np_stage_gather(s, self.out, 0, L, self.storage, self.resident, self.ws, main)
+        else:
+            with torch.cuda.stream(main):
+                self.plan_counts.copy_(self.counts, non_blocking=True)
+                self.plan_ids.copy_(self.lists["in_ids"], non_blocking=True)
+                self.plan_slots.copy_(self.lists["in_slots"], non_blocking=True)
+            self.ev_plan.record(main)
+            self.ev_plan.synchronize()  # the host reads the plan
+            B.np_stage_rows(s, self.plan, 0, L, self.storage, self.resident, self.staging_buf,
+                            self.staging_buf.numel(), self.landing, self.landing.numel(),
+                            self.side, self.ev_plan if self.overlap else None,
+                            self.layer_ready)
+        slots = self.lists["active_slots"]
+        ybytes = cfg.d_model * W.ITEMSIZE[cfg.adtype]
+        for l in range(L):
+            if self.overlap:
+                main.wait_event(self.layer_ready[l])
+            if mlp_events is not None:
+                mlp_events[l][0].record(main)
+            B.np_sparse_mlp(s, l, self.x_ptr(t), self.resident, slots.data_ptr() + l * k * 4, k,
+                            self.y.data_ptr() + l * ybytes, self.ws, main)
+            if mlp_events is not None:
+                mlp_events[l][1].record(main)
+
+    def device_error(self) -> int:
+        return B.np_device_error(self.ws, self.main)
+
+    # host copies for checks -------------------------------------------
+    def host_state(self):
+        L, F, C = self.cfg.layers, self.cfg.d_ffn, self.cfg.capacity
+        return (self.slot_of.cpu().numpy().reshape(L, F), self.neuron_of.cpu().numpy().reshape(L, C),
+                self.last_used.cpu().numpy().reshape(L, F))
+
+    def host_lists(self):
+        L, k = self.cfg.layers, self.cfg.k
+        d = {n: v.cpu().numpy().reshape(L, k) for n, v in self.lists.items()}
+        d["counts"] = self.counts.cpu().numpy().reshape(L, 4)
+        return d

@@ -10,11 +10,13 @@
  * Flood, "Fast splittable pseudorandom number generators", OOPSLA 2014)
  * started from a state derived from (seed, tensor, layer).  Any element can
  * therefore be generated independently, in any order and on any thread.
- * Normal variates use the Box-Muller transform on two consecutive draws.
+ * Normal variates use the Box-Muller transform on two consecutive draws
+ * (in single precision).
  *
  * Floating-point encodings (fp16 = IEEE binary16, bf16 = the top half of
  * binary32) round to nearest, ties to even, from a double.
  */
+#define _GNU_SOURCE /* sincos */
 #include <math.h>
 #include <pthread.h>
 #include <stdint.h>
@@ -47,10 +49,24 @@ static inline double unit_open(uint64_t x) {
   return ((double)(x >> 11) + 0.5) * (1.0 / 9007199254740992.0);
 }
 
+/* Box-Muller: elements 2m and 2m+1 of a stream are the cosine and sine
+ * outputs of the uniform pair (draw 2m, draw 2m+1). */
+static inline void normal_pair(uint64_t stream, uint64_t m, double* z0, double* z1) {
+  /* single-precision transcendental functions: the variates are stored in
+   * 16-bit or 32-bit formats, far coarser than float's rounding error */
+  const float u1 = (float)unit_open(npg_draw(stream, 2 * m));
+  const float u2 = (float)unit_open(npg_draw(stream, 2 * m + 1));
+  const float r = sqrtf(-2.0f * logf(u1));
+  float sn, cs;
+  sincosf(6.28318530717958647692f * u2, &sn, &cs);
+  *z0 = (double)(r * cs);
+  *z1 = (double)(r * sn);
+}
+
 double npg_normal(uint64_t stream, uint64_t i) {
-  double u1 = unit_open(npg_draw(stream, 2 * i));
-  double u2 = unit_open(npg_draw(stream, 2 * i + 1));
-  return sqrt(-2.0 * log(u1)) * cos(6.283185307179586476925 * u2);
+  double z0, z1;
+  normal_pair(stream, i >> 1, &z0, &z1);
+  return (i & 1) ? z1 : z0;
 }
 
 /* Integer uniform on {-m, ..., m}. */
@@ -94,30 +110,35 @@ uint16_t npg_bf16(double v) {
   return bf16_from_f32(f);
 }
 
-/* double -> IEEE binary16, round to nearest even, overflow to infinity. */
+/* double -> IEEE binary16, round to nearest even, overflow to infinity.
+ * Works on the bits of the double: 52-bit fraction, 11-bit exponent. */
 uint16_t npg_f16(double v) {
-  uint16_t sign = signbit(v) ? 0x8000u : 0;
-  double a = fabs(v);
-  if (isnan(v)) return 0x7E00u;
-  if (a >= 65520.0) return sign | 0x7C00u; /* at or above max + half ulp */
-  if (a < ldexp(1.0, -14)) {
-    /* subnormal range: units of 2^-24 */
-    double q = a * 16777216.0; /* a / 2^-24, exact */
-    double fl = floor(q);
-    double rem = q - fl;
-    uint32_t m = (uint32_t)fl;
-    if (rem > 0.5 || (rem == 0.5 && (m & 1u))) m += 1;
-    return sign | (uint16_t)m; /* m == 1024 becomes the smallest normal */
+  uint64_t b;
+  memcpy(&b, &v, 8);
+  const uint16_t sign = (uint16_t)((b >> 48) & 0x8000u);
+  const int ex = (int)((b >> 52) & 0x7FF);
+  const uint64_t frac = b & ((1ULL << 52) - 1);
+  if (ex == 0x7FF) return frac ? 0x7E00u : (uint16_t)(sign | 0x7C00u);
+  const int e = ex - 1023; /* unbiased exponent of a normal double */
+  if (ex == 0 || e < -25) return sign; /* below half the smallest subnormal */
+  if (e > 15) return sign | 0x7C00u;
+  const uint64_t sig = (1ULL << 52) | frac; /* 53-bit significand */
+  int shift, exp16;
+  if (e >= -14) { /* normal binary16: keep 11 significant bits */
+    shift = 42;
+    exp16 = e + 15;
+  } else { /* subnormal binary16: units of 2^-24 */
+    shift = 28 - e;
+    exp16 = 0;
   }
-  int e;
-  double fr = frexp(a, &e); /* a = fr * 2^e, fr in [0.5, 1) */
-  int exp16 = e - 1 + 15;   /* biased exponent of a = 1.xxx * 2^(e-1) */
-  double q = ldexp(fr, 11); /* 1.xxx * 2^10: 11 significant bits */
-  double fl = floor(q);
-  double rem = q - fl;
-  uint32_t m = (uint32_t)fl;
-  if (rem > 0.5 || (rem == 0.5 && (m & 1u))) m += 1;
-  if (m == 2048) { m = 1024; exp16 += 1; }
+  uint64_t m = sig >> shift;
+  const uint64_t rem = sig & ((1ULL << shift) - 1), half = 1ULL << (shift - 1);
+  if (rem > half || (rem == half && (m & 1u))) ++m;
+  if (exp16 == 0) return sign | (uint16_t)m; /* m == 1024 is the smallest normal */
+  if (m == 2048) {
+    m = 1024;
+    ++exp16;
+  }
   if (exp16 >= 31) return sign | 0x7C00u;
   return sign | (uint16_t)((exp16 << 10) | (m - 1024));
 }
@@ -147,6 +168,30 @@ typedef struct {
   int64_t row_begin, row_end; /* rows over the flattened [layers][rows] */
 } fill_job;
 
+/* One row of `len` elements, stream indices idx0 .. idx0+len-1, written at
+ * out[base ..].  Gaussian values are produced a Box-Muller pair at a time;
+ * the result equals element-wise npg_normal. */
+static void fill_row(const fill_job* j, uint64_t st, uint64_t idx0, int64_t len, size_t base) {
+  int64_t c = 0;
+  if (j->dyadic) {
+    for (; c < len; ++c)
+      put(j->dtype, j->out, base + (size_t)c,
+          (double)npg_int(st, idx0 + (uint64_t)c, j->mrange) * j->scale);
+    return;
+  }
+  if (idx0 & 1) { /* odd start: first element is the sine half of a pair */
+    put(j->dtype, j->out, base, npg_normal(st, idx0) * j->scale);
+    c = 1;
+  }
+  for (; c + 1 < len; c += 2) {
+    double z0, z1;
+    normal_pair(st, (idx0 + (uint64_t)c) >> 1, &z0, &z1);
+    put(j->dtype, j->out, base + (size_t)c, z0 * j->scale);
+    put(j->dtype, j->out, base + (size_t)c + 1, z1 * j->scale);
+  }
+  if (c < len) put(j->dtype, j->out, base + (size_t)c, npg_normal(st, idx0 + (uint64_t)c) * j->scale);
+}
+
 /* Records: element c of the gate, up or down^T row of neuron n in layer l is
  * drawn from stream (seed, tensor 1/2/3, l) at index n*d + c. */
 static void* fill_worker(void* p) {
@@ -159,22 +204,12 @@ static void* fill_worker(void* p) {
       for (int part = 0; part < 3; ++part) {
         uint64_t st = npg_stream(j->seed, (uint32_t)(1 + part), (uint32_t)l);
         size_t base = (size_t)rr * 3 * d + (size_t)part * d;
-        for (int64_t c = 0; c < d; ++c) {
-          uint64_t idx = (uint64_t)(n * d + c);
-          double v = j->dyadic ? (double)npg_int(st, idx, j->mrange) * j->scale
-                               : npg_normal(st, idx) * j->scale;
-          put(j->dtype, j->out, base + (size_t)c, v);
-        }
+        fill_row(j, st, (uint64_t)(n * d), d, base);
       }
     } else {
       uint64_t st = npg_stream(j->seed, j->tensor, (uint32_t)l);
       size_t base = (size_t)rr * j->cols;
-      for (int64_t c = 0; c < j->cols; ++c) {
-        uint64_t idx = (uint64_t)(n * j->cols + c);
-        double v = j->dyadic ? (double)npg_int(st, idx, j->mrange) * j->scale
-                             : npg_normal(st, idx) * j->scale;
-        put(j->dtype, j->out, base + (size_t)c, v);
-      }
+      fill_row(j, st, (uint64_t)(n * j->cols), j->cols, base);
     }
   }
   return NULL;

@@ -32,3 +32,20 @@ def wl():
 
     W.build()
     return W
+
+
+def pytest_collection_modifyitems(config, items):
+    if not any("gpu" in it.keywords for it in items):
+        return
+    try:
+        import torch
+
+        has_gpu = torch.cuda.is_available()
+    except Exception:
+        has_gpu = False
+    if has_gpu:
+        return
+    skip = pytest.mark.skip(reason="needs a GPU")
+    for it in items:
+        if "gpu" in it.keywords:
+            it.add_marker(skip)

@@ -1,0 +1,121 @@
+"""The C ABI on the CPU: the HIP library loads, exports every symbol the
+header declares, and its host-side validation answers before anything
+touches a GPU (no compute calls here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_22643_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "neuroprefetch.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(np_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.fail("libneuroprefetch.so is not built (run __graft_entry__.build())")
+    return B.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) == 12, names
+    for n in names:
+        assert hasattr(lib, n), f"missing export {n}"
+    assert set(names) == set(B.EXPORTS)
+
+
+def test_status_strings(lib):
+    assert B.status_name(B.NP_OK) == "NP_OK"
+    assert B.status_name(B.NP_ERR_CAPACITY) == "NP_ERR_CAPACITY"
+    assert B.status_name(99) == "NP_ERR_UNKNOWN"
+
+
+GOOD = dict(layers=31, d_model=4096, d_ffn=11008, rank=416, k=1651, capacity=5504, wdtype="f16")
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(), B.NP_OK),
+    (dict(k=5505), B.NP_ERR_CAPACITY),              # k > C
+    (dict(k=0), B.NP_ERR_INVALID_ARG),
+    (dict(capacity=11009), B.NP_ERR_INVALID_ARG),   # C > F
+    (dict(d_model=4100), B.NP_ERR_INVALID_ARG),     # not a multiple of 8
+    (dict(rank=420), B.NP_ERR_INVALID_ARG),
+    (dict(rank=2048), B.NP_ERR_INVALID_ARG),
+    (dict(d_ffn=70000, capacity=11008), B.NP_ERR_INVALID_ARG),
+    (dict(layers=0), B.NP_ERR_INVALID_ARG),
+    (dict(wdtype=7), B.NP_ERR_INVALID_ARG),
+    (dict(k=9000, capacity=9000), B.NP_ERR_INVALID_ARG),
+])
+def test_shape_validation(lib, change, status):
+    args = dict(GOOD, **change)
+    shape = B.make_shape(**args)
+    st = lib.np_shape_check(ctypes.byref(shape))
+    assert st == status, (st, B.lib().np_last_error())
+
+
+def test_mixed_dtypes_rejected(lib):
+    shape = B.make_shape(**dict(GOOD, wdtype="f16"), adtype="bf16")
+    assert lib.np_shape_check(ctypes.byref(shape)) == B.NP_ERR_INVALID_ARG
+
+
+def test_workspace_size(lib):
+    shape = B.make_shape(**GOOD)
+    n = B.np_workspace_size(shape)
+    # control block + z (31*416 fp32) + 512 partial rows of d fp32
+    assert n >= 4096 + 31 * 416 * 4 + 512 * 4096 * 4
+    assert n % 256 == 0
+
+
+def test_null_and_misaligned_pointers_rejected(lib):
+    shape = B.make_shape(**GOOD)
+    with pytest.raises(B.NPError) as e:
+        B.np_predict(shape, None, 16, 16, 16, 16, None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    with pytest.raises(B.NPError) as e:
+        B.np_select(shape, 18, 16, 16, 16, None)  # misaligned scores
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    with pytest.raises(B.NPError) as e:
+        B.np_sparse_mlp(shape, 31, 16, 16, 16, 1, 16, 16, None)  # layer out of range
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    with pytest.raises(B.NPError) as e:
+        B.np_sparse_mlp(shape, 0, 16, 16, 16, 5505, 16, 16, None)  # n_active > C
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    with pytest.raises(B.NPError) as e:
+        B.np_delta(shape, -1, 16, B.np_state(16, 16, 16), B.np_delta_out(*([16] * 7)), 16, None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    with pytest.raises(B.NPError) as e:
+        B.np_stage_gather(shape, B.np_delta_out(*([16] * 7)), 3, 2, 16, 16, 16, None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    assert "layer range" in B.lib().np_last_error().decode()
+
+
+def test_stage_rows_validates_plan_before_enqueueing(lib):
+    import numpy as np
+
+    shape = B.make_shape(layers=2, d_model=64, d_ffn=100, rank=8, k=4, capacity=8, wdtype="f32")
+    counts = np.zeros(8, np.int32)
+    ids = np.zeros(8, np.int32)
+    slots = np.zeros(8, np.int32)
+    counts[0] = 1
+    ids[0] = 100  # out of range: rejected on the host
+    plan = B.np_stage_plan(counts.ctypes.data, ids.ctypes.data, slots.ctypes.data)
+    buf = np.zeros(1 << 16, np.uint8)
+    with pytest.raises(B.NPError) as e:
+        B.np_stage_rows(shape, plan, 0, 2, buf.ctypes.data, 16, buf.ctypes.data, buf.nbytes, 16,
+                        1 << 16, None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    ids[0] = 3
+    with pytest.raises(B.NPError) as e:  # staging holds no record of 3*64*4+4 bytes per half
+        B.np_stage_rows(shape, plan, 0, 2, buf.ctypes.data, 16, buf.ctypes.data, 1024, 16,
+                        1 << 16, None)
+    assert e.value.status == B.NP_ERR_CAPACITY

@@ -1,0 +1,328 @@
+"""Parity of each HIP step with the CPU oracle, called through the C ABI.
+
+Bars: masks, delta lists, slot maps and resident bytes bit-exact; scores
+within the fp32 accumulation bound of the predictor; MLP outputs within the
+tolerance of the activation type (fp16 2e-2 absolute, fp32 1e-5 relative,
+bf16 max(2e-2, 1 ulp)).  Selection and delta are compared in lockstep: the
+oracle's select runs on the GPU's scores, so both take the same integer
+decisions from the same fp32 values.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_2608_22643_amd import binding as B
+from paper_2608_22643_amd import workload as W
+from gpu_util import DEV, Bufs, compare_delta, decode_y, from_dev, mlp_tolerance, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def cfg_small(name, L, d, F, r, k, C, dt, **kw):
+    return W.Config(name, L, d, F, r, k / F, C / F, dt, dt, 4, rho_given=0.9, k_override=k,
+                    c_override=C, **kw)
+
+
+SHAPES = {
+    "tiny": W.get("tiny"),
+    "ragged_f16": cfg_small("ragged_f16", 2, 264, 1000, 24, 100, 300, "f16"),
+    "ragged_bf16": cfg_small("ragged_bf16", 3, 520, 777, 40, 50, 60, "bf16"),
+    "wide_f16": cfg_small("wide_f16", 2, 5120, 2000, 64, 300, 700, "f16"),
+    "wide_bf16": cfg_small("wide_bf16", 2, 8192, 1500, 96, 200, 450, "bf16"),
+    "k_eq_c": cfg_small("k_eq_c", 2, 128, 640, 16, 64, 64, "f32"),
+    "k_eq_f": cfg_small("k_eq_f", 2, 64, 96, 8, 96, 96, "f32"),
+    "k_one": cfg_small("k_one", 2, 64, 333, 8, 1, 5, "f32"),
+}
+
+
+def score_bound(cfg, A, Bm, h):
+    """fp32 accumulation bound of s = B (A h): (d + r + 2) u sum |B||A||h|."""
+    Ad, Bd = orc.decode(cfg.wdtype, A), orc.decode(cfg.wdtype, Bm)
+    hd = np.abs(orc.decode(cfg.adtype, h))
+    mag = np.einsum("lfr,lr->lf", np.abs(Bd), np.einsum("lrd,d->lr", np.abs(Ad), hd))
+    return (cfg.d_model + cfg.rank + 2) * 2.0 ** -24 * mag
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_predict(name):
+    cfg = SHAPES[name]
+    say(f"[predict] {name} L'={cfg.layers} d={cfg.d_model} F={cfg.d_ffn} r={cfg.rank}")
+    bufs = Bufs(cfg)
+    A, Bm = W.predictor(cfg)
+    h = W.hidden(cfg, 2)
+    dA, dB = to_dev(A), to_dev(Bm)
+    for t in range(2):
+        dh = to_dev(h[t])
+        B.np_predict(bufs.shape, dh, dA, dB, bufs.scores, bufs.ws)
+        torch.cuda.synchronize()
+        got = from_dev(bufs.scores, np.float32, (cfg.layers, cfg.d_ffn)).astype(np.float64)
+        ref = orc.predict(cfg, h[t], A, Bm).astype(np.float64)
+        tol = score_bound(cfg, A, Bm, h[t]) + np.abs(ref) * 2.0 ** -23
+        assert np.all(np.abs(got - ref) <= tol), np.max(np.abs(got - ref) / tol)
+
+
+def run_select(bufs, scores_np):
+    bufs.scores.copy_(torch.from_numpy(scores_np.reshape(-1)))
+    B.np_select(bufs.shape, bufs.scores, bufs.mask, bufs.ids, bufs.ws)
+    torch.cuda.synchronize()
+    L = bufs.cfg.layers
+    return (from_dev(bufs.mask, np.uint32, (L, bufs.words)),
+            from_dev(bufs.ids, np.int32, (L, bufs.cfg.k)))
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_select_lockstep(name):
+    cfg = SHAPES[name]
+    say(f"[select] {name} F={cfg.d_ffn} k={cfg.k}")
+    bufs = Bufs(cfg)
+    rng = np.random.default_rng(11)
+    L, F = cfg.layers, cfg.d_ffn
+    cases = [rng.normal(size=(L, F)).astype(np.float32),
+             # heavy ties, signed zeros, infinities
+             rng.choice(np.array([-np.inf, -1.0, -0.0, 0.0, 0.5, 1.0, np.inf], np.float32),
+                        size=(L, F)),
+             np.zeros((L, F), np.float32),
+             rng.integers(-3, 4, size=(L, F)).astype(np.float32)]
+    for sc in cases:
+        mask, ids = run_select(bufs, sc)
+        rmask, rids = orc.select(sc, cfg.k)
+        assert np.array_equal(ids, rids)
+        assert np.array_equal(mask, rmask)
+    assert B.np_device_error(bufs.ws) == 0
+
+
+def test_select_nan_sets_error_bit():
+    cfg = SHAPES["k_one"]
+    bufs = Bufs(cfg)
+    bufs.reset()
+    sc = np.ones((cfg.layers, cfg.d_ffn), np.float32)
+    sc[1, 7] = np.nan
+    run_select(bufs, sc)
+    assert B.np_device_error(bufs.ws) & B.NP_DEVERR_NAN_SCORE
+
+
+def active_sequence(rng, F, k, T, stay):
+    cur = rng.choice(F, k, replace=False)
+    seq = [np.sort(cur)]
+    for _ in range(T - 1):
+        keep = cur[rng.random(k) < stay]
+        rest = np.setdiff1d(np.arange(F), keep)
+        cur = np.concatenate([keep, rng.choice(rest, k - keep.size, replace=False)])
+        seq.append(np.sort(cur))
+    return seq
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+@pytest.mark.parametrize("stay", [0.0, 0.5, 0.9])
+def test_delta_sequence(name, stay):
+    cfg = SHAPES[name]
+    say(f"[delta] {name} k={cfg.k} C={cfg.capacity} stay={stay}")
+    bufs = Bufs(cfg)
+    bufs.reset()
+    rng = np.random.default_rng(int(stay * 10) + cfg.k)
+    L, k = cfg.layers, cfg.k
+    seqs = [active_sequence(rng, cfg.d_ffn, k, 12, stay) for _ in range(L)]
+    st = orc.State(L, cfg.d_ffn, cfg.capacity)
+    for t in range(12):
+        A = np.stack([seqs[l][t] for l in range(L)]).astype(np.int32)
+        bufs.ids.copy_(torch.from_numpy(A.reshape(-1)))
+        B.np_delta(bufs.shape, t, bufs.ids, bufs.state, bufs.out, bufs.ws)
+        torch.cuda.synchronize()
+        ref = orc.delta(t, A, st, cfg.capacity)
+        compare_delta(bufs.host_lists(), ref, L)
+        P, Q, U = bufs.host_state()
+        assert np.array_equal(P, st.slot_of) and np.array_equal(Q, st.neuron_of)
+        assert np.array_equal(U, st.last_used)
+    assert B.np_device_error(bufs.ws) == 0
+
+
+def stage_and_check(cfg, mode, staging_records=None):
+    """Runs deltas on a random active sequence and stages each token with
+    `mode`; compares the whole resident buffer with the oracle's copy."""
+    bufs = Bufs(cfg)
+    bufs.reset()
+    L, k, C, F = cfg.layers, cfg.k, cfg.capacity, cfg.d_ffn
+    store = W.storage(cfg)
+    rec = cfg.record_bytes
+    if mode == "gather_device":
+        dstore = to_dev(store)
+    else:
+        dstore = torch.empty(store.nbytes, dtype=torch.uint8, pin_memory=True)
+        dstore.numpy()[:] = store.view(np.uint8).reshape(-1)
+    resident = torch.zeros(cfg.resident_bytes, dtype=torch.uint8, device=DEV)
+    ref_res = np.zeros(cfg.resident_bytes, np.uint8)
+    if mode == "memcpy":
+        cap = staging_records or 64
+        staging = torch.empty(2 * cap * (rec + 4) + 512, dtype=torch.uint8, pin_memory=True)
+        landing = torch.empty(cap * (rec + 4), dtype=torch.uint8, device=DEV)
+        pc = torch.empty(L * 4, dtype=torch.int32, pin_memory=True)
+        pi = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
+        ps = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
+        plan = B.np_stage_plan(pc.data_ptr(), pi.data_ptr(), ps.data_ptr())
+    rng = np.random.default_rng(5)
+    seqs = [active_sequence(rng, F, k, 6, 0.7) for _ in range(L)]
+    st = orc.State(L, F, C)
+    for t in range(6):
+        A = np.stack([seqs[l][t] for l in range(L)]).astype(np.int32)
+        bufs.ids.copy_(torch.from_numpy(A.reshape(-1)))
+        B.np_delta(bufs.shape, t, bufs.ids, bufs.state, bufs.out, bufs.ws)
+        if mode == "memcpy":
+            torch.cuda.synchronize()
+            pc.copy_(bufs.counts)
+            pi.copy_(bufs.lists["in_ids"])
+            ps.copy_(bufs.lists["in_slots"])
+            B.np_stage_rows(bufs.shape, plan, 0, L, dstore, resident, staging, staging.numel(),
+                            landing, landing.numel(), torch.cuda.current_stream())
+        else:
+            B.np_stage_gather(bufs.shape, bufs.out, 0, L, dstore, resident, bufs.ws)
+        torch.cuda.synchronize()
+        ref = orc.delta(t, A, st, C)
+        orc.stage(cfg, ref["counts"], ref["in_ids"], ref["in_slots"], store,
+                  ref_res.view(store.dtype).reshape(L, C, -1))
+        got = resident.cpu().numpy()
+        assert np.array_equal(got, ref_res), f"resident bytes differ at token {t}"
+    assert B.np_device_error(bufs.ws) == 0
+    return bufs, resident, store, st
+
+
+@pytest.mark.parametrize("name", ["tiny", "ragged_f16", "ragged_bf16", "k_eq_c"])
+@pytest.mark.parametrize("mode", ["gather_device", "gather_host", "memcpy"])
+def test_stage(name, mode):
+    cfg = SHAPES[name]
+    say(f"[stage] {name} {mode}")
+    stage_and_check(cfg, mode)
+
+
+@pytest.mark.parametrize("records", [1, 3, 1000])
+def test_stage_memcpy_chunk_invariance(records):
+    cfg = SHAPES["ragged_f16"]
+    say(f"[stage chunks] records per chunk {records}")
+    stage_and_check(cfg, "memcpy", staging_records=records)
+
+
+def test_stage_rows_rejects_small_staging():
+    cfg = SHAPES["tiny"]
+    bufs = Bufs(cfg)
+    pc = np.zeros(cfg.layers * 4, np.int32)
+    pi = np.zeros(cfg.layers * cfg.k, np.int32)
+    plan = B.np_stage_plan(pc.ctypes.data, pi.ctypes.data, pi.ctypes.data)
+    stg = torch.empty(1024, dtype=torch.uint8, pin_memory=True)
+    land = torch.empty(1024, dtype=torch.uint8, device=DEV)
+    res = torch.empty(cfg.resident_bytes, dtype=torch.uint8, device=DEV)
+    with pytest.raises(B.NPError) as e:
+        B.np_stage_rows(bufs.shape, plan, 0, cfg.layers, stg, res, stg, stg.numel(), land,
+                        land.numel(), torch.cuda.current_stream())
+    assert e.value.status == B.NP_ERR_CAPACITY
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_sparse_mlp(name):
+    cfg = SHAPES[name]
+    say(f"[mlp] {name} d={cfg.d_model} k={cfg.k}")
+    bufs, resident, store, st = stage_and_check(cfg, "gather_device")
+    L, k, d = cfg.layers, cfg.k, cfg.d_model
+    h = W.hidden(cfg, 1)[0]
+    x = to_dev(h)
+    esz = W.ITEMSIZE[cfg.adtype]
+    y = torch.zeros(L * d * esz, dtype=torch.uint8, device=DEV)
+    slots = bufs.lists["active_slots"]
+    for l in range(L):
+        B.np_sparse_mlp(bufs.shape, l, x, resident, slots.data_ptr() + 4 * l * k, k,
+                        y.data_ptr() + l * d * esz, bufs.ws)
+    torch.cuda.synchronize()
+    lists = bufs.host_lists()
+    ybits = y.cpu().numpy()
+    for l in range(L):
+        active = np.sort(np.concatenate([lists["hit_ids"][l][:lists["counts"][l][1]],
+                                         lists["in_ids"][l][:lists["counts"][l][0]]]))
+        _, ref64 = orc.sparse_mlp(cfg, l, h, store, active.astype(np.int32), want_f64=True)
+        got = decode_y(orc, cfg.adtype, ybits[l * d * esz:(l + 1) * d * esz])
+        tol = mlp_tolerance(cfg.adtype, ref64)
+        assert np.all(np.abs(got - ref64) <= tol), (l, np.max(np.abs(got - ref64)))
+    assert B.np_device_error(bufs.ws) == 0
+
+
+def test_sparse_mlp_empty_and_bad_slot():
+    cfg = SHAPES["ragged_f16"]
+    bufs = Bufs(cfg)
+    bufs.reset()
+    resident = torch.zeros(cfg.resident_bytes, dtype=torch.uint8, device=DEV)
+    x = to_dev(W.hidden(cfg, 1)[0])
+    y = torch.full((cfg.d_model,), 7.0, dtype=torch.float16, device=DEV)
+    B.np_sparse_mlp(bufs.shape, 0, x, resident, None, 0, y, bufs.ws)
+    torch.cuda.synchronize()
+    assert torch.all(y == 0)
+    assert B.np_device_error(bufs.ws) == 0
+    bad = torch.tensor([0, cfg.capacity + 5, -1, 2], dtype=torch.int32, device=DEV)
+    B.np_sparse_mlp(bufs.shape, 1, x, resident, bad, 4, y, bufs.ws)
+    assert B.np_device_error(bufs.ws) & B.NP_DEVERR_NOT_RESIDENT
+
+
+def test_dyadic_end_to_end_bit_exact():
+    """Dyadic inputs: every sum is exact, so the whole token -- scores, masks,
+    delta, resident bytes and MLP output bits -- must match the oracle run
+    on its own (no lockstep)."""
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get("dyadic_tiny")
+    say(f"[dyadic] {cfg.name}")
+    T = 6
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T)
+    h = W.hidden(cfg, T)
+    A, Bm = W.predictor(cfg)
+    store = W.storage(cfg)
+    st = orc.State(cfg.layers, cfg.d_ffn, cfg.capacity)
+    L, d, F = cfg.layers, cfg.d_model, cfg.d_ffn
+    for t in range(T):
+        pipe.step(t)
+        torch.cuda.synchronize()
+        s_ref = orc.predict(cfg, h[t], A, Bm)
+        assert np.array_equal(pipe.scores.cpu().numpy().reshape(L, F), s_ref)
+        mask, ids = orc.select(s_ref, cfg.k)
+        assert np.array_equal(pipe.active_ids.cpu().numpy().reshape(L, -1), ids)
+        ref = orc.delta(t, ids, st, cfg.capacity)
+        compare_delta(pipe.host_lists(), ref, L)
+        y = pipe.y.cpu().numpy().reshape(L, d)
+        for l in range(L):
+            yb = orc.sparse_mlp(cfg, l, h[t], store, ids[l])
+            assert np.array_equal(y[l].view(np.uint32), yb.view(np.uint32)), (t, l)
+    assert pipe.device_error() == 0
+
+
+@pytest.mark.parametrize("tier,staging,overlap", [("device", "gather", False),
+                                                  ("device", "gather", True),
+                                                  ("host", "gather", True),
+                                                  ("host", "memcpy", True),
+                                                  ("host", "memcpy", False)])
+def test_lockstep_tiny(tier, staging, overlap):
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get("tiny")
+    say(f"[lockstep] tiny tier={tier} staging={staging} overlap={overlap}")
+    T = cfg.tokens
+    pipe = DecodePipeline(cfg, tier=tier, staging=staging, overlap=overlap, tokens=T)
+    h = W.hidden(cfg, T)
+    A, Bm = W.predictor(cfg)
+    store = W.storage(cfg)
+    st = orc.State(cfg.layers, cfg.d_ffn, cfg.capacity)
+    L, d, F = cfg.layers, cfg.d_model, cfg.d_ffn
+    res_ref = np.zeros((L, cfg.capacity, 3 * d), np.float32)
+    for t in range(T):
+        pipe.step(t)
+        torch.cuda.synchronize()
+        scores = pipe.scores.cpu().numpy().reshape(L, F)
+        mask, ids = orc.select(scores, cfg.k)
+        assert np.array_equal(pipe.active_ids.cpu().numpy().reshape(L, -1), ids)
+        assert np.array_equal(pipe.mask.cpu().numpy().view(np.uint32).reshape(L, -1), mask)
+        ref = orc.delta(t, ids, st, cfg.capacity)
+        compare_delta(pipe.host_lists(), ref, L)
+        orc.stage(cfg, ref["counts"], ref["in_ids"], ref["in_slots"], store, res_ref)
+        got_res = pipe.resident.cpu().numpy().view(np.float32).reshape(res_ref.shape)
+        occupied = st.neuron_of >= 0  # slots never written hold no defined bytes
+        assert np.array_equal(got_res[occupied], res_ref[occupied])
+        y = pipe.y.cpu().numpy().reshape(L, d).astype(np.float64)
+        for l in range(L):
+            _, ref64 = orc.sparse_mlp(cfg, l, h[t], store, ids[l], want_f64=True)
+            assert np.all(np.abs(y[l] - ref64) <= mlp_tolerance("f32", ref64))
+    assert pipe.device_error() == 0
