@@ -8,8 +8,9 @@ incoming rows are staged from); the step's own work is timed, nothing is
 skipped.  Prints one JSON line.
 
 Extra measurements in the same run:
-  * the sparse-MLP kernel's average launch time, from HIP events around each
-    launch on its stream, against the HBM roofline;
+  * the sparse-MLP call's average time, from HIP events bracketing each
+    token's block of back-to-back calls on their stream, against the HBM
+    roofline;
   * a per-step breakdown (predict / select / delta / stage / mlp);
   * the same step with the storage tier in pinned host memory (staging over
     the host link) -- reported under "host_tier", never as `value`;
@@ -41,23 +42,26 @@ def mlp_bytes_per_launch(cfg) -> int:
 
 
 def timed_steps(pipe, t0, steps, with_mlp_events=True):
+    """Times `steps` decode tokens.  With with_mlp_events, one pair of HIP
+    events on the main stream brackets each token's block of L' back-to-back
+    np_sparse_mlp calls; the mean per call over the timed region is returned
+    (gaps between the calls included)."""
     import torch
 
     L = pipe.cfg.layers
     evs = None
     if with_mlp_events:
-        evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-                for _ in range(L)] for _ in range(steps)]
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(steps):
-        pipe.step(t0 + i, mlp_events=evs[i] if evs else None)
+        pipe.step(t0 + i, mlp_block_events=evs[i] if evs else None)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     mlp_us = None
     if evs:
-        durs = [e[0].elapsed_time(e[1]) * 1e3 for st in evs for e in st]
-        mlp_us = sum(durs) / len(durs)
+        mlp_us = sum(a.elapsed_time(b) * 1e3 for a, b in evs) / (steps * L)
     return wall, mlp_us
 
 
@@ -145,6 +149,7 @@ def main():
     ap.add_argument("--host-tier-steps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--breakdown-steps", type=int, default=10)
+    ap.add_argument("--mlp-steps", type=int, default=20)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -159,7 +164,7 @@ def main():
 
     cfg = W.get(args.config)
     K, Wm = args.steps, args.warmup
-    T = 1 + Wm + K + args.breakdown_steps + args.host_tier_steps + 2
+    T = 1 + Wm + K + args.mlp_steps + args.breakdown_steps + args.host_tier_steps + 2
     log(f"[bench] config {cfg.name}: L'={cfg.layers} d={cfg.d_model} F={cfg.d_ffn} r={cfg.rank} "
         f"k={cfg.k} C={cfg.capacity} {cfg.wdtype}; tokens {T}")
     t = time.perf_counter()
@@ -180,8 +185,13 @@ def main():
         pipe.step(1 + i)
     torch.cuda.synchronize()
     log("[bench] warmup done")
-    wall, mlp_us = timed_steps(pipe, 1 + Wm, K)
-    log(f"[bench] timed {K} steps: {wall * 1e3 / K:.3f} ms/step, mlp launch {mlp_us:.2f} us")
+    wall, _ = timed_steps(pipe, 1 + Wm, K, with_mlp_events=False)
+    log(f"[bench] timed {K} steps: {wall * 1e3 / K:.3f} ms/step")
+    # sparse-MLP roofline: further steps, each token's block of calls
+    # bracketed by events (staging of the token finished before the block)
+    t1 = 1 + Wm + K
+    _, mlp_us = timed_steps(pipe, t1, args.mlp_steps)
+    log(f"[bench] np_sparse_mlp: {mlp_us:.2f} us per call")
     err = pipe.device_error()
     if err:
         log(f"[bench] device error word {err:#x}")
@@ -191,7 +201,7 @@ def main():
     achieved = bytes_launch / (mlp_us * 1e-6) / 1e9
     counts = delta_stats(pipe)
     # per-phase breakdown (no overlap) and persistence statistics
-    t1 = 1 + Wm + K
+    t1 += args.mlp_steps
     bd = breakdown(pipe, t1, args.breakdown_steps)
     log(f"[bench] breakdown us: {bd}")
     n_in = counts[:, 0].astype(np.float64)

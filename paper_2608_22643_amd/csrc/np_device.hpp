@@ -159,6 +159,52 @@ __device__ inline float group_sum(float v) {
   return v;
 }
 
+// Reduce-scatter of N values (N a power of two, 2 <= N <= 64) over a wave:
+// on entry every lane holds v[0..N-1]; on return lane l holds in v[0] the
+// wave sum of value l / (64/N) (every lane of that group of 64/N lanes holds
+// it).  Each halving step sends the half a lane gives up to its partner, so
+// the N sums cost N - 1 + log2(64/N) shuffles instead of N * 6.  Element
+// indices are template constants throughout, so every access is static and
+// each choice between two halves is one select.
+template <int I, int HALF, int M>
+struct RsStep {
+  template <int N>
+  __device__ static inline void run(float (&v)[N], bool hi) {
+    const float send = hi ? v[I] : v[I + HALF];
+    const float keep = hi ? v[I + HALF] : v[I];
+    v[I] = keep + __shfl_xor(send, M, WAVE);
+    RsStep<I + 1, HALF, M>::run(v, hi);
+  }
+};
+template <int HALF, int M>
+struct RsStep<HALF, HALF, M> {
+  template <int N>
+  __device__ static inline void run(float (&)[N], bool) {}
+};
+
+template <int CNT, int M>
+struct RsLevel {  // CNT values left, partner distance M
+  template <int N>
+  __device__ static inline void run(float (&v)[N], int lane) {
+    RsStep<0, CNT / 2, M>::run(v, (lane & M) != 0);
+    RsLevel<CNT / 2, M / 2>::run(v, lane);
+  }
+};
+template <int M>
+struct RsLevel<1, M> {  // one value left: sum it over the remaining lanes
+  template <int N>
+  __device__ static inline void run(float (&v)[N], int) {
+#pragma unroll
+    for (int m = M; m >= 1; m >>= 1) v[0] += __shfl_xor(v[0], m, WAVE);
+  }
+};
+
+template <int N>
+__device__ inline void wave_reduce_scatter(float (&v)[N]) {
+  static_assert(N >= 2 && N <= WAVE && (N & (N - 1)) == 0, "N: power of two in [2, 64]");
+  RsLevel<N, WAVE / 2>::run(v, (int)(threadIdx.x & (WAVE - 1)));
+}
+
 __device__ inline uint32_t wave_incl_scan(uint32_t v) {
   const int lane = threadIdx.x & (WAVE - 1);
 #pragma unroll

@@ -6,7 +6,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/neuroprefetch.h"
+#include "neuroprefetch.h"
 
 namespace np {
 
@@ -14,16 +14,12 @@ namespace np {
 // Device workspace layout (dev_ws).  Offsets are multiples of 256 bytes.
 //   [0, 4096)            control block
 //       +0    int32  sticky error word (NP_DEVERR_* bits)
-//       +256  uint32 sparse-MLP arrival counter
-//       +512  uint32 sparse-MLP reducer-done counter
 //   [4096, +L'*r*4)      predictor intermediate z, fp32 [L'][r]
 //   [.., +MLP_MAX_WG*d*4) sparse-MLP per-workgroup partial sums, fp32
 // ---------------------------------------------------------------------------
 constexpr size_t WS_ERR = 0;
-constexpr size_t WS_MLP_ARRIVE = 256;
-constexpr size_t WS_MLP_DONE = 512;
 constexpr size_t WS_CTRL_BYTES = 4096;
-constexpr int MLP_MAX_WG = 512;
+constexpr int MLP_MAX_WG = 1024;  // partial rows the reduce kernel sums (4 per thread)
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline size_t ws_z_offset() { return WS_CTRL_BYTES; }

@@ -127,10 +127,10 @@ class DecodePipeline:
     def x_ptr(self, t: int) -> int:
         return self.h.data_ptr() + t * self.row_bytes
 
-    def step(self, t: int, mlp_events=None) -> None:
+    def step(self, t: int, mlp_block_events=None) -> None:
         """Enqueue one decode token (index t of the hidden-state sequence).
-        mlp_events: optional list of (start, end) torch events per layer,
-        recorded around each np_sparse_mlp on the main stream."""
+        mlp_block_events: optional (start, end) torch events recorded on the
+        main stream before the first and after the last np_sparse_mlp."""
         s, cfg = self.shape, self.cfg
         L, k = cfg.layers, cfg.k
         main = self.main
@@ -160,15 +160,17 @@ class DecodePipeline:
                             self.layer_ready)
         slots = self.lists["active_slots"]
         ybytes = cfg.d_model * W.ITEMSIZE[cfg.adtype]
+        if mlp_block_events is not None:
+            if self.overlap:  # time the MLP block, not the wait for staging
+                main.wait_event(self.layer_ready[L - 1])
+            mlp_block_events[0].record(main)
         for l in range(L):
             if self.overlap:
                 main.wait_event(self.layer_ready[l])
-            if mlp_events is not None:
-                mlp_events[l][0].record(main)
             B.np_sparse_mlp(s, l, self.x_ptr(t), self.resident, slots.data_ptr() + l * k * 4, k,
                             self.y.data_ptr() + l * ybytes, self.ws, main)
-            if mlp_events is not None:
-                mlp_events[l][1].record(main)
+        if mlp_block_events is not None:
+            mlp_block_events[1].record(main)
 
     def device_error(self) -> int:
         return B.np_device_error(self.ws, self.main)
