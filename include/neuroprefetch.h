@@ -39,7 +39,8 @@
  *  w  = wdtype (MLP records and predictor factors), a = adtype (h, x, y).
  *  Requirements: wdtype == adtype; 1 <= k <= C <= F <= 65535; k <= 8192;
  *  L' >= 1; d and r multiples of 8 for 16-bit types and of 4 for fp32;
- *  d <= 16384 (16-bit) or 8192 (fp32); r <= 1024 (16-bit) or 512 (fp32).
+ *  d <= 16384 (16-bit) or 8192 (fp32); r <= 1024 (16-bit) or 512 (fp32);
+ *  C * 3d * sizeof(w) < 2^31 (one layer's resident buffer below 2 GiB).
  *  k > C is NP_ERR_CAPACITY; any other violation NP_ERR_INVALID_ARG.
  *
  *  Neuron record (Sec. 3.5, neuron-centric layout): row n of gate, row n of up

@@ -51,6 +51,8 @@ np_status check_shape(const np_shape* s) {
     return fail(NP_ERR_INVALID_ARG, "k %d outside [1, min(d_ffn, 8192)]", s->k);
   if (s->capacity < 1 || s->capacity > s->d_ffn)
     return fail(NP_ERR_INVALID_ARG, "capacity %d outside [1, d_ffn]", s->capacity);
+  if ((size_t)s->capacity * 3 * s->d_model * dtype_size(s->wdtype) >= ((size_t)1 << 31))
+    return fail(NP_ERR_INVALID_ARG, "a layer's resident buffer must stay below 2 GiB");
   if (s->k > s->capacity)
     return fail(NP_ERR_CAPACITY, "k %d exceeds the resident capacity %d", s->k, s->capacity);
   return NP_OK;

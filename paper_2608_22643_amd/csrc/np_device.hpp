@@ -24,6 +24,22 @@ __device__ inline uint4 load_nt(const uint4* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Buffer loads: a 128-bit resource (base, size) held in scalar registers plus
+// a 32-bit per-lane byte offset, so no 64-bit address arithmetic per lane.
+// The hardware range-checks the per-lane offset: an offset at or past the
+// size returns zeros without a memory access (BUF_OOB below).
+constexpr uint32_t BUF_OOB = 0x7FFFFFFFu;
+constexpr int BUF_RSRC_WORD3 = 0x00020000;  // raw 32-bit buffer, gfx9 family
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)bytes, BUF_RSRC_WORD3);
+}
+
+__device__ inline uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // ---------------------------------------------------------------------------
 // element types.  A 16-byte vector (uint4) holds V elements.
 // dot(w, x, acc): acc + sum_e w[e] * x[e] in fp32 (packed dot instructions

@@ -34,6 +34,7 @@ struct MlpArgs {
   float* partials;         // [n_wg][d]
   void* ws;
   int n_active, C, NV, n_wg, P, PP, teams;  // PP: P rounded up to a power of two
+  uint32_t layer_bytes;  // resident bytes of the layer (< 2^31)
 };
 
 template <class T, int CPL, int R, int MAXT>
@@ -64,18 +65,21 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
     const int r0 = row_begin + team * R;
     if (lane < R && r0 + lane < row_end) my_slot = a.slots[r0 + lane];
   }
-  // Loads below are unconditional (out-of-range lanes and rows read a clamped,
-  // valid address and are masked in the arithmetic): with no branches around
-  // them the compiler can wait for each stage's loads alone.
+  // Loads below are unconditional, with no branches around them, so the
+  // compiler can wait for each stage's loads alone.  Record loads are buffer
+  // loads: lanes past the slice and rows without a valid slot use an
+  // out-of-range offset and read zeros without touching memory.
+  const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(a.res_layer, a.layer_bytes);
+  const uint32_t third = (uint32_t)a.NV * 16u;
   uint4 xr[CPL];
   bool vok[CPL];
-  int voff[CPL];  // clamped vector offset within a third of the record
+  uint32_t loff[CPL];  // this lane's byte offset within a third of a record
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
     const int v = v0 + lane + WAVE * c;
     vok[c] = v < a.NV;
-    voff[c] = vok[c] ? v : 0;
-    xr[c] = a.x[voff[c]];
+    loff[c] = vok[c] ? (uint32_t)v * 16u : BUF_OOB;
+    xr[c] = a.x[vok[c] ? v : 0];
   }
   float yacc[CPL][V];
 #pragma unroll
@@ -100,12 +104,13 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
     uint4 gw[R][CPL], uw[R][CPL], dw[R][CPL];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      const uint4* rec = a.res_layer + (size_t)(valid[r] ? slot[r] : 0) * 3 * a.NV;
+      const uint32_t roff = valid[r] ? (uint32_t)slot[r] * 3u * third : BUF_OOB;
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
-        gw[r][c] = load_nt(rec + voff[c]);
-        uw[r][c] = load_nt(rec + a.NV + voff[c]);
-        dw[r][c] = load_nt(rec + 2 * a.NV + voff[c]);
+        const uint32_t off = roff + loff[c];  // both < 2^31: no wrap
+        gw[r][c] = buf_load16(rsrc, off, 0);
+        uw[r][c] = buf_load16(rsrc, off, third);
+        dw[r][c] = buf_load16(rsrc, off, 2 * third);
       }
     }
     // next round's slots, in flight behind this round's records
@@ -121,9 +126,9 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
         const int r = st * RS + i;
         float g = 0.f, u = 0.f;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) {  // lanes past the slice add nothing
-          g = vok[c] ? T::dot(gw[r][c], xr[c], g) : g;
-          u = vok[c] ? T::dot(uw[r][c], xr[c], u) : u;
+        for (int c = 0; c < CPL; ++c) {  // lanes past the slice hold zeros
+          g = T::dot(gw[r][c], xr[c], g);
+          u = T::dot(uw[r][c], xr[c], u);
         }
         v[i] = g;
         v[RS + i] = u;
@@ -324,6 +329,7 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   a.C = s.capacity;
   const size_t rec_vecs = (size_t)3 * a.NV;
   a.res_layer = (const uint4*)resident + (size_t)layer * s.capacity * rec_vecs;
+  a.layer_bytes = (uint32_t)((size_t)s.capacity * rec_vecs * 16);
   a.slots = active_slots;
   a.x = (const uint4*)x;
   a.partials = (float*)((char*)ws + ws_partials_offset(s));
