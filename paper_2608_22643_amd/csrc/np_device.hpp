@@ -166,6 +166,12 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
+__device__ inline uint32_t wave_sum_u32(uint32_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, WAVE);
+  return v;
+}
+
 // Sum over aligned groups of G lanes (G a power of two <= 64); every lane of
 // the group receives the group sum.  Fixed order: deterministic.
 template <int G>
@@ -283,13 +289,22 @@ __device__ inline void block_select_largest(const uint32_t (&key)[WPT][32], uint
     const uint32_t nb = 1u << nbits;
     for (uint32_t i = tid; i < nb; i += NT) hist[i] = 0;
     __syncthreads();
+    // Zero keys (ids outside the range, non-candidates) can be the bulk of
+    // the keys and all land in bin 0: they are counted per wave and added
+    // with one atomic, not one same-address LDS atomic each.
+    uint32_t zc = 0;
 #pragma unroll
     for (int w = 0; w < WPT; ++w) {
 #pragma unroll
       for (int b = 0; b < 32; ++b) {
         uint32_t kv = key[w][b];
-        if ((kv & pmask) == prefix) atomicAdd(&hist[(kv >> shift) & (nb - 1)], 1u);
+        if (kv == 0u) ++zc;
+        else if ((kv & pmask) == prefix) atomicAdd(&hist[(kv >> shift) & (nb - 1)], 1u);
       }
+    }
+    if (prefix == 0u) {
+      zc = wave_sum_u32(zc);
+      if ((threadIdx.x & (WAVE - 1)) == 0 && zc) atomicAdd(&hist[0], zc);
     }
     __syncthreads();
     // thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top

@@ -42,55 +42,65 @@ __global__ __launch_bounds__(256) void predict_z_kernel(const uint4* __restrict_
 }
 
 // Stage 2: scores[l][n] = B_l[n] . z_l.  A row of B is r elements (nvr
-// vectors).  Groups of 16 lanes own one row each (4 rows per wave
-// instruction, 256 contiguous bytes per group); each wave covers RG row
-// groups (4*RG rows); a workgroup of 4 waves covers 16*RG rows of one layer.
-// Lane g of a group reads vectors g, g+16, ... of its row (ZPL of them) and
-// keeps the matching z values in registers.
-template <class T, int ZPL, int RG>
+// 16-byte vectors).  A workgroup of 4 waves takes a block of SC_ROWS rows of
+// one layer and stages z_l in LDS once.  Groups of 16 lanes own one row each
+// (4 rows per wave instruction, 256 contiguous bytes per group); lane g of a
+// group reads vectors g, g+16, ... (ZPL of them) and keeps the matching z
+// values in registers.  Each wave walks its rows UNR row groups at a time,
+// all loads of an iteration issued before any arithmetic.
+constexpr int SC_ROWS = 256;
+
+template <class T, int ZPL, int UNR>
 __global__ __launch_bounds__(256) void predict_scores_kernel(const uint4* __restrict__ B,
                                                              const float* __restrict__ z,
                                                              float* __restrict__ scores,
                                                              int F, int r, int nvr) {
   constexpr int V = T::V;
+  __shared__ float zs[16 * 8 * 8];  // r <= 128 vectors of 8 (or 4) elements
   const int lane = threadIdx.x & (WAVE - 1);
   const int wave = threadIdx.x >> 6;
-  const int g = lane & 15;
+  const int g = lane & 15, sub = lane >> 4;
   const int l = blockIdx.y;
   const float* zl = z + (size_t)l * r;
+  for (int i = threadIdx.x; i < r; i += 256) zs[i] = zl[i];
+  __syncthreads();
   float zr[ZPL][V];
 #pragma unroll
   for (int i = 0; i < ZPL; ++i) {
     const int v = g + 16 * i;
 #pragma unroll
-    for (int e = 0; e < V; ++e) zr[i][e] = (v < nvr) ? zl[v * V + e] : 0.f;
+    for (int e = 0; e < V; ++e) zr[i][e] = (v < nvr) ? zs[v * V + e] : 0.f;
   }
-  const int row0 = (blockIdx.x * 4 + wave) * (4 * RG) + (lane >> 4);
-  uint4 wv[RG][ZPL];
+  const uint4* Bl = B + (size_t)l * F * nvr;
+  float* sl = scores + (size_t)l * F;
+  const int row_end = min(F, (int)(blockIdx.x + 1) * SC_ROWS);
+  // wave w covers rows blockIdx.x*SC_ROWS + 16*w*UNR + ... in steps of 64*UNR
+  for (int rb = blockIdx.x * SC_ROWS + wave * 4 * UNR; rb < row_end; rb += 16 * UNR) {
+    uint4 wv[UNR][ZPL];
 #pragma unroll
-  for (int q = 0; q < RG; ++q) {
-    const int n = row0 + 4 * q;
-    const uint4* brow = B + ((size_t)l * F + n) * nvr;
+    for (int u = 0; u < UNR; ++u) {
+      const int n = rb + 4 * u + sub;
+      const uint4* brow = Bl + (size_t)(n < row_end ? n : 0) * nvr;
 #pragma unroll
-    for (int i = 0; i < ZPL; ++i) {
-      const int v = g + 16 * i;
-      if (n < F && v < nvr) wv[q][i] = load_nt(brow + v);
-      else wv[q][i] = make_uint4(0u, 0u, 0u, 0u);
+      for (int i = 0; i < ZPL; ++i) {
+        const int v = g + 16 * i;
+        wv[u][i] = (n < row_end && v < nvr) ? load_nt(brow + v) : make_uint4(0u, 0u, 0u, 0u);
+      }
     }
-  }
 #pragma unroll
-  for (int q = 0; q < RG; ++q) {
-    float acc = 0.f;
+    for (int u = 0; u < UNR; ++u) {
+      float acc = 0.f;
 #pragma unroll
-    for (int i = 0; i < ZPL; ++i) {
-      float wf[V];
-      T::unpack(wv[q][i], wf);
+      for (int i = 0; i < ZPL; ++i) {
+        float wf[V];
+        T::unpack(wv[u][i], wf);
 #pragma unroll
-      for (int e = 0; e < V; ++e) acc = __builtin_fmaf(wf[e], zr[i][e], acc);
+        for (int e = 0; e < V; ++e) acc = __builtin_fmaf(wf[e], zr[i][e], acc);
+      }
+      acc = group_sum<16>(acc);
+      const int n = rb + 4 * u + sub;
+      if (g == 0 && n < row_end) sl[n] = acc;
     }
-    acc = group_sum<16>(acc);
-    const int n = row0 + 4 * q;
-    if (g == 0 && n < F) scores[(size_t)l * F + n] = acc;
   }
 }
 
@@ -107,11 +117,11 @@ static hipError_t predict_t(const np_shape& s, const void* h, const void* A, con
   if (e != hipSuccess) return e;
   const int nvr = s.rank / V;
   const int zpl = (nvr + 15) / 16;
-  constexpr int RG = 4;
-  dim3 grid((s.d_ffn + 16 * RG - 1) / (16 * RG), s.layers);
+  constexpr int UNR = 4;
+  dim3 grid((s.d_ffn + SC_ROWS - 1) / SC_ROWS, s.layers);
 #define NP_SCORES_CASE(Z)                                                                     \
   case Z:                                                                                     \
-    hipLaunchKernelGGL((predict_scores_kernel<T, Z, RG>), grid, dim3(256), 0, stream,         \
+    hipLaunchKernelGGL((predict_scores_kernel<T, Z, UNR>), grid, dim3(256), 0, stream,        \
                        (const uint4*)B, (const float*)z, scores, s.d_ffn, s.rank, nvr);       \
     break;
   switch (zpl) {

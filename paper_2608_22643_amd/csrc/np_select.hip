@@ -8,8 +8,6 @@
 
 namespace np {
 
-constexpr int SEL_NT = 1024;
-
 // Order-preserving unsigned key of an fp32 score: larger score, larger key.
 // -0.0 maps to the key of +0.0.  NaN maps to 0 (below every other key) and
 // is reported through the error word.
@@ -23,36 +21,64 @@ __device__ inline uint32_t score_key(float f, bool* nan) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-template <int WPT>
-__global__ __launch_bounds__(SEL_NT) void select_kernel(const float* __restrict__ scores,
-                                                         uint32_t* __restrict__ mask,
-                                                         int32_t* __restrict__ active_ids,
-                                                         int F, int k, void* ws) {
+// One workgroup of NT threads per layer; thread t owns id words
+// [t*WPT, t*WPT+WPT).  V4: the layer's scores are 16-byte aligned (F a
+// multiple of 4) and are read as float4.
+template <int NT, int WPT, bool V4>
+__global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ scores,
+                                                    uint32_t* __restrict__ mask,
+                                                    int32_t* __restrict__ active_ids, int F,
+                                                    int k, void* ws) {
   __shared__ uint32_t hist[4096];
-  __shared__ uint32_t scan[SEL_NT / WAVE + 1];
+  __shared__ uint32_t scan[NT / WAVE + 1];
   __shared__ uint32_t res[2];
   const int l = blockIdx.x, tid = threadIdx.x;
   const int words = (F + 31) / 32;
   const float* s = scores + (size_t)l * F;
+  // Loads are unconditional (clamped index) so that all of them are in
+  // flight together; the range test only picks the key.
   uint32_t key[WPT][32];
   bool nan = false;
+  if (32 * WPT * tid < F) {
 #pragma unroll
-  for (int w = 0; w < WPT; ++w) {
-    const int word = tid * WPT + w;
+    for (int w = 0; w < WPT; ++w) {
+      const int word = tid * WPT + w;
+      float v[32];
+      if constexpr (V4) {
+        const float4* s4 = reinterpret_cast<const float4*>(s);
+        const int last = F / 4 - 1;
 #pragma unroll
-    for (int b = 0; b < 32; ++b) {
-      const int n = 32 * word + b;
-      key[w][b] = (n < F) ? score_key(s[n], &nan) : 0u;
+        for (int i = 0; i < 8; ++i) {
+          const float4 q = s4[min(8 * word + i, last)];
+          v[4 * i] = q.x;
+          v[4 * i + 1] = q.y;
+          v[4 * i + 2] = q.z;
+          v[4 * i + 3] = q.w;
+        }
+      } else {
+#pragma unroll
+        for (int b = 0; b < 32; ++b) v[b] = s[min(32 * word + b, F - 1)];
+      }
+#pragma unroll
+      for (int b = 0; b < 32; ++b) {
+        const uint32_t kv = score_key(v[b], &nan);
+        key[w][b] = (32 * word + b < F) ? kv : 0u;
+      }
     }
+  } else {
+#pragma unroll
+    for (int w = 0; w < WPT; ++w)
+#pragma unroll
+      for (int b = 0; b < 32; ++b) key[w][b] = 0u;
   }
   if (nan) raise_error(ws, NP_DEVERR_NAN_SCORE);
   uint32_t sel[WPT];
-  block_select_largest<SEL_NT, WPT>(key, (uint32_t)k, sel, hist, scan, res);
+  block_select_largest<NT, WPT>(key, (uint32_t)k, sel, hist, scan, res);
   uint32_t cnt = 0;
 #pragma unroll
   for (int w = 0; w < WPT; ++w) cnt += __builtin_popcount(sel[w]);
   uint32_t tot;
-  uint32_t pos = block_excl_scan<SEL_NT>(cnt, scan, &tot);
+  uint32_t pos = block_excl_scan<NT>(cnt, scan, &tot);
   int32_t* ids = active_ids + (size_t)l * k;
 #pragma unroll
   for (int w = 0; w < WPT; ++w) {
@@ -71,8 +97,10 @@ __global__ __launch_bounds__(SEL_NT) void select_kernel(const float* __restrict_
 // One workgroup per layer.  Thread t owns: actives j in [t*JPT, t*JPT+JPT),
 // id words [t*WPT, t*WPT+WPT) and slot words [t*spt, t*spt+spt), so every
 // list below comes out in ascending order from a prefix sum in thread order.
-template <int WPT, int JPT>
-__global__ __launch_bounds__(SEL_NT) void delta_kernel(int32_t token,
+// Every global gather of a phase is issued unconditionally (clamped index)
+// so that the phase costs one memory round trip, not one per element.
+template <int NT, int WPT, int JPT>
+__global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
                                                         const int32_t* __restrict__ active_ids,
                                                         int32_t* __restrict__ slot_of,
                                                         int32_t* __restrict__ neuron_of,
@@ -81,8 +109,10 @@ __global__ __launch_bounds__(SEL_NT) void delta_kernel(int32_t token,
                                                         int spt, void* ws) {
   __shared__ uint32_t amask[2048];  // active set, bit n of the layer
   __shared__ uint32_t smask[2048];  // slot pool: free slots, then victims' slots
+  __shared__ uint32_t rmask[2048];  // resident rows (neurons held by some slot)
   __shared__ uint32_t hist[4096];
-  __shared__ uint32_t scan[SEL_NT / WAVE + 1];
+  __shared__ int32_t pool[8192];    // the first nI pool slots, ascending
+  __shared__ uint32_t scan[NT / WAVE + 1];
   __shared__ uint32_t res[2];
   const int l = blockIdx.x, tid = threadIdx.x;
   const int idwords = (F + 31) / 32, slotwords = (C + 31) / 32;
@@ -92,100 +122,139 @@ __global__ __launch_bounds__(SEL_NT) void delta_kernel(int32_t token,
   const int32_t* A = active_ids + (size_t)l * k;
   const size_t lo = (size_t)l * k;
 
-  for (int i = tid; i < idwords; i += SEL_NT) amask[i] = 0;
+  for (int i = tid; i < idwords; i += NT) {
+    amask[i] = 0;
+    rmask[i] = 0;
+  }
   __syncthreads();
 
   // 1. hits and incoming rows, in active-list order
   int nj[JPT], pj[JPT];
-  uint32_t hits = 0, incs = 0;
+  uint32_t hits = 0, incs = 0, bad = 0;
+#pragma unroll
+  for (int q = 0; q < JPT; ++q) nj[q] = A[min(tid * JPT + q, k - 1)];
+#pragma unroll
+  for (int q = 0; q < JPT; ++q) {
+    const bool ok = nj[q] >= 0 && nj[q] < F;  // else not a neuron id: counted as a miss
+    if (tid * JPT + q < k) bad |= !ok;
+    if (!ok) nj[q] = -1;
+    pj[q] = P[nj[q] >= 0 ? nj[q] : 0];
+  }
+  int qb[JPT];  // a hit's slot must hold it
+#pragma unroll
+  for (int q = 0; q < JPT; ++q) qb[q] = Q[(pj[q] >= 0 && pj[q] < C) ? pj[q] : 0];
 #pragma unroll
   for (int q = 0; q < JPT; ++q) {
     const int j = tid * JPT + q;
-    nj[q] = -1;
-    pj[q] = -1;
+    if (nj[q] < 0 || pj[q] >= C) {
+      bad |= (j < k) & (pj[q] >= C) & (nj[q] >= 0);
+      pj[q] = -1;
+    }
+    if (pj[q] >= 0 && qb[q] != nj[q]) {
+      bad |= j < k;
+      pj[q] = -1;
+    }
     if (j < k) {
-      int n = A[j];
-      if (n < 0 || n >= F) {  // not a neuron id: reported, counted as a miss
-        raise_error(ws, NP_DEVERR_STATE);
-        n = -1;
-      }
-      nj[q] = n;
-      pj[q] = n >= 0 ? P[n] : -1;
-      if (pj[q] >= C) {
-        raise_error(ws, NP_DEVERR_STATE);
-        pj[q] = -1;
-      }
-      if (n >= 0) atomicOr(&amask[n >> 5], 1u << (n & 31));
+      if (nj[q] >= 0) atomicOr(&amask[nj[q] >> 5], 1u << (nj[q] & 31));
       if (pj[q] >= 0) ++hits;
       else ++incs;
     }
   }
   uint32_t tot;
-  const uint32_t before = block_excl_scan<SEL_NT>(hits | (incs << 16), scan, &tot);
+  const uint32_t before = block_excl_scan<NT>(hits | (incs << 16), scan, &tot);
   const uint32_t nH = tot & 0xFFFFu, nI = tot >> 16;
 
-  // 2. free slots (and a consistency check of the slot map)
+  // 2. free slots and resident rows, and a consistency check of the slot
+  //    map: a used slot's neuron must map back to it
   uint32_t nfree_local = 0;
   for (int q = 0; q < spt; ++q) {
     const int sw = tid * spt + q;
     if (sw >= slotwords) break;
+    int qn[32];
+#pragma unroll
+    for (int b = 0; b < 32; ++b) qn[b] = Q[min(32 * sw + b, C - 1)];
     uint32_t bits = 0;
-    for (int b = 0; b < 32; ++b) {
-      const int sl = 32 * sw + b;
-      if (sl >= C) break;
-      const int qn = Q[sl];
-      if (qn == -1) bits |= 1u << b;
-      else if (qn < 0 || qn >= F || P[qn] != sl) raise_error(ws, NP_DEVERR_STATE);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {  // halves: 16 back-gathers in flight
+      int back[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int qv = qn[16 * h + i];
+        back[i] = P[(qv >= 0 && qv < F) ? qv : 0];
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int b = 16 * h + i, sl = 32 * sw + b, qv = qn[b];
+        if (sl < C) {
+          if (qv == -1) {
+            bits |= 1u << b;
+          } else if (qv < 0 || qv >= F || back[i] != sl) {
+            bad = 1;
+          } else {
+            atomicOr(&rmask[qv >> 5], 1u << (qv & 31));
+          }
+        }
+      }
     }
     smask[sw] = bits;
     nfree_local += __builtin_popcount(bits);
   }
   uint32_t nfree;
-  (void)block_excl_scan<SEL_NT>(nfree_local, scan, &nfree);
+  (void)block_excl_scan<NT>(nfree_local, scan, &nfree);  // its barriers publish rmask
   const uint32_t m = nI > nfree ? nI - nfree : 0u;
 
   // 3. victims: the m resident, non-active rows with the smallest
-  //    (last_used, id) -- the largest keys ~last_used, ties to lower ids
+  //    (last_used, id) -- the largest keys ~last_used, ties to lower ids.
+  //    Each victim leaves the slot map here: its slot joins the pool.
   uint32_t vsel[WPT];
 #pragma unroll
   for (int w = 0; w < WPT; ++w) vsel[w] = 0;
   if (m > 0) {
     uint32_t key[WPT][32];
+    if (32 * WPT * tid < F) {
 #pragma unroll
-    for (int w = 0; w < WPT; ++w) {
-      const int word = tid * WPT + w;
+      for (int w = 0; w < WPT; ++w) {
+        const int word = tid * WPT + w;
 #pragma unroll
-      for (int b = 0; b < 32; ++b) {
-        const int n = 32 * word + b;
-        bool cand = false;
-        if (n < F) {
-          const int pn = P[n];
-          cand = pn >= 0 && pn < C && !((amask[word] >> b) & 1u);
-        }
-        key[w][b] = cand ? ~(uint32_t)U[n] : 0u;
+        for (int b = 0; b < 32; ++b) key[w][b] = (uint32_t)U[min(32 * word + b, F - 1)];
+        // resident, not active, and inside the layer (rmask has no bits past F)
+        const uint32_t cm = word < idwords ? (rmask[word] & ~amask[word]) : 0u;
+#pragma unroll
+        for (int b = 0; b < 32; ++b) key[w][b] = ((cm >> b) & 1u) ? ~key[w][b] : 0u;
       }
+    } else {
+#pragma unroll
+      for (int w = 0; w < WPT; ++w)
+#pragma unroll
+        for (int b = 0; b < 32; ++b) key[w][b] = 0u;
     }
-    block_select_largest<SEL_NT, WPT>(key, m, vsel, hist, scan, res);
+    block_select_largest<NT, WPT>(key, m, vsel, hist, scan, res);
     uint32_t cv = 0;
 #pragma unroll
     for (int w = 0; w < WPT; ++w) cv += __builtin_popcount(vsel[w]);
     uint32_t vt;
-    uint32_t vpos = block_excl_scan<SEL_NT>(cv, scan, &vt);
+    uint32_t vpos = block_excl_scan<NT>(cv, scan, &vt);
 #pragma unroll
     for (int w = 0; w < WPT; ++w) {
-      uint32_t bits = vsel[w];
-      while (bits) {
-        const int n = 32 * (tid * WPT + w) + __builtin_ctz(bits);
-        bits &= bits - 1;
-        const int old = P[n];
+      if (!vsel[w]) continue;
+      const int word = tid * WPT + w;
+      int pn[32];
+#pragma unroll
+      for (int b = 0; b < 32; ++b) pn[b] = P[min(32 * word + b, F - 1)];
+#pragma unroll
+      for (int b = 0; b < 32; ++b) {
+        if (!((vsel[w] >> b) & 1u)) continue;
+        const int n = 32 * word + b, old = pn[b];
         if (old < 0 || old >= C || vpos >= (uint32_t)k) {  // only with a corrupted state
-          raise_error(ws, NP_DEVERR_STATE);
+          bad = 1;
           continue;
         }
         out.ev_ids[lo + vpos] = n;
         out.ev_slots[lo + vpos] = old;
         ++vpos;
         atomicOr(&smask[old >> 5], 1u << (old & 31));
+        Q[old] = -1;
+        P[n] = -1;
       }
     }
   }
@@ -199,7 +268,7 @@ __global__ __launch_bounds__(SEL_NT) void delta_kernel(int32_t token,
     if (sw < slotwords) cs += __builtin_popcount(smask[sw]);
   }
   uint32_t st;
-  uint32_t spos = block_excl_scan<SEL_NT>(cs, scan, &st);
+  uint32_t spos = block_excl_scan<NT>(cs, scan, &st);
   const uint32_t spos_total = st < nI ? st : nI;  // slots actually handed out
   for (int q = 0; q < spt; ++q) {
     const int sw = tid * spt + q;
@@ -209,25 +278,13 @@ __global__ __launch_bounds__(SEL_NT) void delta_kernel(int32_t token,
       const int b = __builtin_ctz(bits);
       bits &= bits - 1;
       out.in_slots[lo + spos] = 32 * sw + b;
+      pool[spos] = 32 * sw + b;
       ++spos;
-    }
-  }
-
-  // 5. victims release their slots
-#pragma unroll
-  for (int w = 0; w < WPT; ++w) {
-    uint32_t bits = vsel[w];
-    while (bits) {
-      const int n = 32 * (tid * WPT + w) + __builtin_ctz(bits);
-      bits &= bits - 1;
-      const int old = P[n];
-      if (old >= 0 && old < C) Q[old] = -1;
-      P[n] = -1;
     }
   }
   __syncthreads();
 
-  // 6. incoming rows take their slots; lists and last_used
+  // 5. incoming rows take their slots; lists and last_used
   uint32_t hb = before & 0xFFFFu, ib = before >> 16;
 #pragma unroll
   for (int q = 0; q < JPT; ++q) {
@@ -241,13 +298,13 @@ __global__ __launch_bounds__(SEL_NT) void delta_kernel(int32_t token,
         ++hb;
       } else {
         // the pool holds at least nI slots unless the state was corrupted
-        slot = ib < spos_total ? out.in_slots[lo + ib] : -1;
+        slot = ib < spos_total ? pool[ib] : -1;
         out.in_ids[lo + ib] = n;
         if (n >= 0 && slot >= 0 && slot < C) {
           P[n] = slot;
           Q[slot] = n;
         } else {
-          raise_error(ws, NP_DEVERR_STATE);
+          bad = 1;
           slot = -1;
         }
         ++ib;
@@ -256,6 +313,7 @@ __global__ __launch_bounds__(SEL_NT) void delta_kernel(int32_t token,
       out.active_slots[lo + j] = slot;
     }
   }
+  if (bad) raise_error(ws, NP_DEVERR_STATE);
   if (tid == 0) {
     out.counts[(size_t)l * 4 + 0] = (int32_t)nI;
     out.counts[(size_t)l * 4 + 1] = (int32_t)nH;
@@ -286,24 +344,33 @@ hipError_t launch_fill_state(const np_shape& s, const np_state& st, void* ws,
 hipError_t launch_select(const np_shape& s, const float* scores, uint32_t* mask,
                          int32_t* active_ids, void* ws, hipStream_t stream) {
   const int words = (s.d_ffn + 31) / 32;
-  if (words <= SEL_NT)
-    hipLaunchKernelGGL((select_kernel<1>), dim3(s.layers), dim3(SEL_NT), 0, stream, scores,
-                       mask, active_ids, s.d_ffn, s.k, ws);
-  else
-    hipLaunchKernelGGL((select_kernel<2>), dim3(s.layers), dim3(SEL_NT), 0, stream, scores,
-                       mask, active_ids, s.d_ffn, s.k, ws);
+  const bool v4 = s.d_ffn % 4 == 0;
+#define NP_SELECT_CASE(NT, W)                                                                \
+  do {                                                                                       \
+    if (v4)                                                                                  \
+      hipLaunchKernelGGL((select_kernel<NT, W, true>), dim3(s.layers), dim3(NT), 0, stream,  \
+                         scores, mask, active_ids, s.d_ffn, s.k, ws);                        \
+    else                                                                                     \
+      hipLaunchKernelGGL((select_kernel<NT, W, false>), dim3(s.layers), dim3(NT), 0, stream, \
+                         scores, mask, active_ids, s.d_ffn, s.k, ws);                        \
+  } while (0)
+  if (words <= 256) NP_SELECT_CASE(256, 1);
+  else if (words <= 512) NP_SELECT_CASE(512, 1);
+  else if (words <= 1024) NP_SELECT_CASE(1024, 1);
+  else NP_SELECT_CASE(1024, 2);
+#undef NP_SELECT_CASE
   return hipGetLastError();
 }
 
-template <int WPT>
+template <int NT, int WPT>
 static hipError_t delta_w(const np_shape& s, int32_t token, const int32_t* active_ids,
                           const np_state& st, const np_delta_out& out, void* ws,
                           hipStream_t stream) {
   const int slotwords = (s.capacity + 31) / 32;
-  const int spt = (slotwords + SEL_NT - 1) / SEL_NT;
-  const int jpt = (s.k + SEL_NT - 1) / SEL_NT;
+  const int spt = (slotwords + NT - 1) / NT;
+  const int jpt = (s.k + NT - 1) / NT;
 #define NP_DELTA_CASE(J)                                                                      \
-  hipLaunchKernelGGL((delta_kernel<WPT, J>), dim3(s.layers), dim3(SEL_NT), 0, stream, token,  \
+  hipLaunchKernelGGL((delta_kernel<NT, WPT, J>), dim3(s.layers), dim3(NT), 0, stream, token,  \
                      active_ids, st.slot_of, st.neuron_of, st.last_used, out, s.d_ffn,        \
                      s.capacity, s.k, spt, ws)
   if (jpt <= 1) NP_DELTA_CASE(1);
@@ -317,9 +384,11 @@ static hipError_t delta_w(const np_shape& s, int32_t token, const int32_t* activ
 hipError_t launch_delta(const np_shape& s, int32_t token, const int32_t* active_ids,
                         const np_state& st, const np_delta_out& out, void* ws,
                         hipStream_t stream) {
+  // 512 threads while every thread owns one id word and at most 4 actives
   const int words = (s.d_ffn + 31) / 32;
-  if (words <= SEL_NT) return delta_w<1>(s, token, active_ids, st, out, ws, stream);
-  return delta_w<2>(s, token, active_ids, st, out, ws, stream);
+  if (words <= 512 && s.k <= 2048) return delta_w<512, 1>(s, token, active_ids, st, out, ws, stream);
+  if (words <= 1024) return delta_w<1024, 1>(s, token, active_ids, st, out, ws, stream);
+  return delta_w<1024, 2>(s, token, active_ids, st, out, ws, stream);
 }
 
 }  // namespace np

@@ -33,6 +33,10 @@ SHAPES = {
     "k_eq_c": cfg_small("k_eq_c", 2, 128, 640, 16, 64, 64, "f32"),
     "k_eq_f": cfg_small("k_eq_f", 2, 64, 96, 8, 96, 96, "f32"),
     "k_one": cfg_small("k_one", 2, 64, 333, 8, 1, 5, "f32"),
+    # wide layers: the per-layer kernels size their workgroups by F
+    "f_11001": cfg_small("f_11001", 2, 64, 11001, 8, 1650, 5000, "f16"),
+    "f_20000": cfg_small("f_20000", 2, 64, 20000, 16, 2500, 6000, "bf16"),
+    "f_max": cfg_small("f_max", 1, 64, 65535, 8, 8192, 8192, "f32"),
 }
 
 
