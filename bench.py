@@ -5,9 +5,11 @@ np_delta, staging of the incoming rows and np_sparse_mlp for every downstream
 layer.  Inputs are synthetic and already resident in HBM when the timed
 region starts (predictor factors, hidden states, and the storage tier the
 incoming rows are staged from); the step's own work is timed, nothing is
-skipped.  Prints one JSON line.
+skipped.  Prints one JSON line.  By default the step is captured once as a
+HIP graph and replayed per token (--graph 0: one launch per call from Python).
 
 Extra measurements in the same run:
+  * the same steps with eager launches ("eager_tok_s");
   * the sparse-MLP call's average time, from HIP events bracketing each
     token's block of back-to-back calls on their stream, against the HBM
     roofline;
@@ -39,6 +41,18 @@ def mlp_bytes_per_launch(cfg) -> int:
     k int32 slots, x and y."""
     esz = 4 if cfg.wdtype == "f32" else 2
     return cfg.k * 3 * cfg.d_model * esz + cfg.k * 4 + 2 * cfg.d_model * esz
+
+
+def timed_graph_steps(pipe, t0, steps):
+    """Times `steps` decode tokens replayed from the captured step graph."""
+    import torch
+
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(steps):
+        pipe.step_graph(t0 + i)
+    torch.cuda.synchronize()
+    return time.perf_counter() - t_start
 
 
 def timed_steps(pipe, t0, steps, with_mlp_events=True):
@@ -150,6 +164,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--breakdown-steps", type=int, default=10)
     ap.add_argument("--mlp-steps", type=int, default=20)
+    ap.add_argument("--graph", type=int, default=1,
+                    help="time the step replayed from a captured HIP graph (else eager launches)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -164,7 +180,7 @@ def main():
 
     cfg = W.get(args.config)
     K, Wm = args.steps, args.warmup
-    T = 1 + Wm + K + args.mlp_steps + args.breakdown_steps + args.host_tier_steps + 2
+    T = 1 + Wm + 2 * K + args.mlp_steps + args.breakdown_steps + args.host_tier_steps + 2
     log(f"[bench] config {cfg.name}: L'={cfg.layers} d={cfg.d_model} F={cfg.d_ffn} r={cfg.rank} "
         f"k={cfg.k} C={cfg.capacity} {cfg.wdtype}; tokens {T}")
     t = time.perf_counter()
@@ -175,21 +191,35 @@ def main():
     pipe = DecodePipeline(cfg, tier="device", staging="gather", overlap=bool(args.overlap),
                           tokens=T, host_storage=host_storage)
     log("[bench] pipeline ready (storage tier in HBM)")
+    graph = bool(args.graph)
+    if graph:
+        pipe.capture_graph()
+        log("[bench] decode step captured as a HIP graph")
+    step = pipe.step_graph if graph else pipe.step
     # cold start, then warmup
     torch.cuda.synchronize()
     c0 = time.perf_counter()
-    pipe.step(0)
+    step(0)
     torch.cuda.synchronize()
     cold_ms = (time.perf_counter() - c0) * 1e3
     for i in range(Wm):
-        pipe.step(1 + i)
+        step(1 + i)
     torch.cuda.synchronize()
     log("[bench] warmup done")
-    wall, _ = timed_steps(pipe, 1 + Wm, K, with_mlp_events=False)
-    log(f"[bench] timed {K} steps: {wall * 1e3 / K:.3f} ms/step")
+    if graph:
+        wall = timed_graph_steps(pipe, 1 + Wm, K)
+    else:
+        wall, _ = timed_steps(pipe, 1 + Wm, K, with_mlp_events=False)
+    log(f"[bench] timed {K} steps ({'graph' if graph else 'eager'}): {wall * 1e3 / K:.3f} ms/step")
+    t1 = 1 + Wm + K
+    eager_ms = None
+    if graph:  # the same steps launched one call at a time, for comparison
+        ew, _ = timed_steps(pipe, t1, K, with_mlp_events=False)
+        eager_ms = ew * 1e3 / K
+        log(f"[bench] eager launches: {eager_ms:.3f} ms/step")
+        t1 += K
     # sparse-MLP roofline: further steps, each token's block of calls
     # bracketed by events (staging of the token finished before the block)
-    t1 = 1 + Wm + K
     _, mlp_us = timed_steps(pipe, t1, args.mlp_steps)
     log(f"[bench] np_sparse_mlp: {mlp_us:.2f} us per call")
     err = pipe.device_error()
@@ -255,11 +285,13 @@ def main():
                                f"({cfg.active_frac:.0%}), C={cfg.capacity} "
                                f"({cfg.resident_frac:.0%}), {cfg.wdtype}, batch 1",
                    "storage_tier": "HBM", "staging": "np_stage_gather",
-                   "overlap": bool(args.overlap)},
+                   "overlap": bool(args.overlap),
+                   "launch": "hip_graph" if graph else "eager"},
         "roofline": {"bound": "hbm", "kernel": "np_sparse_mlp",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
                      "bytes_per_launch": bytes_launch, "avg_launch_us": round(mlp_us, 3)},
+        "eager_tok_s": round(1e3 / eager_ms, 2) if eager_ms else None,
         "sparse_mlp_tok_s": round(1e6 / (mlp_us * cfg.layers), 1),
         "cold_start_ms": round(cold_ms, 2),
         "breakdown_us": bd,

@@ -161,6 +161,9 @@ np_status np_predict(const np_shape* shape, const void* h, const void* A,
 np_status np_select(const np_shape* shape, const float* scores, uint32_t* mask,
                     int32_t* active_ids, void* dev_ws, hipStream_t stream);
 
+/* token argument of np_delta: use the workspace's step counter (below). */
+#define NP_TOKEN_AUTO (-1)
+
 /* Delta against the resident set (Sec. 3.4, eqs. 2-3 and the slot-map
  * paragraph), for token index `token` >= 0:
  *   hits H = active neurons with slot_of >= 0; incoming I = the rest;
@@ -171,7 +174,13 @@ np_status np_select(const np_shape* shape, const float* scores, uint32_t* mask,
  *   every active neuron.  With C == k this is exactly D_in = A_t \ A_{t-1},
  *   D_out = A_{t-1} \ A_t.
  * active_ids [L'][k] ascending (np_select output), device.  `state` is read
- * and updated in place; `out` lists are written.  One workgroup per layer. */
+ * and updated in place; `out` lists are written.  One workgroup per layer.
+ * token == NP_TOKEN_AUTO: the index is read on the device from a step counter
+ * in dev_ws (np_state_reset sets it to 0), and a second kernel advances the
+ * counter by one after the delta.  With it a decode step has no per-token
+ * argument besides its input buffers, so a captured HIP graph of the step can
+ * be replayed as is; tokens 0, 1, 2, ... then match explicit indices.
+ * token < -1 is NP_ERR_INVALID_ARG. */
 np_status np_delta(const np_shape* shape, int32_t token,
                    const int32_t* active_ids, const np_state* state,
                    const np_delta_out* out, void* dev_ws, hipStream_t stream);
@@ -224,8 +233,17 @@ np_status np_stage_gather(const np_shape* shape, const np_delta_out* out,
  * where row j is slot active_slots[j] (j < n_active) of layer `layer` of
  * dev_resident.  x [d] and y [d] of type a, device; accumulation in fp32 and
  * one rounding of y to type a.  A slot outside [0, C) sets
- * NP_DEVERR_NOT_RESIDENT and is skipped.  One kernel on `stream`; call it once
- * per layer, in layer order.  n_active = 0 gives y = 0. */
+ * NP_DEVERR_NOT_RESIDENT and is skipped.  Two kernels on `stream` (rows into
+ * per-workgroup fp32 partials in dev_ws, then a column reduction in a fixed
+ * order: deterministic); call it once per layer, in layer order.
+ * n_active = 0 gives y = 0.
+ * With the environment variable NP_MLP_FUSED=1 the reduction runs inside the
+ * rows kernel after a grid-wide barrier (one kernel) when the whole grid fits
+ * on the device at once.  That path must not run concurrently with another
+ * np_sparse_mlp on the same device; its wait is bounded and sets
+ * NP_DEVERR_SPIN_LIMIT (y then undefined until np_state_reset) if the grid
+ * never meets.  dev_ws must have been zeroed or passed to np_state_reset
+ * before its first use. */
 np_status np_sparse_mlp(const np_shape* shape, int32_t layer, const void* x,
                         const void* dev_resident, const int32_t* active_slots,
                         int32_t n_active, void* y, void* dev_ws,

@@ -21,6 +21,7 @@ NP_DEVERR_NAN_SCORE = 0x1
 NP_DEVERR_NOT_RESIDENT = 0x2
 NP_DEVERR_STATE = 0x4
 NP_DEVERR_SPIN_LIMIT = 0x8
+NP_TOKEN_AUTO = -1  # np_delta: token index from the workspace step counter
 
 # every symbol the header declares
 EXPORTS = ("np_status_str", "np_last_error", "np_shape_check", "np_workspace_size",

@@ -127,7 +127,7 @@ np_status np_delta(const np_shape* s, int32_t token, const int32_t* ids, const n
                    const np_delta_out* out, void* ws, hipStream_t stream) {
   np_status st = check_shape(s);
   if (st != NP_OK) return st;
-  if (token < 0) return fail(NP_ERR_INVALID_ARG, "token %d < 0", token);
+  if (token < NP_TOKEN_AUTO) return fail(NP_ERR_INVALID_ARG, "token %d < 0", token);
   if (!aligned16(ids) || !state || !aligned16(state->slot_of) || !aligned16(state->neuron_of) ||
       !aligned16(state->last_used) || !aligned16(ws))
     return fail(NP_ERR_INVALID_ARG, "np_delta: pointers must be non-NULL and 16-byte aligned");

@@ -40,6 +40,27 @@ __device__ inline uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Cache policy "sc1" on gfx950: agent (device) scope.  A store with it is
+// written through to the point of coherence shared by all XCDs, and a load
+// with it reads that point, so data passes between workgroups on different
+// XCDs inside one kernel without an L2 write-back or invalidate.
+constexpr int CPOL_SC1 = 16;
+
+__device__ inline float4 buf_load16_agent(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, 0, CPOL_SC1);
+  return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                     __uint_as_float(v.w));
+}
+
+__device__ inline void buf_store16_agent(__amdgpu_buffer_rsrc_t r, uint32_t voff, float4 f) {
+  u32x4_t v;
+  v.x = __float_as_uint(f.x);
+  v.y = __float_as_uint(f.y);
+  v.z = __float_as_uint(f.z);
+  v.w = __float_as_uint(f.w);
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, 0, CPOL_SC1);
+}
+
 // ---------------------------------------------------------------------------
 // element types.  A 16-byte vector (uint4) holds V elements.
 // dot(w, x, acc): acc + sum_e w[e] * x[e] in fp32 (packed dot instructions
@@ -166,12 +187,6 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
-__device__ inline uint32_t wave_sum_u32(uint32_t v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, WAVE);
-  return v;
-}
-
 // Sum over aligned groups of G lanes (G a power of two <= 64); every lane of
 // the group receives the group sum.  Fixed order: deterministic.
 template <int G>
@@ -272,90 +287,135 @@ __device__ inline void raise_error(void* ws, int bits) {
 // consecutive 32-id words (thread t: words t*WPT .. t*WPT+WPT-1), and key[w][b]
 // is the 32-bit unsigned key of id 32*(t*WPT+w)+b.  Selects the `kk` largest
 // keys; ties at the kk-th key go to the smaller ids.  On return sel[w] holds
-// the selected bits of each owned word.  Radix select from the top in three
-// passes (12 + 10 + 10 bits) on an LDS histogram, then an ordered scan of the
-// ties.  hist: 4096 uint32 of LDS; scan: NT/64 + 1 uint32; res: 2 uint32.
+// the selected bits of each owned word.
+//
+// Key 0 marks ids that are outside the range or not candidates; such keys
+// are taken only when fewer than kk keys are nonzero (then in id order).
+// Radix select from the top over the nonzero keys on an LDS histogram of up
+// to 12 bits per pass, starting at the highest bit in which the nonzero keys
+// differ: fp32 score keys need three passes, least-recently-used keys (a
+// narrow range of token indices under a common prefix) usually one, and no
+// pass piles every key onto one histogram bin.  Then an ordered scan of the
+// ties.  hist: 4096 uint32 of LDS; scan: 3*NT/64 + 1 uint32; res: 2 uint32.
 // ---------------------------------------------------------------------------
 template <int NT, int WPT>
 __device__ inline void block_select_largest(const uint32_t (&key)[WPT][32], uint32_t kk,
                                             uint32_t (&sel)[WPT], uint32_t* hist,
                                             uint32_t* scan, uint32_t* res) {
-  const int tid = threadIdx.x;
-  uint32_t prefix = 0, pmask = 0, rem = kk;
+  constexpr int NW = NT / WAVE;
+  const int tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
+  // count, max and min of the nonzero keys
+  uint32_t nz = 0, kmax = 0, kmin = 0xFFFFFFFFu;
 #pragma unroll
-  for (int pass = 0; pass < 3; ++pass) {
-    const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
-    const int nbits = pass == 0 ? 12 : 10;
-    const uint32_t nb = 1u << nbits;
-    for (uint32_t i = tid; i < nb; i += NT) hist[i] = 0;
-    __syncthreads();
-    // Zero keys (ids outside the range, non-candidates) can be the bulk of
-    // the keys and all land in bin 0: they are counted per wave and added
-    // with one atomic, not one same-address LDS atomic each.
-    uint32_t zc = 0;
+  for (int i = 0; i < WPT; ++i)
 #pragma unroll
-    for (int w = 0; w < WPT; ++w) {
-#pragma unroll
-      for (int b = 0; b < 32; ++b) {
-        uint32_t kv = key[w][b];
-        if (kv == 0u) ++zc;
-        else if ((kv & pmask) == prefix) atomicAdd(&hist[(kv >> shift) & (nb - 1)], 1u);
-      }
+    for (int b = 0; b < 32; ++b) {
+      const uint32_t kv = key[i][b];
+      nz += kv != 0u;
+      kmax = kv > kmax ? kv : kmax;
+      kmin = (kv != 0u && kv < kmin) ? kv : kmin;
     }
-    if (prefix == 0u) {
-      zc = wave_sum_u32(zc);
-      if ((threadIdx.x & (WAVE - 1)) == 0 && zc) atomicAdd(&hist[0], zc);
-    }
-    __syncthreads();
-    // thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top
-    const uint32_t bpt = nb / NT;  // 4 or 1 (nb >= NT)
-    const uint32_t hi_bin = nb - (uint32_t)tid * bpt;  // exclusive
-    uint32_t local = 0;
-    for (uint32_t i = 0; i < bpt; ++i) local += hist[hi_bin - 1 - i];
-    uint32_t tot;
-    uint32_t above = block_excl_scan<NT>(local, scan, &tot);
-    if (above < rem && above + local >= rem) {
-      uint32_t c = above;
-      for (uint32_t i = 0; i < bpt; ++i) {
-        uint32_t bin = hi_bin - 1 - i;
-        if (c + hist[bin] >= rem) {
-          res[0] = bin;
-          res[1] = rem - c;
-          break;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    nz += __shfl_xor(nz, off, WAVE);
+    const uint32_t a = __shfl_xor(kmax, off, WAVE), c = __shfl_xor(kmin, off, WAVE);
+    kmax = a > kmax ? a : kmax;
+    kmin = c < kmin ? c : kmin;
+  }
+  if (lane == 0) {
+    scan[w] = nz;
+    scan[NW + w] = kmax;
+    scan[2 * NW + w] = kmin;
+  }
+  __syncthreads();
+  nz = 0;
+  kmax = 0;
+  kmin = 0xFFFFFFFFu;
+  for (int i = 0; i < NW; ++i) {
+    nz += scan[i];
+    kmax = scan[NW + i] > kmax ? scan[NW + i] : kmax;
+    kmin = scan[2 * NW + i] < kmin ? scan[2 * NW + i] : kmin;
+  }
+  __syncthreads();  // scan is reused below
+
+  uint32_t prefix, rem;
+  if (kk >= nz) {  // every nonzero key, then the first kk - nz zero keys
+    prefix = 0u;
+    rem = kk - nz;
+  } else {  // the kk-th largest key is nonzero: zero keys take no part
+    const uint32_t diff = kmax ^ kmin;
+    int hi = diff ? 31 - __builtin_clz(diff) : -1;  // highest differing bit
+    const uint32_t low = hi >= 0 ? (uint32_t)((2ull << hi) - 1ull) : 0u;
+    prefix = kmax & ~low;  // bits above hi are common to all nonzero keys
+    uint32_t pmask = ~low;
+    rem = kk;
+    while (hi >= 0) {  // uniform: every thread runs the same passes
+      const int nbits = hi + 1 < 12 ? hi + 1 : 12;
+      const int shift = hi + 1 - nbits;
+      const uint32_t nb = 1u << nbits;
+      for (uint32_t i = tid; i < nb; i += NT) hist[i] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < WPT; ++i)
+#pragma unroll
+        for (int b = 0; b < 32; ++b) {
+          const uint32_t kv = key[i][b];
+          if (kv != 0u && (kv & pmask) == prefix) atomicAdd(&hist[(kv >> shift) & (nb - 1)], 1u);
         }
-        c += hist[bin];
+      __syncthreads();
+      // thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top
+      const uint32_t bpt = nb >= (uint32_t)NT ? nb / NT : 1u;
+      const bool owner = (uint32_t)tid * bpt < nb;
+      const uint32_t hi_bin = nb - (uint32_t)tid * bpt;  // exclusive
+      uint32_t local = 0;
+      if (owner)
+        for (uint32_t i = 0; i < bpt; ++i) local += hist[hi_bin - 1 - i];
+      uint32_t tot;
+      const uint32_t above = block_excl_scan<NT>(local, scan, &tot);
+      if (owner && above < rem && above + local >= rem) {
+        uint32_t c = above;
+        for (uint32_t i = 0; i < bpt; ++i) {
+          const uint32_t bin = hi_bin - 1 - i;
+          if (c + hist[bin] >= rem) {
+            res[0] = bin;
+            res[1] = rem - c;
+            break;
+          }
+          c += hist[bin];
+        }
       }
+      __syncthreads();
+      prefix |= res[0] << shift;
+      pmask |= (nb - 1) << shift;
+      rem = res[1];
+      hi = shift - 1;
+      __syncthreads();
     }
-    __syncthreads();
-    prefix |= res[0] << shift;
-    pmask |= (nb - 1) << shift;
-    rem = res[1];
-    __syncthreads();
   }
   // prefix is the kk-th largest key; take all larger keys and the first `rem`
   // equal keys in id order.
   uint32_t eqm[WPT], neq = 0;
 #pragma unroll
-  for (int w = 0; w < WPT; ++w) {
+  for (int i = 0; i < WPT; ++i) {
     uint32_t gt = 0, eq = 0;
 #pragma unroll
     for (int b = 0; b < 32; ++b) {
-      gt |= (key[w][b] > prefix ? 1u : 0u) << b;
-      eq |= (key[w][b] == prefix ? 1u : 0u) << b;
+      gt |= (key[i][b] > prefix ? 1u : 0u) << b;
+      eq |= (key[i][b] == prefix ? 1u : 0u) << b;
     }
-    sel[w] = gt;
-    eqm[w] = eq;
+    sel[i] = gt;
+    eqm[i] = eq;
     neq += __builtin_popcount(eq);
   }
   uint32_t tot;
   uint32_t before = block_excl_scan<NT>(neq, scan, &tot);
 #pragma unroll
-  for (int w = 0; w < WPT; ++w) {
-    uint32_t e = eqm[w];
+  for (int i = 0; i < WPT; ++i) {
+    uint32_t e = eqm[i];
     while (e && before < rem) {
-      uint32_t low = e & (0u - e);
-      sel[w] |= low;
-      e ^= low;
+      uint32_t lowbit = e & (0u - e);
+      sel[i] |= lowbit;
+      e ^= lowbit;
       ++before;
     }
   }

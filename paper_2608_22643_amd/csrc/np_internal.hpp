@@ -14,10 +14,16 @@ namespace np {
 // Device workspace layout (dev_ws).  Offsets are multiples of 256 bytes.
 //   [0, 4096)            control block
 //       +0    int32  sticky error word (NP_DEVERR_* bits)
+//       +64   int32  np_delta step counter (NP_TOKEN_AUTO)
+//       +256  int32  sparse-MLP grid barrier: arrivals of the current call
+//       +384  int32  sparse-MLP grid barrier: generation (calls completed)
 //   [4096, +L'*r*4)      predictor intermediate z, fp32 [L'][r]
 //   [.., +MLP_MAX_WG*d*4) sparse-MLP per-workgroup partial sums, fp32
 // ---------------------------------------------------------------------------
 constexpr size_t WS_ERR = 0;
+constexpr size_t WS_TOKEN = 64;
+constexpr size_t WS_BAR_ARRIVE = 256;  // own cache lines: polled by every workgroup
+constexpr size_t WS_BAR_GEN = 384;
 constexpr size_t WS_CTRL_BYTES = 4096;
 constexpr int MLP_MAX_WG = 1024;  // partial rows the reduce kernel sums (4 per thread)
 

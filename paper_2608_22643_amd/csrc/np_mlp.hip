@@ -16,12 +16,24 @@
 //   * the wave's share of y (its column slice) stays in registers; the teams'
 //     partial y meet once in LDS at the end (fixed order) and team 0 writes
 //     the workgroup's partial y to the workspace.
-// Kernel 2 (reduce): sums the per-workgroup partials of each column in
-// workgroup order and rounds y once to the activation type.  The kernel
-// boundary makes the partials visible across XCDs; no in-kernel fences.
+// Reduction of the per-workgroup partials, one of two ways:
+//  * single kernel (opt-in with NP_MLP_FUSED=1, when the whole grid fits on
+//    the device at once; measured no faster than two kernels at 7B shape):
+//    the rows kernel writes its partial with agent-scope stores (coherent
+//    across the XCDs' L2s without a cache write-back), meets every other
+//    workgroup in a grid barrier (an arrival counter and a generation word in
+//    the workspace; bounded spin, NP_DEVERR_SPIN_LIMIT when it runs out), and
+//    then each workgroup reduces a slice of the columns over all partials
+//    with agent-scope loads, in a fixed order, and rounds y once;
+//  * two kernels: a separate reduce kernel sums the partials of each column
+//    in workgroup order; the kernel boundary makes them visible.
+// Both orders are fixed, so each path is deterministic.
 #include <stdlib.h>
 
 #include <algorithm>
+#include <map>
+#include <mutex>
+#include <tuple>
 
 #include "np_device.hpp"
 
@@ -35,9 +47,111 @@ struct MlpArgs {
   void* ws;
   int n_active, C, NV, n_wg, P, PP, teams;  // PP: P rounded up to a power of two
   uint32_t layer_bytes;  // resident bytes of the layer (< 2^31)
+  void* y;               // single-kernel path: the output
 };
 
-template <class T, int CPL, int R, int MAXT>
+// Single-kernel path.  Partial rows are stored in "position" order: float4
+// position pos = ((p*CPL + c)*(V/4) + q)*64 + lane holds columns
+// v*V + 4q .. v*V + 4q + 3 of vector v = (p*CPL + c)*64 + lane, so each wave
+// store instruction writes 1 KiB of contiguous memory.  The reduction works
+// on chunks of 4 positions (64 bytes of every partial row): workgroup b takes
+// chunks b, b + n_wg, ...; thread t reads position t % 4 of partial rows
+// t/4, t/4 + nt/4, ...  FUSED_CH chunks and FUSED_RPT rows per thread at
+// most; the barrier's spin is bounded (polls of about 1 us each).
+constexpr int FUSED_CH = 4;
+constexpr int FUSED_RPT = 4;
+constexpr uint32_t MLP_SPIN_LIMIT = 1u << 20;
+
+template <class T>
+__device__ inline void store_y1(void* y, int col, float v) {
+  if constexpr (T::dtype == NP_F32) ((float*)y)[col] = v;
+  else ((uint16_t*)y)[col] = (uint16_t)T::from_f32(v);
+}
+
+// Grid barrier, then the column reduction of this workgroup's chunks.  Every
+// thread of the workgroup calls it; thread 0 holds `gen0`, the generation
+// read at entry.
+template <class T>
+__device__ inline void fused_reduce(const MlpArgs& a, int gen0) {
+  constexpr int V = T::V;
+  __shared__ float4 wsum[FUSED_CH][16][4];  // chunk, wave, position
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are complete
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int* arrive = (int*)((char*)a.ws + WS_BAR_ARRIVE);
+    int* gen = (int*)((char*)a.ws + WS_BAR_GEN);
+    const int old = __hip_atomic_fetch_add(arrive, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == a.n_wg - 1) {  // last to arrive: every partial is written
+      (void)__hip_atomic_exchange(arrive, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      (void)__hip_atomic_fetch_add(gen, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      uint32_t spins = 0;
+      while (__hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gen0) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++spins == MLP_SPIN_LIMIT) {
+          raise_error(a.ws, NP_DEVERR_SPIN_LIMIT);
+          break;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int d = a.NV * V, nchunks = d / 16;
+  const int b = blockIdx.x, t = threadIdx.x, nt = blockDim.x;
+  const int q = t & 3, rsub = t >> 2, rstep = nt >> 2;
+  const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.partials, (uint32_t)a.n_wg * d * 4u);
+  float4 v[FUSED_CH][FUSED_RPT];
+#pragma unroll
+  for (int j = 0; j < FUSED_CH; ++j) {
+    const int chunk = b + j * a.n_wg;
+#pragma unroll
+    for (int m = 0; m < FUSED_RPT; ++m) {
+      const int row = rsub + m * rstep;
+      const bool ok = chunk < nchunks && row < a.n_wg;
+      const uint32_t off = ok ? ((uint32_t)row * d + (uint32_t)(chunk * 4 + q) * 4u) * 4u : BUF_OOB;
+      v[j][m] = buf_load16_agent(prs, off);  // zeros out of range
+    }
+  }
+  const int lane = t & (WAVE - 1), w = t / WAVE;
+#pragma unroll
+  for (int j = 0; j < FUSED_CH; ++j) {
+    float4 s = v[j][0];
+#pragma unroll
+    for (int m = 1; m < FUSED_RPT; ++m) {
+      s.x += v[j][m].x;
+      s.y += v[j][m].y;
+      s.z += v[j][m].z;
+      s.w += v[j][m].w;
+    }
+    // lanes with the same position: a butterfly over the row bits of the lane
+#pragma unroll
+    for (int off = 32; off >= 4; off >>= 1) {
+      s.x += __shfl_xor(s.x, off, WAVE);
+      s.y += __shfl_xor(s.y, off, WAVE);
+      s.z += __shfl_xor(s.z, off, WAVE);
+      s.w += __shfl_xor(s.w, off, WAVE);
+    }
+    if (lane < 4) wsum[j][w][lane] = s;
+  }
+  __syncthreads();
+  if (t < FUSED_CH * 16) {  // one column of one chunk each: waves in order
+    const int j = t >> 4, pq = (t >> 2) & 3, comp = t & 3;
+    const int chunk = b + j * a.n_wg;
+    if (chunk < nchunks) {
+      float acc = 0.f;
+      for (int ww = 0; ww < nt / WAVE; ++ww) {
+        const float4 f = wsum[j][ww][pq];
+        acc += comp == 0 ? f.x : comp == 1 ? f.y : comp == 2 ? f.z : f.w;
+      }
+      const int pos = chunk * 4 + pq;
+      const int tt = pos / WAVE, vq = tt % (V / 4);
+      const int vec = (tt / (V / 4)) * WAVE + pos % WAVE;
+      store_y1<T>(a.y, vec * V + 4 * vq + comp, acc);
+    }
+  }
+}
+
+template <class T, int CPL, int R, int MAXT, bool FUSED>
 __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   constexpr int V = T::V;
   // a round's R rows are finished in S stages of RS rows: the gate/up sums of
@@ -57,6 +171,10 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   const int row_begin = (int)(((long long)b * a.n_active) / a.n_wg);
   const int row_end = (int)(((long long)(b + 1) * a.n_active) / a.n_wg);
   const int v0 = p * WAVE * CPL;  // first vector of this wave's column slice
+  int gen0 = 0;  // grid barrier generation at entry (thread 0)
+  if (FUSED && threadIdx.x == 0)
+    gen0 = __hip_atomic_load((int*)((char*)a.ws + WS_BAR_GEN), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
 
   // first round's slots (lane r: row r) and x, both in flight before the
   // first wait
@@ -183,7 +301,9 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
         }
     }
     __syncthreads();
-    if (team > 0) return;
+    if (team > 0) {
+      if constexpr (!FUSED) return;
+    } else {
     for (int t = 1; t < teams; ++t) {
       const float* src = (const float*)team_part + (size_t)(t - 1) * a.NV * V;
 #pragma unroll
@@ -200,17 +320,34 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
           }
         }
     }
-  }
-  // this wave's column slice of the workgroup's partial y
-  float* dst = a.partials + (size_t)b * a.NV * V;
-#pragma unroll
-  for (int c = 0; c < CPL; ++c)
-    if (vok[c]) {
-      float4* d4 = (float4*)(dst + (size_t)(v0 + lane + WAVE * c) * V);
-#pragma unroll
-      for (int e = 0; e < V; e += 4)
-        d4[e / 4] = make_float4(yacc[c][e], yacc[c][e + 1], yacc[c][e + 2], yacc[c][e + 3]);
     }
+  }
+  // this wave's column slice of the workgroup's partial y (team 0)
+  float* dst = a.partials + (size_t)b * a.NV * V;
+  if (team == 0) {
+    if constexpr (FUSED) {  // position order, agent-scope stores (see above)
+      const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.partials, (uint32_t)a.n_wg * a.NV * V * 4u);
+#pragma unroll
+      for (int c = 0; c < CPL; ++c)
+#pragma unroll
+        for (int q = 0; q < V / 4; ++q) {
+          const uint32_t pos = (uint32_t)(((p * CPL + c) * (V / 4) + q) * WAVE + lane);
+          const uint32_t off = vok[c] ? ((uint32_t)b * a.NV * V + pos * 4u) * 4u : BUF_OOB;
+          buf_store16_agent(prs, off, make_float4(yacc[c][4 * q], yacc[c][4 * q + 1],
+                                                  yacc[c][4 * q + 2], yacc[c][4 * q + 3]));
+        }
+    } else {
+#pragma unroll
+      for (int c = 0; c < CPL; ++c)
+        if (vok[c]) {
+          float4* d4 = (float4*)(dst + (size_t)(v0 + lane + WAVE * c) * V);
+#pragma unroll
+          for (int e = 0; e < V; e += 4)
+            d4[e / 4] = make_float4(yacc[c][e], yacc[c][e + 1], yacc[c][e + 2], yacc[c][e + 3]);
+        }
+    }
+  }
+  if constexpr (FUSED) fused_reduce<T>(a, gen0);
 }
 
 template <class T>
@@ -283,15 +420,51 @@ static int env_int(const char* name, int dflt) {
   return x > 0 ? x : dflt;
 }
 
+// Workgroups of `kernel` that fit on the current device at once (cached).
+static int coresident(const void* kernel, int threads, size_t lds) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, const void*, int, size_t>, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> g(mu);
+  auto key = std::make_tuple(dev, kernel, threads, lds);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int per_cu = 0, cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, lds) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    per_cu = 0;
+  }
+  return cache[key] = per_cu * cus;
+}
+
+template <class T, int CPL, int R, int MAXT>
+static void launch_rows_t(const MlpArgs& a, size_t lds, bool want_fused, bool* fused,
+                          hipStream_t stream) {
+  const int threads = a.teams * a.P * WAVE;
+  *fused = false;
+  if (want_fused) {
+    const void* k = (const void*)sparse_mlp_rows_kernel<T, CPL, R, MAXT, true>;
+    if (a.n_wg <= coresident(k, threads, lds)) {
+      *fused = true;
+      hipLaunchKernelGGL((sparse_mlp_rows_kernel<T, CPL, R, MAXT, true>), dim3(a.n_wg),
+                         dim3(threads), lds, stream, a);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((sparse_mlp_rows_kernel<T, CPL, R, MAXT, false>), dim3(a.n_wg),
+                     dim3(threads), lds, stream, a);
+}
+
 template <class T, int CPL, int R>
-static void launch_rows(const MlpArgs& a, int n_wg, size_t lds, hipStream_t stream) {
+static void launch_rows(const MlpArgs& a, size_t lds, bool want_fused, bool* fused,
+                        hipStream_t stream) {
   const int threads = a.teams * a.P * WAVE;
   if (threads <= 512) {  // up to 8 waves: a register budget of 256 per lane
-    hipLaunchKernelGGL((sparse_mlp_rows_kernel<T, CPL, R, 512>), dim3(n_wg), dim3(threads), lds,
-                       stream, a);
+    launch_rows_t<T, CPL, R, 512>(a, lds, want_fused, fused, stream);
   } else if constexpr (R <= 4) {  // 128 registers per lane: at most 4 rows a round
-    hipLaunchKernelGGL((sparse_mlp_rows_kernel<T, CPL, R, 1024>), dim3(n_wg), dim3(threads), lds,
-                       stream, a);
+    launch_rows_t<T, CPL, R, 1024>(a, lds, want_fused, fused, stream);
   }
 }
 
@@ -334,16 +507,27 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   a.x = (const uint4*)x;
   a.partials = (float*)((char*)ws + ws_partials_offset(s));
   a.ws = ws;
+  a.y = y;
   const size_t lds = (size_t)(teams - 1) * a.NV * V * sizeof(float);
+  // single kernel while the reduction layout holds: whole wave slices (every
+  // lane owns a vector), at least a wave of partial rows, at most FUSED_RPT
+  // rows and FUSED_CH chunks per thread (a co-resident grid is checked at
+  // launch)
+  const int threads = teams * a.P * WAVE;
+  const int nchunks = s.d_model / 16;
+  const bool want_fused = env_int("NP_MLP_FUSED", 0) == 1 && a.NV % (WAVE * cpl) == 0 &&
+                          n_wg >= WAVE && n_wg <= FUSED_RPT * (threads / 4) &&
+                          nchunks <= FUSED_CH * n_wg && threads / WAVE <= 16;
+  bool fused = false;
   if (cpl == 1) {
-    if (R == 4) launch_rows<T, 1, 4>(a, n_wg, lds, stream);
-    else if (R == 2) launch_rows<T, 1, 2>(a, n_wg, lds, stream);
-    else launch_rows<T, 1, 8>(a, n_wg, lds, stream);
+    if (R == 4) launch_rows<T, 1, 4>(a, lds, want_fused, &fused, stream);
+    else if (R == 2) launch_rows<T, 1, 2>(a, lds, want_fused, &fused, stream);
+    else launch_rows<T, 1, 8>(a, lds, want_fused, &fused, stream);
   } else {
-    launch_rows<T, 2, 2>(a, n_wg, lds, stream);
+    launch_rows<T, 2, 2>(a, lds, want_fused, &fused, stream);
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || fused) return e;
   const int groups = (s.d_model + RED_COLS - 1) / RED_COLS;
   hipLaunchKernelGGL(mlp_reduce_kernel<T>, dim3(groups), dim3(256), 0, stream,
                      (const float*)a.partials, n_wg, s.d_model, y);

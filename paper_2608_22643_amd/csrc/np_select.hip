@@ -30,7 +30,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ sc
                                                     int32_t* __restrict__ active_ids, int F,
                                                     int k, void* ws) {
   __shared__ uint32_t hist[4096];
-  __shared__ uint32_t scan[NT / WAVE + 1];
+  __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
   __shared__ uint32_t res[2];
   const int l = blockIdx.x, tid = threadIdx.x;
   const int words = (F + 31) / 32;
@@ -112,9 +112,10 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
   __shared__ uint32_t rmask[2048];  // resident rows (neurons held by some slot)
   __shared__ uint32_t hist[4096];
   __shared__ int32_t pool[8192];    // the first nI pool slots, ascending
-  __shared__ uint32_t scan[NT / WAVE + 1];
+  __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
   __shared__ uint32_t res[2];
   const int l = blockIdx.x, tid = threadIdx.x;
+  if (token == NP_TOKEN_AUTO) token = *(const int32_t*)((const char*)ws + WS_TOKEN);
   const int idwords = (F + 31) / 32, slotwords = (C + 31) / 32;
   int32_t* P = slot_of + (size_t)l * F;
   int32_t* Q = neuron_of + (size_t)l * C;
@@ -322,6 +323,11 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
   }
 }
 
+// Advances np_delta's step counter (NP_TOKEN_AUTO) once the delta is done.
+__global__ void token_advance_kernel(void* ws) {
+  if (threadIdx.x == 0) *(int32_t*)((char*)ws + WS_TOKEN) += 1;
+}
+
 __global__ void fill_state_kernel(int32_t* __restrict__ a, size_t na, int32_t* __restrict__ b,
                                   size_t nb, int32_t* __restrict__ c, size_t nc,
                                   int32_t* __restrict__ ctrl) {
@@ -386,9 +392,13 @@ hipError_t launch_delta(const np_shape& s, int32_t token, const int32_t* active_
                         hipStream_t stream) {
   // 512 threads while every thread owns one id word and at most 4 actives
   const int words = (s.d_ffn + 31) / 32;
-  if (words <= 512 && s.k <= 2048) return delta_w<512, 1>(s, token, active_ids, st, out, ws, stream);
-  if (words <= 1024) return delta_w<1024, 1>(s, token, active_ids, st, out, ws, stream);
-  return delta_w<1024, 2>(s, token, active_ids, st, out, ws, stream);
+  hipError_t e;
+  if (words <= 512 && s.k <= 2048) e = delta_w<512, 1>(s, token, active_ids, st, out, ws, stream);
+  else if (words <= 1024) e = delta_w<1024, 1>(s, token, active_ids, st, out, ws, stream);
+  else e = delta_w<1024, 2>(s, token, active_ids, st, out, ws, stream);
+  if (e != hipSuccess || token != NP_TOKEN_AUTO) return e;
+  hipLaunchKernelGGL(token_advance_kernel, dim3(1), dim3(64), 0, stream, ws);
+  return hipGetLastError();
 }
 
 }  // namespace np

@@ -16,11 +16,20 @@ Staging modes:
             each chunk goes over with hipMemcpyAsync on a side stream, then a
             scatter kernel places the records.  Needs the "host" tier.
 
-With overlap=True staging runs on a side stream and layer l's MLP waits only
-for layer l's rows (a per-layer event), so staging later layers overlaps the
-MLP of earlier ones.  The side stream waits for np_delta of the same token,
+With overlap=True staging runs on a side stream in a few layer chunks
+(layer 0, layers 1-2, the rest), each followed by an event, and layer l's MLP
+waits only for the chunk holding layer l: staging later layers overlaps the
+MLP of earlier ones with three staging launches per token, not one per layer.  The side stream waits for np_delta of the same token,
 which itself follows the previous token's MLP on the main stream, so a victim
 slot is never overwritten while the previous token still reads it.
+
+Graph mode (capture_graph / step_graph): one decode step is captured once as
+a HIP graph and replayed per token.  The step then has no per-token argument:
+h_t is copied into a fixed input buffer before each replay and np_delta takes
+the token index from the workspace step counter (NP_TOKEN_AUTO), which
+np_state_reset sets to 0, so graph tokens must start at a cold start (t = 0)
+and run in order.  Only "gather" staging can be captured (np_stage_rows waits
+on the host for the plan).
 """
 from __future__ import annotations
 
@@ -101,6 +110,9 @@ class DecodePipeline:
         self.side = torch.cuda.Stream(device=dev) if overlap else self.main
         self.ev_delta = torch.cuda.Event()
         self.layer_ready = [torch.cuda.Event() for _ in range(L)] if overlap else None
+        # staging chunks of the overlapped gather path: [0,1), [1,3), [3,L)
+        cuts = sorted({0, min(1, L), min(3, L), L})
+        self.chunks = list(zip(cuts[:-1], cuts[1:]))
         if staging == "memcpy":
             self.plan_counts = torch.empty(L * 4, dtype=torch.int32, pin_memory=True)
             self.plan_ids = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
@@ -131,20 +143,43 @@ class DecodePipeline:
         """Enqueue one decode token (index t of the hidden-state sequence).
         mlp_block_events: optional (start, end) torch events recorded on the
         main stream before the first and after the last np_sparse_mlp."""
+        self._enqueue(t, self.x_ptr(t), mlp_block_events)
+
+    def capture_graph(self) -> None:
+        """Capture one decode step (token index from the device counter, x
+        from a fixed buffer) as a HIP graph.  Nothing runs until replay."""
+        if self.staging != "gather":
+            raise ValueError("only gather staging can be captured in a graph")
+        self.x_static = torch.empty(self.row_bytes, dtype=torch.uint8, device=self.device)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph, stream=self.main, capture_error_mode="thread_local"):
+            self._enqueue(B.NP_TOKEN_AUTO, self.x_static.data_ptr(), None)
+
+    def step_graph(self, t: int) -> None:
+        """Replay the captured step for token t (tokens 0, 1, 2, ... in order
+        after a cold start)."""
+        with torch.cuda.stream(self.main):
+            self.x_static.copy_(self.h[t], non_blocking=True)
+            self.graph.replay()
+
+    def _enqueue(self, token: int, x_ptr: int, mlp_block_events) -> None:
         s, cfg = self.shape, self.cfg
         L, k = cfg.layers, cfg.k
         main = self.main
-        B.np_predict(s, self.x_ptr(t), self.A, self.B, self.scores, self.ws, main)
+        B.np_predict(s, x_ptr, self.A, self.B, self.scores, self.ws, main)
         B.np_select(s, self.scores, self.mask, self.active_ids, self.ws, main)
-        B.np_delta(s, t, self.active_ids, self.state, self.out, self.ws, main)
+        B.np_delta(s, token, self.active_ids, self.state, self.out, self.ws, main)
+        ready = None  # ready[l]: the event layer l's MLP waits for
         if self.staging == "gather":
             if self.overlap:
                 self.ev_delta.record(main)
                 self.side.wait_event(self.ev_delta)
-                for l in range(L):
-                    B.np_stage_gather(s, self.out, l, l + 1, self.storage, self.resident,
+                ready = [None] * L
+                for lb, le in self.chunks:
+                    B.np_stage_gather(s, self.out, lb, le, self.storage, self.resident,
                                       self.ws, self.side)
-                    self.layer_ready[l].record(self.side)
+                    self.layer_ready[lb].record(self.side)
+                    ready[lb] = self.layer_ready[lb]
             else:
                 B.np_stage_gather(s, self.out, 0, L, self.storage, self.resident, self.ws, main)
         else:
@@ -158,16 +193,20 @@ class DecodePipeline:
                             self.staging_buf.numel(), self.landing, self.landing.numel(),
                             self.side, self.ev_plan if self.overlap else None,
                             self.layer_ready)
+            if self.overlap:
+                ready = self.layer_ready
         slots = self.lists["active_slots"]
         ybytes = cfg.d_model * W.ITEMSIZE[cfg.adtype]
         if mlp_block_events is not None:
-            if self.overlap:  # time the MLP block, not the wait for staging
-                main.wait_event(self.layer_ready[L - 1])
+            if ready is not None:  # time the MLP block, not the wait for staging
+                for e in ready:
+                    if e is not None:
+                        main.wait_event(e)
             mlp_block_events[0].record(main)
         for l in range(L):
-            if self.overlap:
-                main.wait_event(self.layer_ready[l])
-            B.np_sparse_mlp(s, l, self.x_ptr(t), self.resident, slots.data_ptr() + l * k * 4, k,
+            if ready is not None and ready[l] is not None:
+                main.wait_event(ready[l])
+            B.np_sparse_mlp(s, l, x_ptr, self.resident, slots.data_ptr() + l * k * 4, k,
                             self.y.data_ptr() + l * ybytes, self.ws, main)
         if mlp_block_events is not None:
             mlp_block_events[1].record(main)

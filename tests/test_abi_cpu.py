@@ -91,7 +91,7 @@ def test_null_and_misaligned_pointers_rejected(lib):
         B.np_sparse_mlp(shape, 0, 16, 16, 16, 5505, 16, 16, None)  # n_active > C
     assert e.value.status == B.NP_ERR_INVALID_ARG
     with pytest.raises(B.NPError) as e:
-        B.np_delta(shape, -1, 16, B.np_state(16, 16, 16), B.np_delta_out(*([16] * 7)), 16, None)
+        B.np_delta(shape, -2, 16, B.np_state(16, 16, 16), B.np_delta_out(*([16] * 7)), 16, None)
     assert e.value.status == B.NP_ERR_INVALID_ARG
     with pytest.raises(B.NPError) as e:
         B.np_stage_gather(shape, B.np_delta_out(*([16] * 7)), 3, 2, 16, 16, 16, None)

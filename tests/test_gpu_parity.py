@@ -222,8 +222,43 @@ def test_stage_rows_rejects_small_staging():
 
 @pytest.mark.parametrize("name", list(SHAPES))
 def test_sparse_mlp(name):
-    cfg = SHAPES[name]
-    say(f"[mlp] {name} d={cfg.d_model} k={cfg.k}")
+    check_sparse_mlp(SHAPES[name])
+
+
+# the single-kernel reduction (grid barrier) applies to whole wave slices and
+# at least 64 rows; the two-kernel one to every shape: both against the oracle
+@pytest.mark.parametrize("name", ["wide_f16", "wide_bf16"])
+@pytest.mark.parametrize("fused", ["0", "1"])
+def test_sparse_mlp_both_reductions(name, fused, monkeypatch):
+    monkeypatch.setenv("NP_MLP_FUSED", fused)
+    check_sparse_mlp(SHAPES[name])
+
+
+def test_sparse_mlp_row_counts():
+    """Prefixes of the active list: fewer rows than workgroups, exactly one
+    wave of partial rows, and the full list (both reductions' boundaries)."""
+    cfg = SHAPES["wide_f16"]
+    say(f"[mlp rows] {cfg.name}")
+    bufs, resident, store, st = stage_and_check(cfg, "gather_device")
+    d, k, esz = cfg.d_model, cfg.k, W.ITEMSIZE[cfg.adtype]
+    h = W.hidden(cfg, 1)[0]
+    x = to_dev(h)
+    slots = bufs.lists["active_slots"].cpu().numpy().reshape(cfg.layers, k)
+    neuron_of = st.neuron_of
+    y = torch.zeros(d * esz, dtype=torch.uint8, device=DEV)
+    for n in (1, 63, 64, 65, 255, 256, 257, k):
+        B.np_sparse_mlp(bufs.shape, 1, x, resident, bufs.lists["active_slots"].data_ptr() + 4 * k,
+                        n, y, bufs.ws)
+        torch.cuda.synchronize()
+        ids = np.sort(neuron_of[1][slots[1][:n]]).astype(np.int32)
+        _, ref64 = orc.sparse_mlp(cfg, 1, h, store, ids, want_f64=True)
+        got = decode_y(orc, cfg.adtype, y.cpu().numpy())
+        assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), n
+    assert B.np_device_error(bufs.ws) == 0
+
+
+def check_sparse_mlp(cfg):
+    say(f"[mlp] {cfg.name} d={cfg.d_model} k={cfg.k}")
     bufs, resident, store, st = stage_and_check(cfg, "gather_device")
     L, k, d = cfg.layers, cfg.k, cfg.d_model
     h = W.hidden(cfg, 1)[0]
@@ -330,3 +365,40 @@ def test_lockstep_tiny(tier, staging, overlap):
             _, ref64 = orc.sparse_mlp(cfg, l, h[t], store, ids[l], want_f64=True)
             assert np.all(np.abs(y[l] - ref64) <= mlp_tolerance("f32", ref64))
     assert pipe.device_error() == 0
+
+
+@pytest.mark.parametrize("name,overlap", [("tiny", True), ("tiny", False),
+                                          ("dyadic_tiny", True)])
+def test_graph_replay_matches_eager(name, overlap):
+    """A captured decode step replayed per token (token index from the device
+    step counter, x from a fixed buffer) gives bit for bit what the eager step
+    gives, on every replay, with eager work and synchronisation between the
+    replays; both follow the oracle's delta in lockstep."""
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get(name)
+    T = min(cfg.tokens, 8)
+    say(f"[graph] {name} overlap={overlap} tokens={T}")
+    eager = DecodePipeline(cfg, tier="device", staging="gather", overlap=overlap, tokens=T)
+    graph = DecodePipeline(cfg, tier="device", staging="gather", overlap=overlap, tokens=T)
+    graph.capture_graph()
+    st = orc.State(cfg.layers, cfg.d_ffn, cfg.capacity)
+    L = cfg.layers
+    for t in range(T):
+        eager.step(t)
+        graph.step_graph(t)
+        torch.cuda.synchronize()
+        _ = (torch.arange(4096, device="cuda", dtype=torch.float32) * t).sum().item()
+        for a in ("scores", "mask", "active_ids", "y", "counts"):
+            ga, ea = getattr(graph, a), getattr(eager, a)
+            assert torch.equal(ga.view(torch.uint8), ea.view(torch.uint8)), (t, a)
+        for (gs, es) in zip(graph.host_state(), eager.host_state()):
+            assert np.array_equal(gs, es), t
+        gl, el = graph.host_lists(), eager.host_lists()
+        ids = graph.active_ids.cpu().numpy().reshape(L, -1)
+        ref = orc.delta(t, ids, st, cfg.capacity)
+        compare_delta(gl, ref, L)
+        compare_delta(el, ref, L)
+        occupied = torch.from_numpy(np.repeat(st.neuron_of.reshape(-1) >= 0, cfg.record_bytes))
+        assert torch.equal(graph.resident.cpu()[occupied], eager.resident.cpu()[occupied]), t
+    assert graph.device_error() == 0 and eager.device_error() == 0
