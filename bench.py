@@ -31,6 +31,45 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 
+# Hardware byte counters of the two np_sparse_mlp kernels at the 7B shape,
+# from two rocprofv3 --pmc passes over this benchmark (FETCH_SIZE, then
+# WRITE_SIZE; mean KiB per dispatch), and the same counters for the
+# calibration copy (--calib-mib 256: 262144 KiB read and written once).  The
+# figures hold only for the kernel sources they were taken on (hash below);
+# after any change to those sources "traffic" is reported as null.
+MLP_COUNTERS = {
+    "config": "7b",
+    "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
+    "sha256": "9e0791d0c60ca967345f6edaea0d98b9bb264c9b2ff37bb41bdbe0682a6ea2f2"
+              "753eac23b781ed50788521c47469bf5e9c3fb1e925f19d8a10eea91c62a914a9",
+    "fetch_kib": {"rows": 19918.2, "reduce": 4114.5},
+    "write_kib": {"rows": 4096.0, "reduce": 8.0},
+    "copy_fetch_kib": 131088.3, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+}
+
+
+def mlp_traffic(cfg):
+    """HBM bytes per np_sparse_mlp call from the counters above (each counter
+    scaled by true bytes / counter for the plain copy), or None when they do
+    not apply to this configuration or these kernel sources."""
+    import hashlib
+
+    c = MLP_COUNTERS
+    if cfg.name != c["config"]:
+        return None, None
+    h = "".join(hashlib.sha256(open(os.path.join(ROOT, f), "rb").read()).hexdigest()
+                for f in c["sources"])
+    if h != c["sha256"]:
+        return None, None
+    rf = c["copy_kib"] / c["copy_fetch_kib"]
+    wf = c["copy_kib"] / c["copy_write_kib"]
+    detail = {k: {"read_MB": round(c["fetch_kib"][k] * rf * 1024 / 1e6, 2),
+                  "write_MB": round(c["write_kib"][k] * wf * 1024 / 1e6, 2)}
+              for k in ("rows", "reduce")}
+    total = sum((c["fetch_kib"][k] * rf + c["write_kib"][k] * wf) * 1024 for k in ("rows", "reduce"))
+    detail["scale"] = {"fetch": round(rf, 4), "write": round(wf, 4)}
+    return int(total), detail
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -164,6 +203,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--breakdown-steps", type=int, default=10)
     ap.add_argument("--mlp-steps", type=int, default=20)
+    ap.add_argument("--calib-mib", type=int, default=256,
+                    help="size of one plain device-to-device copy run after the timing, "
+                         "the reference for hardware byte counters")
     ap.add_argument("--graph", type=int, default=1,
                     help="time the step replayed from a captured HIP graph (else eager launches)")
     args = ap.parse_args()
@@ -228,6 +270,7 @@ def main():
         sys.exit(1)
     ms_per_step = wall * 1e3 / K
     bytes_launch = mlp_bytes_per_launch(cfg)
+    traffic, traffic_detail = mlp_traffic(cfg)
     achieved = bytes_launch / (mlp_us * 1e-6) / 1e9
     counts = delta_stats(pipe)
     # per-phase breakdown (no overlap) and persistence statistics
@@ -263,6 +306,13 @@ def main():
                 "note": "storage tier in pinned host memory; staging crosses the host link"}
         log(f"[bench] host tier: {host}")
         del hp, hg
+    if args.calib_mib > 0:  # a copy of known size: reads and writes calib_mib MiB once
+        src = torch.ones(args.calib_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(cfg, host_storage, args.cpu_seconds)
@@ -289,7 +339,8 @@ def main():
                    "launch": "hip_graph" if graph else "eager"},
         "roofline": {"bound": "hbm", "kernel": "np_sparse_mlp",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "traffic_detail": traffic_detail,
                      "bytes_per_launch": bytes_launch, "avg_launch_us": round(mlp_us, 3)},
         "eager_tok_s": round(1e3 / eager_ms, 2) if eager_ms else None,
         "sparse_mlp_tok_s": round(1e6 / (mlp_us * cfg.layers), 1),
