@@ -93,3 +93,16 @@ def decode_y(orc, adtype: str, y_bits: np.ndarray) -> np.ndarray:
     if adtype == "f32":
         return y_bits.view(np.float32).astype(np.float64)
     return orc.decode(adtype, y_bits.view(np.uint16))
+
+
+def score_bound(cfg, A, Bm, h):
+    """fp32 accumulation bound of s = B (A h): (d + r + 2) u sum |B||A||h|."""
+    import oracle as orc
+
+    Ad, Bd = orc.decode(cfg.wdtype, A), orc.decode(cfg.wdtype, Bm)
+    hd = np.abs(orc.decode(cfg.adtype, h))
+    L = cfg.layers
+    Ad = np.abs(Ad).reshape(L, cfg.rank, cfg.d_model)
+    Bd = np.abs(Bd).reshape(L, cfg.d_ffn, cfg.rank)
+    mag = np.stack([Bd[l] @ (Ad[l] @ hd) for l in range(L)])
+    return (cfg.d_model + cfg.rank + 2) * 2.0 ** -24 * mag

@@ -14,7 +14,8 @@ import torch
 import oracle as orc
 from paper_2608_22643_amd import binding as B
 from paper_2608_22643_amd import workload as W
-from gpu_util import DEV, Bufs, compare_delta, decode_y, from_dev, mlp_tolerance, say, to_dev
+from gpu_util import (DEV, Bufs, compare_delta, decode_y, from_dev, mlp_tolerance, say,
+                      score_bound, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -38,14 +39,6 @@ SHAPES = {
     "f_20000": cfg_small("f_20000", 2, 64, 20000, 16, 2500, 6000, "bf16"),
     "f_max": cfg_small("f_max", 1, 64, 65535, 8, 8192, 8192, "f32"),
 }
-
-
-def score_bound(cfg, A, Bm, h):
-    """fp32 accumulation bound of s = B (A h): (d + r + 2) u sum |B||A||h|."""
-    Ad, Bd = orc.decode(cfg.wdtype, A), orc.decode(cfg.wdtype, Bm)
-    hd = np.abs(orc.decode(cfg.adtype, h))
-    mag = np.einsum("lfr,lr->lf", np.abs(Bd), np.einsum("lrd,d->lr", np.abs(Ad), hd))
-    return (cfg.d_model + cfg.rank + 2) * 2.0 ** -24 * mag
 
 
 @pytest.mark.parametrize("name", list(SHAPES))
