@@ -5,11 +5,13 @@ np_delta, staging of the incoming rows and np_sparse_mlp for every downstream
 layer.  Inputs are synthetic and already resident in HBM when the timed
 region starts (predictor factors, hidden states, and the storage tier the
 incoming rows are staged from); the step's own work is timed, nothing is
-skipped.  Prints one JSON line.  By default the step is captured once as a
-HIP graph and replayed per token (--graph 0: one launch per call from Python).
+skipped.  Prints one JSON line.  By default each call is launched from
+Python on one stream (--graph 1: the step captured once as a HIP graph and
+replayed per token).
 
 Extra measurements in the same run:
-  * the same steps with eager launches ("eager_tok_s");
+  * the same steps replayed from a captured HIP graph ("graph_tok_s", or
+    "eager_tok_s" for the eager launches when --graph 1);
   * the sparse-MLP call's average time, from HIP events bracketing each
     token's block of back-to-back calls on their stream, against the HBM
     roofline;
@@ -129,6 +131,7 @@ def breakdown(pipe, t0, steps):
     L, k = cfg.layers, cfg.k
     names = ("predict", "select", "delta", "stage", "mlp")
     acc = {n: 0.0 for n in names}
+    counts = []
     ybytes = cfg.d_model * (4 if cfg.adtype == "f32" else 2)
     for i in range(steps):
         t = t0 + i
@@ -151,7 +154,42 @@ def breakdown(pipe, t0, steps):
         torch.cuda.synchronize()
         for j, n in enumerate(names):
             acc[n] += ev[j].elapsed_time(ev[j + 1]) * 1e3
-    return {n: round(v / steps, 2) for n, v in acc.items()}
+        counts.append(delta_stats(pipe))
+    return {n: round(v / steps, 2) for n, v in acc.items()}, counts
+
+
+def h2d_peak_gbps(nbytes: int = 1 << 30) -> float:
+    """One pinned host -> device hipMemcpyAsync of `nbytes`, timed with events."""
+    import torch
+
+    src = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst.copy_(src, non_blocking=True)  # first touch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    dst.copy_(src, non_blocking=True)
+    e1.record()
+    torch.cuda.synchronize()
+    return nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9
+
+
+def staging_rates(pipe, t0: int, steps: int) -> dict:
+    """np_stage_rows alone (memcpy tier): staged bytes over the time from the
+    call (host packing included) to the end of its copies and scatters, next
+    to a 1 GiB pinned hipMemcpyAsync measured in the same run."""
+    pipe.stage_log = []
+    for i in range(steps):
+        pipe.step(t0 + i)
+    import torch
+
+    torch.cuda.synchronize()
+    nb = sum(b for b, _ in pipe.stage_log)
+    sec = sum(x for _, x in pipe.stage_log)
+    pipe.stage_log = None
+    return {"staging_h2d_GBps": round(nb / sec / 1e9, 2),
+            "staged_MB_per_token": round(nb / steps / 1e6, 2),
+            "h2d_peak_GBps": round(h2d_peak_gbps(), 2)}
 
 
 def delta_stats(pipe):
@@ -159,6 +197,62 @@ def delta_stats(pipe):
 
     c = pipe.counts.cpu().numpy().reshape(-1, 4)
     return c
+
+
+def extra_config(name: str, steps: int, graph: bool, overlap: bool) -> dict:
+    """The same measurements, shorter, on another configuration (13B shape):
+    steps with the storage tier in HBM (launched as the main measurement),
+    the sparse-MLP call against the HBM roofline, and the step with the
+    storage tier in pinned host memory (memcpy staging) with its staging
+    rate."""
+    import torch
+
+    from paper_2608_22643_amd import workload as W
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get(name)
+    T = 1 + 3 + 3 * steps + 8
+    t = time.perf_counter()
+    host_storage = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
+    W.fill_storage(cfg, host_storage.data_ptr())
+    log(f"[bench] {name}: storage tier generated: {cfg.storage_bytes / 1e9:.2f} GB in "
+        f"{time.perf_counter() - t:.1f} s")
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", overlap=overlap, tokens=T,
+                          host_storage=host_storage)
+    if graph:
+        pipe.capture_graph()
+        for i in range(4):
+            pipe.step_graph(i)
+        wall = timed_graph_steps(pipe, 4, steps)
+    else:
+        for i in range(4):
+            pipe.step(i)
+        wall, _ = timed_steps(pipe, 4, steps, with_mlp_events=False)
+    _, mlp_us = timed_steps(pipe, 4 + steps, steps)
+    counts = delta_stats(pipe)
+    if pipe.device_error():
+        raise RuntimeError(f"{name}: device error word {pipe.device_error():#x}")
+    bytes_launch = mlp_bytes_per_launch(cfg)
+    achieved = bytes_launch / (mlp_us * 1e-6) / 1e9
+    out = {"workload": f"{cfg.name}-shaped decode: {cfg.layers} downstream layers, d={cfg.d_model}, "
+                       f"F={cfg.d_ffn}, rank {cfg.rank}, k={cfg.k}, C={cfg.capacity}, {cfg.wdtype}",
+           "tok_s": round(steps / wall, 2), "ms_per_step": round(wall * 1e3 / steps, 4),
+           "sparse_mlp": {"avg_launch_us": round(mlp_us, 3), "bytes_per_launch": bytes_launch,
+                          "achieved_GBps": round(achieved, 1),
+                          "frac": round(achieved / HBM_PEAK_GBPS, 4)},
+           "incoming_rows_per_token": int(counts[:, 0].sum())}
+    del pipe
+    torch.cuda.empty_cache()
+    hp = DecodePipeline(cfg, tier="host", staging="memcpy", overlap=True, tokens=T,
+                        host_storage=host_storage)
+    for i in range(4):
+        hp.step(i)
+    hw, _ = timed_steps(hp, 4, steps, with_mlp_events=False)
+    out["host_tier"] = {"memcpy_staging_tok_s": round(steps / hw, 2)}
+    out["host_tier"].update(staging_rates(hp, 4 + steps, max(3, steps // 4)))
+    del hp, host_storage
+    torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(cfg, host_storage, seconds: float):
@@ -198,16 +292,23 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="7b")
-    ap.add_argument("--overlap", type=int, default=1)
+    ap.add_argument("--overlap", type=int, default=0,
+                    help="stage on a side stream in layer chunks (measured slower: each "
+                         "cross-stream event costs about 10 us on the GPU)")
     ap.add_argument("--host-tier-steps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--breakdown-steps", type=int, default=10)
     ap.add_argument("--mlp-steps", type=int, default=20)
+    ap.add_argument("--extra-configs", default="13b",
+                    help="comma-separated further configurations measured after the main one")
+    ap.add_argument("--extra-steps", type=int, default=30)
     ap.add_argument("--calib-mib", type=int, default=256,
                     help="size of one plain device-to-device copy run after the timing, "
                          "the reference for hardware byte counters")
-    ap.add_argument("--graph", type=int, default=1,
-                    help="time the step replayed from a captured HIP graph (else eager launches)")
+    ap.add_argument("--graph", type=int, default=0,
+                    help="time the step replayed from a captured HIP graph (default: eager "
+                         "launches, which need no per-token input copy; the graph's rate is "
+                         "reported as graph_tok_s)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -222,7 +323,7 @@ def main():
 
     cfg = W.get(args.config)
     K, Wm = args.steps, args.warmup
-    T = 1 + Wm + 2 * K + args.mlp_steps + args.breakdown_steps + args.host_tier_steps + 2
+    T = 1 + Wm + 2 * K + args.mlp_steps + args.breakdown_steps + 2 * args.host_tier_steps + 8
     log(f"[bench] config {cfg.name}: L'={cfg.layers} d={cfg.d_model} F={cfg.d_ffn} r={cfg.rank} "
         f"k={cfg.k} C={cfg.capacity} {cfg.wdtype}; tokens {T}")
     t = time.perf_counter()
@@ -254,12 +355,22 @@ def main():
         wall, _ = timed_steps(pipe, 1 + Wm, K, with_mlp_events=False)
     log(f"[bench] timed {K} steps ({'graph' if graph else 'eager'}): {wall * 1e3 / K:.3f} ms/step")
     t1 = 1 + Wm + K
-    eager_ms = None
+    other_ms = None
     if graph:  # the same steps launched one call at a time, for comparison
         ew, _ = timed_steps(pipe, t1, K, with_mlp_events=False)
-        eager_ms = ew * 1e3 / K
-        log(f"[bench] eager launches: {eager_ms:.3f} ms/step")
+        other_ms = ew * 1e3 / K
+        log(f"[bench] eager launches: {other_ms:.3f} ms/step")
         t1 += K
+    else:  # the same steps replayed from a graph (a second pipeline from token 0)
+        gp = DecodePipeline(cfg, tier="device", staging="gather", overlap=bool(args.overlap),
+                            tokens=T, host_storage=host_storage)
+        gp.capture_graph()
+        for i in range(1 + Wm):
+            gp.step_graph(i)
+        other_ms = timed_graph_steps(gp, 1 + Wm, K) * 1e3 / K
+        log(f"[bench] graph replay: {other_ms:.3f} ms/step")
+        del gp
+        torch.cuda.empty_cache()
     # sparse-MLP roofline: further steps, each token's block of calls
     # bracketed by events (staging of the token finished before the block)
     _, mlp_us = timed_steps(pipe, t1, args.mlp_steps)
@@ -272,16 +383,17 @@ def main():
     bytes_launch = mlp_bytes_per_launch(cfg)
     traffic, traffic_detail = mlp_traffic(cfg)
     achieved = bytes_launch / (mlp_us * 1e-6) / 1e9
-    counts = delta_stats(pipe)
-    # per-phase breakdown (no overlap) and persistence statistics
+    # per-phase breakdown (no overlap) and delta statistics over its tokens
     t1 += args.mlp_steps
-    bd = breakdown(pipe, t1, args.breakdown_steps)
+    bd, per_tok = breakdown(pipe, t1, max(1, args.breakdown_steps))
     log(f"[bench] breakdown us: {bd}")
-    n_in = counts[:, 0].astype(np.float64)
+    n_in = np.mean([c[:, 0].sum() for c in per_tok])
+    n_hit = np.mean([c[:, 1].sum() for c in per_tok])
     rec = cfg.record_bytes
-    stats = {"incoming_rows_per_token": int(n_in.sum()),
-             "staged_MB_per_token": round(float(n_in.sum()) * rec / 1e6, 2),
-             "reuse_pct": round(100.0 * float(counts[:, 1].sum()) / (cfg.k * cfg.layers), 2)}
+    stats = {"incoming_rows_per_token": round(float(n_in), 1),
+             "staged_MB_per_token": round(float(n_in) * rec / 1e6, 2),
+             "reuse_pct": round(100.0 * float(n_hit) / (cfg.k * cfg.layers), 2),
+             "tokens": len(per_tok)}
     del pipe
     torch.cuda.empty_cache()
     # storage tier in pinned host memory: the PCIe-inclusive rate
@@ -304,6 +416,7 @@ def main():
         host = {"memcpy_staging_tok_s": round(args.host_tier_steps / hw, 2),
                 "mapped_gather_tok_s": round(args.host_tier_steps / gw, 2),
                 "note": "storage tier in pinned host memory; staging crosses the host link"}
+        host.update(staging_rates(hp, 4 + args.host_tier_steps, max(3, args.host_tier_steps // 4)))
         log(f"[bench] host tier: {host}")
         del hp, hg
     if args.calib_mib > 0:  # a copy of known size: reads and writes calib_mib MiB once
@@ -317,6 +430,12 @@ def main():
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(cfg, host_storage, args.cpu_seconds)
         log(f"[bench] cpu baseline: {cpu}")
+    extra = {}
+    for name in [n for n in args.extra_configs.split(",") if n]:
+        del host_storage
+        host_storage = None
+        extra[name] = extra_config(name, args.extra_steps, graph, bool(args.overlap))
+        log(f"[bench] {name}: {extra[name]}")
     line = {
         "metric": "sparse-MLP decode tokens/sec + achieved HBM GB/s (% peak), 7B-shaped, batch 1",
         "value": round(1e3 / ms_per_step, 2),
@@ -342,13 +461,14 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "traffic_detail": traffic_detail,
                      "bytes_per_launch": bytes_launch, "avg_launch_us": round(mlp_us, 3)},
-        "eager_tok_s": round(1e3 / eager_ms, 2) if eager_ms else None,
+        ("eager_tok_s" if graph else "graph_tok_s"): round(1e3 / other_ms, 2),
         "sparse_mlp_tok_s": round(1e6 / (mlp_us * cfg.layers), 1),
         "cold_start_ms": round(cold_ms, 2),
         "breakdown_us": bd,
         "delta": stats,
         "host_tier": host,
         "cpu_baseline": cpu,
+        "other_configs": extra or None,
     }
     print(json.dumps(line), flush=True)
 

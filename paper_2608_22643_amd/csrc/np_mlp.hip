@@ -55,9 +55,10 @@ struct MlpArgs {
 // v*V + 4q .. v*V + 4q + 3 of vector v = (p*CPL + c)*64 + lane, so each wave
 // store instruction writes 1 KiB of contiguous memory.  The reduction works
 // on chunks of 4 positions (64 bytes of every partial row): workgroup b takes
-// chunks b, b + n_wg, ...; thread t reads position t % 4 of partial rows
-// t/4, t/4 + nt/4, ...  FUSED_CH chunks and FUSED_RPT rows per thread at
-// most; the barrier's spin is bounded (polls of about 1 us each).
+// chunks b, b + n_wg, ... (at most FUSED_CH); for each, thread t reads
+// position t % 4 of partial rows t/4, t/4 + nt/4, ... (at most FUSED_RPT),
+// the per-thread sums meet in LDS and one thread per column adds them in
+// row order.  The barrier's spin is bounded (polls of about 1 us each).
 constexpr int FUSED_CH = 4;
 constexpr int FUSED_RPT = 4;
 constexpr uint32_t MLP_SPIN_LIMIT = 1u << 20;
@@ -70,11 +71,10 @@ __device__ inline void store_y1(void* y, int col, float v) {
 
 // Grid barrier, then the column reduction of this workgroup's chunks.  Every
 // thread of the workgroup calls it; thread 0 holds `gen0`, the generation
-// read at entry.
+// read at entry.  red: blockDim.x float4 of LDS.
 template <class T>
-__device__ inline void fused_reduce(const MlpArgs& a, int gen0) {
+__device__ inline void fused_reduce(const MlpArgs& a, int gen0, float4* red) {
   constexpr int V = T::V;
-  __shared__ float4 wsum[FUSED_CH][16][4];  // chunk, wave, position
   __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are complete
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -87,7 +87,6 @@ __device__ inline void fused_reduce(const MlpArgs& a, int gen0) {
     } else {
       uint32_t spins = 0;
       while (__hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gen0) {
-        __builtin_amdgcn_s_sleep(1);
         if (++spins == MLP_SPIN_LIMIT) {
           raise_error(a.ws, NP_DEVERR_SPIN_LIMIT);
           break;
@@ -99,55 +98,53 @@ __device__ inline void fused_reduce(const MlpArgs& a, int gen0) {
   const int d = a.NV * V, nchunks = d / 16;
   const int b = blockIdx.x, t = threadIdx.x, nt = blockDim.x;
   const int q = t & 3, rsub = t >> 2, rstep = nt >> 2;
+  const int rpt = (a.n_wg + rstep - 1) / rstep;  // partial rows per thread, uniform
   const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.partials, (uint32_t)a.n_wg * d * 4u);
-  float4 v[FUSED_CH][FUSED_RPT];
-#pragma unroll
-  for (int j = 0; j < FUSED_CH; ++j) {
-    const int chunk = b + j * a.n_wg;
+  for (int chunk = b, j = 0; chunk < nchunks && j < FUSED_CH; chunk += a.n_wg, ++j) {
+    float4 v[FUSED_RPT];
 #pragma unroll
     for (int m = 0; m < FUSED_RPT; ++m) {
       const int row = rsub + m * rstep;
-      const bool ok = chunk < nchunks && row < a.n_wg;
-      const uint32_t off = ok ? ((uint32_t)row * d + (uint32_t)(chunk * 4 + q) * 4u) * 4u : BUF_OOB;
-      v[j][m] = buf_load16_agent(prs, off);  // zeros out of range
+      const uint32_t off = (m < rpt && row < a.n_wg)
+                               ? ((uint32_t)row * d + (uint32_t)(chunk * 4 + q) * 4u) * 4u
+                               : BUF_OOB;
+      v[m] = m < rpt ? buf_load16_agent(prs, off) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-  }
-  const int lane = t & (WAVE - 1), w = t / WAVE;
-#pragma unroll
-  for (int j = 0; j < FUSED_CH; ++j) {
-    float4 s = v[j][0];
+    float4 s = v[0];
 #pragma unroll
     for (int m = 1; m < FUSED_RPT; ++m) {
-      s.x += v[j][m].x;
-      s.y += v[j][m].y;
-      s.z += v[j][m].z;
-      s.w += v[j][m].w;
+      s.x += v[m].x;
+      s.y += v[m].y;
+      s.z += v[m].z;
+      s.w += v[m].w;
     }
-    // lanes with the same position: a butterfly over the row bits of the lane
-#pragma unroll
-    for (int off = 32; off >= 4; off >>= 1) {
-      s.x += __shfl_xor(s.x, off, WAVE);
-      s.y += __shfl_xor(s.y, off, WAVE);
-      s.z += __shfl_xor(s.z, off, WAVE);
-      s.w += __shfl_xor(s.w, off, WAVE);
-    }
-    if (lane < 4) wsum[j][w][lane] = s;
-  }
-  __syncthreads();
-  if (t < FUSED_CH * 16) {  // one column of one chunk each: waves in order
-    const int j = t >> 4, pq = (t >> 2) & 3, comp = t & 3;
-    const int chunk = b + j * a.n_wg;
-    if (chunk < nchunks) {
+    red[t] = s;
+    __syncthreads();
+    if (t < WAVE) {  // lane = (quarter, column): each quarter sums a quarter of the row groups
+      const int col = t & 15, quarter = t >> 4, pq = col >> 2, comp = col & 3;
+      const float* redf = (const float*)red + 4 * pq + comp;
+      const int r0 = quarter * rstep / 4, r1 = (quarter + 1) * rstep / 4;
       float acc = 0.f;
-      for (int ww = 0; ww < nt / WAVE; ++ww) {
-        const float4 f = wsum[j][ww][pq];
-        acc += comp == 0 ? f.x : comp == 1 ? f.y : comp == 2 ? f.z : f.w;
+      int r = r0;
+      for (; r + 8 <= r1; r += 8) {  // eight reads in flight, added in row order
+        float f[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) f[i] = redf[16 * (r + i)];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc += f[i];
       }
-      const int pos = chunk * 4 + pq;
-      const int tt = pos / WAVE, vq = tt % (V / 4);
-      const int vec = (tt / (V / 4)) * WAVE + pos % WAVE;
-      store_y1<T>(a.y, vec * V + 4 * vq + comp, acc);
+      for (; r < r1; ++r) acc += redf[16 * r];
+      // quarters in order: lane col gets q0 + q1 + q2 + q3
+      const float a1 = __shfl(acc, col + 16, WAVE), a2 = __shfl(acc, col + 32, WAVE),
+                  a3 = __shfl(acc, col + 48, WAVE);
+      if (quarter == 0) {
+        const int pos = chunk * 4 + pq;
+        const int tt = pos / WAVE, vq = tt % (V / 4);
+        const int vec = (tt / (V / 4)) * WAVE + pos % WAVE;
+        store_y1<T>(a.y, vec * V + 4 * vq + comp, ((acc + a1) + a2) + a3);
+      }
     }
+    __syncthreads();  // red is reused by the next chunk
   }
 }
 
@@ -347,7 +344,7 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
         }
     }
   }
-  if constexpr (FUSED) fused_reduce<T>(a, gen0);
+  if constexpr (FUSED) fused_reduce<T>(a, gen0, (float4*)team_part + (size_t)(teams - 1) * a.NV * V / 4);
 }
 
 template <class T>
@@ -440,16 +437,16 @@ static int coresident(const void* kernel, int threads, size_t lds) {
 }
 
 template <class T, int CPL, int R, int MAXT>
-static void launch_rows_t(const MlpArgs& a, size_t lds, bool want_fused, bool* fused,
-                          hipStream_t stream) {
+static void launch_rows_t(const MlpArgs& a, size_t lds, size_t lds_fused, bool want_fused,
+                          bool* fused, hipStream_t stream) {
   const int threads = a.teams * a.P * WAVE;
   *fused = false;
   if (want_fused) {
     const void* k = (const void*)sparse_mlp_rows_kernel<T, CPL, R, MAXT, true>;
-    if (a.n_wg <= coresident(k, threads, lds)) {
+    if (a.n_wg <= coresident(k, threads, lds_fused)) {
       *fused = true;
       hipLaunchKernelGGL((sparse_mlp_rows_kernel<T, CPL, R, MAXT, true>), dim3(a.n_wg),
-                         dim3(threads), lds, stream, a);
+                         dim3(threads), lds_fused, stream, a);
       return;
     }
   }
@@ -458,13 +455,13 @@ static void launch_rows_t(const MlpArgs& a, size_t lds, bool want_fused, bool* f
 }
 
 template <class T, int CPL, int R>
-static void launch_rows(const MlpArgs& a, size_t lds, bool want_fused, bool* fused,
-                        hipStream_t stream) {
+static void launch_rows(const MlpArgs& a, size_t lds, size_t lds_fused, bool want_fused,
+                        bool* fused, hipStream_t stream) {
   const int threads = a.teams * a.P * WAVE;
   if (threads <= 512) {  // up to 8 waves: a register budget of 256 per lane
-    launch_rows_t<T, CPL, R, 512>(a, lds, want_fused, fused, stream);
+    launch_rows_t<T, CPL, R, 512>(a, lds, lds_fused, want_fused, fused, stream);
   } else if constexpr (R <= 4) {  // 128 registers per lane: at most 4 rows a round
-    launch_rows_t<T, CPL, R, 1024>(a, lds, want_fused, fused, stream);
+    launch_rows_t<T, CPL, R, 1024>(a, lds, lds_fused, want_fused, fused, stream);
   }
 }
 
@@ -509,6 +506,8 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   a.ws = ws;
   a.y = y;
   const size_t lds = (size_t)(teams - 1) * a.NV * V * sizeof(float);
+  // the single-kernel reduction adds one float4 per thread of LDS
+  const size_t lds_fused = lds + (size_t)teams * a.P * WAVE * sizeof(float4);
   // single kernel while the reduction layout holds: whole wave slices (every
   // lane owns a vector), at least a wave of partial rows, at most FUSED_RPT
   // rows and FUSED_CH chunks per thread (a co-resident grid is checked at
@@ -520,11 +519,11 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
                           nchunks <= FUSED_CH * n_wg && threads / WAVE <= 16;
   bool fused = false;
   if (cpl == 1) {
-    if (R == 4) launch_rows<T, 1, 4>(a, lds, want_fused, &fused, stream);
-    else if (R == 2) launch_rows<T, 1, 2>(a, lds, want_fused, &fused, stream);
-    else launch_rows<T, 1, 8>(a, lds, want_fused, &fused, stream);
+    if (R == 4) launch_rows<T, 1, 4>(a, lds, lds_fused, want_fused, &fused, stream);
+    else if (R == 2) launch_rows<T, 1, 2>(a, lds, lds_fused, want_fused, &fused, stream);
+    else launch_rows<T, 1, 8>(a, lds, lds_fused, want_fused, &fused, stream);
   } else {
-    launch_rows<T, 2, 2>(a, lds, want_fused, &fused, stream);
+    launch_rows<T, 2, 2>(a, lds, lds_fused, want_fused, &fused, stream);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || fused) return e;

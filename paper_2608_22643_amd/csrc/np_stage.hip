@@ -30,32 +30,53 @@ __device__ inline void copy_record(uint4* __restrict__ dst, const uint4* __restr
 
 // Gather: the plan is np_delta's device output.  Records of layers
 // [lb, le) are numbered layer by layer; workgroup b copies records
-// b, b + gridDim.x, ...  Entries outside [0, F) x [0, C) raise
-// NP_DEVERR_NOT_RESIDENT and are skipped.
+// b, b + gridDim.x, ...  The layers' counts are read in one round (thread t:
+// layer lb + t, STAGE_NT layers at a time) and a prefix sum in LDS places
+// each record.  Entries outside [0, F) x [0, C) raise NP_DEVERR_NOT_RESIDENT
+// and are skipped.
 __global__ __launch_bounds__(STAGE_NT) void stage_gather_kernel(
     const int32_t* __restrict__ counts, const int32_t* __restrict__ in_ids,
     const int32_t* __restrict__ in_slots, int k, int F, int C, int lb, int le,
     const uint4* __restrict__ storage, uint4* __restrict__ resident, int rec_vecs, void* ws) {
-  const int G = gridDim.x, bid = blockIdx.x;
-  int base = 0;
-  for (int l = lb; l < le; ++l) {
-    int n = counts[(size_t)l * 4];
-    if (n < 0 || n > k) {  // not a count np_delta can produce
-      if (threadIdx.x == 0 && bid == 0) raise_error(ws, NP_DEVERR_STATE);
-      n = n < 0 ? 0 : k;
+  __shared__ int pre[STAGE_NT + 1];  // records before layer base + i
+  __shared__ uint32_t scan[STAGE_NT / WAVE + 1];
+  const int G = gridDim.x, bid = blockIdx.x, tid = threadIdx.x;
+  int done = 0;  // records of the layers before this block of layers
+  for (int base = lb; base < le; base += STAGE_NT) {
+    const int l = base + tid;
+    int n = 0;
+    if (l < le) {
+      n = counts[(size_t)l * 4];
+      if (n < 0 || n > k) {  // not a count np_delta can produce
+        raise_error(ws, NP_DEVERR_STATE);
+        n = n < 0 ? 0 : k;
+      }
     }
-    int j = ((bid - base) % G + G) % G;
-    for (; j < n; j += G) {
-      const int id = in_ids[(size_t)l * k + j];
-      const int slot = in_slots[(size_t)l * k + j];
+    uint32_t tot;
+    const uint32_t before = block_excl_scan<STAGE_NT>((uint32_t)n, scan, &tot);
+    pre[tid] = (int)before;
+    if (tid == 0) pre[STAGE_NT] = (int)tot;
+    __syncthreads();
+    const int nl = le - base < STAGE_NT ? le - base : STAGE_NT;
+    for (int r = ((bid - done) % G + G) % G; r < (int)tot; r += G) {
+      int lo = 0, hi = nl - 1;  // the layer i with pre[i] <= r < pre[i + 1]
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (pre[mid] <= r) lo = mid;
+        else hi = mid - 1;
+      }
+      const int ll = base + lo, j = r - pre[lo];
+      const int id = in_ids[(size_t)ll * k + j];
+      const int slot = in_slots[(size_t)ll * k + j];
       if (id < 0 || id >= F || slot < 0 || slot >= C) {
-        if (threadIdx.x == 0) raise_error(ws, NP_DEVERR_NOT_RESIDENT);
+        if (tid == 0) raise_error(ws, NP_DEVERR_NOT_RESIDENT);
         continue;
       }
-      copy_record(resident + ((size_t)l * C + slot) * rec_vecs,
-                  storage + ((size_t)l * F + id) * rec_vecs, rec_vecs);
+      copy_record(resident + ((size_t)ll * C + slot) * rec_vecs,
+                  storage + ((size_t)ll * F + id) * rec_vecs, rec_vecs);
     }
-    base += n;
+    done += (int)tot;
+    __syncthreads();  // pre is rewritten by the next block of layers
   }
 }
 

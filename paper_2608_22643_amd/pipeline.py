@@ -16,22 +16,26 @@ Staging modes:
             each chunk goes over with hipMemcpyAsync on a side stream, then a
             scatter kernel places the records.  Needs the "host" tier.
 
-With overlap=True staging runs on a side stream in a few layer chunks
-(layer 0, layers 1-2, the rest), each followed by an event, and layer l's MLP
-waits only for the chunk holding layer l: staging later layers overlaps the
-MLP of earlier ones with three staging launches per token, not one per layer.  The side stream waits for np_delta of the same token,
+With overlap=True staging runs in a few layer chunks (layer 0, layers 1-2,
+the rest): the first on the main stream right after np_delta, the others on a
+side stream, each followed by an event, and layer l's MLP waits only for the
+chunk holding layer l: staging later layers overlaps the MLP of earlier ones
+with three staging launches per token, not one per layer.  The side stream waits for np_delta of the same token,
 which itself follows the previous token's MLP on the main stream, so a victim
 slot is never overwritten while the previous token still reads it.
 
 Graph mode (capture_graph / step_graph): one decode step is captured once as
 a HIP graph and replayed per token.  The step then has no per-token argument:
-h_t is copied into a fixed input buffer before each replay and np_delta takes
-the token index from the workspace step counter (NP_TOKEN_AUTO), which
+the graph's first nodes copy h_t into a fixed input buffer, t taken from a
+device-side row index that its last node advances, and np_delta takes the
+token index from the workspace step counter (NP_TOKEN_AUTO), which
 np_state_reset sets to 0, so graph tokens must start at a cold start (t = 0)
 and run in order.  Only "gather" staging can be captured (np_stage_rows waits
 on the host for the plan).
 """
 from __future__ import annotations
+
+import time
 
 import numpy as np
 import torch
@@ -127,6 +131,9 @@ class DecodePipeline:
                 e.record(self.side)
             self.ev_delta.record(self.main)
             torch.cuda.synchronize()
+        # memcpy staging: when a list, each step appends (bytes staged, seconds
+        # from the call to the end of its copies) and waits for the staging
+        self.stage_log = None
         self.reset()
 
     # ------------------------------------------------------------------
@@ -150,17 +157,23 @@ class DecodePipeline:
         from a fixed buffer) as a HIP graph.  Nothing runs until replay."""
         if self.staging != "gather":
             raise ValueError("only gather staging can be captured in a graph")
-        self.x_static = torch.empty(self.row_bytes, dtype=torch.uint8, device=self.device)
+        self.x_static = torch.empty((1, self.row_bytes), dtype=torch.uint8, device=self.device)
+        self.x_row = torch.zeros(1, dtype=torch.int64, device=self.device)  # next token's row of h
+        self.graph_t = 0
         self.graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(self.graph, stream=self.main, capture_error_mode="thread_local"):
+            torch.index_select(self.h, 0, self.x_row, out=self.x_static)
             self._enqueue(B.NP_TOKEN_AUTO, self.x_static.data_ptr(), None)
+            self.x_row.add_(1)
 
     def step_graph(self, t: int) -> None:
         """Replay the captured step for token t (tokens 0, 1, 2, ... in order
         after a cold start)."""
+        if t != self.graph_t:
+            raise ValueError(f"graph tokens run in order from 0: expected {self.graph_t}, got {t}")
         with torch.cuda.stream(self.main):
-            self.x_static.copy_(self.h[t], non_blocking=True)
             self.graph.replay()
+        self.graph_t += 1
 
     def _enqueue(self, token: int, x_ptr: int, mlp_block_events) -> None:
         s, cfg = self.shape, self.cfg
@@ -172,10 +185,14 @@ class DecodePipeline:
         ready = None  # ready[l]: the event layer l's MLP waits for
         if self.staging == "gather":
             if self.overlap:
+                # the first chunk on the main stream (the first MLP follows it
+                # in stream order), the others on the side stream
+                lb0, le0 = self.chunks[0]
+                B.np_stage_gather(s, self.out, lb0, le0, self.storage, self.resident, self.ws, main)
                 self.ev_delta.record(main)
                 self.side.wait_event(self.ev_delta)
                 ready = [None] * L
-                for lb, le in self.chunks:
+                for lb, le in self.chunks[1:]:
                     B.np_stage_gather(s, self.out, lb, le, self.storage, self.resident,
                                       self.ws, self.side)
                     self.layer_ready[lb].record(self.side)
@@ -189,10 +206,15 @@ class DecodePipeline:
                 self.plan_slots.copy_(self.lists["in_slots"], non_blocking=True)
             self.ev_plan.record(main)
             self.ev_plan.synchronize()  # the host reads the plan
+            t0 = time.perf_counter()
             B.np_stage_rows(s, self.plan, 0, L, self.storage, self.resident, self.staging_buf,
                             self.staging_buf.numel(), self.landing, self.landing.numel(),
                             self.side, self.ev_plan if self.overlap else None,
                             self.layer_ready)
+            if self.stage_log is not None:  # staging alone: host packing + copies + scatter
+                self.side.synchronize()
+                n_rec = int(self.plan_counts.view(L, 4)[:, 0].sum())
+                self.stage_log.append((n_rec * cfg.record_bytes, time.perf_counter() - t0))
             if self.overlap:
                 ready = self.layer_ready
         slots = self.lists["active_slots"]
