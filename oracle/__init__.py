@@ -65,7 +65,11 @@ def lib():
         L.orc_stage.argtypes = [i32] * 6 + [vp] * 5
         L.orc_sparse_mlp.argtypes = [i32] * 5 + [vp, vp, vp, i32, vp, vp]
         L.orc_dense_mlp.argtypes = [i32] * 5 + [vp, vp, vp, vp]
-        for f in ("orc_predict", "orc_select", "orc_delta", "orc_sparse_mlp", "orc_dense_mlp"):
+        L.orc_delta_n.argtypes = [i32, i32, i32, i32, ctypes.c_int32] + [vp] * 12
+        L.orc_centroid_logits.argtypes = [i32] * 5 + [vp, vp, vp]
+        L.orc_centroid_active.argtypes = [i32] * 4 + [vp] * 6
+        for f in ("orc_predict", "orc_select", "orc_delta", "orc_sparse_mlp", "orc_dense_mlp",
+                  "orc_delta_n", "orc_centroid_logits", "orc_centroid_active"):
             getattr(L, f).restype = i32
         L.orc_stage.restype = None
         _lib = L
@@ -161,6 +165,59 @@ def delta(token: int, active_ids: np.ndarray, state: State, C: int) -> dict:
                          _ptr(out["counts"]))
     if rc:
         raise OracleError(f"orc_delta precondition failed ({rc})")
+    return out
+
+
+def delta_n(token: int, active_ids: np.ndarray, active_counts, state: State, C: int) -> dict:
+    """O3 with per-layer active counts (the first active_counts[l] entries of
+    row l of active_ids); otherwise as delta()."""
+    active_ids = np.ascontiguousarray(active_ids, dtype=np.int32)
+    active_counts = np.ascontiguousarray(active_counts, dtype=np.int32)
+    L, k = active_ids.shape
+    assert active_counts.shape == (L,)
+    F = state.slot_of.shape[1]
+    out = {n: np.full((L, k), -1, dtype=np.int32)
+           for n in ("in_ids", "in_slots", "ev_ids", "ev_slots", "hit_ids", "active_slots")}
+    out["counts"] = np.zeros((L, 4), dtype=np.int32)
+    rc = lib().orc_delta_n(L, F, C, k, int(token), _ptr(active_ids), _ptr(active_counts),
+                           _ptr(state.slot_of), _ptr(state.neuron_of), _ptr(state.last_used),
+                           _ptr(out["in_ids"]), _ptr(out["in_slots"]), _ptr(out["ev_ids"]),
+                           _ptr(out["ev_slots"]), _ptr(out["hit_ids"]), _ptr(out["active_slots"]),
+                           _ptr(out["counts"]))
+    if rc:
+        raise OracleError(f"orc_delta_n precondition failed ({rc})")
+    return out
+
+
+def centroid_logits(heads, feat, H: int, K: int, D: int, wdtype: str, adtype: str) -> np.ndarray:
+    """O7: logits [H][K] float32 of the centroid heads ([H][K][D] storage bits)
+    on the feature vector ([D] storage bits)."""
+    heads, feat = np.ascontiguousarray(heads), np.ascontiguousarray(feat)
+    assert heads.size == H * K * D and feat.size == D
+    out = np.empty((H, K), dtype=np.float32)
+    rc = lib().orc_centroid_logits(H, K, D, DTYPES[wdtype], DTYPES[adtype], _ptr(heads),
+                                   _ptr(feat), _ptr(out))
+    if rc:
+        raise OracleError(f"orc_centroid_logits failed ({rc})")
+    return out
+
+
+def centroid_active(logits: np.ndarray, bank: np.ndarray, L: int, F: int, K: int, k: int) -> dict:
+    """O8: centroid ids [2][L'], intersection mask [L'][W], active_ids [L'][k]
+    (-1 beyond the count), counts [L'], overflow (a layer had more than k)."""
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    bank = np.ascontiguousarray(bank, dtype=np.uint32)
+    W = (F + 31) // 32
+    assert logits.shape == (2 * L, K) and bank.size == 2 * L * K * W
+    out = {"cids": np.empty((2, L), dtype=np.int32), "mask": np.empty((L, W), dtype=np.uint32),
+           "active_ids": np.full((L, k), -1, dtype=np.int32), "counts": np.empty(L, dtype=np.int32)}
+    rc = lib().orc_centroid_active(L, F, K, k, _ptr(logits), _ptr(bank), _ptr(out["cids"]),
+                                   _ptr(out["mask"]), _ptr(out["active_ids"]), _ptr(out["counts"]))
+    if rc == 1:
+        raise OracleError("orc_centroid_active: NaN logit")
+    if rc not in (0, 3):
+        raise OracleError(f"orc_centroid_active failed ({rc})")
+    out["overflow"] = rc == 3
     return out
 
 

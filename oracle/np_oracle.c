@@ -260,11 +260,14 @@ static int by_lastused_then_id(const void* pa, const void* pb) {
   return a < b ? -1 : (a > b ? 1 : 0);
 }
 
-int orc_delta(int L, int F, int C, int k, int32_t t, const int32_t* active_ids,
-              int32_t* slot_of, int32_t* neuron_of, int32_t* last_used,
-              int32_t* in_ids, int32_t* in_slots, int32_t* ev_ids,
-              int32_t* ev_slots, int32_t* hit_ids, int32_t* active_slots,
-              int32_t* counts) {
+/* active_counts: NULL for k active neurons per layer, else n_l <= k of them
+ * (active_ids[l][0..n_l) ascending) -- the variable-size sets of the
+ * centroid predictor (Sec. 3.4: the intersection of two masks). */
+static int orc_delta_impl(int L, int F, int C, int k, int32_t t, const int32_t* active_ids,
+                          const int32_t* active_counts, int32_t* slot_of, int32_t* neuron_of,
+                          int32_t* last_used, int32_t* in_ids, int32_t* in_slots,
+                          int32_t* ev_ids, int32_t* ev_slots, int32_t* hit_ids,
+                          int32_t* active_slots, int32_t* counts) {
   if (k > C) return 2;
   char* in_a = (char*)malloc((size_t)F);
   int32_t* fr = (int32_t*)malloc(sizeof(int32_t) * (size_t)C);
@@ -286,9 +289,11 @@ int orc_delta(int L, int F, int C, int k, int32_t t, const int32_t* active_ids,
     int32_t* VS = ev_slots + (size_t)l * k;
     int32_t* H = hit_ids + (size_t)l * k;
     int32_t* AS = active_slots + (size_t)l * k;
+    const int na = active_counts ? active_counts[l] : k;
 
     /* preconditions */
-    for (int j = 0; j < k; ++j) {
+    if (na < 0 || na > k) rc = 2;
+    for (int j = 0; j < na && rc == 0; ++j) {
       if (A[j] < 0 || A[j] >= F || (j > 0 && A[j] <= A[j - 1])) rc = 2;
     }
     for (int n = 0; n < F && rc == 0; ++n)
@@ -298,10 +303,10 @@ int orc_delta(int L, int F, int C, int k, int32_t t, const int32_t* active_ids,
     if (rc) break;
 
     memset(in_a, 0, (size_t)F);
-    for (int j = 0; j < k; ++j) in_a[A[j]] = 1;
+    for (int j = 0; j < na; ++j) in_a[A[j]] = 1;
 
     int nh = 0, ni = 0;
-    for (int j = 0; j < k; ++j) {
+    for (int j = 0; j < na; ++j) {
       if (P[A[j]] >= 0) H[nh++] = A[j];
       else I[ni++] = A[j];
     }
@@ -335,8 +340,8 @@ int orc_delta(int L, int F, int C, int k, int32_t t, const int32_t* active_ids,
       P[I[j]] = pool[j];
       Q[pool[j]] = I[j];
     }
-    for (int j = 0; j < k; ++j) U[A[j]] = t;
-    for (int j = 0; j < k; ++j) AS[j] = P[A[j]];
+    for (int j = 0; j < na; ++j) U[A[j]] = t;
+    for (int j = 0; j < na; ++j) AS[j] = P[A[j]];
     int32_t* cnt = counts + (size_t)l * 4;
     cnt[0] = ni;
     cnt[1] = nh;
@@ -348,6 +353,23 @@ int orc_delta(int L, int F, int C, int k, int32_t t, const int32_t* active_ids,
   free(cand);
   free(pool);
   return rc;
+}
+
+int orc_delta(int L, int F, int C, int k, int32_t t, const int32_t* active_ids,
+              int32_t* slot_of, int32_t* neuron_of, int32_t* last_used,
+              int32_t* in_ids, int32_t* in_slots, int32_t* ev_ids,
+              int32_t* ev_slots, int32_t* hit_ids, int32_t* active_slots,
+              int32_t* counts) {
+  return orc_delta_impl(L, F, C, k, t, active_ids, NULL, slot_of, neuron_of, last_used, in_ids,
+                        in_slots, ev_ids, ev_slots, hit_ids, active_slots, counts);
+}
+
+int orc_delta_n(int L, int F, int C, int k, int32_t t, const int32_t* active_ids,
+                const int32_t* active_counts, int32_t* slot_of, int32_t* neuron_of,
+                int32_t* last_used, int32_t* in_ids, int32_t* in_slots, int32_t* ev_ids,
+                int32_t* ev_slots, int32_t* hit_ids, int32_t* active_slots, int32_t* counts) {
+  return orc_delta_impl(L, F, C, k, t, active_ids, active_counts, slot_of, neuron_of, last_used,
+                        in_ids, in_slots, ev_ids, ev_slots, hit_ids, active_slots, counts);
 }
 
 /* ---------------- O4: staging -------------------------------------------- */
@@ -444,4 +466,69 @@ int orc_dense_mlp(int F, int d, int wdtype, int adtype, int layer,
   }
   free(xv); free(gv); free(uv); free(yv);
   return 0;
+}
+
+/* ---------------- O7: centroid-ID heads ---------------------------------- */
+/* Sec. 3.3 (architecture, third stage): two groups of L' linear heads map the
+ * predictor's feature vector to gate and up logits over K centroids.  Head h
+ * (0..H-1; gate heads of layers 0..L'-1, then up heads) is a K x D matrix:
+ * logits[h][c] = heads[h][c] . feat, summed in double, rounded to binary32. */
+int orc_centroid_logits(int H, int K, int D, int wdtype, int adtype, const void* heads,
+                        const void* feat, float* logits) {
+  double* f = (double*)malloc(sizeof(double) * (size_t)D);
+  if (!f) return -1;
+  for (int i = 0; i < D; ++i) f[i] = orc_load(adtype, feat, (size_t)i);
+  for (int64_t row = 0; row < (int64_t)H * K; ++row) {
+    double acc = 0.0;
+    for (int i = 0; i < D; ++i) acc += orc_load(wdtype, heads, (size_t)row * D + i) * f[i];
+    logits[row] = (float)orc_round_to(ORC_F32, acc);
+  }
+  free(f);
+  return 0;
+}
+
+/* ---------------- O8: centroid choice and the intersected active set ----- */
+/* Sec. 3.3: each head selects its highest-scoring centroid (a tie goes to the
+ * smaller index).  Sec. 3.4: the active set of layer l is the intersection of
+ * the chosen gate and up centroid masks.  bank [2][L'][K][W] holds the masks
+ * (W = ceil(F/32) words, bit n%32 of word n/32), gate masks first.  Outputs:
+ * cids [2][L'] (gate ids, then up ids), mask [L'][W] (the intersection),
+ * active_ids [L'][k] ascending, counts [L'].  The list of a layer holds at
+ * most k ids (its buffer capacity): a larger intersection keeps its k
+ * smallest ids, its mask keeps every member, and the function returns 3.
+ * A NaN logit returns 1 (nothing else is checked for it). */
+int orc_centroid_active(int L, int F, int K, int k, const float* logits, const uint32_t* bank,
+                        int32_t* cids, uint32_t* mask, int32_t* active_ids, int32_t* counts) {
+  const int W = (F + 31) / 32;
+  int rc = 0;
+  for (int h = 0; h < 2 * L; ++h) {
+    const float* lg = logits + (size_t)h * K;
+    int best = 0;
+    for (int c = 0; c < K; ++c) {
+      if (isnan(lg[c])) return 1;
+      if (lg[c] > lg[best]) best = c;  /* strict: the first maximum wins */
+    }
+    cids[h] = best;
+  }
+  for (int l = 0; l < L; ++l) {
+    const uint32_t* g = bank + ((size_t)l * K + cids[l]) * W;
+    const uint32_t* u = bank + (((size_t)L + l) * K + cids[L + l]) * W;
+    int n = 0;
+    for (int w = 0; w < W; ++w) {
+      uint32_t m = g[w] & u[w];
+      if (w == W - 1 && (F & 31)) m &= (1u << (F & 31)) - 1u;
+      mask[(size_t)l * W + w] = m;
+      for (int b = 0; b < 32; ++b) {
+        if (!((m >> b) & 1u)) continue;
+        if (n < k) active_ids[(size_t)l * k + n] = 32 * w + b;
+        ++n;
+      }
+    }
+    if (n > k) {
+      rc = 3;
+      n = k;
+    }
+    counts[l] = n;
+  }
+  return rc;
 }

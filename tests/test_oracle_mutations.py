@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "np_oracle.c")
 PINS = ["tests/test_oracle_encoding.py", "tests/test_oracle_predict.py",
         "tests/test_oracle_select.py", "tests/test_oracle_delta.py",
-        "tests/test_oracle_mlp.py"]
+        "tests/test_oracle_mlp.py", "tests/test_oracle_centroid.py"]
 
 MUTATIONS = {
     # predictor: transposed / shifted A operand
@@ -36,7 +36,7 @@ MUTATIONS = {
         ("qsort(pool, (size_t)npool, sizeof(int32_t), by_int_asc);", ""),
     # delta: last_used not refreshed for hits
     "delta_lastused_only_incoming":
-        ("for (int j = 0; j < k; ++j) U[A[j]] = t;", "for (int j = 0; j < ni; ++j) U[I[j]] = t;"),
+        ("for (int j = 0; j < na; ++j) U[A[j]] = t;", "for (int j = 0; j < ni; ++j) U[I[j]] = t;"),
     # MLP: ReLU dropped, wrong row for down^T
     "mlp_no_relu":
         ("double a = (g > 0.0 ? g : 0.0) * u;", "double a = g * u;"),
@@ -44,6 +44,15 @@ MUTATIONS = {
         ("acc[c] += a * orc_load(wdtype, storage, base + 2 * (size_t)d + c);",
          "acc[c] += a * orc_load(wdtype, storage, base + (size_t)d + c);"),
     # rounding: ties away from zero
+    # centroid predictor: tie to the last maximum, union instead of intersection
+    "centroid_tie_to_last":
+        ("if (lg[c] > lg[best]) best = c;", "if (lg[c] >= lg[best]) best = c;"),
+    "centroid_union":
+        ("uint32_t m = g[w] & u[w];", "uint32_t m = g[w] | u[w];"),
+    # off by one in the active-slot list of a variable-size set
+    "delta_active_slots_off_by_one":
+        ("for (int j = 0; j < na; ++j) AS[j] = P[A[j]];",
+         "for (int j = 0; j + 1 < na; ++j) AS[j] = P[A[j]];"),
     "round_ties_away":
         ("if (frac > 0.5 || (frac == 0.5 && fmod(lo, 2.0) != 0.0)) r = lo + 1.0;",
          "if (frac >= 0.5) r = lo + 1.0;"),
