@@ -13,6 +13,13 @@
  *   np_stage_rows  incoming neuron records, storage tier -> their device slots
  *   np_sparse_mlp  ReLU-gated MLP over the resident active rows of one layer
  *
+ * and, for the paper's own predictor (centroid IDs, variable-size sets):
+ *
+ *   np_centroid_select  centroid heads -> gate/up centroid ids -> the
+ *                       intersected active set of every layer (Sec. 3.3-3.4)
+ *   np_delta_n, np_sparse_mlp_n   np_delta / np_sparse_mlp with per-layer
+ *                       active counts read on the device
+ *
  * Conventions shared by every call
  * --------------------------------
  *  - extern "C"; plain pointers and sizes only.  All memory is owned by the
@@ -76,6 +83,7 @@ typedef enum np_dtype { NP_F32 = 0, NP_F16 = 1, NP_BF16 = 2 } np_dtype;
 #define NP_DEVERR_NOT_RESIDENT 0x2  /* a slot outside [0, C) or id outside [0, F) */
 #define NP_DEVERR_STATE        0x4  /* inconsistent state or plan (ids, slots, counts) */
 #define NP_DEVERR_SPIN_LIMIT   0x8  /* a bounded in-kernel wait gave up */
+#define NP_DEVERR_OVERFLOW     0x10 /* an active set larger than k was cut to k */
 
 typedef struct np_shape {
   int32_t layers;   /* L' */
@@ -111,6 +119,22 @@ typedef struct np_delta_out {
   int32_t* active_slots; /* slot of active_ids[j] after the update, k per layer */
   int32_t* counts;
 } np_delta_out;
+
+/* The centroid-ID predictor (Sec. 3.3, third stage, and Sec. 3.4): 2 L'
+ * linear heads over K centroids, gate heads of every downstream layer first,
+ * then up heads, and a bank of sparse binary centroid masks per layer and
+ * projection.  All device memory.
+ * heads [2][L'][K][D] of type w (row c of head h: the logit weights of
+ * centroid c); bank [2][L'][K][ceil(F/32)] uint32 (bit n%32 of word n/32 set
+ * when centroid c keeps neuron n; pad bits ignored).  Requirements:
+ * 1 <= K <= 4096; D a multiple of 8 (16-bit types) or 4 (fp32), D <= 16384
+ * (16-bit) or 8192 (fp32). */
+typedef struct np_centroid_model {
+  int32_t n_centroids; /* K */
+  int32_t feat_dim;    /* D */
+  const void* heads;
+  const uint32_t* bank;
+} np_centroid_model;
 
 /* Host copy of the parts of np_delta_out that staging needs ([L'][4] and
  * [L'][k] int32, any host memory; pinned makes the device->host copy async). */
@@ -248,6 +272,44 @@ np_status np_sparse_mlp(const np_shape* shape, int32_t layer, const void* x,
                         const void* dev_resident, const int32_t* active_slots,
                         int32_t n_active, void* y, void* dev_ws,
                         hipStream_t stream);
+
+/* Centroid-ID prediction and the intersected active sets (Sec. 3.3: each
+ * head selects its highest-scoring centroid; Sec. 3.4: the active set of a
+ * layer is the intersection of its gate and up centroid masks):
+ *   logits[h][c] = heads[h][c] . feat            (fp32, [2][L'][K])
+ *   centroid_ids[h] = argmax_c logits[h][c]      (ties: the smaller c; [2][L'])
+ *   mask[l] = bank[0][l][gate id] & bank[1][l][up id]   ([L'][ceil(F/32)])
+ *   active_ids[l] = members of mask[l] ascending ([L'][k]), active_counts[l]
+ * feat [D] of type a.  Lists hold at most k ids (the buffer capacity of a
+ * layer): a larger intersection keeps its k smallest ids (mask keeps every
+ * member) and sets NP_DEVERR_OVERFLOW; a NaN logit sets NP_DEVERR_NAN_SCORE
+ * and never wins.  Entries of active_ids past the count are not written.
+ * Two kernels on `stream`. */
+np_status np_centroid_select(const np_shape* shape, const np_centroid_model* model,
+                             const void* feat, float* logits, int32_t* centroid_ids,
+                             uint32_t* mask, int32_t* active_ids,
+                             int32_t* active_counts, void* dev_ws,
+                             hipStream_t stream);
+
+/* np_delta for active sets of variable size: layer l has active_counts[l]
+ * (device int32, 0..k) neurons, active_ids[l][0..count) ascending.  Every
+ * output and the state update follow np_delta with k replaced by the count;
+ * active_slots[l] is written for the first count entries only.  A count
+ * outside [0, k] sets NP_DEVERR_STATE and is clamped. */
+np_status np_delta_n(const np_shape* shape, int32_t token,
+                     const int32_t* active_ids, const int32_t* active_counts,
+                     const np_state* state, const np_delta_out* out,
+                     void* dev_ws, hipStream_t stream);
+
+/* np_sparse_mlp over the first active_counts[layer] entries of active_slots
+ * (active_counts: device int32 [L'], read on the device, so a count produced
+ * on the GPU needs no host round trip; active_slots and active_counts need
+ * 4-byte alignment only, so a layer's row of a [L'][k] list can be passed).
+ * A count outside [0, k] sets NP_DEVERR_STATE and is clamped. */
+np_status np_sparse_mlp_n(const np_shape* shape, int32_t layer, const void* x,
+                          const void* dev_resident, const int32_t* active_slots,
+                          const int32_t* active_counts, void* y, void* dev_ws,
+                          hipStream_t stream);
 
 /* Waits for `stream`, then returns the sticky device error word in *code
  * (0 = none; NP_DEVERR_* bits otherwise).  Synchronous. */

@@ -21,12 +21,14 @@ NP_DEVERR_NAN_SCORE = 0x1
 NP_DEVERR_NOT_RESIDENT = 0x2
 NP_DEVERR_STATE = 0x4
 NP_DEVERR_SPIN_LIMIT = 0x8
+NP_DEVERR_OVERFLOW = 0x10
 NP_TOKEN_AUTO = -1  # np_delta: token index from the workspace step counter
 
 # every symbol the header declares
 EXPORTS = ("np_status_str", "np_last_error", "np_shape_check", "np_workspace_size",
            "np_state_reset", "np_predict", "np_select", "np_delta", "np_stage_rows",
-           "np_stage_gather", "np_sparse_mlp", "np_device_error")
+           "np_stage_gather", "np_sparse_mlp", "np_centroid_select", "np_delta_n",
+           "np_sparse_mlp_n", "np_device_error")
 
 
 class NPError(RuntimeError):
@@ -50,6 +52,11 @@ class np_state(ctypes.Structure):
 class np_delta_out(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("in_ids", "in_slots", "ev_ids", "ev_slots", "hit_ids", "active_slots", "counts")]
+
+
+class np_centroid_model(ctypes.Structure):
+    _fields_ = [("n_centroids", ctypes.c_int32), ("feat_dim", ctypes.c_int32),
+                ("heads", ctypes.c_void_p), ("bank", ctypes.c_void_p)]
 
 
 class np_stage_plan(ctypes.Structure):
@@ -85,6 +92,11 @@ def lib():
         L.np_stage_gather.argtypes = [S, ctypes.POINTER(np_delta_out), i32, i32, vp, vp, vp, vp]
         L.np_sparse_mlp.argtypes = [S, i32, vp, vp, vp, i32, vp, vp, vp]
         L.np_device_error.argtypes = [vp, vp, ctypes.POINTER(i32)]
+        L.np_centroid_select.argtypes = [S, ctypes.POINTER(np_centroid_model), vp, vp, vp, vp,
+                                         vp, vp, vp, vp]
+        L.np_delta_n.argtypes = [S, i32, vp, vp, ctypes.POINTER(np_state),
+                                 ctypes.POINTER(np_delta_out), vp, vp]
+        L.np_sparse_mlp_n.argtypes = [S, i32, vp, vp, vp, vp, vp, vp, vp]
         for f in EXPORTS[2:]:
             getattr(L, f).restype = i32
         _lib = L
@@ -181,6 +193,27 @@ def np_sparse_mlp(shape, layer: int, x, dev_resident, active_slots, n_active: in
     _check(lib().np_sparse_mlp(ctypes.byref(shape), int(layer), _p(x), _p(dev_resident),
                                _p(active_slots), int(n_active), _p(y), _p(ws), _s(stream)),
            "np_sparse_mlp")
+
+
+def np_centroid_select(shape, model: np_centroid_model, feat, logits, centroid_ids, mask,
+                       active_ids, active_counts, ws, stream=None) -> None:
+    _check(lib().np_centroid_select(ctypes.byref(shape), ctypes.byref(model), _p(feat),
+                                    _p(logits), _p(centroid_ids), _p(mask), _p(active_ids),
+                                    _p(active_counts), _p(ws), _s(stream)), "np_centroid_select")
+
+
+def np_delta_n(shape, token: int, active_ids, active_counts, state: np_state, out: np_delta_out,
+               ws, stream=None) -> None:
+    _check(lib().np_delta_n(ctypes.byref(shape), int(token), _p(active_ids), _p(active_counts),
+                            ctypes.byref(state), ctypes.byref(out), _p(ws), _s(stream)),
+           "np_delta_n")
+
+
+def np_sparse_mlp_n(shape, layer: int, x, dev_resident, active_slots, active_counts, y, ws,
+                    stream=None) -> None:
+    _check(lib().np_sparse_mlp_n(ctypes.byref(shape), int(layer), _p(x), _p(dev_resident),
+                                 _p(active_slots), _p(active_counts), _p(y), _p(ws), _s(stream)),
+           "np_sparse_mlp_n")
 
 
 def np_device_error(ws, stream=None) -> int:

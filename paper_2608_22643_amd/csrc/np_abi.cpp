@@ -123,20 +123,60 @@ np_status np_select(const np_shape* s, const float* scores, uint32_t* mask, int3
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_select launch");
 }
 
-np_status np_delta(const np_shape* s, int32_t token, const int32_t* ids, const np_state* state,
-                   const np_delta_out* out, void* ws, hipStream_t stream) {
+static np_status delta_common(const char* fn, const np_shape* s, int32_t token,
+                              const int32_t* ids, const int32_t* counts, const np_state* state,
+                              const np_delta_out* out, void* ws, hipStream_t stream) {
   np_status st = check_shape(s);
   if (st != NP_OK) return st;
   if (token < NP_TOKEN_AUTO) return fail(NP_ERR_INVALID_ARG, "token %d < 0", token);
   if (!aligned16(ids) || !state || !aligned16(state->slot_of) || !aligned16(state->neuron_of) ||
       !aligned16(state->last_used) || !aligned16(ws))
-    return fail(NP_ERR_INVALID_ARG, "np_delta: pointers must be non-NULL and 16-byte aligned");
+    return fail(NP_ERR_INVALID_ARG, "%s: pointers must be non-NULL and 16-byte aligned", fn);
   if (!out || !aligned16(out->in_ids) || !aligned16(out->in_slots) || !aligned16(out->ev_ids) ||
       !aligned16(out->ev_slots) || !aligned16(out->hit_ids) || !aligned16(out->active_slots) ||
       !aligned16(out->counts))
-    return fail(NP_ERR_INVALID_ARG, "np_delta: output lists must be non-NULL and 16-byte aligned");
-  hipError_t e = launch_delta(*s, token, ids, *state, *out, ws, stream);
+    return fail(NP_ERR_INVALID_ARG, "%s: output lists must be non-NULL and 16-byte aligned", fn);
+  hipError_t e = launch_delta(*s, token, ids, *state, *out, ws, stream, counts);
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_delta launch");
+}
+
+np_status np_delta(const np_shape* s, int32_t token, const int32_t* ids, const np_state* state,
+                   const np_delta_out* out, void* ws, hipStream_t stream) {
+  return delta_common("np_delta", s, token, ids, nullptr, state, out, ws, stream);
+}
+
+np_status np_delta_n(const np_shape* s, int32_t token, const int32_t* ids, const int32_t* counts,
+                     const np_state* state, const np_delta_out* out, void* ws,
+                     hipStream_t stream) {
+  if (!aligned16(counts))
+    return fail(NP_ERR_INVALID_ARG, "np_delta_n: active_counts must be non-NULL and aligned");
+  return delta_common("np_delta_n", s, token, ids, counts, state, out, ws, stream);
+}
+
+np_status np_centroid_select(const np_shape* s, const np_centroid_model* m, const void* feat,
+                             float* logits, int32_t* cids, uint32_t* mask, int32_t* active_ids,
+                             int32_t* counts, void* ws, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (!m) return fail(NP_ERR_INVALID_ARG, "np_centroid_select: model is NULL");
+  if (m->n_centroids < 1 || m->n_centroids > 4096)
+    return fail(NP_ERR_INVALID_ARG, "n_centroids %d outside [1, 4096]", m->n_centroids);
+  const int V = vec_elems(s->wdtype);
+  const int dmax = s->wdtype == NP_F32 ? 8192 : 16384;
+  if (m->feat_dim < V || m->feat_dim % V || m->feat_dim > dmax)
+    return fail(NP_ERR_INVALID_ARG, "feat_dim %d: a multiple of %d in [%d, %d]", m->feat_dim, V,
+                V, dmax);
+  if ((size_t)2 * s->layers * m->n_centroids > (size_t)1 << 30)
+    return fail(NP_ERR_INVALID_ARG, "2 * layers * n_centroids too large");
+  if (!aligned16(m->heads) || !aligned16(m->bank) || !aligned16(feat) || !aligned16(logits) ||
+      !aligned16(cids) || !aligned16(mask) || !aligned16(active_ids) || !aligned16(counts) ||
+      !aligned16(ws))
+    return fail(NP_ERR_INVALID_ARG,
+                "np_centroid_select: pointers must be non-NULL and 16-byte aligned");
+  hipError_t e = launch_centroid_logits(*s, *m, feat, logits, stream);
+  if (e != hipSuccess) return hip_fail(e, "np_centroid_select heads launch");
+  e = launch_centroid_active(*s, *m, logits, cids, mask, active_ids, counts, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_centroid_select launch");
 }
 
 np_status np_stage_gather(const np_shape* s, const np_delta_out* out, int32_t lb, int32_t le,
@@ -179,6 +219,21 @@ np_status np_sparse_mlp(const np_shape* s, int32_t layer, const void* x, const v
     return fail(NP_ERR_INVALID_ARG, "np_sparse_mlp: pointers must be non-NULL and aligned");
   hipError_t e = launch_sparse_mlp(*s, layer, x, resident, slots, n_active, y, ws, stream);
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp launch");
+}
+
+np_status np_sparse_mlp_n(const np_shape* s, int32_t layer, const void* x, const void* resident,
+                          const int32_t* slots, const int32_t* counts, void* y, void* ws,
+                          hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (layer < 0 || layer >= s->layers)
+    return fail(NP_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, s->layers);
+  // slots and counts are read as single int32 values: 4-byte alignment
+  if (!aligned16(x) || !aligned16(resident) || !aligned16(y) || !aligned16(ws) || !slots ||
+      !counts || ((uintptr_t)slots & 3) || ((uintptr_t)counts & 3))
+    return fail(NP_ERR_INVALID_ARG, "np_sparse_mlp_n: pointers must be non-NULL and aligned");
+  hipError_t e = launch_sparse_mlp(*s, layer, x, resident, slots, s->k, y, ws, stream, counts);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp_n launch");
 }
 
 np_status np_device_error(const void* ws, hipStream_t stream, int32_t* code) {

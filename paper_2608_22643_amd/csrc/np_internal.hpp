@@ -48,17 +48,26 @@ hipError_t launch_predict(const np_shape& s, const void* h, const void* A, const
                           float* scores, void* ws, hipStream_t stream);
 hipError_t launch_select(const np_shape& s, const float* scores, uint32_t* mask,
                          int32_t* active_ids, void* ws, hipStream_t stream);
+// active_counts: nullptr for k active neurons per layer, else device [L'].
 hipError_t launch_delta(const np_shape& s, int32_t token, const int32_t* active_ids,
                         const np_state& st, const np_delta_out& out, void* ws,
-                        hipStream_t stream);
+                        hipStream_t stream, const int32_t* active_counts = nullptr);
+hipError_t launch_centroid_logits(const np_shape& s, const np_centroid_model& m,
+                                  const void* feat, float* logits, hipStream_t stream);
+hipError_t launch_centroid_active(const np_shape& s, const np_centroid_model& m,
+                                  const float* logits, int32_t* centroid_ids, uint32_t* mask,
+                                  int32_t* active_ids, int32_t* active_counts, void* ws,
+                                  hipStream_t stream);
 hipError_t launch_stage_gather(const np_shape& s, const np_delta_out& out, int layer_begin,
                                int layer_end, const void* storage, void* resident, void* ws,
                                hipStream_t stream);
 hipError_t launch_stage_scatter(const np_shape& s, const void* landing, int n_records,
                                 void* resident, hipStream_t stream);
+// n_dev: nullptr for n_active rows, else the row count is n_dev[layer]
+// (device), at most n_active.
 hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const void* resident,
                              const int32_t* active_slots, int n_active, void* y, void* ws,
-                             hipStream_t stream);
+                             hipStream_t stream, const int32_t* n_dev = nullptr);
 
 // host-side helpers shared by the ABI files (np_abi.cpp)
 np_status fail(np_status st, const char* fmt, ...);

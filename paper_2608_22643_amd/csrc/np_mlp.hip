@@ -48,6 +48,8 @@ struct MlpArgs {
   int n_active, C, NV, n_wg, P, PP, teams;  // PP: P rounded up to a power of two
   uint32_t layer_bytes;  // resident bytes of the layer (< 2^31)
   void* y;               // single-kernel path: the output
+  const int32_t* n_dev;  // nullptr, or the row count at n_dev[layer] (<= n_active)
+  int layer;
 };
 
 // Single-kernel path.  Partial rows are stored in "position" order: float4
@@ -164,9 +166,17 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   const int P = a.P, teams = a.teams;
   const int team = wid / P, p = wid % P;
   const int b = blockIdx.x;
+  int n_active = a.n_active;
+  if (a.n_dev) {  // a row count produced on the device (variable-size sets)
+    n_active = a.n_dev[a.layer];
+    if (n_active < 0 || n_active > a.n_active) {
+      if (threadIdx.x == 0 && b == 0) raise_error(a.ws, NP_DEVERR_STATE);
+      n_active = n_active < 0 ? 0 : a.n_active;
+    }
+  }
   // balanced contiguous ranges: workgroup b takes rows [b*n/G, (b+1)*n/G)
-  const int row_begin = (int)(((long long)b * a.n_active) / a.n_wg);
-  const int row_end = (int)(((long long)(b + 1) * a.n_active) / a.n_wg);
+  const int row_begin = (int)(((long long)b * n_active) / a.n_wg);
+  const int row_end = (int)(((long long)(b + 1) * n_active) / a.n_wg);
   const int v0 = p * WAVE * CPL;  // first vector of this wave's column slice
   int gen0 = 0;  // grid barrier generation at entry (thread 0)
   if (FUSED && threadIdx.x == 0)
@@ -468,7 +478,7 @@ static void launch_rows(const MlpArgs& a, size_t lds, size_t lds_fused, bool wan
 template <class T>
 static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void* resident,
                         const int32_t* active_slots, int n_active, void* y, void* ws,
-                        hipStream_t stream) {
+                        hipStream_t stream, const int32_t* n_dev) {
   constexpr int V = T::V;
   MlpArgs a;
   a.NV = s.d_model / V;
@@ -505,6 +515,8 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   a.partials = (float*)((char*)ws + ws_partials_offset(s));
   a.ws = ws;
   a.y = y;
+  a.n_dev = n_dev;
+  a.layer = layer;
   const size_t lds = (size_t)(teams - 1) * a.NV * V * sizeof(float);
   // the single-kernel reduction adds one float4 per thread of LDS
   const size_t lds_fused = lds + (size_t)teams * a.P * WAVE * sizeof(float4);
@@ -535,11 +547,14 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
 
 hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const void* resident,
                              const int32_t* active_slots, int n_active, void* y, void* ws,
-                             hipStream_t stream) {
+                             hipStream_t stream, const int32_t* n_dev) {
   switch (s.wdtype) {
-    case NP_F32: return mlp_t<TF32>(s, layer, x, resident, active_slots, n_active, y, ws, stream);
-    case NP_F16: return mlp_t<TF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream);
-    default: return mlp_t<TBF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream);
+    case NP_F32:
+      return mlp_t<TF32>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev);
+    case NP_F16:
+      return mlp_t<TF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev);
+    default:
+      return mlp_t<TBF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev);
   }
 }
 

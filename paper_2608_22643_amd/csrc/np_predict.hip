@@ -107,6 +107,27 @@ __global__ __launch_bounds__(256) void predict_scores_kernel(const uint4* __rest
   }
 }
 
+// Row dot products out[i] = A[i] . x over rows of nv 16-byte vectors (the
+// first stage of the predictor; also the centroid heads).
+template <class T>
+static hipError_t gemv_rows_t(const void* A, const void* x, float* out, int rows, int nv,
+                              hipStream_t stream) {
+  hipLaunchKernelGGL((predict_z_kernel<T, 8>), dim3((rows + 3) / 4), dim3(256), 0, stream,
+                     (const uint4*)A, (const uint4*)x, out, rows, nv);
+  return hipGetLastError();
+}
+
+hipError_t launch_centroid_logits(const np_shape& s, const np_centroid_model& m,
+                                  const void* feat, float* logits, hipStream_t stream) {
+  const int rows = 2 * s.layers * m.n_centroids;
+  const int nv = m.feat_dim / vec_elems(s.wdtype);
+  switch (s.wdtype) {
+    case NP_F32: return gemv_rows_t<TF32>(m.heads, feat, logits, rows, nv, stream);
+    case NP_F16: return gemv_rows_t<TF16>(m.heads, feat, logits, rows, nv, stream);
+    default: return gemv_rows_t<TBF16>(m.heads, feat, logits, rows, nv, stream);
+  }
+}
+
 template <class T>
 static hipError_t predict_t(const np_shape& s, const void* h, const void* A, const void* B,
                             float* scores, void* ws, hipStream_t stream) {

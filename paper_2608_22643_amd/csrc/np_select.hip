@@ -106,7 +106,8 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
                                                         int32_t* __restrict__ neuron_of,
                                                         int32_t* __restrict__ last_used,
                                                         np_delta_out out, int F, int C, int k,
-                                                        int spt, void* ws) {
+                                                        int spt, void* ws,
+                                                        const int32_t* __restrict__ counts) {
   __shared__ uint32_t amask[2048];  // active set, bit n of the layer
   __shared__ uint32_t smask[2048];  // slot pool: free slots, then victims' slots
   __shared__ uint32_t rmask[2048];  // resident rows (neurons held by some slot)
@@ -122,6 +123,16 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
   int32_t* U = last_used + (size_t)l * F;
   const int32_t* A = active_ids + (size_t)l * k;
   const size_t lo = (size_t)l * k;
+  // active neurons of this layer: k, or a device count in [0, k]
+  int na = k;
+  bool bad_count = false;
+  if (counts) {
+    na = counts[l];
+    if (na < 0 || na > k) {
+      bad_count = true;
+      na = na < 0 ? 0 : k;
+    }
+  }
 
   for (int i = tid; i < idwords; i += NT) {
     amask[i] = 0;
@@ -133,11 +144,11 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
   int nj[JPT], pj[JPT];
   uint32_t hits = 0, incs = 0, bad = 0;
 #pragma unroll
-  for (int q = 0; q < JPT; ++q) nj[q] = A[min(tid * JPT + q, k - 1)];
+  for (int q = 0; q < JPT; ++q) nj[q] = A[min(tid * JPT + q, na > 0 ? na - 1 : 0)];
 #pragma unroll
   for (int q = 0; q < JPT; ++q) {
     const bool ok = nj[q] >= 0 && nj[q] < F;  // else not a neuron id: counted as a miss
-    if (tid * JPT + q < k) bad |= !ok;
+    if (tid * JPT + q < na) bad |= !ok;
     if (!ok) nj[q] = -1;
     pj[q] = P[nj[q] >= 0 ? nj[q] : 0];
   }
@@ -148,14 +159,14 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
   for (int q = 0; q < JPT; ++q) {
     const int j = tid * JPT + q;
     if (nj[q] < 0 || pj[q] >= C) {
-      bad |= (j < k) & (pj[q] >= C) & (nj[q] >= 0);
+      bad |= (j < na) & (pj[q] >= C) & (nj[q] >= 0);
       pj[q] = -1;
     }
     if (pj[q] >= 0 && qb[q] != nj[q]) {
-      bad |= j < k;
+      bad |= j < na;
       pj[q] = -1;
     }
-    if (j < k) {
+    if (j < na) {
       if (nj[q] >= 0) atomicOr(&amask[nj[q] >> 5], 1u << (nj[q] & 31));
       if (pj[q] >= 0) ++hits;
       else ++incs;
@@ -290,7 +301,7 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
 #pragma unroll
   for (int q = 0; q < JPT; ++q) {
     const int j = tid * JPT + q;
-    if (j < k) {
+    if (j < na) {
       const int n = nj[q];
       int slot;
       if (pj[q] >= 0) {
@@ -314,13 +325,109 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
       out.active_slots[lo + j] = slot;
     }
   }
-  if (bad) raise_error(ws, NP_DEVERR_STATE);
+  if (bad || (bad_count && tid == 0)) raise_error(ws, NP_DEVERR_STATE);
   if (tid == 0) {
     out.counts[(size_t)l * 4 + 0] = (int32_t)nI;
     out.counts[(size_t)l * 4 + 1] = (int32_t)nH;
     out.counts[(size_t)l * 4 + 2] = (int32_t)m;
     out.counts[(size_t)l * 4 + 3] = (int32_t)(nI - m);
   }
+}
+
+// Centroid choice and the intersected active set (Sec. 3.3-3.4), one
+// workgroup per layer.  Waves 0 and 1 take the argmax of the layer's gate and
+// up heads over the K logits (lane c reads c, c+64, ...; a NaN never wins and
+// sets the error bit; equal values go to the smaller index).  Then thread t
+// owns id words [t*WPT, t*WPT+WPT) of the AND of the two chosen masks, and a
+// workgroup prefix sum places its ids in ascending order.
+template <int NT, int WPT>
+__global__ __launch_bounds__(NT) void centroid_active_kernel(
+    const float* __restrict__ logits, const uint32_t* __restrict__ bank,
+    int32_t* __restrict__ cids, uint32_t* __restrict__ mask, int32_t* __restrict__ active_ids,
+    int32_t* __restrict__ counts, int L, int F, int K, int k, void* ws) {
+  __shared__ int chosen[2];
+  __shared__ uint32_t scan[NT / WAVE + 1];
+  const int l = blockIdx.x, tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
+  if (w < 2) {
+    const int h = w * L + l;
+    const float* lg = logits + (size_t)h * K;
+    float best = 0.f;
+    int bi = K;  // K: nothing seen yet
+    bool nan = false;
+    for (int c = lane; c < K; c += WAVE) {
+      const float v = lg[c];
+      if (v != v) {
+        nan = true;
+        continue;
+      }
+      if (bi == K || v > best) {  // ascending c: a lane keeps its first maximum
+        best = v;
+        bi = c;
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const float ob = __shfl_xor(best, off, WAVE);
+      const int oi = __shfl_xor(bi, off, WAVE);
+      if (oi != K && (bi == K || ob > best || (ob == best && oi < bi))) {
+        best = ob;
+        bi = oi;
+      }
+    }
+    if (nan) raise_error(ws, NP_DEVERR_NAN_SCORE);
+    if (lane == 0) {
+      if (bi == K) bi = 0;  // every logit NaN: reported above
+      chosen[w] = bi;
+      cids[h] = bi;
+    }
+  }
+  __syncthreads();
+  const int W = (F + 31) / 32;
+  const uint32_t* g = bank + ((size_t)l * K + chosen[0]) * W;
+  const uint32_t* u = bank + (((size_t)L + l) * K + chosen[1]) * W;
+  uint32_t m[WPT], cnt = 0;
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int word = tid * WPT + i;
+    m[i] = word < W ? (g[word] & u[word]) : 0u;
+    if (word == W - 1 && (F & 31)) m[i] &= (1u << (F & 31)) - 1u;
+    if (word < W) mask[(size_t)l * W + word] = m[i];
+    cnt += __builtin_popcount(m[i]);
+  }
+  uint32_t tot;
+  uint32_t pos = block_excl_scan<NT>(cnt, scan, &tot);
+  int32_t* ids = active_ids + (size_t)l * k;
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    uint32_t bits = m[i];
+    while (bits) {
+      const int b = __builtin_ctz(bits);
+      bits &= bits - 1;
+      if (pos < (uint32_t)k) ids[pos] = 32 * (tid * WPT + i) + b;
+      ++pos;
+    }
+  }
+  if (tid == 0) {
+    counts[l] = tot < (uint32_t)k ? (int32_t)tot : k;
+    if (tot > (uint32_t)k) raise_error(ws, NP_DEVERR_OVERFLOW);
+  }
+}
+
+hipError_t launch_centroid_active(const np_shape& s, const np_centroid_model& m,
+                                  const float* logits, int32_t* centroid_ids, uint32_t* mask,
+                                  int32_t* active_ids, int32_t* active_counts, void* ws,
+                                  hipStream_t stream) {
+  const int words = (s.d_ffn + 31) / 32;
+#define NP_CENTROID_CASE(NT, W)                                                            \
+  hipLaunchKernelGGL((centroid_active_kernel<NT, W>), dim3(s.layers), dim3(NT), 0, stream, \
+                     logits, m.bank, centroid_ids, mask, active_ids, active_counts,         \
+                     s.layers, s.d_ffn, m.n_centroids, s.k, ws)
+  if (words <= 256) NP_CENTROID_CASE(256, 1);
+  else if (words <= 512) NP_CENTROID_CASE(512, 1);
+  else if (words <= 1024) NP_CENTROID_CASE(1024, 1);
+  else NP_CENTROID_CASE(1024, 2);
+#undef NP_CENTROID_CASE
+  return hipGetLastError();
 }
 
 // Advances np_delta's step counter (NP_TOKEN_AUTO) once the delta is done.
@@ -371,14 +478,14 @@ hipError_t launch_select(const np_shape& s, const float* scores, uint32_t* mask,
 template <int NT, int WPT>
 static hipError_t delta_w(const np_shape& s, int32_t token, const int32_t* active_ids,
                           const np_state& st, const np_delta_out& out, void* ws,
-                          hipStream_t stream) {
+                          hipStream_t stream, const int32_t* counts) {
   const int slotwords = (s.capacity + 31) / 32;
   const int spt = (slotwords + NT - 1) / NT;
   const int jpt = (s.k + NT - 1) / NT;
 #define NP_DELTA_CASE(J)                                                                      \
   hipLaunchKernelGGL((delta_kernel<NT, WPT, J>), dim3(s.layers), dim3(NT), 0, stream, token,  \
                      active_ids, st.slot_of, st.neuron_of, st.last_used, out, s.d_ffn,        \
-                     s.capacity, s.k, spt, ws)
+                     s.capacity, s.k, spt, ws, counts)
   if (jpt <= 1) NP_DELTA_CASE(1);
   else if (jpt <= 2) NP_DELTA_CASE(2);
   else if (jpt <= 4) NP_DELTA_CASE(4);
@@ -389,13 +496,13 @@ static hipError_t delta_w(const np_shape& s, int32_t token, const int32_t* activ
 
 hipError_t launch_delta(const np_shape& s, int32_t token, const int32_t* active_ids,
                         const np_state& st, const np_delta_out& out, void* ws,
-                        hipStream_t stream) {
+                        hipStream_t stream, const int32_t* counts) {
   // 512 threads while every thread owns one id word and at most 4 actives
   const int words = (s.d_ffn + 31) / 32;
   hipError_t e;
-  if (words <= 512 && s.k <= 2048) e = delta_w<512, 1>(s, token, active_ids, st, out, ws, stream);
-  else if (words <= 1024) e = delta_w<1024, 1>(s, token, active_ids, st, out, ws, stream);
-  else e = delta_w<1024, 2>(s, token, active_ids, st, out, ws, stream);
+  if (words <= 512 && s.k <= 2048) e = delta_w<512, 1>(s, token, active_ids, st, out, ws, stream, counts);
+  else if (words <= 1024) e = delta_w<1024, 1>(s, token, active_ids, st, out, ws, stream, counts);
+  else e = delta_w<1024, 2>(s, token, active_ids, st, out, ws, stream, counts);
   if (e != hipSuccess || token != NP_TOKEN_AUTO) return e;
   hipLaunchKernelGGL(token_advance_kernel, dim3(1), dim3(64), 0, stream, ws);
   return hipGetLastError();

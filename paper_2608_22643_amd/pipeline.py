@@ -54,7 +54,10 @@ class DecodePipeline:
     def __init__(self, cfg: W.Config, device: str = "cuda:0", tier: str = "device",
                  staging: str = "gather", overlap: bool = False, tokens: int | None = None,
                  staging_mib: int = 64, landing_mib: int = 32,
-                 host_storage: torch.Tensor | None = None):
+                 host_storage: torch.Tensor | None = None, predictor: str = "lowrank"):
+        if predictor not in ("lowrank", "centroid"):
+            raise ValueError(f"unknown predictor {predictor!r}")
+        self.predictor = predictor
         if staging == "memcpy" and tier != "host":
             raise ValueError("memcpy staging reads a pinned host storage tier")
         self.cfg, self.device, self.tier, self.staging, self.overlap = cfg, device, tier, staging, overlap
@@ -65,9 +68,11 @@ class DecodePipeline:
         self.T = cfg.tokens if tokens is None else tokens
         dev = torch.device(device)
         # inputs resident in HBM: predictor factors and hidden states
-        A, Bm = W.predictor(cfg)
-        self.A = torch.from_numpy(A.view(np.uint8)).to(dev)
-        self.B = torch.from_numpy(Bm.view(np.uint8)).to(dev)
+        self.A = self.B = None
+        if predictor == "lowrank":
+            A, Bm = W.predictor(cfg)
+            self.A = torch.from_numpy(A.view(np.uint8)).to(dev)
+            self.B = torch.from_numpy(Bm.view(np.uint8)).to(dev)
         h = W.hidden(cfg, self.T)
         self.h = torch.from_numpy(h.view(np.uint8).reshape(self.T, -1)).to(dev)
         self.row_bytes = d * W.ITEMSIZE[cfg.adtype]
@@ -109,6 +114,17 @@ class DecodePipeline:
         self.mask = _i32(L * self.words, dev)
         self.active_ids = _i32(L * k, dev)
         self.y = torch.empty(L * d, dtype=TORCH_DT[cfg.adtype], device=dev)
+        if predictor == "centroid":  # Sec. 3.3-3.4: centroid heads and mask bank
+            K, D = cfg.centroid_k, cfg.feat_dim
+            self.heads = torch.from_numpy(W.centroid_heads(cfg).view(np.uint8).reshape(-1)).to(dev)
+            self.bank = torch.from_numpy(W.centroid_bank(cfg).view(np.uint8).reshape(-1)).to(dev)
+            f = W.features(cfg, self.T)
+            self.feat = torch.from_numpy(f.view(np.uint8).reshape(self.T, -1)).to(dev)
+            self.feat_bytes = D * W.ITEMSIZE[cfg.adtype]
+            self.model = B.np_centroid_model(K, D, self.heads.data_ptr(), self.bank.data_ptr())
+            self.logits = torch.empty(2 * L * K, dtype=torch.float32, device=dev)
+            self.cids = _i32(max(2 * L, 4), dev)
+            self.active_counts = _i32(max(L, 4), dev)
         self.ws = torch.zeros(B.np_workspace_size(self.shape), dtype=torch.uint8, device=dev)
         self.main = torch.cuda.Stream(device=dev)
         self.side = torch.cuda.Stream(device=dev) if overlap else self.main
@@ -146,11 +162,15 @@ class DecodePipeline:
     def x_ptr(self, t: int) -> int:
         return self.h.data_ptr() + t * self.row_bytes
 
+    def f_ptr(self, t: int) -> int:
+        return self.feat.data_ptr() + t * self.feat_bytes
+
     def step(self, t: int, mlp_block_events=None) -> None:
         """Enqueue one decode token (index t of the hidden-state sequence).
         mlp_block_events: optional (start, end) torch events recorded on the
         main stream before the first and after the last np_sparse_mlp."""
-        self._enqueue(t, self.x_ptr(t), mlp_block_events)
+        f = self.f_ptr(t) if self.predictor == "centroid" else None
+        self._enqueue(t, self.x_ptr(t), mlp_block_events, f)
 
     def capture_graph(self) -> None:
         """Capture one decode step (token index from the device counter, x
@@ -161,9 +181,16 @@ class DecodePipeline:
         self.x_row = torch.zeros(1, dtype=torch.int64, device=self.device)  # next token's row of h
         self.graph_t = 0
         self.graph = torch.cuda.CUDAGraph()
+        f_ptr = None
+        if self.predictor == "centroid":
+            self.f_static = torch.empty((1, self.feat_bytes), dtype=torch.uint8,
+                                        device=self.device)
+            f_ptr = self.f_static.data_ptr()
         with torch.cuda.graph(self.graph, stream=self.main, capture_error_mode="thread_local"):
             torch.index_select(self.h, 0, self.x_row, out=self.x_static)
-            self._enqueue(B.NP_TOKEN_AUTO, self.x_static.data_ptr(), None)
+            if f_ptr is not None:
+                torch.index_select(self.feat, 0, self.x_row, out=self.f_static)
+            self._enqueue(B.NP_TOKEN_AUTO, self.x_static.data_ptr(), None, f_ptr)
             self.x_row.add_(1)
 
     def step_graph(self, t: int) -> None:
@@ -175,13 +202,20 @@ class DecodePipeline:
             self.graph.replay()
         self.graph_t += 1
 
-    def _enqueue(self, token: int, x_ptr: int, mlp_block_events) -> None:
+    def _enqueue(self, token: int, x_ptr: int, mlp_block_events, f_ptr=None) -> None:
         s, cfg = self.shape, self.cfg
         L, k = cfg.layers, cfg.k
         main = self.main
-        B.np_predict(s, x_ptr, self.A, self.B, self.scores, self.ws, main)
-        B.np_select(s, self.scores, self.mask, self.active_ids, self.ws, main)
-        B.np_delta(s, token, self.active_ids, self.state, self.out, self.ws, main)
+        centroid = self.predictor == "centroid"
+        if centroid:
+            B.np_centroid_select(s, self.model, f_ptr, self.logits, self.cids, self.mask,
+                                 self.active_ids, self.active_counts, self.ws, main)
+            B.np_delta_n(s, token, self.active_ids, self.active_counts, self.state, self.out,
+                         self.ws, main)
+        else:
+            B.np_predict(s, x_ptr, self.A, self.B, self.scores, self.ws, main)
+            B.np_select(s, self.scores, self.mask, self.active_ids, self.ws, main)
+            B.np_delta(s, token, self.active_ids, self.state, self.out, self.ws, main)
         ready = None  # ready[l]: the event layer l's MLP waits for
         if self.staging == "gather":
             if self.overlap:
@@ -228,8 +262,13 @@ class DecodePipeline:
         for l in range(L):
             if ready is not None and ready[l] is not None:
                 main.wait_event(ready[l])
-            B.np_sparse_mlp(s, l, x_ptr, self.resident, slots.data_ptr() + l * k * 4, k,
-                            self.y.data_ptr() + l * ybytes, self.ws, main)
+            if centroid:
+                B.np_sparse_mlp_n(s, l, x_ptr, self.resident, slots.data_ptr() + l * k * 4,
+                                  self.active_counts, self.y.data_ptr() + l * ybytes, self.ws,
+                                  main)
+            else:
+                B.np_sparse_mlp(s, l, x_ptr, self.resident, slots.data_ptr() + l * k * 4, k,
+                                self.y.data_ptr() + l * ybytes, self.ws, main)
         if mlp_block_events is not None:
             mlp_block_events[1].record(main)
 

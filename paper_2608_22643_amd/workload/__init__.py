@@ -37,6 +37,7 @@ STORAGE_NP = {"f32": np.float32, "f16": np.uint16, "bf16": np.uint16}
 
 TENSOR_PRED_A = 4
 TENSOR_PRED_B = 5
+TENSOR_HEADS = 25   # centroid heads [2][L'][K][D]
 
 _lib = None
 
@@ -63,6 +64,8 @@ def _gen():
         L.npg_fill_records.argtypes = [i32, u64, i64, i64, i64, i64, i32, f64, i64, vp, i32]
         L.npg_fill_matrix.argtypes = [i32, u64, u32, i64, i64, i64, i64, i32, f64, i64, vp, i32]
         L.npg_hidden.argtypes = [i32, u64, i64, i64, f64, i32, i64, vp, vp]
+        L.npg_features.argtypes = [i32, u64, i64, i64, f64, vp]
+        L.npg_fill_bank.argtypes = [u64, i64, i64, i64, f64, f64, f64, vp, i32]
         L.npg_encode.argtypes = [i32, vp, i64, vp]
         L.npg_stream.argtypes = [u64, u32, u32]
         L.npg_stream.restype = u64
@@ -131,6 +134,15 @@ class Config:
     dyadic_redraw: float = 0.1          # per-token redraw rate of h coordinates
     k_override: int | None = None
     c_override: int | None = None
+    # centroid predictor (Sec. 3.3): K centroids per layer and projection,
+    # D-dimensional features; mask bank: hot neurons set with p_hot, others
+    # with p_cold, the hot fraction chosen so that a gate/up intersection
+    # holds about bank_fill * k neurons on average
+    centroid_k: int = 512
+    feat_dim: int = 4096
+    bank_p_hot: float = 0.78
+    bank_p_cold: float = 0.05
+    bank_fill: float = 0.85
     extra: dict = field(default_factory=dict, compare=False, hash=False)
 
     @property
@@ -148,6 +160,13 @@ class Config:
         if self.rho_given is not None:
             return self.rho_given
         return rho_for_persistence(self.k / self.d_ffn, self.persistence)
+
+    @property
+    def bank_hot(self) -> float:
+        """Hot fraction q: E|gate mask & up mask| / F = q p_hot^2 + (1-q) p_cold^2
+        set to bank_fill * k / F."""
+        ph, pc = self.bank_p_hot ** 2, self.bank_p_cold ** 2
+        return min(1.0, max(0.0, (self.bank_fill * self.k / self.d_ffn - pc) / (ph - pc)))
 
     @property
     def record_bytes(self) -> int:
@@ -246,6 +265,35 @@ def predictor(cfg: Config) -> tuple[np.ndarray, np.ndarray]:
     g.npg_fill_matrix(DTYPE_CODES[cfg.wdtype], cfg.seed, TENSOR_PRED_B, 0, L, F, r,
                       sb[0], sb[1], sb[2], B.ctypes.data, _threads())
     return A, B
+
+
+def centroid_heads(cfg: Config) -> np.ndarray:
+    """Heads [2][L'][K][D] ~ N(0, 1/D) (storage bits of wdtype): gate heads of
+    every downstream layer, then up heads."""
+    L, K, D = cfg.layers, cfg.centroid_k, cfg.feat_dim
+    out = np.empty((2, L, K, D), dtype=STORAGE_NP[cfg.wdtype])
+    _gen().npg_fill_matrix(DTYPE_CODES[cfg.wdtype], cfg.seed, TENSOR_HEADS, 0, 2 * L, K, D,
+                           0, 1.0 / math.sqrt(D), 0, out.ctypes.data, _threads())
+    return out
+
+
+def features(cfg: Config, tokens: int | None = None) -> np.ndarray:
+    """Predictor features f_0..f_{T-1} [T][D] (storage bits of adtype), AR(1)
+    with the configuration's rho."""
+    T = cfg.tokens if tokens is None else tokens
+    out = np.empty((T, cfg.feat_dim), dtype=STORAGE_NP[cfg.adtype])
+    _gen().npg_features(DTYPE_CODES[cfg.adtype], cfg.seed, T, cfg.feat_dim, cfg.rho,
+                        out.ctypes.data)
+    return out
+
+
+def centroid_bank(cfg: Config) -> np.ndarray:
+    """Centroid masks [2][L'][K][ceil(F/32)] uint32 (gate, then up)."""
+    L, K, F = cfg.layers, cfg.centroid_k, cfg.d_ffn
+    out = np.empty((2, L, K, (F + 31) // 32), dtype=np.uint32)
+    _gen().npg_fill_bank(cfg.seed, L, K, F, cfg.bank_hot, cfg.bank_p_hot, cfg.bank_p_cold,
+                         out.ctypes.data, _threads())
+    return out
 
 
 def hidden(cfg: Config, tokens: int | None = None, want_f64: bool = False):

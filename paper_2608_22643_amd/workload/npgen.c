@@ -1,8 +1,9 @@
 /*
  * npgen.c -- seeded synthetic inputs for the NeuroPrefetcher decode path.
  *
- * This file generates inputs only: MLP neuron records, predictor factors and
- * the hidden-state sequence.  It holds none of the method's arithmetic; both
+ * This file generates inputs only: MLP neuron records, predictor factors,
+ * the hidden-state sequence, and the centroid predictor's feature sequence,
+ * head matrices and centroid mask bank.  It holds none of the method's arithmetic; both
  * the HIP path and the CPU oracle consume what it writes.
  *
  * Random numbers come from a counter-based generator: value i of the stream
@@ -313,6 +314,79 @@ int npg_hidden(int dtype, uint64_t seed, int64_t T, int64_t d, double rho,
       if (out_f64) out_f64[t * d + c] = h;
     }
   }
+  return 0;
+}
+
+/* The centroid predictor's feature vectors f_0..f_{T-1}, [T][D], the same
+ * AR(1) recursion as the hidden states on stream (seed, 20, t). */
+int npg_features(int dtype, uint64_t seed, int64_t T, int64_t D, double rho, void* out) {
+  double prev_scale = rho, fresh_scale = sqrt(1.0 - rho * rho);
+  for (int64_t c = 0; c < D; ++c) {
+    double f = 0.0;
+    for (int64_t t = 0; t < T; ++t) {
+      double e = npg_normal(npg_stream(seed, 20, (uint32_t)t), (uint64_t)c);
+      f = (t == 0) ? e : prev_scale * f + fresh_scale * e;
+      put(dtype, out, (size_t)(t * D + c), f);
+    }
+  }
+  return 0;
+}
+
+/* Centroid mask bank [2][L][K][W] (W = ceil(F/32) words, bit n%32 of word
+ * n/32; gate masks, then up masks).  Neuron n of layer l is "hot" (for both
+ * projections) when a uniform draw of stream (seed, 21, l) at index n is
+ * below q_hot; bit n of centroid c of projection p is set when a uniform draw
+ * of stream (seed, 23 + p, l) at index c*F + n is below p_hot (hot) or
+ * p_cold (not). */
+typedef struct {
+  uint64_t seed;
+  int64_t L, K, F;
+  double q_hot, p_hot, p_cold;
+  uint32_t* out;
+  int next, total;
+  pthread_mutex_t mu;
+} bank_job;
+
+static void* bank_worker(void* arg) {
+  bank_job* j = (bank_job*)arg;
+  const int64_t W = (j->F + 31) / 32;
+  for (;;) {
+    pthread_mutex_lock(&j->mu);
+    int pl = j->next++;
+    pthread_mutex_unlock(&j->mu);
+    if (pl >= j->total) return NULL;
+    const int p = (int)(pl / j->L);
+    const int64_t l = pl % j->L;
+    uint64_t st_hot = npg_stream(j->seed, 21, (uint32_t)l);
+    uint64_t st_bit = npg_stream(j->seed, 23 + (uint32_t)p, (uint32_t)l);
+    for (int64_t c = 0; c < j->K; ++c) {
+      uint32_t* m = j->out + ((size_t)pl * j->K + c) * W;
+      memset(m, 0, sizeof(uint32_t) * (size_t)W);
+      for (int64_t n = 0; n < j->F; ++n) {
+        const int hot = unit_open(npg_draw(st_hot, (uint64_t)n)) < j->q_hot;
+        const double u = unit_open(npg_draw(st_bit, (uint64_t)(c * j->F + n)));
+        if (u < (hot ? j->p_hot : j->p_cold)) m[n >> 5] |= 1u << (n & 31);
+      }
+    }
+  }
+}
+
+int npg_fill_bank(uint64_t seed, int64_t L, int64_t K, int64_t F, double q_hot, double p_hot,
+                  double p_cold, uint32_t* out, int nthreads) {
+  bank_job j;
+  j.seed = seed; j.L = L; j.K = K; j.F = F;
+  j.q_hot = q_hot; j.p_hot = p_hot; j.p_cold = p_cold;
+  j.out = out; j.next = 0; j.total = (int)(2 * L);
+  pthread_mutex_init(&j.mu, NULL);
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > 64) nthreads = 64;
+  pthread_t th[64];
+  int started = 0;
+  for (int t = 0; t < nthreads; ++t)
+    if (pthread_create(&th[t], NULL, bank_worker, &j) == 0) ++started;
+  if (started == 0) bank_worker(&j);
+  for (int t = 0; t < started; ++t) pthread_join(th[t], NULL);
+  pthread_mutex_destroy(&j.mu);
   return 0;
 }
 

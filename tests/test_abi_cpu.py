@@ -28,7 +28,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 12, names
+    assert len(names) == 15, names
     for n in names:
         assert hasattr(lib, n), f"missing export {n}"
     assert set(names) == set(B.EXPORTS)
@@ -119,3 +119,25 @@ def test_stage_rows_validates_plan_before_enqueueing(lib):
         B.np_stage_rows(shape, plan, 0, 2, buf.ctypes.data, 16, buf.ctypes.data, 1024, 16,
                         1 << 16, None)
     assert e.value.status == B.NP_ERR_CAPACITY
+
+
+def test_centroid_select_validates_model(lib):
+    shape = B.make_shape(**GOOD)
+    good = dict(n_centroids=512, feat_dim=4096, heads=16, bank=16)
+    for change in (dict(n_centroids=0), dict(n_centroids=5000), dict(feat_dim=4100),
+                   dict(feat_dim=20000), dict(heads=18), dict(bank=0)):
+        m = B.np_centroid_model(**dict(good, **change))
+        with pytest.raises(B.NPError) as e:
+            B.np_centroid_select(shape, m, 16, 16, 16, 16, 16, 16, 16, None)
+        assert e.value.status == B.NP_ERR_INVALID_ARG, change
+
+
+def test_variable_count_calls_need_counts(lib):
+    shape = B.make_shape(**GOOD)
+    with pytest.raises(B.NPError) as e:
+        B.np_delta_n(shape, 0, 16, None, B.np_state(16, 16, 16), B.np_delta_out(*([16] * 7)), 16,
+                     None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    with pytest.raises(B.NPError) as e:
+        B.np_sparse_mlp_n(shape, 0, 16, 16, 16, None, 16, 16, None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
