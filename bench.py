@@ -265,6 +265,57 @@ def extra_config(name: str, steps: int, graph: bool, overlap: bool) -> dict:
     return out
 
 
+def centroid_run(cfg, host_storage, steps: int) -> dict:
+    """The decode step with the paper's own predictor (centroid-ID heads and
+    gate/up mask intersection; variable-size active sets) on the same
+    workload: step rate, the predictor's time, set sizes, persistence."""
+    import numpy as np
+    import torch
+
+    from paper_2608_22643_amd import binding as B
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    T = 1 + 3 + steps + 8
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T,
+                          host_storage=host_storage, predictor="centroid")
+    for i in range(4):
+        pipe.step(i)
+    wall, _ = timed_steps(pipe, 4, steps, with_mlp_events=False)
+    # the predictor alone, and the set statistics of a few tokens
+    L, k = cfg.layers, cfg.k
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    sizes, overlap, prev = [], [], None
+    pred_us = 0.0
+    for i in range(4):
+        t = 4 + steps + i
+        torch.cuda.synchronize()
+        e0.record(pipe.main)
+        B.np_centroid_select(pipe.shape, pipe.model, pipe.f_ptr(t), pipe.logits, pipe.cids,
+                             pipe.mask, pipe.active_ids, pipe.active_counts, pipe.ws, pipe.main)
+        e1.record(pipe.main)
+        torch.cuda.synchronize()
+        pred_us += e0.elapsed_time(e1) * 1e3
+        n = pipe.active_counts.cpu().numpy()[:L]
+        ids = pipe.active_ids.cpu().numpy().reshape(L, k)
+        sets = [set(ids[l][:n[l]].tolist()) for l in range(L)]
+        sizes.append(float(n.mean()))
+        if prev is not None:
+            overlap.append(np.mean([len(a & b) / max(1, len(b)) for a, b in zip(prev, sets)]))
+        prev = sets
+    if pipe.device_error():
+        raise RuntimeError(f"centroid run: device error word {pipe.device_error():#x}")
+    K, D = cfg.centroid_k, cfg.feat_dim
+    out = {"tok_s": round(steps / wall, 2), "ms_per_step": round(wall * 1e3 / steps, 4),
+           "predictor_us": round(pred_us / 4, 2),
+           "predictor_heads_MB": round(2 * L * K * D * (4 if cfg.wdtype == "f32" else 2) / 1e6, 1),
+           "mean_active_per_layer": round(float(np.mean(sizes)), 1),
+           "persistence": round(float(np.mean(overlap)), 4),
+           "centroids": K, "feat_dim": D}
+    del pipe
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(cfg, host_storage, seconds: float):
     """The oracle (plain C, fp64, one thread) on whole tokens of the same
     workload until `seconds` of CPU work have run (at least one token)."""
@@ -312,6 +363,8 @@ def main():
     ap.add_argument("--extra-configs", default="13b",
                     help="comma-separated further configurations measured after the main one")
     ap.add_argument("--extra-steps", type=int, default=30)
+    ap.add_argument("--centroid-steps", type=int, default=30,
+                    help="steps with the centroid-ID predictor (0: skip)")
     ap.add_argument("--calib-mib", type=int, default=256,
                     help="size of one plain device-to-device copy run after the timing, "
                          "the reference for hardware byte counters")
@@ -431,6 +484,10 @@ def main():
         host.update(staging_rates(hp, 4 + args.host_tier_steps, max(3, args.host_tier_steps // 4)))
         log(f"[bench] host tier: {host}")
         del hp, hg
+    centroid = None
+    if args.centroid_steps > 0:
+        centroid = centroid_run(cfg, host_storage, args.centroid_steps)
+        log(f"[bench] centroid predictor: {centroid}")
     if args.calib_mib > 0:  # a copy of known size: reads and writes calib_mib MiB once
         src = torch.ones(args.calib_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -480,6 +537,7 @@ def main():
         "delta": stats,
         "host_tier": host,
         "cpu_baseline": cpu,
+        "centroid_predictor": centroid,
         "other_configs": extra or None,
     }
     print(json.dumps(line), flush=True)
