@@ -20,6 +20,8 @@
  *   np_delta_n, np_sparse_mlp_n   np_delta / np_sparse_mlp with per-layer
  *                       active counts read on the device
  *
+ * and np_dense_mlp for the layers of a dense prefix (Sec. 3.1).
+ *
  * Conventions shared by every call
  * --------------------------------
  *  - extern "C"; plain pointers and sizes only.  All memory is owned by the
@@ -310,6 +312,15 @@ np_status np_sparse_mlp_n(const np_shape* shape, int32_t layer, const void* x,
                           const void* dev_resident, const int32_t* active_slots,
                           const int32_t* active_counts, void* y, void* dev_ws,
                           hipStream_t stream);
+
+/* Dense MLP of one layer of the dense prefix (Sec. 3.1: the first d layers
+ * keep their MLP weights fully resident and run dense): the np_sparse_mlp
+ * computation over all F neurons of `weights`, one layer's [F][3d] records of
+ * type w in the storage layout (gate | up | down^T per neuron), device.
+ * Requires F * 3d * sizeof(w) < 2^31.  x [d], y [d] of type a.  Two kernels on
+ * `stream`. */
+np_status np_dense_mlp(const np_shape* shape, const void* weights, const void* x, void* y,
+                       void* dev_ws, hipStream_t stream);
 
 /* Waits for `stream`, then returns the sticky device error word in *code
  * (0 = none; NP_DEVERR_* bits otherwise).  Synchronous. */

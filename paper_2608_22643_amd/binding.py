@@ -28,7 +28,7 @@ NP_TOKEN_AUTO = -1  # np_delta: token index from the workspace step counter
 EXPORTS = ("np_status_str", "np_last_error", "np_shape_check", "np_workspace_size",
            "np_state_reset", "np_predict", "np_select", "np_delta", "np_stage_rows",
            "np_stage_gather", "np_sparse_mlp", "np_centroid_select", "np_delta_n",
-           "np_sparse_mlp_n", "np_device_error")
+           "np_sparse_mlp_n", "np_dense_mlp", "np_device_error")
 
 
 class NPError(RuntimeError):
@@ -97,6 +97,7 @@ def lib():
         L.np_delta_n.argtypes = [S, i32, vp, vp, ctypes.POINTER(np_state),
                                  ctypes.POINTER(np_delta_out), vp, vp]
         L.np_sparse_mlp_n.argtypes = [S, i32, vp, vp, vp, vp, vp, vp, vp]
+        L.np_dense_mlp.argtypes = [S, vp, vp, vp, vp, vp]
         for f in EXPORTS[2:]:
             getattr(L, f).restype = i32
         _lib = L
@@ -214,6 +215,11 @@ def np_sparse_mlp_n(shape, layer: int, x, dev_resident, active_slots, active_cou
     _check(lib().np_sparse_mlp_n(ctypes.byref(shape), int(layer), _p(x), _p(dev_resident),
                                  _p(active_slots), _p(active_counts), _p(y), _p(ws), _s(stream)),
            "np_sparse_mlp_n")
+
+
+def np_dense_mlp(shape, weights, x, y, ws, stream=None) -> None:
+    _check(lib().np_dense_mlp(ctypes.byref(shape), _p(weights), _p(x), _p(y), _p(ws),
+                              _s(stream)), "np_dense_mlp")
 
 
 def np_device_error(ws, stream=None) -> int:

@@ -221,6 +221,19 @@ np_status np_sparse_mlp(const np_shape* s, int32_t layer, const void* x, const v
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp launch");
 }
 
+np_status np_dense_mlp(const np_shape* s, const void* weights, const void* x, void* y, void* ws,
+                       hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if ((size_t)s->d_ffn * 3 * s->d_model * dtype_size(s->wdtype) >= ((size_t)1 << 31))
+    return fail(NP_ERR_UNSUPPORTED, "np_dense_mlp: a layer of %d records of %d elements >= 2 GiB",
+                s->d_ffn, 3 * s->d_model);
+  if (!aligned16(weights) || !aligned16(x) || !aligned16(y) || !aligned16(ws))
+    return fail(NP_ERR_INVALID_ARG, "np_dense_mlp: pointers must be non-NULL and aligned");
+  hipError_t e = launch_dense_mlp(*s, weights, x, y, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_dense_mlp launch");
+}
+
 np_status np_sparse_mlp_n(const np_shape* s, int32_t layer, const void* x, const void* resident,
                           const int32_t* slots, const int32_t* counts, void* y, void* ws,
                           hipStream_t stream) {

@@ -63,6 +63,8 @@ hipError_t launch_stage_gather(const np_shape& s, const np_delta_out& out, int l
                                hipStream_t stream);
 hipError_t launch_stage_scatter(const np_shape& s, const void* landing, int n_records,
                                 void* resident, hipStream_t stream);
+hipError_t launch_dense_mlp(const np_shape& s, const void* weights, const void* x, void* y,
+                            void* ws, hipStream_t stream);
 // n_dev: nullptr for n_active rows, else the row count is n_dev[layer]
 // (device), at most n_active.
 hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const void* resident,

@@ -41,7 +41,7 @@ namespace np {
 
 struct MlpArgs {
   const uint4* res_layer;  // first record of the layer in the resident buffer
-  const int32_t* slots;    // active_slots of the layer
+  const int32_t* slots;    // active_slots of the layer; nullptr: row j is slot j (dense layer)
   const uint4* x;
   float* partials;         // [n_wg][d]
   void* ws;
@@ -188,7 +188,7 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   int my_slot = -1;
   {
     const int r0 = row_begin + team * R;
-    if (lane < R && r0 + lane < row_end) my_slot = a.slots[r0 + lane];
+    if (lane < R && r0 + lane < row_end) my_slot = a.slots ? a.slots[r0 + lane] : r0 + lane;
   }
   // Loads below are unconditional, with no branches around them, so the
   // compiler can wait for each stage's loads alone.  Record loads are buffer
@@ -241,7 +241,7 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
     // next round's slots, in flight behind this round's records
     {
       const int rn = r0 + teams * R;
-      my_slot = (lane < R && rn + lane < row_end) ? a.slots[rn + lane] : -1;
+      my_slot = (lane < R && rn + lane < row_end) ? (a.slots ? a.slots[rn + lane] : rn + lane) : -1;
     }
 #pragma unroll
     for (int st = 0; st < S; ++st) {
@@ -543,6 +543,16 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   hipLaunchKernelGGL(mlp_reduce_kernel<T>, dim3(groups), dim3(256), 0, stream,
                      (const float*)a.partials, n_wg, s.d_model, y);
   return hipGetLastError();
+}
+
+// Dense layer (the dense prefix, Sec. 3.1): every one of the F records of
+// `weights` ([F][3d]) is a row, in order; the rows kernel with the identity
+// row -> record map.
+hipError_t launch_dense_mlp(const np_shape& s, const void* weights, const void* x, void* y,
+                            void* ws, hipStream_t stream) {
+  np_shape d = s;
+  d.capacity = s.d_ffn;  // the layer buffer is the whole layer
+  return launch_sparse_mlp(d, 0, x, weights, nullptr, s.d_ffn, y, ws, stream);
 }
 
 hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const void* resident,

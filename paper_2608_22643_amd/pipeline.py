@@ -16,6 +16,10 @@ Staging modes:
             each chunk goes over with hipMemcpyAsync on a side stream, then a
             scatter kernel places the records.  Needs the "host" tier.
 
+With dense_layers = d > 0, d dense-prefix layers (all F records of each kept
+resident, Sec. 3.1) run with np_dense_mlp after staging is enqueued and
+before the sparse layers, so side-stream staging overlaps them.
+
 With overlap=True staging runs in a few layer chunks (layer 0, layers 1-2,
 the rest): the first on the main stream right after np_delta, the others on a
 side stream, each followed by an event, and layer l's MLP waits only for the
@@ -54,10 +58,14 @@ class DecodePipeline:
     def __init__(self, cfg: W.Config, device: str = "cuda:0", tier: str = "device",
                  staging: str = "gather", overlap: bool = False, tokens: int | None = None,
                  staging_mib: int = 64, landing_mib: int = 32,
-                 host_storage: torch.Tensor | None = None, predictor: str = "lowrank"):
+                 host_storage: torch.Tensor | None = None, predictor: str = "lowrank",
+                 dense_layers: int = 0):
         if predictor not in ("lowrank", "centroid"):
             raise ValueError(f"unknown predictor {predictor!r}")
+        if dense_layers < 0:
+            raise ValueError("dense_layers must be >= 0")
         self.predictor = predictor
+        self.dense_layers = dense_layers
         if staging == "memcpy" and tier != "host":
             raise ValueError("memcpy staging reads a pinned host storage tier")
         self.cfg, self.device, self.tier, self.staging, self.overlap = cfg, device, tier, staging, overlap
@@ -99,6 +107,19 @@ class DecodePipeline:
                 del buf
             torch.cuda.synchronize()
         self.resident = torch.empty(cfg.resident_bytes, dtype=torch.uint8, device=dev)
+        # dense prefix (Sec. 3.1): dense_layers layers with all F records resident
+        if dense_layers:
+            dcfg = W.dense_config(cfg, dense_layers)
+            self.dense_layer_bytes = F * cfg.record_bytes
+            self.dense_w = torch.empty(dense_layers * self.dense_layer_bytes, dtype=torch.uint8,
+                                       device=dev)
+            buf = torch.empty(self.dense_layer_bytes, dtype=torch.uint8, pin_memory=True)
+            for l in range(dense_layers):
+                W.fill_storage(dcfg, buf.data_ptr(), l, 1)
+                self.dense_w[l * self.dense_layer_bytes:(l + 1) * self.dense_layer_bytes].copy_(buf)
+            torch.cuda.synchronize()
+            del buf
+            self.y_dense = torch.empty(dense_layers * d, dtype=TORCH_DT[cfg.adtype], device=dev)
         # residency state and step outputs
         self.slot_of, self.neuron_of, self.last_used = _i32(L * F, dev), _i32(L * C, dev), _i32(L * F, dev)
         self.state = B.np_state(self.slot_of.data_ptr(), self.neuron_of.data_ptr(),
@@ -253,6 +274,11 @@ class DecodePipeline:
                 ready = self.layer_ready
         slots = self.lists["active_slots"]
         ybytes = cfg.d_model * W.ITEMSIZE[cfg.adtype]
+        # the dense prefix runs while the sparse layers' rows are staged (on the
+        # side stream when overlapping)
+        for l in range(self.dense_layers):
+            B.np_dense_mlp(s, self.dense_w.data_ptr() + l * self.dense_layer_bytes, x_ptr,
+                           self.y_dense.data_ptr() + l * ybytes, self.ws, main)
         if mlp_block_events is not None:
             if ready is not None:  # time the MLP block, not the wait for staging
                 for e in ready:

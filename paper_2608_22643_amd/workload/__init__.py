@@ -241,6 +241,15 @@ def fill_storage(cfg: Config, dst_ptr: int, layer0: int = 0, layers: int | None 
                             cfg.d_model, dy, scale, mr, dst_ptr, nthreads or _threads())
 
 
+DENSE_SEED_OFFSET = 7919  # dense-prefix weights: records of a separate seed
+
+
+def dense_config(cfg: Config, layers: int) -> Config:
+    """The configuration whose records are the weights of a dense prefix of
+    `layers` layers in front of cfg's sparse layers (same shapes, own seed)."""
+    return cfg.with_(name=cfg.name + "-dense", layers=layers, seed=cfg.seed + DENSE_SEED_OFFSET)
+
+
 def storage(cfg: Config, layer0: int = 0, layers: int | None = None) -> np.ndarray:
     """Records as a numpy array [layers][F][3d] of storage bits."""
     layers = cfg.layers - layer0 if layers is None else layers
