@@ -316,6 +316,82 @@ def centroid_run(cfg, host_storage, steps: int) -> dict:
     return out
 
 
+def dense_mlp_roofline(cfg, host_storage, reps: int = 3) -> dict:
+    """np_dense_mlp over every layer of the storage tier (all F records of a
+    layer: the dense prefix's MLP), back to back, against the HBM roofline."""
+    import torch
+
+    from paper_2608_22643_amd import binding as B
+
+    L, d = cfg.layers, cfg.d_model
+    esz = 4 if cfg.wdtype == "f32" else 2
+    layer_bytes = cfg.d_ffn * cfg.record_bytes
+    dev = torch.device("cuda")
+    w = torch.empty(cfg.storage_bytes, dtype=torch.uint8, device=dev)
+    w.copy_(host_storage)
+    x = torch.zeros(d, dtype=torch.float16 if esz == 2 else torch.float32, device=dev)
+    y = torch.empty(L * d, dtype=x.dtype, device=dev)
+    shape = B.make_shape(L, d, cfg.d_ffn, cfg.rank, cfg.k, cfg.capacity, cfg.wdtype, cfg.adtype)
+    ws = torch.zeros(B.np_workspace_size(shape), dtype=torch.uint8, device=dev)
+    st = torch.cuda.current_stream()
+
+    def block():
+        for l in range(L):
+            B.np_dense_mlp(shape, w.data_ptr() + l * layer_bytes, x, y.data_ptr() + l * d * esz,
+                           ws, st)
+    block()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(st)
+    for _ in range(reps):
+        block()
+    e1.record(st)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * L)
+    byts = layer_bytes + 2 * d * esz
+    if B.np_device_error(ws):
+        raise RuntimeError("dense MLP: device error")
+    del w
+    torch.cuda.empty_cache()
+    return {"avg_launch_us": round(us, 3), "bytes_per_launch": byts,
+            "achieved_GBps": round(byts / (us * 1e-6) / 1e9, 1),
+            "frac": round(byts / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)}
+
+
+def dense_prefix_sweep(cfg, host_storage, prefixes, steps: int) -> dict:
+    """Decode steps with d of the downstream layers run dense (weights
+    resident) and the other L' - d sparse, for each d: storage tier in HBM
+    (gather staging) and in pinned host memory (memcpy staging on a side
+    stream, overlapping the dense prefix).  The synthetic analogue of the
+    paper's dense-prefix sweep, without its memory cap (see split.py for d*)."""
+    import torch
+
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    out = {}
+    layer_bytes = cfg.d_ffn * cfg.record_bytes
+    for dl in prefixes:
+        sc = cfg.with_(layers=cfg.layers - dl)
+        hs = host_storage[:sc.storage_bytes]  # the first L' - d layers' records
+        row = {}
+        for tier, staging, overlap in (("device", "gather", False), ("host", "memcpy", True)):
+            T = 4 + steps + 2
+            p = DecodePipeline(sc, tier=tier, staging=staging, overlap=overlap, tokens=T,
+                               host_storage=hs, dense_layers=dl)
+            for i in range(4):
+                p.step(i)
+            wall, _ = timed_steps(p, 4, steps, with_mlp_events=False)
+            if p.device_error():
+                raise RuntimeError(f"dense sweep d={dl}: device error {p.device_error():#x}")
+            row[f"{tier}_tok_s"] = round(steps / wall, 2)
+            del p
+            torch.cuda.empty_cache()
+        row["resident_GB"] = round((dl * layer_bytes + sc.resident_bytes) / 1e9, 2)
+        out[str(dl)] = row
+        log(f"[bench] dense prefix {dl}: {row}")
+    return out
+
+
 def cpu_baseline(cfg, host_storage, seconds: float):
     """The oracle (plain C, fp64, one thread) on whole tokens of the same
     workload until `seconds` of CPU work have run (at least one token)."""
@@ -363,6 +439,9 @@ def main():
     ap.add_argument("--extra-configs", default="13b",
                     help="comma-separated further configurations measured after the main one")
     ap.add_argument("--extra-steps", type=int, default=30)
+    ap.add_argument("--dense-prefixes", default="0,8,16",
+                    help="comma-separated dense-prefix lengths for the split sweep ('' to skip)")
+    ap.add_argument("--dense-steps", type=int, default=10)
     ap.add_argument("--centroid-steps", type=int, default=30,
                     help="steps with the centroid-ID predictor (0: skip)")
     ap.add_argument("--calib-mib", type=int, default=256,
@@ -484,6 +563,12 @@ def main():
         host.update(staging_rates(hp, 4 + args.host_tier_steps, max(3, args.host_tier_steps // 4)))
         log(f"[bench] host tier: {host}")
         del hp, hg
+    dense = dense_mlp_roofline(cfg, host_storage)
+    log(f"[bench] dense MLP: {dense}")
+    sweep = None
+    prefixes = [int(v) for v in args.dense_prefixes.split(",") if v]
+    if prefixes:
+        sweep = dense_prefix_sweep(cfg, host_storage, prefixes, args.dense_steps)
     centroid = None
     if args.centroid_steps > 0:
         centroid = centroid_run(cfg, host_storage, args.centroid_steps)
@@ -537,6 +622,8 @@ def main():
         "delta": stats,
         "host_tier": host,
         "cpu_baseline": cpu,
+        "dense_mlp": dense,
+        "dense_prefix_sweep": sweep,
         "centroid_predictor": centroid,
         "other_configs": extra or None,
     }
