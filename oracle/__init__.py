@@ -11,8 +11,12 @@ Functions (each cites the passage it follows in ``np_oracle.c``):
   select        O2  top-k by (score desc, id asc), mask + ids         Sec. 3.4
   delta         O3  hits / incoming / LRU victims / slot map update   Sec. 3.4 eqs. 2-3
   stage         O4  record copy storage[l][id] -> resident[l][slot]   Sec. 3.5
-  sparse_mlp    O5  sum over active n of relu(g_n) u_n downT_n        Sec. 3.3/3.4
+  sparse_mlp    O5  sum over active n of eq1(act(g_n, u_n)) downT_n   Sec. 3.3/3.4, eq. 1
   dense_mlp     O6  matrix form over all F neurons (pins O5)
+  centroid_logits / centroid_active  O7/O8  heads, argmax, mask AND    Sec. 3.3/3.4
+  act_batch     O9  activations of a batch of tokens                  Sec. 3.2
+  percentile    O10 nearest-rank alpha-th percentile of |A|           Sec. 3.2
+  threshold_active O11 eq. 1 as a mask + ascending ids                eq. 1
   decode/encode     IEEE binary16 / bfloat16 / binary32 <-> float64
 """
 from __future__ import annotations
@@ -28,6 +32,7 @@ _SRC = os.path.join(_HERE, "np_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
 DTYPES = {"f32": 0, "f16": 1, "bf16": 2}
+ACTS = {"relu": 0, "swiglu": 1}
 _ITEMSIZE = {"f32": 4, "f16": 2, "bf16": 2}
 _NP_STORAGE = {"f32": np.float32, "f16": np.uint16, "bf16": np.uint16}
 
@@ -63,13 +68,20 @@ def lib():
         L.orc_select.argtypes = [i32, i32, i32, vp, vp, vp]
         L.orc_delta.argtypes = [i32, i32, i32, i32, ctypes.c_int32] + [vp] * 11
         L.orc_stage.argtypes = [i32] * 6 + [vp] * 5
-        L.orc_sparse_mlp.argtypes = [i32] * 5 + [vp, vp, vp, i32, vp, vp]
-        L.orc_dense_mlp.argtypes = [i32] * 5 + [vp, vp, vp, vp]
+        f64 = ctypes.c_double
+        L.orc_sparse_mlp.argtypes = [i32] * 5 + [f64, i32] + [vp, vp, vp, i32, vp, vp]
+        L.orc_dense_mlp.argtypes = [i32] * 5 + [f64, i32] + [vp, vp, vp, vp]
+        L.orc_act_batch.argtypes = [i32] * 5 + [vp, vp, i32, vp]
+        L.orc_percentile_rank.argtypes = [i64, f64]
+        L.orc_percentile_rank.restype = i64
+        L.orc_percentile.argtypes = [vp, i32, i64, f64, vp]
+        L.orc_threshold_active.argtypes = [i32] * 3 + [vp] * 5
         L.orc_delta_n.argtypes = [i32, i32, i32, i32, ctypes.c_int32] + [vp] * 12
         L.orc_centroid_logits.argtypes = [i32] * 5 + [vp, vp, vp]
         L.orc_centroid_active.argtypes = [i32] * 4 + [vp] * 6
         for f in ("orc_predict", "orc_select", "orc_delta", "orc_sparse_mlp", "orc_dense_mlp",
-                  "orc_delta_n", "orc_centroid_logits", "orc_centroid_active"):
+                  "orc_delta_n", "orc_centroid_logits", "orc_centroid_active", "orc_act_batch",
+                  "orc_percentile", "orc_threshold_active"):
             getattr(L, f).restype = i32
         L.orc_stage.restype = None
         _lib = L
@@ -232,29 +244,87 @@ def stage(shape, counts, in_ids, in_slots, storage: np.ndarray, resident: np.nda
                     _ptr(in_slots), _ptr(storage), _ptr(resident))
 
 
-def sparse_mlp(shape, layer: int, x, storage, ids, want_f64: bool = False):
-    """O5 from the storage tier.  Returns y (storage bits of adtype), and the
-    unrounded float64 sums when want_f64."""
+def _act(shape) -> int:
+    return ACTS[getattr(shape, "act", "relu")]
+
+
+def sparse_mlp(shape, layer: int, x, storage, ids, want_f64: bool = False,
+               threshold: float = 0.0):
+    """O5 from the storage tier, with the activation ``shape.act`` ("relu"
+    when absent) and the eq. 1 threshold.  Returns y (storage bits of
+    adtype), and the unrounded float64 sums when want_f64."""
     F, d = shape.d_ffn, shape.d_model
     x = np.ascontiguousarray(x)
     ids = np.ascontiguousarray(ids, dtype=np.int32)
     y = np.empty(d, dtype=_NP_STORAGE[shape.adtype])
     y64 = np.empty(d, dtype=np.float64)
-    rc = lib().orc_sparse_mlp(F, d, DTYPES[shape.wdtype], DTYPES[shape.adtype], int(layer),
-                              _ptr(x), _ptr(storage), _ptr(ids), ids.size, _ptr(y), _ptr(y64))
+    rc = lib().orc_sparse_mlp(F, d, DTYPES[shape.wdtype], DTYPES[shape.adtype], _act(shape),
+                              float(threshold), int(layer), _ptr(x), _ptr(storage), _ptr(ids),
+                              ids.size, _ptr(y), _ptr(y64))
     if rc:
         raise OracleError(f"orc_sparse_mlp failed ({rc})")
     return (y, y64) if want_f64 else y
 
 
-def dense_mlp(shape, layer: int, x, storage, want_f64: bool = False):
-    """O6: the dense matrix-form MLP over all F neurons."""
+def dense_mlp(shape, layer: int, x, storage, want_f64: bool = False, threshold: float = 0.0):
+    """O6: the dense matrix-form MLP over all F neurons (activation and
+    threshold as in sparse_mlp)."""
     F, d = shape.d_ffn, shape.d_model
     x = np.ascontiguousarray(x)
     y = np.empty(d, dtype=_NP_STORAGE[shape.adtype])
     y64 = np.empty(d, dtype=np.float64)
-    rc = lib().orc_dense_mlp(F, d, DTYPES[shape.wdtype], DTYPES[shape.adtype], int(layer),
-                             _ptr(x), _ptr(storage), _ptr(y), _ptr(y64))
+    rc = lib().orc_dense_mlp(F, d, DTYPES[shape.wdtype], DTYPES[shape.adtype], _act(shape),
+                             float(threshold), int(layer), _ptr(x), _ptr(storage), _ptr(y),
+                             _ptr(y64))
     if rc:
         raise OracleError(f"orc_dense_mlp failed ({rc})")
     return (y, y64) if want_f64 else y
+
+
+def act_batch(shape, weights, x, n: int) -> np.ndarray:
+    """O9: activations [n][F] (float64, unrounded) of one layer's records
+    ``weights`` ([F][3d] storage bits) over the tokens ``x`` ([n][d])."""
+    F, d = shape.d_ffn, shape.d_model
+    weights, x = np.ascontiguousarray(weights), np.ascontiguousarray(x)
+    assert weights.size == F * 3 * d and x.size == n * d
+    out = np.empty((n, F), dtype=np.float64)
+    rc = lib().orc_act_batch(F, d, DTYPES[shape.wdtype], DTYPES[shape.adtype], _act(shape),
+                             _ptr(weights), _ptr(x), int(n), _ptr(out))
+    if rc:
+        raise OracleError(f"orc_act_batch failed ({rc})")
+    return out
+
+
+def percentile_rank(n: int, alpha: float) -> int:
+    """m = ceil(alpha * n / 100) in double, clamped to [1, n] (O10)."""
+    return int(lib().orc_percentile_rank(int(n), float(alpha)))
+
+
+def percentile(values: np.ndarray, alpha: float) -> np.ndarray:
+    """O10: per row of ``values`` ([rows][n] float32), the nearest-rank
+    alpha-th percentile of the magnitudes, as float32 [rows]."""
+    v = np.ascontiguousarray(values, dtype=np.float32)
+    v2 = v.reshape(-1, v.shape[-1]) if v.ndim > 1 else v.reshape(1, -1)
+    out = np.empty(v2.shape[0], dtype=np.float32)
+    rc = lib().orc_percentile(_ptr(v2), v2.shape[0], v2.shape[1], float(alpha), _ptr(out))
+    if rc:
+        raise OracleError(f"orc_percentile failed ({rc})")
+    return out
+
+
+def threshold_active(acts: np.ndarray, thresholds, k: int) -> dict:
+    """O11: eq. 1 as a mask.  acts [rows][F] float32, thresholds [rows]
+    float32 -> mask [rows][W] uint32, active_ids [rows][k] (-1 past the
+    count), counts [rows], overflow (some row had more than k)."""
+    a = np.ascontiguousarray(acts, dtype=np.float32)
+    rows, F = a.shape
+    t = np.ascontiguousarray(np.broadcast_to(np.asarray(thresholds, dtype=np.float32), (rows,)))
+    W = (F + 31) // 32
+    mask = np.empty((rows, W), dtype=np.uint32)
+    ids = np.full((rows, k), -1, dtype=np.int32)
+    counts = np.empty(rows, dtype=np.int32)
+    rc = lib().orc_threshold_active(rows, F, int(k), _ptr(a), _ptr(t), _ptr(mask), _ptr(ids),
+                                    _ptr(counts))
+    if rc not in (0, 3):
+        raise OracleError(f"orc_threshold_active failed ({rc})")
+    return {"mask": mask, "active_ids": ids, "counts": counts, "overflow": rc == 3}

@@ -389,14 +389,31 @@ void orc_stage(int L, int F, int C, int k, int d, int wdtype,
   }
 }
 
+/* ---------------- gated activations and eq. 1 ---------------------------- */
+/* The two gated forms of an MLP neuron with gate sum g and up sum u:
+ *   ReLU-gated (the synthetic models):  a = max(g, 0) * u;
+ *   SwiGLU (the paper's evaluated models, Sec. 4):  a = SiLU(g) * u with
+ *   SiLU(g) = g * sigmoid(g) = g / (1 + e^-g)  (exp from the C library).
+ * Eq. 1 (Sec. 3.2): a magnitude below the layer's threshold T is set to zero;
+ * T = 0 leaves every value as it is. */
+#define ORC_ACT_RELU 0
+#define ORC_ACT_SWIGLU 1
+
+static double orc_act(int act, double g, double u) {
+  if (act == ORC_ACT_SWIGLU) return g / (1.0 + exp(-g)) * u;
+  return (g > 0.0 ? g : 0.0) * u;
+}
+
+static double orc_eq1(double a, double thr) { return fabs(a) < thr ? 0.0 : a; }
+
 /* ---------------- O5: sparse MLP over the active rows ------------------ */
 /* Sec. 3.4 (row i of gate, up and down^T for each active neuron; row order
- * irrelevant) and Sec. 3.3 (the down projection's output stays dense), with
- * the ReLU-gated form a = max(g, 0) * u.  Computed from the storage tier,
- * indexed by neuron id -- the definition, not the resident buffer.
- * y = sum over n in ids of max(G[n].x, 0) * (U[n].x) * D[n]; y is rounded
- * once to adtype; y64 (optional) receives the unrounded sums. */
-int orc_sparse_mlp(int F, int d, int wdtype, int adtype, int layer,
+ * irrelevant) and Sec. 3.3 (the down projection's output stays dense).
+ * Computed from the storage tier, indexed by neuron id -- the definition, not
+ * the resident buffer.  y = sum over n in ids of eq1(act(G[n].x, U[n].x)) *
+ * D[n] with the activation `act` and threshold `thr` above; y is rounded once
+ * to adtype; y64 (optional) receives the unrounded sums. */
+int orc_sparse_mlp(int F, int d, int wdtype, int adtype, int act, double thr, int layer,
                    const void* x, const void* storage, const int32_t* ids,
                    int n_ids, void* y, double* y64) {
   double* xv = (double*)malloc(sizeof(double) * (size_t)d);
@@ -412,7 +429,7 @@ int orc_sparse_mlp(int F, int d, int wdtype, int adtype, int layer,
       g += orc_load(wdtype, storage, base + c) * xv[c];
       u += orc_load(wdtype, storage, base + d + c) * xv[c];
     }
-    double a = (g > 0.0 ? g : 0.0) * u;
+    double a = orc_eq1(orc_act(act, g, u), thr);
     for (int c = 0; c < d; ++c)
       acc[c] += a * orc_load(wdtype, storage, base + 2 * (size_t)d + c);
   }
@@ -426,10 +443,11 @@ int orc_sparse_mlp(int F, int d, int wdtype, int adtype, int layer,
 }
 
 /* ---------------- O6: dense MLP, matrix form ----------------------------- */
-/* The same ReLU-gated MLP over all F neurons, written as whole-matrix
- * products: gvec = G x, uvec = U x, act = relu(gvec) * uvec, y = D^T act.
- * Used only to pin O5 (all neurons active must give the dense result). */
-int orc_dense_mlp(int F, int d, int wdtype, int adtype, int layer,
+/* The same MLP over all F neurons, written as whole-matrix products:
+ * gvec = G x, uvec = U x, avec = eq1(act(gvec, uvec)), y = D^T avec.  Pins
+ * O5 (all neurons active must give the dense result) and is the dense
+ * layer of the dense prefix (Sec. 3.1). */
+int orc_dense_mlp(int F, int d, int wdtype, int adtype, int act, double thr, int layer,
                   const void* x, const void* storage, void* y, double* y64) {
   double* xv = (double*)malloc(sizeof(double) * (size_t)d);
   double* gv = (double*)malloc(sizeof(double) * (size_t)F);
@@ -455,8 +473,8 @@ int orc_dense_mlp(int F, int d, int wdtype, int adtype, int layer,
   for (int c = 0; c < d; ++c) {
     double s = 0.0;
     for (int n = 0; n < F; ++n) {
-      double act = (gv[n] > 0.0 ? gv[n] : 0.0) * uv[n];
-      s += orc_load(wdtype, storage, lbase + (size_t)n * 3 * d + 2 * (size_t)d + c) * act;
+      double an = orc_eq1(orc_act(act, gv[n], uv[n]), thr);
+      s += orc_load(wdtype, storage, lbase + (size_t)n * 3 * d + 2 * (size_t)d + c) * an;
     }
     yv[c] = s;
   }
@@ -529,6 +547,100 @@ int orc_centroid_active(int L, int F, int K, int k, const float* logits, const u
       n = k;
     }
     counts[l] = n;
+  }
+  return rc;
+}
+
+/* ---------------- O9: activations of a batch of tokens -------------------- */
+/* Sec. 3.2: the activations A_i = f_l(x_i) of layer l over tokens x_i, the
+ * input of the percentile calibration.  weights is one layer's [F][3d]
+ * records, x is [n][d]; acts[i][f] = act(G[f].x_i, U[f].x_i) in double,
+ * unrounded. */
+int orc_act_batch(int F, int d, int wdtype, int adtype, int act, const void* weights,
+                  const void* x, int n, double* acts) {
+  double* xv = (double*)malloc(sizeof(double) * (size_t)d);
+  if (!xv) return -1;
+  for (int i = 0; i < n; ++i) {
+    for (int c = 0; c < d; ++c) xv[c] = orc_load(adtype, x, (size_t)i * d + c);
+    for (int f = 0; f < F; ++f) {
+      size_t base = (size_t)f * 3 * d;
+      double g = 0.0, u = 0.0;
+      for (int c = 0; c < d; ++c) {
+        g += orc_load(wdtype, weights, base + c) * xv[c];
+        u += orc_load(wdtype, weights, base + d + c) * xv[c];
+      }
+      acts[(size_t)i * F + f] = orc_act(act, g, u);
+    }
+  }
+  free(xv);
+  return 0;
+}
+
+/* ---------------- O10: the alpha-th percentile of the magnitudes ---------- */
+/* Sec. 3.2: T(l, alpha) is the alpha-th percentile of |A| over the
+ * calibration activations of layer l.  Reading: the nearest-rank percentile,
+ * the m-th smallest magnitude with m = ceil(alpha * n / 100) evaluated in
+ * double and clamped to [1, n]; it is a value of the set itself, so eq. 1
+ * then zeroes fewer than m of the n values.  values: [rows][n] binary32, one
+ * row per layer; out: [rows].  alpha outside [0, 100] or n < 1 returns 2, a
+ * NaN value returns 1. */
+static int by_float_asc(const void* pa, const void* pb) {
+  float a = *(const float*)pa, b = *(const float*)pb;
+  return a < b ? -1 : (a > b ? 1 : 0);
+}
+
+int64_t orc_percentile_rank(int64_t n, double alpha) {
+  double m = ceil(alpha * (double)n / 100.0);
+  if (m < 1.0) m = 1.0;
+  if (m > (double)n) m = (double)n;
+  return (int64_t)m;
+}
+
+int orc_percentile(const float* values, int rows, int64_t n, double alpha, float* out) {
+  if (n < 1 || !(alpha >= 0.0 && alpha <= 100.0)) return 2;
+  float* mag = (float*)malloc(sizeof(float) * (size_t)n);
+  if (!mag) return -1;
+  int64_t m = orc_percentile_rank(n, alpha);
+  for (int r = 0; r < rows; ++r) {
+    for (int64_t i = 0; i < n; ++i) {
+      float v = values[(size_t)r * n + i];
+      if (isnan(v)) { free(mag); return 1; }
+      mag[i] = fabsf(v);
+    }
+    qsort(mag, (size_t)n, sizeof(float), by_float_asc);
+    out[r] = mag[m - 1];
+  }
+  free(mag);
+  return 0;
+}
+
+/* ---------------- O11: the thresholded active set ------------------------ */
+/* Eq. 1 as a mask: neuron f of row r is active when |acts[r][f]| >= thr[r]
+ * (what eq. 1 keeps), in the layout of the selection: mask [rows][W] (bit
+ * f%32 of word f/32), active_ids [rows][k] ascending, counts [rows].  A row
+ * with more than k active neurons keeps its k smallest ids in the list and
+ * every member in the mask, and the function returns 3; a NaN returns 1. */
+int orc_threshold_active(int rows, int F, int k, const float* acts, const float* thr,
+                         uint32_t* mask, int32_t* active_ids, int32_t* counts) {
+  const int W = (F + 31) / 32;
+  int rc = 0;
+  for (int r = 0; r < rows; ++r) {
+    int n = 0;
+    for (int w = 0; w < W; ++w) mask[(size_t)r * W + w] = 0u;
+    for (int f = 0; f < F; ++f) {
+      float v = acts[(size_t)r * F + f];
+      if (isnan(v)) return 1;
+      if (fabsf(v) >= thr[r]) {
+        mask[(size_t)r * W + f / 32] |= 1u << (f % 32);
+        if (n < k) active_ids[(size_t)r * k + n] = f;
+        ++n;
+      }
+    }
+    if (n > k) {
+      rc = 3;
+      n = k;
+    }
+    counts[r] = n;
   }
   return rc;
 }

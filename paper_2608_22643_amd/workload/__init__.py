@@ -143,6 +143,7 @@ class Config:
     bank_p_hot: float = 0.78
     bank_p_cold: float = 0.05
     bank_fill: float = 0.85
+    act: str = "relu"                   # gated activation: "relu" or "swiglu"
     extra: dict = field(default_factory=dict, compare=False, hash=False)
 
     @property
@@ -193,6 +194,13 @@ CONFIGS = {
     "13b": Config("13b", 39, 5120, 13824, 512, 0.12, 0.40, "f16", "f16", 256, persistence=0.835),
     # 80 layers, bf16, 10% active, 35% resident, 85% persistence
     "70b": Config("70b", 79, 8192, 28672, 768, 0.10, 0.35, "bf16", "bf16", 128, persistence=0.85),
+    # SwiGLU, shaped like the paper's evaluated 7B model (Sec. 4: 32 layers,
+    # d 4096, intermediate 14336, fp16) at its smallest budget K_max = 5500
+    # (38.4% active); 50% resident
+    "7b_swiglu": Config("7b_swiglu", 31, 4096, 14336, 416, 5500 / 14336, 0.50, "f16", "f16", 256,
+                        persistence=0.835, k_override=5500, act="swiglu"),
+    "tiny_swiglu": Config("tiny_swiglu", 3, 256, 1024, 32, 0.10, 0.50, "f32", "f32", 16,
+                          rho_given=0.95, act="swiglu"),
     # dyadic-exact variants (test only)
     "dyadic_tiny": Config("dyadic_tiny", 3, 256, 1024, 32, 0.10, 0.50, "f32", "f32", 16,
                           rho_given=0.0, dyadic=True, dyadic_w_range=3, dyadic_h_range=4),

@@ -14,7 +14,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "np_oracle.c")
 PINS = ["tests/test_oracle_encoding.py", "tests/test_oracle_predict.py",
         "tests/test_oracle_select.py", "tests/test_oracle_delta.py",
-        "tests/test_oracle_mlp.py", "tests/test_oracle_centroid.py"]
+        "tests/test_oracle_mlp.py", "tests/test_oracle_centroid.py",
+        "tests/test_oracle_swiglu.py"]
 
 MUTATIONS = {
     # predictor: transposed / shifted A operand
@@ -39,7 +40,17 @@ MUTATIONS = {
         ("for (int j = 0; j < na; ++j) U[A[j]] = t;", "for (int j = 0; j < ni; ++j) U[I[j]] = t;"),
     # MLP: ReLU dropped, wrong row for down^T
     "mlp_no_relu":
-        ("double a = (g > 0.0 ? g : 0.0) * u;", "double a = g * u;"),
+        ("return (g > 0.0 ? g : 0.0) * u;", "return g * u;"),
+    # SwiGLU: sigmoid of -g; eq. 1 zeroing a magnitude equal to T
+    "silu_exp_sign":
+        ("return g / (1.0 + exp(-g)) * u;", "return g / (1.0 + exp(g)) * u;"),
+    "eq1_drops_equal_magnitude":
+        ("return fabs(a) < thr ? 0.0 : a;", "return fabs(a) <= thr ? 0.0 : a;"),
+    # percentile: the (m+1)-th smallest; thresholded set strictly above T
+    "percentile_off_by_one":
+        ("out[r] = mag[m - 1];", "out[r] = mag[m < n ? m : m - 1];"),
+    "threshold_active_strict":
+        ("if (fabsf(v) >= thr[r]) {", "if (fabsf(v) > thr[r]) {"),
     "mlp_down_reads_up_row":
         ("acc[c] += a * orc_load(wdtype, storage, base + 2 * (size_t)d + c);",
          "acc[c] += a * orc_load(wdtype, storage, base + (size_t)d + c);"),
