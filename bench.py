@@ -331,7 +331,8 @@ def dense_mlp_roofline(cfg, host_storage, reps: int = 3) -> dict:
     w.copy_(host_storage)
     x = torch.zeros(d, dtype=torch.float16 if esz == 2 else torch.float32, device=dev)
     y = torch.empty(L * d, dtype=x.dtype, device=dev)
-    shape = B.make_shape(L, d, cfg.d_ffn, cfg.rank, cfg.k, cfg.capacity, cfg.wdtype, cfg.adtype)
+    shape = B.make_shape(L, d, cfg.d_ffn, cfg.rank, cfg.k, cfg.capacity, cfg.wdtype, cfg.adtype,
+                         cfg.act)
     ws = torch.zeros(B.np_workspace_size(shape), dtype=torch.uint8, device=dev)
     st = torch.cuda.current_stream()
 

@@ -22,6 +22,16 @@
  *
  * and np_dense_mlp for the layers of a dense prefix (Sec. 3.1).
  *
+ * The MLP calls evaluate either gated form (np_shape.act): the ReLU-gated
+ * MLP of the synthetic models or the SwiGLU MLP of the paper's evaluated
+ * models (Sec. 4).  For the magnitude-threshold sparsity of Sec. 3.2 (eq. 1):
+ *
+ *   np_sparse_mlp_t      np_sparse_mlp with eq. 1 applied to each active row
+ *   np_act_batch         activations of one layer over a batch of tokens
+ *                        (matrix cores; the calibration input)
+ *   np_percentile        per-layer alpha-th percentile of |activation|: T(l, alpha)
+ *   np_threshold_active  eq. 1 as an active set: |a| >= T -> mask + ascending ids
+ *
  * Conventions shared by every call
  * --------------------------------
  *  - extern "C"; plain pointers and sizes only.  All memory is owned by the
@@ -46,6 +56,7 @@
  *  d  = d_model, F = d_ffn (MLP intermediate size), r = predictor rank,
  *  k  = active rows per layer, C = resident slots per layer.
  *  w  = wdtype (MLP records and predictor factors), a = adtype (h, x, y).
+ *  act = gated activation of the MLP neurons (np_act).
  *  Requirements: wdtype == adtype; 1 <= k <= C <= F <= 65535; k <= 8192;
  *  L' >= 1; d and r multiples of 8 for 16-bit types and of 4 for fp32;
  *  d <= 16384 (16-bit) or 8192 (fp32); r <= 1024 (16-bit) or 512 (fp32);
@@ -80,8 +91,14 @@ typedef enum np_status {
 
 typedef enum np_dtype { NP_F32 = 0, NP_F16 = 1, NP_BF16 = 2 } np_dtype;
 
+/* Gated activation of an MLP neuron with gate sum g and up sum u:
+ * NP_ACT_RELU a = max(g, 0) * u; NP_ACT_SWIGLU a = SiLU(g) * u with
+ * SiLU(g) = g / (1 + exp(-g)) (the SwiGLU MLP of the paper's models, Sec. 4;
+ * exp is HIP's expf, the division IEEE fp32). */
+typedef enum np_act { NP_ACT_RELU = 0, NP_ACT_SWIGLU = 1 } np_act;
+
 /* Device error word bits (sticky, OR-ed; see np_device_error). */
-#define NP_DEVERR_NAN_SCORE    0x1  /* np_select saw a NaN score */
+#define NP_DEVERR_NAN_SCORE    0x1  /* a NaN score, logit or activation was read */
 #define NP_DEVERR_NOT_RESIDENT 0x2  /* a slot outside [0, C) or id outside [0, F) */
 #define NP_DEVERR_STATE        0x4  /* inconsistent state or plan (ids, slots, counts) */
 #define NP_DEVERR_SPIN_LIMIT   0x8  /* a bounded in-kernel wait gave up */
@@ -96,6 +113,7 @@ typedef struct np_shape {
   int32_t capacity; /* C: resident slots per layer */
   int32_t wdtype;   /* np_dtype of MLP records and predictor factors */
   int32_t adtype;   /* np_dtype of activations h, x, y */
+  int32_t act;      /* np_act of the MLP neurons */
 } np_shape;
 
 /* Residency state of every downstream layer, device memory, int32.
@@ -255,7 +273,8 @@ np_status np_stage_gather(const np_shape* shape, const np_delta_out* out,
 /* Sparse MLP of one downstream layer over its resident active rows
  * (Sec. 3.4: the slot map locates each active row; row order is irrelevant;
  * Sec. 3.3: the down projection's output stays dense):
- *     g_j = gate_j . x,  u_j = up_j . x,  y = sum_j max(g_j, 0) * u_j * downT_j
+ *     g_j = gate_j . x,  u_j = up_j . x,  y = sum_j act(g_j, u_j) * downT_j
+ * with act the gated form shape->act (max(g, 0) * u or SiLU(g) * u)
  * where row j is slot active_slots[j] (j < n_active) of layer `layer` of
  * dev_resident.  x [d] and y [d] of type a, device; accumulation in fp32 and
  * one rounding of y to type a.  A slot outside [0, C) sets
@@ -321,6 +340,61 @@ np_status np_sparse_mlp_n(const np_shape* shape, int32_t layer, const void* x,
  * `stream`. */
 np_status np_dense_mlp(const np_shape* shape, const void* weights, const void* x, void* y,
                        void* dev_ws, hipStream_t stream);
+
+/* np_sparse_mlp with the magnitude threshold of eq. 1 (Sec. 3.2) applied to
+ * each active row: a_j = act(g_j, u_j) is replaced by 0 when
+ * |a_j| < thresholds[layer] (fp32 comparison), so
+ *     y = sum_j [|a_j| >= T] a_j downT_j.
+ * thresholds: device fp32 [L'] (T of every downstream layer, e.g. from
+ * np_percentile), or NULL for no threshold (T = 0 keeps every row too).
+ * active_counts: NULL for n_active rows, else device int32 [L'] read on the
+ * device as in np_sparse_mlp_n, with the row count min(count, n_active) and
+ * a count outside [0, n_active] setting NP_DEVERR_STATE.  active_slots,
+ * active_counts and thresholds need 4-byte alignment.  Everything else as
+ * np_sparse_mlp (n_active in [0, C]). */
+np_status np_sparse_mlp_t(const np_shape* shape, int32_t layer, const void* x,
+                          const void* dev_resident, const int32_t* active_slots,
+                          int32_t n_active, const int32_t* active_counts,
+                          const float* thresholds, void* y, void* dev_ws,
+                          hipStream_t stream);
+
+/* Activations of one layer over a batch of tokens, the A(i, l) = f_l(x_i) that
+ * Sec. 3.2 collects to set the per-layer thresholds:
+ *     acts[i][f] = act(gate_f . x_i, up_f . x_i)     (i < n, f < F)
+ * weights: one layer's [F][3d] records of type w (storage layout), device;
+ * x: [n][d] of type a, device; acts: [n][F] fp32, device.  The two
+ * projections are matrix products over the batch, run on the matrix cores
+ * (MFMA, fp32 accumulation); acts is not rounded further.  Requires
+ * 1 <= n <= 65536, F * 3d * sizeof(w) < 2^31 and n * d * sizeof(a) < 2^31.
+ * A launch per 128 tokens on `stream`; dev_ws is not used (may be NULL). */
+np_status np_act_batch(const np_shape* shape, const void* weights, const void* x, int32_t n,
+                       float* acts, void* dev_ws, hipStream_t stream);
+
+/* Per row r of `values` ([rows][n] fp32, device): the alpha-th percentile of
+ * the magnitudes |values[r][.]|, the threshold T(l, alpha) of Sec. 3.2 when
+ * row r holds layer l's calibration activations.  Nearest rank: out[r] is
+ * the m-th smallest magnitude, m = ceil(alpha * n / 100) computed in double
+ * on the host and clamped to [1, n], so out[r] is one of the magnitudes and
+ * eq. 1 zeroes fewer than m of them.  alpha in [0, 100]; 1 <= rows <= 65535;
+ * 1 <= n < 2^31; rows * n * 4 bytes of values.  out: device fp32 [rows].  A
+ * NaN value sets NP_DEVERR_NAN_SCORE (out[r] is then undefined).  One
+ * workgroup per row, radix selection on the magnitude bits; dev_ws holds
+ * only the error word. */
+np_status np_percentile(const float* values, int32_t rows, int64_t n, double alpha, float* out,
+                        void* dev_ws, hipStream_t stream);
+
+/* Eq. 1 as an active set, in np_select's layout: for each row r of acts
+ * ([rows][F] fp32, device) with threshold thresholds[r] (device fp32
+ * [rows]), neuron f is active when |acts[r][f]| >= thresholds[r].  mask:
+ * [rows][ceil(F/32)] uint32 (bit f%32 of word f/32); active_ids: [rows][k]
+ * ascending (only the first active_counts[r] entries are written);
+ * active_counts: [rows] int32, all device.  A row with more than k active
+ * neurons lists its k smallest ids, keeps every member in its mask, counts k
+ * and sets NP_DEVERR_OVERFLOW; a NaN activation sets NP_DEVERR_NAN_SCORE.
+ * F and k from `shape`; 1 <= rows <= 65535. */
+np_status np_threshold_active(const np_shape* shape, const float* acts, int32_t rows,
+                              const float* thresholds, uint32_t* mask, int32_t* active_ids,
+                              int32_t* active_counts, void* dev_ws, hipStream_t stream);
 
 /* Waits for `stream`, then returns the sticky device error word in *code
  * (0 = none; NP_DEVERR_* bits otherwise).  Synchronous. */

@@ -18,7 +18,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["np_abi.cpp", "np_stage_host.cpp", "np_predict.hip", "np_select.hip",
-           "np_stage.hip", "np_mlp.hip"]
+           "np_stage.hip", "np_mlp.hip", "np_calib.hip"]
 
 FLAGS = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

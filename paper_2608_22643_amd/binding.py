@@ -17,6 +17,8 @@ LIB_PATH = os.path.join(_HERE, "libneuroprefetch.so")
 NP_OK, NP_ERR_INVALID_ARG, NP_ERR_CAPACITY, NP_ERR_HIP, NP_ERR_UNSUPPORTED, NP_ERR_STATE = range(6)
 NP_F32, NP_F16, NP_BF16 = 0, 1, 2
 DTYPE_CODE = {"f32": NP_F32, "f16": NP_F16, "bf16": NP_BF16}
+NP_ACT_RELU, NP_ACT_SWIGLU = 0, 1
+ACT_CODE = {"relu": NP_ACT_RELU, "swiglu": NP_ACT_SWIGLU}
 NP_DEVERR_NAN_SCORE = 0x1
 NP_DEVERR_NOT_RESIDENT = 0x2
 NP_DEVERR_STATE = 0x4
@@ -28,7 +30,8 @@ NP_TOKEN_AUTO = -1  # np_delta: token index from the workspace step counter
 EXPORTS = ("np_status_str", "np_last_error", "np_shape_check", "np_workspace_size",
            "np_state_reset", "np_predict", "np_select", "np_delta", "np_stage_rows",
            "np_stage_gather", "np_sparse_mlp", "np_centroid_select", "np_delta_n",
-           "np_sparse_mlp_n", "np_dense_mlp", "np_device_error")
+           "np_sparse_mlp_n", "np_dense_mlp", "np_sparse_mlp_t", "np_act_batch",
+           "np_percentile", "np_threshold_active", "np_device_error")
 
 
 class NPError(RuntimeError):
@@ -41,7 +44,7 @@ class np_shape(ctypes.Structure):
     _fields_ = [("layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
                 ("d_ffn", ctypes.c_int32), ("rank", ctypes.c_int32), ("k", ctypes.c_int32),
                 ("capacity", ctypes.c_int32), ("wdtype", ctypes.c_int32),
-                ("adtype", ctypes.c_int32)]
+                ("adtype", ctypes.c_int32), ("act", ctypes.c_int32)]
 
 
 class np_state(ctypes.Structure):
@@ -98,6 +101,10 @@ def lib():
                                  ctypes.POINTER(np_delta_out), vp, vp]
         L.np_sparse_mlp_n.argtypes = [S, i32, vp, vp, vp, vp, vp, vp, vp]
         L.np_dense_mlp.argtypes = [S, vp, vp, vp, vp, vp]
+        L.np_sparse_mlp_t.argtypes = [S, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp]
+        L.np_act_batch.argtypes = [S, vp, vp, i32, vp, vp, vp]
+        L.np_percentile.argtypes = [vp, i32, ctypes.c_int64, ctypes.c_double, vp, vp, vp]
+        L.np_threshold_active.argtypes = [S, vp, i32, vp, vp, vp, vp, vp, vp]
         for f in EXPORTS[2:]:
             getattr(L, f).restype = i32
         _lib = L
@@ -132,10 +139,11 @@ def _check(st: int, fn: str) -> None:
         raise NPError(st, fn, lib().np_last_error().decode())
 
 
-def make_shape(layers, d_model, d_ffn, rank, k, capacity, wdtype, adtype=None) -> np_shape:
+def make_shape(layers, d_model, d_ffn, rank, k, capacity, wdtype, adtype=None,
+               act="relu") -> np_shape:
     wd = DTYPE_CODE.get(wdtype, wdtype)
     ad = wd if adtype is None else DTYPE_CODE.get(adtype, adtype)
-    return np_shape(layers, d_model, d_ffn, rank, k, capacity, wd, ad)
+    return np_shape(layers, d_model, d_ffn, rank, k, capacity, wd, ad, ACT_CODE.get(act, act))
 
 
 def np_shape_check(shape: np_shape) -> None:
@@ -220,6 +228,30 @@ def np_sparse_mlp_n(shape, layer: int, x, dev_resident, active_slots, active_cou
 def np_dense_mlp(shape, weights, x, y, ws, stream=None) -> None:
     _check(lib().np_dense_mlp(ctypes.byref(shape), _p(weights), _p(x), _p(y), _p(ws),
                               _s(stream)), "np_dense_mlp")
+
+
+def np_sparse_mlp_t(shape, layer: int, x, dev_resident, active_slots, n_active: int,
+                    active_counts, thresholds, y, ws, stream=None) -> None:
+    _check(lib().np_sparse_mlp_t(ctypes.byref(shape), int(layer), _p(x), _p(dev_resident),
+                                 _p(active_slots), int(n_active), _p(active_counts),
+                                 _p(thresholds), _p(y), _p(ws), _s(stream)), "np_sparse_mlp_t")
+
+
+def np_act_batch(shape, weights, x, n: int, acts, ws=None, stream=None) -> None:
+    _check(lib().np_act_batch(ctypes.byref(shape), _p(weights), _p(x), int(n), _p(acts), _p(ws),
+                              _s(stream)), "np_act_batch")
+
+
+def np_percentile(values, rows: int, n: int, alpha: float, out, ws, stream=None) -> None:
+    _check(lib().np_percentile(_p(values), int(rows), int(n), float(alpha), _p(out), _p(ws),
+                               _s(stream)), "np_percentile")
+
+
+def np_threshold_active(shape, acts, rows: int, thresholds, mask, active_ids, active_counts, ws,
+                        stream=None) -> None:
+    _check(lib().np_threshold_active(ctypes.byref(shape), _p(acts), int(rows), _p(thresholds),
+                                     _p(mask), _p(active_ids), _p(active_counts), _p(ws),
+                                     _s(stream)), "np_threshold_active")
 
 
 def np_device_error(ws, stream=None) -> int:

@@ -1,6 +1,7 @@
 // np_abi.cpp -- host side of the C ABI: argument validation, status text,
 // workspace sizing and dispatch to the kernel launchers.  Validation runs
 // before anything is enqueued.
+#include <cmath>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -35,6 +36,8 @@ np_status check_shape(const np_shape* s) {
     return fail(NP_ERR_INVALID_ARG, "wdtype %d is not an np_dtype", s->wdtype);
   if (s->adtype != s->wdtype)
     return fail(NP_ERR_INVALID_ARG, "adtype %d must equal wdtype %d", s->adtype, s->wdtype);
+  if (s->act != NP_ACT_RELU && s->act != NP_ACT_SWIGLU)
+    return fail(NP_ERR_INVALID_ARG, "act %d is not an np_act", s->act);
   const int V = vec_elems(s->wdtype);
   if (s->layers < 1) return fail(NP_ERR_INVALID_ARG, "layers %d < 1", s->layers);
   if (s->d_model < V || s->d_model % V)
@@ -247,6 +250,69 @@ np_status np_sparse_mlp_n(const np_shape* s, int32_t layer, const void* x, const
     return fail(NP_ERR_INVALID_ARG, "np_sparse_mlp_n: pointers must be non-NULL and aligned");
   hipError_t e = launch_sparse_mlp(*s, layer, x, resident, slots, s->k, y, ws, stream, counts);
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp_n launch");
+}
+
+np_status np_sparse_mlp_t(const np_shape* s, int32_t layer, const void* x, const void* resident,
+                          const int32_t* slots, int32_t n_active, const int32_t* counts,
+                          const float* thr, void* y, void* ws, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (layer < 0 || layer >= s->layers)
+    return fail(NP_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, s->layers);
+  if (n_active < 0 || n_active > s->capacity)
+    return fail(NP_ERR_INVALID_ARG, "n_active %d outside [0, capacity]", n_active);
+  if (!aligned16(x) || !aligned16(resident) || !aligned16(y) || !aligned16(ws) ||
+      (n_active > 0 && !slots) || ((uintptr_t)slots & 3) || ((uintptr_t)counts & 3) ||
+      ((uintptr_t)thr & 3))
+    return fail(NP_ERR_INVALID_ARG, "np_sparse_mlp_t: pointers must be non-NULL and aligned");
+  hipError_t e = launch_sparse_mlp(*s, layer, x, resident, slots, n_active, y, ws, stream, counts,
+                                   thr);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp_t launch");
+}
+
+np_status np_act_batch(const np_shape* s, const void* weights, const void* x, int32_t n,
+                       float* acts, void* ws, hipStream_t stream) {
+  (void)ws;
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (n < 1 || n > 65536) return fail(NP_ERR_INVALID_ARG, "n %d outside [1, 65536]", n);
+  const size_t w = dtype_size(s->wdtype);
+  if ((size_t)s->d_ffn * 3 * s->d_model * w >= ((size_t)1 << 31) ||
+      (size_t)n * s->d_model * w >= ((size_t)1 << 31))
+    return fail(NP_ERR_UNSUPPORTED, "np_act_batch: weights or tokens of 2 GiB or more");
+  if (!aligned16(weights) || !aligned16(x) || !aligned16(acts))
+    return fail(NP_ERR_INVALID_ARG, "np_act_batch: pointers must be non-NULL and aligned");
+  hipError_t e = launch_act_batch(*s, weights, x, n, acts, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_act_batch launch");
+}
+
+np_status np_percentile(const float* values, int32_t rows, int64_t n, double alpha, float* out,
+                        void* ws, hipStream_t stream) {
+  if (rows < 1 || rows > 65535) return fail(NP_ERR_INVALID_ARG, "rows %d outside [1, 65535]", rows);
+  if (n < 1 || n >= ((int64_t)1 << 31))
+    return fail(NP_ERR_INVALID_ARG, "n %lld outside [1, 2^31)", (long long)n);
+  if (!(alpha >= 0.0 && alpha <= 100.0))
+    return fail(NP_ERR_INVALID_ARG, "alpha %g outside [0, 100]", alpha);
+  if (!aligned16(values) || ((uintptr_t)out & 3) || !out || !aligned16(ws))
+    return fail(NP_ERR_INVALID_ARG, "np_percentile: pointers must be non-NULL and aligned");
+  // nearest rank: the m-th smallest magnitude, m = ceil(alpha n / 100) in [1, n]
+  double md = std::ceil(alpha * (double)n / 100.0);
+  int64_t m = md < 1.0 ? 1 : (md > (double)n ? n : (int64_t)md);
+  hipError_t e = launch_percentile(values, rows, n, m, out, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_percentile launch");
+}
+
+np_status np_threshold_active(const np_shape* s, const float* acts, int32_t rows,
+                              const float* thr, uint32_t* mask, int32_t* ids, int32_t* counts,
+                              void* ws, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (rows < 1 || rows > 65535) return fail(NP_ERR_INVALID_ARG, "rows %d outside [1, 65535]", rows);
+  if (!aligned16(acts) || !aligned16(mask) || !aligned16(ids) || !aligned16(ws) || !thr ||
+      !counts || ((uintptr_t)thr & 3) || ((uintptr_t)counts & 3))
+    return fail(NP_ERR_INVALID_ARG, "np_threshold_active: pointers must be non-NULL and aligned");
+  hipError_t e = launch_threshold_active(*s, acts, rows, thr, mask, ids, counts, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_threshold_active launch");
 }
 
 np_status np_device_error(const void* ws, hipStream_t stream, int32_t* code) {

@@ -1,0 +1,377 @@
+// np_calib.hip -- the magnitude-threshold sparsity of Sec. 3.2 (eq. 1):
+//  * act_batch_kernel: activations A(i, l) = act(G x_i, U x_i) of one layer
+//    over a batch of calibration tokens, on the matrix cores;
+//  * percentile_kernel: per layer, the nearest-rank alpha-th percentile of
+//    |A| (the threshold T(l, alpha)) by radix selection;
+//  * threshold_active_kernel: eq. 1 as an active set, |a| >= T, in the
+//    selection's mask + ascending-id layout.
+#include "np_device.hpp"
+
+namespace np {
+
+// ---------------------------------------------------------------------------
+// activations of a token batch
+// ---------------------------------------------------------------------------
+// The gate and up projections of a batch are two matrix products, G X^T and
+// U X^T (neurons x tokens, reduction over d), so they run on MFMA with fp32
+// accumulation.  Each 32 x 32 output tile is a v_mfma_f32_32x32x16 (16-bit
+// types) or four v_mfma_f32_32x32x2f32 (fp32) per "step" of 2*V reduction
+// elements: lane l holds row l%32 of the A operand (a neuron's gate or up
+// record) and column l%32 of the B operand (a token), each as the V
+// consecutive elements starting at step*2V + V*(l/32), so the two operands
+// pair the same reduction indices whatever order the unit sums them in.  The
+// accumulator layout: lane l, register r holds output row
+// 8*(r/4) + 4*(l/32) + r%4 (neuron) and column l%32 (token).
+//
+// A workgroup owns 32 neurons; its four waves split the reduction (d) into
+// quarters and hold every token tile of the launch (up to 4, 128 tokens), so
+// each record is read from HBM once per launch.  Operands come straight from
+// memory with 16-byte buffer loads (a record's row is contiguous in d; the
+// tokens are L2-resident); the quarters meet in LDS, one token tile at a
+// time, and wave 0 applies the activation and writes acts[token][neuron].
+constexpr int AB_WAVES = 4;
+constexpr int AB_MAX_TILES = 4;
+constexpr int AB_UNROLL = 4;
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+template <class T>
+__device__ inline f32x16 mfma_step(uint4 a, uint4 b, f32x16 c) {
+  if constexpr (T::dtype == NP_F16) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  } else if constexpr (T::dtype == NP_BF16) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  } else {
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0,
+                                                0, 0);
+  }
+}
+
+struct ActBatchArgs {
+  const void* w;    // one layer's [F][3d] records
+  const void* x;    // [n][d] tokens of this launch
+  float* acts;      // [n][F] rows of this launch
+  uint32_t w_bytes, x_bytes;
+  int F, d, n, act;
+};
+
+template <class T, int NTT>
+__global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs a) {
+  constexpr int V = T::V, ESZ = 16 / V, KS = 2 * V;
+  __shared__ float xch[AB_WAVES - 1][2][16][WAVE];  // one tile's quarters, wave 1..3
+  const int lane = threadIdx.x & (WAVE - 1), q = threadIdx.x / WAVE;
+  const int n0 = blockIdx.x * 32, grp = lane / 32;
+  const int row = n0 + (lane & 31);
+  const int steps = (a.d + KS - 1) / KS;
+  const int s0 = q * steps / AB_WAVES, s1 = (q + 1) * steps / AB_WAVES;
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes), xr = make_rsrc(a.x, a.x_bytes);
+  // byte offsets of this lane's operands at reduction index 0 (OOB past the
+  // neurons / tokens of the launch)
+  const uint32_t rec = (uint32_t)(3 * a.d * ESZ);
+  const uint32_t g_off = row < a.F ? (uint32_t)row * rec : BUF_OOB;
+  uint32_t t_off[NTT];
+#pragma unroll
+  for (int t = 0; t < NTT; ++t) {
+    const int tok = t * 32 + (lane & 31);
+    t_off[t] = tok < a.n ? (uint32_t)tok * (uint32_t)(a.d * ESZ) : BUF_OOB;
+  }
+  const uint32_t up = (uint32_t)(a.d * ESZ);
+  f32x16 accg[NTT], accu[NTT];
+#pragma unroll
+  for (int t = 0; t < NTT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) accg[t][r] = accu[t][r] = 0.f;
+
+  for (int s = s0; s < s1; s += AB_UNROLL) {
+    uint4 ag[AB_UNROLL], au[AB_UNROLL], bx[AB_UNROLL][NTT];
+#pragma unroll
+    for (int u = 0; u < AB_UNROLL; ++u) {
+      const int k = (s + u) * KS + grp * V;  // first reduction index of the lane
+      const bool ok = s + u < s1 && k < a.d;
+      const uint32_t kb = (uint32_t)k * ESZ;
+      ag[u] = buf_load16(wr, ok && g_off != BUF_OOB ? g_off + kb : BUF_OOB, 0);
+      au[u] = buf_load16(wr, ok && g_off != BUF_OOB ? g_off + up + kb : BUF_OOB, 0);
+#pragma unroll
+      for (int t = 0; t < NTT; ++t)
+        bx[u][t] = buf_load16(xr, ok && t_off[t] != BUF_OOB ? t_off[t] + kb : BUF_OOB, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < AB_UNROLL; ++u)
+#pragma unroll
+      for (int t = 0; t < NTT; ++t) {
+        accg[t] = mfma_step<T>(ag[u], bx[u][t], accg[t]);
+        accu[t] = mfma_step<T>(au[u], bx[u][t], accu[t]);
+      }
+  }
+  // the quarters meet in LDS, tile by tile, in wave order
+#pragma unroll
+  for (int t = 0; t < NTT; ++t) {
+    if (q > 0) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        xch[q - 1][0][r][lane] = accg[t][r];
+        xch[q - 1][1][r][lane] = accu[t][r];
+      }
+    }
+    __syncthreads();
+    if (q == 0) {
+      float g[16], u[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        g[r] = accg[t][r];
+        u[r] = accu[t][r];
+#pragma unroll
+        for (int w = 0; w < AB_WAVES - 1; ++w) {
+          g[r] += xch[w][0][r][lane];
+          u[r] += xch[w][1][r][lane];
+        }
+      }
+      const int tok = t * 32 + (lane & 31);
+      if (tok < a.n) {
+        float* dst = a.acts + (size_t)tok * a.F;
+#pragma unroll
+        for (int r0 = 0; r0 < 16; r0 += 4) {
+          const int nb = n0 + 8 * (r0 / 4) + 4 * grp;  // neurons nb .. nb + 3
+          float o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = gated(a.act, g[r0 + e], u[r0 + e]);
+          if ((a.F & 3) == 0) {
+            if (nb < a.F) *(float4*)(dst + nb) = make_float4(o[0], o[1], o[2], o[3]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (nb + e < a.F) dst[nb + e] = o[e];
+          }
+        }
+      }
+    }
+    __syncthreads();  // xch is reused by the next tile
+  }
+}
+
+template <class T>
+static hipError_t act_batch_t(const np_shape& s, const void* weights, const void* x, int n,
+                              float* acts, hipStream_t stream) {
+  constexpr int ESZ = 16 / T::V;
+  const int tiles = (s.d_ffn + 31) / 32;
+  for (int i0 = 0; i0 < n; i0 += 32 * AB_MAX_TILES) {
+    ActBatchArgs a;
+    a.w = weights;
+    a.x = (const char*)x + (size_t)i0 * s.d_model * ESZ;
+    a.acts = acts + (size_t)i0 * s.d_ffn;
+    a.n = std::min(n - i0, 32 * AB_MAX_TILES);
+    a.w_bytes = (uint32_t)((size_t)s.d_ffn * 3 * s.d_model * ESZ);
+    a.x_bytes = (uint32_t)((size_t)a.n * s.d_model * ESZ);
+    a.F = s.d_ffn;
+    a.d = s.d_model;
+    a.act = s.act;
+    const int ntt = (a.n + 31) / 32;
+#define NP_AB_CASE(N) \
+  hipLaunchKernelGGL((act_batch_kernel<T, N>), dim3(tiles), dim3(AB_WAVES * WAVE), 0, stream, a)
+    if (ntt == 1) NP_AB_CASE(1);
+    else if (ntt == 2) NP_AB_CASE(2);
+    else if (ntt == 3) NP_AB_CASE(3);
+    else NP_AB_CASE(4);
+#undef NP_AB_CASE
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_act_batch(const np_shape& s, const void* weights, const void* x, int n,
+                            float* acts, hipStream_t stream) {
+  switch (s.wdtype) {
+    case NP_F32: return act_batch_t<TF32>(s, weights, x, n, acts, stream);
+    case NP_F16: return act_batch_t<TF16>(s, weights, x, n, acts, stream);
+    default: return act_batch_t<TBF16>(s, weights, x, n, acts, stream);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// per-row nearest-rank percentile of the magnitudes
+// ---------------------------------------------------------------------------
+// The magnitude's bits (sign cleared) order non-negative floats like
+// integers, so the m-th smallest magnitude is found digit by digit from the
+// top: 11, 10 and 10 bits.  Each pass streams the row once, counts the
+// values that match the digits decided so far into a histogram of the next
+// digit (four LDS copies, by wave, against atomic contention on the few bins
+// a narrow exponent range fills), and a prefix sum over the bins finds the
+// digit that holds the m-th value.
+constexpr int PCT_NT = 1024;
+constexpr int PCT_BINS = 2048;
+constexpr int PCT_COPIES = 4;
+
+template <bool V4>
+__global__ __launch_bounds__(PCT_NT) void percentile_kernel(const float* __restrict__ values,
+                                                            int64_t n, int64_t m, float* out,
+                                                            void* ws) {
+  __shared__ uint32_t hist[PCT_COPIES][PCT_BINS];
+  __shared__ uint32_t scan[PCT_NT / WAVE + 1];
+  __shared__ uint32_t sel[2];  // chosen digit, rank left within it
+  const int tid = threadIdx.x, copy = (tid / WAVE) % PCT_COPIES;
+  const float* row = values + (size_t)blockIdx.x * (size_t)n;
+  uint32_t prefix = 0, known = 0;  // decided high bits and their mask
+  uint32_t rank = (uint32_t)m;     // 1-based rank within the matching values
+  bool nan = false;
+  const int shifts[3] = {20, 10, 0}, widths[3] = {11, 10, 10};
+  for (int pass = 0; pass < 3; ++pass) {
+    const int sh = shifts[pass], nb = 1 << widths[pass];
+    for (int i = tid; i < PCT_COPIES * PCT_BINS; i += PCT_NT) (&hist[0][0])[i] = 0u;
+    __syncthreads();
+    auto count = [&](float v) {
+      const uint32_t key = __float_as_uint(v) & 0x7FFFFFFFu;
+      if (pass == 0 && key > 0x7F800000u) nan = true;
+      if ((key & known) == prefix) atomicAdd(&hist[copy][(key >> sh) & (nb - 1)], 1u);
+    };
+    if constexpr (V4) {
+      const float4* r4 = (const float4*)row;
+      for (int64_t i = tid; i < n / 4; i += PCT_NT) {
+        const float4 v = r4[i];
+        count(v.x);
+        count(v.y);
+        count(v.z);
+        count(v.w);
+      }
+    } else {
+      for (int64_t i = tid; i < n; i += PCT_NT) count(row[i]);
+    }
+    __syncthreads();
+    // thread t owns bins 2t, 2t + 1
+    uint32_t c[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int b = 2 * tid + j;
+      c[j] = 0u;
+      if (b < nb)
+#pragma unroll
+        for (int cp = 0; cp < PCT_COPIES; ++cp) c[j] += hist[cp][b];
+    }
+    uint32_t tot;
+    const uint32_t before = block_excl_scan<PCT_NT>(c[0] + c[1], scan, &tot);
+    if (before < rank && rank <= before + c[0]) {
+      sel[0] = 2 * tid;
+      sel[1] = rank - before;
+    } else if (before + c[0] < rank && rank <= before + c[0] + c[1]) {
+      sel[0] = 2 * tid + 1;
+      sel[1] = rank - before - c[0];
+    }
+    __syncthreads();
+    prefix |= sel[0] << sh;
+    known |= (uint32_t)(nb - 1) << sh;
+    rank = sel[1];
+    __syncthreads();  // sel and hist are rewritten by the next pass
+  }
+  if (nan) raise_error(ws, NP_DEVERR_NAN_SCORE);
+  if (tid == 0) out[blockIdx.x] = __uint_as_float(prefix);
+}
+
+hipError_t launch_percentile(const float* values, int rows, int64_t n, int64_t m, float* out,
+                             void* ws, hipStream_t stream) {
+  if (n % 4 == 0)
+    hipLaunchKernelGGL(percentile_kernel<true>, dim3(rows), dim3(PCT_NT), 0, stream, values, n,
+                       m, out, ws);
+  else
+    hipLaunchKernelGGL(percentile_kernel<false>, dim3(rows), dim3(PCT_NT), 0, stream, values, n,
+                       m, out, ws);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// eq. 1 as an active set
+// ---------------------------------------------------------------------------
+// One workgroup per row; thread t owns id words [t*WPT, t*WPT + WPT): it
+// compares the word's 32 activations with the row's threshold, and a
+// workgroup prefix sum over the words' popcounts places the ids in ascending
+// order (the selection's layout).
+template <int NT, int WPT, bool V4>
+__global__ __launch_bounds__(NT) void threshold_active_kernel(
+    const float* __restrict__ acts, const float* __restrict__ thr, uint32_t* __restrict__ mask,
+    int32_t* __restrict__ active_ids, int32_t* __restrict__ counts, int F, int k, void* ws) {
+  __shared__ uint32_t scan[NT / WAVE + 1];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const int W = (F + 31) / 32;
+  const float T = thr[r];
+  const float* row = acts + (size_t)r * F;
+  uint32_t m[WPT], cnt = 0;
+  bool nan = false;
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int word = tid * WPT + i;
+    m[i] = 0u;
+    if (word < W) {
+      if (V4 && 32 * word + 32 <= F) {
+        const float4* p = (const float4*)(row + 32 * word);
+        float4 v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = p[j];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float e[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            nan |= e[c] != e[c];
+            if (fabsf(e[c]) >= T) m[i] |= 1u << (4 * j + c);
+          }
+        }
+      } else {
+        for (int b = 0; b < 32 && 32 * word + b < F; ++b) {
+          const float e = row[32 * word + b];
+          nan |= e != e;
+          if (fabsf(e) >= T) m[i] |= 1u << b;
+        }
+      }
+      mask[(size_t)r * W + word] = m[i];
+    }
+    cnt += __builtin_popcount(m[i]);
+  }
+  if (nan) raise_error(ws, NP_DEVERR_NAN_SCORE);
+  uint32_t tot;
+  uint32_t pos = block_excl_scan<NT>(cnt, scan, &tot);
+  int32_t* ids = active_ids + (size_t)r * k;
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    uint32_t bits = m[i];
+    while (bits) {
+      const int b = __builtin_ctz(bits);
+      bits &= bits - 1;
+      if (pos < (uint32_t)k) ids[pos] = 32 * (tid * WPT + i) + b;
+      ++pos;
+    }
+  }
+  if (tid == 0) {
+    counts[r] = tot < (uint32_t)k ? (int32_t)tot : k;
+    if (tot > (uint32_t)k) raise_error(ws, NP_DEVERR_OVERFLOW);
+  }
+}
+
+hipError_t launch_threshold_active(const np_shape& s, const float* acts, int rows,
+                                   const float* thr, uint32_t* mask, int32_t* active_ids,
+                                   int32_t* active_counts, void* ws, hipStream_t stream) {
+  const int words = (s.d_ffn + 31) / 32;
+  const bool v4 = s.d_ffn % 4 == 0;
+#define NP_THR_CASE(NT, W)                                                                     \
+  do {                                                                                         \
+    if (v4)                                                                                    \
+      hipLaunchKernelGGL((threshold_active_kernel<NT, W, true>), dim3(rows), dim3(NT), 0,      \
+                         stream, acts, thr, mask, active_ids, active_counts, s.d_ffn, s.k, ws); \
+    else                                                                                       \
+      hipLaunchKernelGGL((threshold_active_kernel<NT, W, false>), dim3(rows), dim3(NT), 0,     \
+                         stream, acts, thr, mask, active_ids, active_counts, s.d_ffn, s.k, ws); \
+  } while (0)
+  if (words <= 256) NP_THR_CASE(256, 1);
+  else if (words <= 512) NP_THR_CASE(512, 1);
+  else if (words <= 1024) NP_THR_CASE(1024, 1);
+  else NP_THR_CASE(1024, 2);
+#undef NP_THR_CASE
+  return hipGetLastError();
+}
+
+}  // namespace np

@@ -276,6 +276,15 @@ __device__ inline uint32_t block_excl_scan(uint32_t v, uint32_t* lds, uint32_t* 
 }
 
 // ---------------------------------------------------------------------------
+// gated activation of an MLP neuron: a = act(g, u), ReLU-gated max(g, 0) u or
+// SwiGLU SiLU(g) u with SiLU(g) = g / (1 + e^-g) (HIP's expf, IEEE divide)
+// ---------------------------------------------------------------------------
+__device__ inline float gated(int act, float g, float u) {
+  if (act == NP_ACT_SWIGLU) return g / (1.f + expf(-g)) * u;
+  return fmaxf(g, 0.f) * u;
+}
+
+// ---------------------------------------------------------------------------
 // sticky device error word
 // ---------------------------------------------------------------------------
 __device__ inline void raise_error(void* ws, int bits) {

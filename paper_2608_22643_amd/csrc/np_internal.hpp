@@ -66,10 +66,22 @@ hipError_t launch_stage_scatter(const np_shape& s, const void* landing, int n_re
 hipError_t launch_dense_mlp(const np_shape& s, const void* weights, const void* x, void* y,
                             void* ws, hipStream_t stream);
 // n_dev: nullptr for n_active rows, else the row count is n_dev[layer]
-// (device), at most n_active.
+// (device), at most n_active.  thr: nullptr, or the eq. 1 threshold of each
+// layer (device fp32 [L']).
 hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const void* resident,
                              const int32_t* active_slots, int n_active, void* y, void* ws,
-                             hipStream_t stream, const int32_t* n_dev = nullptr);
+                             hipStream_t stream, const int32_t* n_dev = nullptr,
+                             const float* thr = nullptr);
+// activations of one layer over n tokens (matrix cores), acts [n][F] fp32
+hipError_t launch_act_batch(const np_shape& s, const void* weights, const void* x, int n,
+                            float* acts, hipStream_t stream);
+// per row: the m-th smallest magnitude of n values (1 <= m <= n)
+hipError_t launch_percentile(const float* values, int rows, int64_t n, int64_t m, float* out,
+                             void* ws, hipStream_t stream);
+// eq. 1 masks and ascending ids of rows x F activations
+hipError_t launch_threshold_active(const np_shape& s, const float* acts, int rows,
+                                   const float* thr, uint32_t* mask, int32_t* active_ids,
+                                   int32_t* active_counts, void* ws, hipStream_t stream);
 
 // host-side helpers shared by the ABI files (np_abi.cpp)
 np_status fail(np_status st, const char* fmt, ...);

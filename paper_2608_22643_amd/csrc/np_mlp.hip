@@ -1,7 +1,9 @@
-// np_mlp.hip -- sparse ReLU-gated MLP of one downstream layer over its
-// resident active rows (Sec. 3.4: the slot map locates each active row, row
-// order is irrelevant; Sec. 3.3: the down projection's output stays dense):
-//     y = sum_j max(gate_j . x, 0) * (up_j . x) * downT_j
+// np_mlp.hip -- sparse gated MLP of one downstream layer over its resident
+// active rows (Sec. 3.4: the slot map locates each active row, row order is
+// irrelevant; Sec. 3.3: the down projection's output stays dense):
+//     y = sum_j eq1(act(gate_j . x, up_j . x)) * downT_j
+// with act ReLU-gated (max(g, 0) u) or SwiGLU (SiLU(g) u, Sec. 4) and eq1 the
+// optional magnitude threshold of Sec. 3.2 (|a| < T -> 0).
 // Row j is one resident record [gate | up | downT] (3d contiguous elements),
 // so the work is a stream of whole records: HBM-bound.
 //
@@ -50,7 +52,10 @@ struct MlpArgs {
   void* y;               // single-kernel path: the output
   const int32_t* n_dev;  // nullptr, or the row count at n_dev[layer] (<= n_active)
   int layer;
+  int act;               // np_act
+  const float* thr;      // nullptr, or the eq. 1 threshold of each layer at thr[layer]
 };
+
 
 // Single-kernel path.  Partial rows are stored in "position" order: float4
 // position pos = ((p*CPL + c)*(V/4) + q)*64 + lane holds columns
@@ -174,6 +179,7 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
       n_active = n_active < 0 ? 0 : a.n_active;
     }
   }
+  const float thr = a.thr ? a.thr[a.layer] : 0.f;  // eq. 1; 0 keeps every row
   // balanced contiguous ranges: workgroup b takes rows [b*n/G, (b+1)*n/G)
   const int row_begin = (int)(((long long)b * n_active) / a.n_wg);
   const int row_end = (int)(((long long)(b + 1) * n_active) / a.n_wg);
@@ -284,7 +290,8 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
       for (int i = 0; i < RS; ++i) {
         const int r = st * RS + i;
         if (valid[r]) {  // lanes past the slice accumulate values never written
-          const float act = fmaxf(gs[i], 0.f) * us[i];
+          float act = gated(a.act, gs[i], us[i]);
+          if (fabsf(act) < thr) act = 0.f;
 #pragma unroll
           for (int c = 0; c < CPL; ++c) T::axpy(yacc[c], act, dw[r][c]);
         }
@@ -478,9 +485,11 @@ static void launch_rows(const MlpArgs& a, size_t lds, size_t lds_fused, bool wan
 template <class T>
 static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void* resident,
                         const int32_t* active_slots, int n_active, void* y, void* ws,
-                        hipStream_t stream, const int32_t* n_dev) {
+                        hipStream_t stream, const int32_t* n_dev, const float* thr) {
   constexpr int V = T::V;
   MlpArgs a;
+  a.act = s.act;
+  a.thr = thr;
   a.NV = s.d_model / V;
   // column slice per wave: 64 vectors (CPL = 1) while that needs at most 16
   // waves, else 128 vectors (CPL = 2)
@@ -557,14 +566,15 @@ hipError_t launch_dense_mlp(const np_shape& s, const void* weights, const void* 
 
 hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const void* resident,
                              const int32_t* active_slots, int n_active, void* y, void* ws,
-                             hipStream_t stream, const int32_t* n_dev) {
+                             hipStream_t stream, const int32_t* n_dev, const float* thr) {
   switch (s.wdtype) {
     case NP_F32:
-      return mlp_t<TF32>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev);
+      return mlp_t<TF32>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev, thr);
     case NP_F16:
-      return mlp_t<TF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev);
+      return mlp_t<TF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev, thr);
     default:
-      return mlp_t<TBF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev);
+      return mlp_t<TBF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev,
+                          thr);
   }
 }
 

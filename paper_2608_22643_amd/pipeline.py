@@ -71,7 +71,7 @@ class DecodePipeline:
         self.cfg, self.device, self.tier, self.staging, self.overlap = cfg, device, tier, staging, overlap
         torch.cuda.set_device(device)
         L, d, F, r, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.rank, cfg.k, cfg.capacity
-        self.shape = B.make_shape(L, d, F, r, k, C, cfg.wdtype, cfg.adtype)
+        self.shape = B.make_shape(L, d, F, r, k, C, cfg.wdtype, cfg.adtype, cfg.act)
         B.np_shape_check(self.shape)
         self.T = cfg.tokens if tokens is None else tokens
         dev = torch.device(device)

@@ -33,7 +33,7 @@ class Bufs:
     def __init__(self, cfg: W.Config):
         self.cfg = cfg
         L, F, C, k, d = cfg.layers, cfg.d_ffn, cfg.capacity, cfg.k, cfg.d_model
-        self.shape = B.make_shape(L, d, F, cfg.rank, k, C, cfg.wdtype, cfg.adtype)
+        self.shape = B.make_shape(L, d, F, cfg.rank, k, C, cfg.wdtype, cfg.adtype, cfg.act)
         i32 = lambda n: torch.full((n,), -7, dtype=torch.int32, device=DEV)
         self.slot_of, self.neuron_of, self.last_used = i32(L * F), i32(L * C), i32(L * F)
         self.state = B.np_state(self.slot_of.data_ptr(), self.neuron_of.data_ptr(),

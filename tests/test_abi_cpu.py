@@ -28,7 +28,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 16, names
+    assert len(names) == 20, names
     for n in names:
         assert hasattr(lib, n), f"missing export {n}"
     assert set(names) == set(B.EXPORTS)
@@ -55,6 +55,8 @@ GOOD = dict(layers=31, d_model=4096, d_ffn=11008, rank=416, k=1651, capacity=550
     (dict(layers=0), B.NP_ERR_INVALID_ARG),
     (dict(wdtype=7), B.NP_ERR_INVALID_ARG),
     (dict(k=9000, capacity=9000), B.NP_ERR_INVALID_ARG),
+    (dict(act="swiglu"), B.NP_OK),
+    (dict(act=2), B.NP_ERR_INVALID_ARG),
 ])
 def test_shape_validation(lib, change, status):
     args = dict(GOOD, **change)
@@ -141,3 +143,35 @@ def test_variable_count_calls_need_counts(lib):
     with pytest.raises(B.NPError) as e:
         B.np_sparse_mlp_n(shape, 0, 16, 16, 16, None, 16, 16, None)
     assert e.value.status == B.NP_ERR_INVALID_ARG
+
+
+def test_threshold_calls_validate_before_enqueueing(lib):
+    shape = B.make_shape(**GOOD, act="swiglu")
+    cases = [
+        # np_sparse_mlp_t: n_active above C, misaligned thresholds
+        lambda: B.np_sparse_mlp_t(shape, 0, 16, 16, 16, 5505, None, None, 16, 16),
+        lambda: B.np_sparse_mlp_t(shape, 0, 16, 16, 16, 8, None, 18, 16, 16),
+        lambda: B.np_sparse_mlp_t(shape, 31, 16, 16, 16, 8, None, None, 16, 16),
+        # np_act_batch: n outside [1, 65536], misaligned tokens
+        lambda: B.np_act_batch(shape, 16, 16, 0, 16),
+        lambda: B.np_act_batch(shape, 16, 16, 70000, 16),
+        lambda: B.np_act_batch(shape, 16, 24, 8, 16),
+        # np_percentile: alpha outside [0, 100], no rows, NULL output
+        lambda: B.np_percentile(16, 1, 100, 100.5, 16, 16),
+        lambda: B.np_percentile(16, 1, 100, float("nan"), 16, 16),
+        lambda: B.np_percentile(16, 0, 100, 50.0, 16, 16),
+        lambda: B.np_percentile(16, 1, 0, 50.0, 16, 16),
+        lambda: B.np_percentile(16, 1, 100, 50.0, None, 16),
+        # np_threshold_active: no thresholds, no rows
+        lambda: B.np_threshold_active(shape, 16, 1, None, 16, 16, 16, 16),
+        lambda: B.np_threshold_active(shape, 16, 0, 16, 16, 16, 16, 16),
+    ]
+    for i, call in enumerate(cases):
+        with pytest.raises(B.NPError) as e:
+            call()
+        assert e.value.status == B.NP_ERR_INVALID_ARG, i
+    big = B.make_shape(layers=1, d_model=16384, d_ffn=65535, rank=8, k=8, capacity=8,
+                       wdtype="f16")
+    with pytest.raises(B.NPError) as e:
+        B.np_act_batch(big, 16, 16, 1, 16)
+    assert e.value.status == B.NP_ERR_UNSUPPORTED
