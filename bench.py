@@ -316,6 +316,95 @@ def centroid_run(cfg, host_storage, steps: int) -> dict:
     return out
 
 
+def swiglu_run(steps: int, calib_tokens: int = 128, alpha: float = 61.6) -> dict:
+    """The SwiGLU model shape (Sec. 4: d 4096, intermediate 14336, fp16, the
+    K_max = 5500 budget) with magnitude-threshold sparsity (eq. 1, Sec. 3.2):
+    per-layer thresholds calibrated on the GPU from calib_tokens synthetic
+    tokens at alpha = 61.6 (38.4% of the activations kept), then the decode
+    step with the centroid predictor and the thresholded SwiGLU MLP.  Reports
+    the calibration kernels against their rooflines and the step rate."""
+    import numpy as np
+    import torch
+
+    from paper_2608_22643_amd import binding as B
+    from paper_2608_22643_amd import calibrate
+    from paper_2608_22643_amd import workload as W
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get("7b_swiglu")
+    L, F, d = cfg.layers, cfg.d_ffn, cfg.d_model
+    esz = W.ITEMSIZE[cfg.wdtype]
+    T = 1 + 4 + 2 * steps + 8
+    hs = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
+    W.fill_storage(cfg, hs.data_ptr())
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T, host_storage=hs,
+                          predictor="centroid")
+    del hs
+    xc = W.hidden(cfg.with_(seed=cfg.seed + 101), calib_tokens)
+    xc = torch.from_numpy(np.ascontiguousarray(xc).view(np.uint8).reshape(-1).copy()).cuda()
+    acts = torch.empty(L * calib_tokens * F, dtype=torch.float32, device="cuda")
+    thr = calibrate.thresholds(cfg, pipe.storage, xc, calib_tokens, alpha, pipe.ws, acts=acts)
+    torch.cuda.synchronize()
+    # the calibration kernels, timed on their stream
+    shape = pipe.shape
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    layer_bytes = F * cfg.record_bytes
+    stream = torch.cuda.current_stream()
+    ev[0].record(stream)
+    for l in range(L):
+        B.np_act_batch(shape, pipe.storage.data_ptr() + l * layer_bytes, xc, calib_tokens,
+                       acts.data_ptr() + l * calib_tokens * F * 4, pipe.ws, stream)
+    ev[1].record(stream)
+    out = torch.empty(L, dtype=torch.float32, device="cuda")
+    B.np_percentile(acts, L, calib_tokens * F, alpha, out, pipe.ws, stream)
+    ev[2].record(stream)
+    torch.cuda.synchronize()
+    ab_us = ev[0].elapsed_time(ev[1]) * 1e3 / L
+    pct_us = ev[1].elapsed_time(ev[2]) * 1e3
+    if not torch.equal(out, thr):
+        raise RuntimeError("calibration: thresholds differ between two identical runs")
+    ab_bytes = F * 2 * d * esz + calib_tokens * d * esz + calib_tokens * F * 4
+    ab_flops = 4.0 * F * d * calib_tokens
+    ab_gbps = ab_bytes / (ab_us * 1e-6) / 1e9
+    kept = float((acts.view(L, -1).abs() >= thr.view(L, 1)).float().mean())
+    pipe.set_thresholds(thr)
+    for i in range(5):
+        pipe.step(i)
+    wall, _ = timed_steps(pipe, 5, steps, with_mlp_events=False)
+    _, mlp_us = timed_steps(pipe, 5 + steps, steps)
+    counts = []  # rows per np_sparse_mlp_t call, over a few more tokens
+    for i in range(6):
+        pipe.step(5 + 2 * steps + i)
+        counts.append(pipe.active_counts.cpu().numpy()[:L].mean())
+    if pipe.device_error():
+        raise RuntimeError(f"swiglu run: device error word {pipe.device_error():#x}")
+    rows = float(np.mean(counts))
+    mlp_bytes = rows * 3 * d * esz
+    mlp_gbps = mlp_bytes / (mlp_us * 1e-6) / 1e9
+    res = {"config": f"{L} downstream layers, d={d}, F={F}, K_max={cfg.k}, C={cfg.capacity}, "
+                     f"{cfg.wdtype}, SwiGLU, centroid predictor, eq. 1 thresholds",
+           "tok_s": round(steps / wall, 2), "ms_per_step": round(wall * 1e3 / steps, 4),
+           "mean_active_per_layer": round(rows, 1),
+           "mlp_us_per_call": round(mlp_us, 3), "mlp_GBps": round(mlp_gbps, 1),
+           "mlp_frac": round(mlp_gbps / HBM_PEAK_GBPS, 4),
+           "calibration": {
+               "tokens": calib_tokens, "alpha": alpha,
+               "kept_fraction": round(kept, 4),
+               "threshold_mean": round(float(thr.mean()), 5),
+               "act_batch_us_per_layer": round(ab_us, 2),
+               "act_batch_roofline": {"bound": "hbm", "achieved": round(ab_gbps, 1),
+                                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                      "frac": round(ab_gbps / HBM_PEAK_GBPS, 4),
+                                      "bytes_per_launch": ab_bytes,
+                                      "mfma_TFLOPs": round(ab_flops / (ab_us * 1e-6) / 1e12, 1),
+                                      "mfma_peak_TFLOPs": 2500.0},
+               "percentile_us": round(pct_us, 1),
+               "percentile_values": L * calib_tokens * F}}
+    del pipe, acts
+    torch.cuda.empty_cache()
+    return res
+
+
 def dense_mlp_roofline(cfg, host_storage, reps: int = 3) -> dict:
     """np_dense_mlp over every layer of the storage tier (all F records of a
     layer: the dense prefix's MLP), back to back, against the HBM roofline."""
@@ -445,6 +534,8 @@ def main():
     ap.add_argument("--dense-steps", type=int, default=10)
     ap.add_argument("--centroid-steps", type=int, default=30,
                     help="steps with the centroid-ID predictor (0: skip)")
+    ap.add_argument("--swiglu-steps", type=int, default=30,
+                    help="steps of the SwiGLU 7B shape with calibrated eq. 1 thresholds (0: skip)")
     ap.add_argument("--calib-mib", type=int, default=256,
                     help="size of one plain device-to-device copy run after the timing, "
                          "the reference for hardware byte counters")
@@ -574,6 +665,10 @@ def main():
     if args.centroid_steps > 0:
         centroid = centroid_run(cfg, host_storage, args.centroid_steps)
         log(f"[bench] centroid predictor: {centroid}")
+    swiglu = None
+    if args.swiglu_steps > 0:
+        swiglu = swiglu_run(args.swiglu_steps)
+        log(f"[bench] swiglu: {swiglu}")
     if args.calib_mib > 0:  # a copy of known size: reads and writes calib_mib MiB once
         src = torch.ones(args.calib_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -626,6 +721,7 @@ def main():
         "dense_mlp": dense,
         "dense_prefix_sweep": sweep,
         "centroid_predictor": centroid,
+        "swiglu_7b": swiglu,
         "other_configs": extra or None,
     }
     print(json.dumps(line), flush=True)

@@ -16,6 +16,10 @@ Staging modes:
             each chunk goes over with hipMemcpyAsync on a side stream, then a
             scatter kernel places the records.  Needs the "host" tier.
 
+The MLP's gated form follows cfg.act (ReLU-gated or SwiGLU).  With
+thresholds (one per downstream layer, e.g. from calibrate.thresholds) every
+sparse layer applies eq. 1 to its active rows (np_sparse_mlp_t).
+
 With dense_layers = d > 0, d dense-prefix layers (all F records of each kept
 resident, Sec. 3.1) run with np_dense_mlp after staging is enqueued and
 before the sparse layers, so side-stream staging overlaps them.
@@ -59,7 +63,7 @@ class DecodePipeline:
                  staging: str = "gather", overlap: bool = False, tokens: int | None = None,
                  staging_mib: int = 64, landing_mib: int = 32,
                  host_storage: torch.Tensor | None = None, predictor: str = "lowrank",
-                 dense_layers: int = 0):
+                 dense_layers: int = 0, thresholds=None):
         if predictor not in ("lowrank", "centroid"):
             raise ValueError(f"unknown predictor {predictor!r}")
         if dense_layers < 0:
@@ -73,6 +77,9 @@ class DecodePipeline:
         L, d, F, r, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.rank, cfg.k, cfg.capacity
         self.shape = B.make_shape(L, d, F, r, k, C, cfg.wdtype, cfg.adtype, cfg.act)
         B.np_shape_check(self.shape)
+        self.thr = None  # eq. 1 thresholds, device float32 [L']
+        if thresholds is not None:
+            self.set_thresholds(thresholds)
         self.T = cfg.tokens if tokens is None else tokens
         dev = torch.device(device)
         # inputs resident in HBM: predictor factors and hidden states
@@ -288,7 +295,11 @@ class DecodePipeline:
         for l in range(L):
             if ready is not None and ready[l] is not None:
                 main.wait_event(ready[l])
-            if centroid:
+            if self.thr is not None:
+                B.np_sparse_mlp_t(s, l, x_ptr, self.resident, slots.data_ptr() + l * k * 4, k,
+                                  self.active_counts if centroid else None, self.thr,
+                                  self.y.data_ptr() + l * ybytes, self.ws, main)
+            elif centroid:
                 B.np_sparse_mlp_n(s, l, x_ptr, self.resident, slots.data_ptr() + l * k * 4,
                                   self.active_counts, self.y.data_ptr() + l * ybytes, self.ws,
                                   main)
@@ -297,6 +308,15 @@ class DecodePipeline:
                                 self.y.data_ptr() + l * ybytes, self.ws, main)
         if mlp_block_events is not None:
             mlp_block_events[1].record(main)
+
+    def set_thresholds(self, thresholds) -> None:
+        """Eq. 1 thresholds of the downstream layers (float32 [L'], host or
+        device); every later step applies them.  Not for a captured graph:
+        set them before capture_graph."""
+        t = torch.as_tensor(thresholds, dtype=torch.float32).reshape(-1)
+        if t.numel() != self.cfg.layers:
+            raise ValueError(f"need {self.cfg.layers} thresholds, got {t.numel()}")
+        self.thr = t.to(self.device).contiguous()
 
     def device_error(self) -> int:
         return B.np_device_error(self.ws, self.main)

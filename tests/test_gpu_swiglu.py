@@ -16,7 +16,7 @@ import torch
 import oracle as orc
 from paper_2608_22643_amd import binding as B
 from paper_2608_22643_amd import workload as W
-from gpu_util import DEV, Bufs, decode_y, mlp_tolerance, say, to_dev
+from gpu_util import DEV, Bufs, compare_delta, decode_y, mlp_tolerance, say, to_dev
 from test_gpu_parity import SHAPES
 
 pytestmark = pytest.mark.gpu
@@ -299,3 +299,70 @@ def test_calibration_chain_7b_swiglu():
     got_y = decode_y(orc, cfg.adtype, y.cpu().numpy().view(np.uint16))
     assert np.all(np.abs(got_y - ref64) <= mlp_tolerance(cfg.adtype, ref64) + extra)
     assert B.np_device_error(ws) == 0
+
+
+# ---------------- calibration + the decode path with thresholds ------------------
+
+@pytest.mark.parametrize("graph", [False, True])
+def test_swiglu_centroid_threshold_pipeline(graph):
+    """Thresholds from calibrate.thresholds (bit for bit the oracle's
+    percentile of the GPU's activations, those within the O9 bound), then the
+    decode path with the centroid predictor and the thresholded SwiGLU MLP,
+    token by token against the oracle."""
+    from paper_2608_22643_amd import calibrate
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get("tiny_swiglu").with_(centroid_k=64, feat_dim=128)
+    L, d, F, K, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.centroid_k, cfg.k, cfg.capacity
+    n = 48
+    say(f"[swiglu pipeline] graph={graph}")
+    store = W.storage(cfg)
+    xc = W.hidden(cfg.with_(seed=cfg.seed + 101), n)
+    bufs = Bufs(cfg)
+    bufs.reset()
+    acts = torch.empty(L * n * F, dtype=torch.float32, device=DEV)
+    thr = calibrate.thresholds(cfg, to_dev(store), to_dev(xc), n, 55.0, bufs.ws, acts=acts)
+    torch.cuda.synchronize()
+    ah = acts.cpu().numpy().reshape(L, n * F)
+    Th = thr.cpu().numpy()
+    assert np.array_equal(Th, orc.percentile(ah, 55.0))
+    for l in range(L):
+        rows = [0, n - 1]
+        ref = orc.act_batch(cfg, store[l], xc[rows], 2)
+        g, u, sg, su = parts(cfg, store[l], xc[rows])
+        bound, _ = act_bound(cfg, g, u, sg, su)
+        assert np.all(np.abs(ah[l].reshape(n, F)[rows] - ref) <= bound), l
+    T = 6
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T, predictor="centroid",
+                          thresholds=thr)
+    if graph:
+        pipe.capture_graph()
+    h = W.hidden(cfg, T)
+    bank = W.centroid_bank(cfg)
+    st = orc.State(L, F, C)
+    for t in range(T):
+        pipe.step_graph(t) if graph else pipe.step(t)
+        torch.cuda.synchronize()
+        logits = pipe.logits.cpu().numpy().reshape(2 * L, K)
+        o = orc.centroid_active(logits, bank, L, F, K, k)
+        cnt = pipe.active_counts.cpu().numpy()[:L]
+        assert np.array_equal(cnt, o["counts"])
+        ref = orc.delta_n(t, o["active_ids"], o["counts"], st, C)
+        got = pipe.host_lists()
+        for l in range(L):
+            got["active_slots"][l][cnt[l]:] = -1
+        compare_delta(got, ref, L)
+        y = pipe.y.cpu().numpy().reshape(L, d).astype(np.float64)
+        for l in range(L):
+            ids = o["active_ids"][l][:cnt[l]].astype(np.int32)
+            _, ref64 = orc.sparse_mlp(cfg, l, h[t], store, ids, want_f64=True,
+                                      threshold=float(Th[l]))
+            g, u, sg, su = parts(cfg, store[l][ids], h[t])
+            bound, a = act_bound(cfg, g[0], u[0], sg[0], su[0])
+            near = np.abs(np.abs(a) - Th[l]) <= bound
+            extra = 0.0
+            if near.any():
+                D = np.abs(orc.decode(cfg.wdtype, store[l][ids][near][:, 2 * d:]))
+                extra = np.abs(a[near]) @ D
+            assert np.all(np.abs(y[l] - ref64) <= mlp_tolerance("f32", ref64) + extra), (t, l)
+    assert pipe.device_error() == 0
