@@ -202,6 +202,60 @@ def staging_rates(pipe, t0: int, steps: int) -> dict:
             "h2d_peak_GBps": round(h2d_peak_gbps(), 2)}
 
 
+def file_tier_run(cfg, host_storage, steps: int) -> dict:
+    """The storage tier as a file on the local disk (Sec. 3.5: neuron-centric
+    layer-major file, O_DIRECT, io_uring at queue depth 256): the decode step
+    with file staging, the staging rate (reads + copies + scatter), and the
+    record-read rate of np_read_records on a token-like read list (about 70
+    sorted random records per layer) at queue depths 1, 32 and 256."""
+    import os
+
+    import numpy as np
+    import torch
+
+    from paper_2608_22643_amd import binding as B
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    T = 1 + 3 + 2 * steps + 4
+    t = time.perf_counter()
+    # staging halves (and the read buffer) of 128 MiB: a token's delta is
+    # read as one batch, the paper's token-level submission
+    pipe = DecodePipeline(cfg, tier="file", staging="file", overlap=True, tokens=T,
+                          host_storage=host_storage, staging_mib=256, landing_mib=128)
+    write_s = time.perf_counter() - t
+    for i in range(4):
+        pipe.step(i)
+    torch.cuda.synchronize()
+    wall, _ = timed_steps(pipe, 4, steps, with_mlp_events=False)
+    rates = staging_rates(pipe, 4 + steps, max(3, steps // 2))
+    rec = cfg.record_bytes
+    rng = np.random.default_rng(1)
+    ids = np.concatenate([l * cfg.d_ffn + np.sort(rng.choice(cfg.d_ffn, 70, replace=False))
+                          for l in range(cfg.layers)]).astype(np.int32)
+    dst = B.HostBuffer(ids.size * rec)  # ordinary memory: the target of direct reads
+    reads = {}
+    for qd in (1, 32, 256):
+        os.environ["NP_IO_QD"] = str(qd)
+        t = time.perf_counter()
+        B.np_read_records(pipe.storage_fd, 0, rec, ids.ctypes.data, ids.size, dst)
+        reads[f"qd{qd}_GBps"] = round(ids.size * rec / (time.perf_counter() - t) / 1e9, 2)
+    os.environ.pop("NP_IO_QD", None)
+    if pipe.device_error():
+        raise RuntimeError(f"file tier: device error word {pipe.device_error():#x}")
+    out = {"tok_s": round(steps / wall, 2), "ms_per_step": round(wall * 1e3 / steps, 3),
+           "direct_io": pipe.storage_direct, "file_GB": round(cfg.storage_bytes / 1e9, 2),
+           "file_write_s": round(write_s, 1),
+           "stage_GBps": rates["staging_h2d_GBps"],
+           "staged_MB_per_token": rates["staged_MB_per_token"],
+           "record_reads": dict(reads, records=int(ids.size), MB=round(ids.size * rec / 1e6, 1)),
+           "note": "local virtio block device of the GPU host (no NVMe present); O_DIRECT "
+                   "reads bypass the page cache"}
+    pipe.close()
+    del pipe, dst
+    torch.cuda.empty_cache()
+    return out
+
+
 def delta_stats(pipe):
     import numpy as np
 
@@ -534,6 +588,8 @@ def main():
     ap.add_argument("--dense-steps", type=int, default=10)
     ap.add_argument("--centroid-steps", type=int, default=30,
                     help="steps with the centroid-ID predictor (0: skip)")
+    ap.add_argument("--file-tier-steps", type=int, default=10,
+                    help="steps with the storage tier in a local file (0: skip)")
     ap.add_argument("--swiglu-steps", type=int, default=30,
                     help="steps of the SwiGLU 7B shape with calibrated eq. 1 thresholds (0: skip)")
     ap.add_argument("--calib-mib", type=int, default=256,
@@ -655,6 +711,10 @@ def main():
         host.update(staging_rates(hp, 4 + args.host_tier_steps, max(3, args.host_tier_steps // 4)))
         log(f"[bench] host tier: {host}")
         del hp, hg
+    file_tier = None
+    if args.file_tier_steps > 0:
+        file_tier = file_tier_run(cfg, host_storage, args.file_tier_steps)
+        log(f"[bench] file tier: {file_tier}")
     dense = dense_mlp_roofline(cfg, host_storage)
     log(f"[bench] dense MLP: {dense}")
     sweep = None
@@ -717,6 +777,7 @@ def main():
         "breakdown_us": bd,
         "delta": stats,
         "host_tier": host,
+        "file_tier": file_tier,
         "cpu_baseline": cpu,
         "dense_mlp": dense,
         "dense_prefix_sweep": sweep,

@@ -11,6 +11,7 @@
  *   np_delta       active set vs. the GPU-resident row buffer -> incoming rows,
  *                  evicted slots, hits; updates the slot map (Sec. 3.4, eqs. 2-3)
  *   np_stage_rows  incoming neuron records, storage tier -> their device slots
+ *                  (np_stage_file: the storage tier in a file, read with io_uring)
  *   np_sparse_mlp  ReLU-gated MLP over the resident active rows of one layer
  *
  * and, for the paper's own predictor (centroid IDs, variable-size sets):
@@ -86,7 +87,8 @@ typedef enum np_status {
   NP_ERR_CAPACITY = 2,    /* k > C, staging buffer smaller than one record, ... */
   NP_ERR_HIP = 3,         /* a HIP runtime call failed; detail in np_last_error() */
   NP_ERR_UNSUPPORTED = 4, /* valid request this build does not implement */
-  NP_ERR_STATE = 5        /* reserved */
+  NP_ERR_STATE = 5,       /* reserved */
+  NP_ERR_IO = 6           /* a storage-tier file read failed (detail in np_last_error()) */
 } np_status;
 
 typedef enum np_dtype { NP_F32 = 0, NP_F16 = 1, NP_BF16 = 2 } np_dtype;
@@ -255,6 +257,40 @@ np_status np_stage_rows(const np_shape* shape, const np_stage_plan* plan,
                         void* dev_landing, size_t landing_bytes,
                         hipStream_t side, hipEvent_t wait_before,
                         hipEvent_t* layer_ready);
+
+/* np_stage_rows with the storage tier in a file (Sec. 3.5, I/O path): the
+ * file holds the [L'][F][3d] records starting at byte file_offset (the
+ * neuron-centric, layer-major layout).  The coalesced record ranges of each
+ * chunk are read through Linux io_uring with up to 256 reads in flight
+ * (NP_IO_QD lowers it) into io_buffer, copied into the pinned staging half
+ * by the worker threads, then sent and scattered as in np_stage_rows.
+ * io_buffer: ordinary host memory of io_buffer_bytes (a chunk holds at most
+ * io_buffer_bytes of records), owned by the caller; NULL reads straight into
+ * host_staging.  Memory pinned through the HIP runtime cannot be the target
+ * of a direct (O_DIRECT) read on this platform (the read fails with EFAULT),
+ * so a direct-I/O descriptor needs io_buffer.  fd: a readable descriptor
+ * owned by the caller; opened with O_DIRECT, the reads bypass the page cache
+ * and the record size, file_offset and the read target must be multiples of
+ * 512 bytes.  A failed or short read (end of file) returns NP_ERR_IO; chunks
+ * already enqueued stay enqueued.  Everything else as np_stage_rows. */
+np_status np_stage_file(const np_shape* shape, const np_stage_plan* plan,
+                        int32_t layer_begin, int32_t layer_end, int32_t fd,
+                        int64_t file_offset, void* dev_resident, void* host_staging,
+                        size_t host_staging_bytes, void* io_buffer, size_t io_buffer_bytes,
+                        void* dev_landing, size_t dev_landing_bytes, hipStream_t side,
+                        hipEvent_t wait_before, hipEvent_t* layer_ready);
+
+/* Host-side record gather from a storage-tier file (the reads of
+ * np_stage_file without the device steps): dst[j] <- the record_bytes
+ * record at file_offset + ids[j] * record_bytes, for j < n, with runs of
+ * consecutive ids read as one range and up to 256 reads in flight through
+ * io_uring.  dst: host memory of n * record_bytes bytes (ordinary memory
+ * for an O_DIRECT fd, see np_stage_file).  With an O_DIRECT fd, file_offset,
+ * record_bytes and dst must be multiples of 512.  Returns
+ * NP_ERR_IO when a read fails or the file ends early.  Synchronous; calls
+ * from several threads are serialised. */
+np_status np_read_records(int32_t fd, int64_t file_offset, int64_t record_bytes,
+                          const int32_t* ids, int32_t n, void* dst);
 
 /* Staging without a host round trip: one kernel per call copies, for layers
  * [layer_begin, layer_end), resident[l][in_slots[l][j]] <- storage[l][in_ids[l][j]]

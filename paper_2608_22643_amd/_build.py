@@ -17,7 +17,7 @@ LIB = os.path.join(HERE, "libneuroprefetch.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["np_abi.cpp", "np_stage_host.cpp", "np_predict.hip", "np_select.hip",
+SOURCES = ["np_abi.cpp", "np_stage_host.cpp", "np_file.cpp", "np_predict.hip", "np_select.hip",
            "np_stage.hip", "np_mlp.hip", "np_calib.hip"]
 
 FLAGS = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}", "-Wall",

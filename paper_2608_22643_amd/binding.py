@@ -14,7 +14,8 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libneuroprefetch.so")
 
-NP_OK, NP_ERR_INVALID_ARG, NP_ERR_CAPACITY, NP_ERR_HIP, NP_ERR_UNSUPPORTED, NP_ERR_STATE = range(6)
+(NP_OK, NP_ERR_INVALID_ARG, NP_ERR_CAPACITY, NP_ERR_HIP, NP_ERR_UNSUPPORTED, NP_ERR_STATE,
+ NP_ERR_IO) = range(7)
 NP_F32, NP_F16, NP_BF16 = 0, 1, 2
 DTYPE_CODE = {"f32": NP_F32, "f16": NP_F16, "bf16": NP_BF16}
 NP_ACT_RELU, NP_ACT_SWIGLU = 0, 1
@@ -31,7 +32,8 @@ EXPORTS = ("np_status_str", "np_last_error", "np_shape_check", "np_workspace_siz
            "np_state_reset", "np_predict", "np_select", "np_delta", "np_stage_rows",
            "np_stage_gather", "np_sparse_mlp", "np_centroid_select", "np_delta_n",
            "np_sparse_mlp_n", "np_dense_mlp", "np_sparse_mlp_t", "np_act_batch",
-           "np_percentile", "np_threshold_active", "np_device_error")
+           "np_percentile", "np_threshold_active", "np_stage_file", "np_read_records",
+           "np_device_error")
 
 
 class NPError(RuntimeError):
@@ -105,6 +107,10 @@ def lib():
         L.np_act_batch.argtypes = [S, vp, vp, i32, vp, vp, vp]
         L.np_percentile.argtypes = [vp, i32, ctypes.c_int64, ctypes.c_double, vp, vp, vp]
         L.np_threshold_active.argtypes = [S, vp, i32, vp, vp, vp, vp, vp, vp]
+        i64 = ctypes.c_int64
+        L.np_stage_file.argtypes = [S, ctypes.POINTER(np_stage_plan), i32, i32, i32, i64, vp, vp,
+                                    sz, vp, sz, vp, sz, vp, vp, vp]
+        L.np_read_records.argtypes = [i32, i64, i64, vp, i32, vp]
         for f in EXPORTS[2:]:
             getattr(L, f).restype = i32
         _lib = L
@@ -188,6 +194,41 @@ def np_stage_rows(shape, plan: np_stage_plan, layer_begin: int, layer_end: int, 
                                _p(host_staging), int(staging_bytes), _p(dev_landing),
                                int(landing_bytes), _s(side), _ev(wait_before), ev_arr),
            "np_stage_rows")
+
+
+def np_stage_file(shape, plan: np_stage_plan, layer_begin: int, layer_end: int, fd: int,
+                  file_offset: int, dev_resident, host_staging, staging_bytes: int, io_buffer,
+                  io_buffer_bytes: int, dev_landing, landing_bytes: int, side=None,
+                  wait_before=None, layer_ready=None) -> None:
+    ev_arr = None
+    if layer_ready is not None:
+        ev_arr = (ctypes.c_void_p * len(layer_ready))(*[_ev(e) for e in layer_ready])
+    _check(lib().np_stage_file(ctypes.byref(shape), ctypes.byref(plan), int(layer_begin),
+                               int(layer_end), int(fd), int(file_offset), _p(dev_resident),
+                               _p(host_staging), int(staging_bytes), _p(io_buffer),
+                               int(io_buffer_bytes), _p(dev_landing), int(landing_bytes),
+                               _s(side), _ev(wait_before), ev_arr), "np_stage_file")
+
+
+class HostBuffer:
+    """Ordinary page-aligned host memory (an anonymous mapping): the read
+    target of direct file I/O.  `ptr` is its address; it lives as long as
+    this object."""
+
+    def __init__(self, nbytes: int):
+        import mmap
+
+        self.nbytes = int(nbytes)
+        self._map = mmap.mmap(-1, max(self.nbytes, 1))
+        self.ptr = ctypes.addressof(ctypes.c_char.from_buffer(self._map))
+
+    def data_ptr(self) -> int:
+        return self.ptr
+
+
+def np_read_records(fd: int, file_offset: int, record_bytes: int, ids, n: int, dst) -> None:
+    _check(lib().np_read_records(int(fd), int(file_offset), int(record_bytes), _p(ids), int(n),
+                                 _p(dst)), "np_read_records")
 
 
 def np_stage_gather(shape, out: np_delta_out, layer_begin: int, layer_end: int, storage,

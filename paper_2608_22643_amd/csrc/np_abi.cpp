@@ -75,6 +75,7 @@ const char* np_status_str(int32_t st) {
     case NP_ERR_HIP: return "NP_ERR_HIP";
     case NP_ERR_UNSUPPORTED: return "NP_ERR_UNSUPPORTED";
     case NP_ERR_STATE: return "NP_ERR_STATE";
+    case NP_ERR_IO: return "NP_ERR_IO";
     default: return "NP_ERR_UNKNOWN";
   }
 }

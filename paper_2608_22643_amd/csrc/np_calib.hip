@@ -14,43 +14,45 @@ namespace np {
 // ---------------------------------------------------------------------------
 // The gate and up projections of a batch are two matrix products, G X^T and
 // U X^T (neurons x tokens, reduction over d), so they run on MFMA with fp32
-// accumulation.  Each 32 x 32 output tile is a v_mfma_f32_32x32x16 (16-bit
-// types) or four v_mfma_f32_32x32x2f32 (fp32) per "step" of 2*V reduction
-// elements: lane l holds row l%32 of the A operand (a neuron's gate or up
-// record) and column l%32 of the B operand (a token), each as the V
-// consecutive elements starting at step*2V + V*(l/32), so the two operands
-// pair the same reduction indices whatever order the unit sums them in.  The
-// accumulator layout: lane l, register r holds output row
-// 8*(r/4) + 4*(l/32) + r%4 (neuron) and column l%32 (token).
+// accumulation: 16 x 16 output tiles, each a v_mfma_f32_16x16x32 (16-bit
+// types) or four v_mfma_f32_16x16x4f32 (fp32) per "step" of 4*V reduction
+// elements.  Lane l holds row l%16 of the A operand (a neuron's gate or up
+// row) and column l%16 of the B operand (a token), each as the V consecutive
+// elements starting at step*4V + V*(l/16), so the two operands pair the same
+// reduction indices whatever order the unit sums them in, and one 16-byte
+// load instruction reads 64 contiguous bytes of each of 16 rows.  The
+// accumulator layout: lane l, register r holds output row 4*(l/16) + r
+// (neuron) and column l%16 (token).
 //
-// A workgroup owns 32 neurons; its four waves split the reduction (d) into
-// quarters and hold every token tile of the launch (up to 4, 128 tokens), so
-// each record is read from HBM once per launch.  Operands come straight from
-// memory with 16-byte buffer loads (a record's row is contiguous in d; the
-// tokens are L2-resident); the quarters meet in LDS, one token tile at a
-// time, and wave 0 applies the activation and writes acts[token][neuron].
+// A workgroup owns 32 neurons (two row tiles that share every token
+// fragment); its four waves split the reduction (d) into quarters and hold
+// every token tile of the launch (up to 8, 128 tokens), so each record is
+// read from HBM once per launch.  Operands come straight from memory with
+// 16-byte buffer loads (a record's row is contiguous in d; the tokens are
+// L2-resident); the quarters meet in LDS, two token tiles at a time, and wave
+// 0 applies the activation and writes acts[token][neuron].
 constexpr int AB_WAVES = 4;
-constexpr int AB_MAX_TILES = 4;
-constexpr int AB_UNROLL = 4;
+constexpr int AB_MAX_TILES = 8;   // token tiles of 16
+constexpr int AB_UNROLL = 2;
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 template <class T>
-__device__ inline f32x16 mfma_step(uint4 a, uint4 b, f32x16 c) {
+__device__ inline f32x4 mfma_step(uint4 a, uint4 b, f32x4 c) {
   if constexpr (T::dtype == NP_F16) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
   } else if constexpr (T::dtype == NP_BF16) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
   } else {
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
-    return __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0,
-                                                0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0,
+                                                0);
   }
 }
 
@@ -64,40 +66,50 @@ struct ActBatchArgs {
 
 template <class T, int NTT>
 __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs a) {
-  constexpr int V = T::V, ESZ = 16 / V, KS = 2 * V;
-  __shared__ float xch[AB_WAVES - 1][2][16][WAVE];  // one tile's quarters, wave 1..3
+  constexpr int V = T::V, ESZ = 16 / V, KS = 4 * V;
+  constexpr int XT = 2;  // token tiles exchanged per round
+  __shared__ f32x4 xch[AB_WAVES - 1][2][2][XT][WAVE];  // wave, g/u, row tile, tile, lane
   const int lane = threadIdx.x & (WAVE - 1), q = threadIdx.x / WAVE;
-  const int n0 = blockIdx.x * 32, grp = lane / 32;
-  const int row = n0 + (lane & 31);
+  const int n0 = blockIdx.x * 32, grp = lane / 16;
   const int steps = (a.d + KS - 1) / KS;
   const int s0 = q * steps / AB_WAVES, s1 = (q + 1) * steps / AB_WAVES;
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes), xr = make_rsrc(a.x, a.x_bytes);
   // byte offsets of this lane's operands at reduction index 0 (OOB past the
   // neurons / tokens of the launch)
-  const uint32_t rec = (uint32_t)(3 * a.d * ESZ);
-  const uint32_t g_off = row < a.F ? (uint32_t)row * rec : BUF_OOB;
+  const uint32_t rec = (uint32_t)(3 * a.d * ESZ), up = (uint32_t)(a.d * ESZ);
+  uint32_t r_off[2];
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    const int row = n0 + 16 * m + (lane & 15);
+    r_off[m] = row < a.F ? (uint32_t)row * rec : BUF_OOB;
+  }
   uint32_t t_off[NTT];
 #pragma unroll
   for (int t = 0; t < NTT; ++t) {
-    const int tok = t * 32 + (lane & 31);
+    const int tok = t * 16 + (lane & 15);
     t_off[t] = tok < a.n ? (uint32_t)tok * (uint32_t)(a.d * ESZ) : BUF_OOB;
   }
-  const uint32_t up = (uint32_t)(a.d * ESZ);
-  f32x16 accg[NTT], accu[NTT];
+  f32x4 accg[2][NTT], accu[2][NTT];
 #pragma unroll
-  for (int t = 0; t < NTT; ++t)
+  for (int m = 0; m < 2; ++m)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) accg[t][r] = accu[t][r] = 0.f;
+    for (int t = 0; t < NTT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) accg[m][t][r] = accu[m][t][r] = 0.f;
 
   for (int s = s0; s < s1; s += AB_UNROLL) {
-    uint4 ag[AB_UNROLL], au[AB_UNROLL], bx[AB_UNROLL][NTT];
+    uint4 ag[AB_UNROLL][2], au[AB_UNROLL][2], bx[AB_UNROLL][NTT];
 #pragma unroll
     for (int u = 0; u < AB_UNROLL; ++u) {
       const int k = (s + u) * KS + grp * V;  // first reduction index of the lane
       const bool ok = s + u < s1 && k < a.d;
       const uint32_t kb = (uint32_t)k * ESZ;
-      ag[u] = buf_load16(wr, ok && g_off != BUF_OOB ? g_off + kb : BUF_OOB, 0);
-      au[u] = buf_load16(wr, ok && g_off != BUF_OOB ? g_off + up + kb : BUF_OOB, 0);
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const bool rok = ok && r_off[m] != BUF_OOB;
+        ag[u][m] = buf_load16(wr, rok ? r_off[m] + kb : BUF_OOB, 0);
+        au[u][m] = buf_load16(wr, rok ? r_off[m] + up + kb : BUF_OOB, 0);
+      }
 #pragma unroll
       for (int t = 0; t < NTT; ++t)
         bx[u][t] = buf_load16(xr, ok && t_off[t] != BUF_OOB ? t_off[t] + kb : BUF_OOB, 0);
@@ -105,54 +117,58 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
 #pragma unroll
     for (int u = 0; u < AB_UNROLL; ++u)
 #pragma unroll
-      for (int t = 0; t < NTT; ++t) {
-        accg[t] = mfma_step<T>(ag[u], bx[u][t], accg[t]);
-        accu[t] = mfma_step<T>(au[u], bx[u][t], accu[t]);
-      }
-  }
-  // the quarters meet in LDS, tile by tile, in wave order
+      for (int t = 0; t < NTT; ++t)
 #pragma unroll
-  for (int t = 0; t < NTT; ++t) {
+        for (int m = 0; m < 2; ++m) {
+          accg[m][t] = mfma_step<T>(ag[u][m], bx[u][t], accg[m][t]);
+          accu[m][t] = mfma_step<T>(au[u][m], bx[u][t], accu[m][t]);
+        }
+  }
+  // the quarters meet in LDS, XT token tiles at a time, in wave order
+#pragma unroll
+  for (int t0 = 0; t0 < NTT; t0 += XT) {
     if (q > 0) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        xch[q - 1][0][r][lane] = accg[t][r];
-        xch[q - 1][1][r][lane] = accu[t][r];
-      }
+      for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int i = 0; i < XT; ++i)
+          if (t0 + i < NTT) {
+            xch[q - 1][0][m][i][lane] = accg[m][t0 + i];
+            xch[q - 1][1][m][i][lane] = accu[m][t0 + i];
+          }
     }
     __syncthreads();
     if (q == 0) {
-      float g[16], u[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        g[r] = accg[t][r];
-        u[r] = accu[t][r];
+      for (int i = 0; i < XT; ++i) {
+        if (t0 + i >= NTT) break;
+        const int tok = (t0 + i) * 16 + (lane & 15);
 #pragma unroll
-        for (int w = 0; w < AB_WAVES - 1; ++w) {
-          g[r] += xch[w][0][r][lane];
-          u[r] += xch[w][1][r][lane];
-        }
-      }
-      const int tok = t * 32 + (lane & 31);
-      if (tok < a.n) {
-        float* dst = a.acts + (size_t)tok * a.F;
+        for (int m = 0; m < 2; ++m) {
+          f32x4 g = accg[m][t0 + i], u = accu[m][t0 + i];
 #pragma unroll
-        for (int r0 = 0; r0 < 16; r0 += 4) {
-          const int nb = n0 + 8 * (r0 / 4) + 4 * grp;  // neurons nb .. nb + 3
-          float o[4];
+          for (int w = 0; w < AB_WAVES - 1; ++w) {
+            g += xch[w][0][m][i][lane];
+            u += xch[w][1][m][i][lane];
+          }
+          const int nb = n0 + 16 * m + 4 * grp;  // neurons nb .. nb + 3
+          if (tok < a.n) {
+            float* dst = a.acts + (size_t)tok * a.F;
+            float o[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) o[e] = gated(a.act, g[r0 + e], u[r0 + e]);
-          if ((a.F & 3) == 0) {
-            if (nb < a.F) *(float4*)(dst + nb) = make_float4(o[0], o[1], o[2], o[3]);
-          } else {
+            for (int e = 0; e < 4; ++e) o[e] = gated(a.act, g[e], u[e]);
+            if ((a.F & 3) == 0) {
+              if (nb < a.F) *(float4*)(dst + nb) = make_float4(o[0], o[1], o[2], o[3]);
+            } else {
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (nb + e < a.F) dst[nb + e] = o[e];
+              for (int e = 0; e < 4; ++e)
+                if (nb + e < a.F) dst[nb + e] = o[e];
+            }
           }
         }
       }
     }
-    __syncthreads();  // xch is reused by the next tile
+    __syncthreads();  // xch is reused by the next round
   }
 }
 
@@ -161,24 +177,25 @@ static hipError_t act_batch_t(const np_shape& s, const void* weights, const void
                               float* acts, hipStream_t stream) {
   constexpr int ESZ = 16 / T::V;
   const int tiles = (s.d_ffn + 31) / 32;
-  for (int i0 = 0; i0 < n; i0 += 32 * AB_MAX_TILES) {
+  for (int i0 = 0; i0 < n; i0 += 16 * AB_MAX_TILES) {
     ActBatchArgs a;
     a.w = weights;
     a.x = (const char*)x + (size_t)i0 * s.d_model * ESZ;
     a.acts = acts + (size_t)i0 * s.d_ffn;
-    a.n = std::min(n - i0, 32 * AB_MAX_TILES);
+    a.n = std::min(n - i0, 16 * AB_MAX_TILES);
     a.w_bytes = (uint32_t)((size_t)s.d_ffn * 3 * s.d_model * ESZ);
     a.x_bytes = (uint32_t)((size_t)a.n * s.d_model * ESZ);
     a.F = s.d_ffn;
     a.d = s.d_model;
     a.act = s.act;
-    const int ntt = (a.n + 31) / 32;
+    const int ntt = (a.n + 15) / 16;
 #define NP_AB_CASE(N) \
   hipLaunchKernelGGL((act_batch_kernel<T, N>), dim3(tiles), dim3(AB_WAVES * WAVE), 0, stream, a)
-    if (ntt == 1) NP_AB_CASE(1);
-    else if (ntt == 2) NP_AB_CASE(2);
-    else if (ntt == 3) NP_AB_CASE(3);
-    else NP_AB_CASE(4);
+    if (ntt <= 1) NP_AB_CASE(1);
+    else if (ntt <= 2) NP_AB_CASE(2);
+    else if (ntt <= 4) NP_AB_CASE(4);
+    else if (ntt <= 6) NP_AB_CASE(6);
+    else NP_AB_CASE(8);
 #undef NP_AB_CASE
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "neuroprefetch.h"
 
 namespace np {
@@ -82,6 +84,25 @@ hipError_t launch_percentile(const float* values, int rows, int64_t n, int64_t m
 hipError_t launch_threshold_active(const np_shape& s, const float* acts, int rows,
                                    const float* thr, uint32_t* mask, int32_t* active_ids,
                                    int32_t* active_counts, void* ws, hipStream_t stream);
+
+// storage-tier file reads (np_file.cpp): io_uring, up to IO_QD_MAX requests
+// in flight, runs cut into pieces of IO_PIECE bytes; an O_DIRECT file needs
+// offsets, sizes and buffers aligned to IO_ALIGN bytes
+constexpr int IO_QD_MAX = 256;
+constexpr size_t IO_PIECE = (size_t)1 << 20;
+constexpr int IO_ALIGN = 512;
+struct ReadRun {
+  char* dst;
+  uint64_t offset;  // file offset
+  size_t bytes;
+};
+int io_depth();  // NP_IO_QD clamped to [1, IO_QD_MAX], default IO_QD_MAX
+bool file_is_direct(int fd);
+// done (optional): called on the calling thread for each piece once it is
+// read in full (dst, bytes), while the other reads are still in flight
+typedef void (*PieceDone)(void* ctx, char* dst, size_t bytes);
+np_status read_runs(int fd, const std::vector<ReadRun>& runs, int qd, PieceDone done = nullptr,
+                    void* ctx = nullptr);
 
 // host-side helpers shared by the ABI files (np_abi.cpp)
 np_status fail(np_status st, const char* fmt, ...);

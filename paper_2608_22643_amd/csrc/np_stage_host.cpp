@@ -6,7 +6,9 @@
 // that scatters the chunk's records into their slots.  The staging area is
 // used as two halves so that packing one chunk overlaps the copy of the
 // previous one; a delta larger than a chunk runs as several independent
-// submit-and-scatter chunks.
+// submit-and-scatter chunks.  The source is the storage tier in host memory
+// (np_stage_rows: the ranges are copied by a thread pool) or in a file
+// (np_stage_file: the ranges are read through io_uring, np_file.cpp).
 #include <stdlib.h>
 #include <string.h>
 
@@ -109,26 +111,42 @@ static DeviceStaging* device_staging(int dev) {
   return (dev >= 0 && dev < 64) ? &slots[dev] : nullptr;
 }
 
-}  // namespace np
+// Where the records come from: host memory (`host`) or a file (`fd` >= 0,
+// the storage tier starting at byte `file_offset`), read into `io_buf`
+// (ordinary host memory of io_bytes bytes; nullptr: straight into staging).
+struct StageSource {
+  const char* host;
+  int fd;
+  int64_t file_offset;
+  char* io_buf;
+  size_t io_bytes;
+};
 
-using namespace np;
-
-extern "C" np_status np_stage_rows(const np_shape* s, const np_stage_plan* plan, int32_t lb,
-                                   int32_t le, const void* host_storage, void* dev_resident,
-                                   void* host_staging, size_t staging_bytes, void* dev_landing,
-                                   size_t landing_bytes, hipStream_t side, hipEvent_t wait_before,
-                                   hipEvent_t* layer_ready) {
+static np_status stage_common(const char* fn, const np_shape* s, const np_stage_plan* plan,
+                              int32_t lb, int32_t le, const StageSource& src, void* dev_resident,
+                              void* host_staging, size_t staging_bytes, void* dev_landing,
+                              size_t landing_bytes, hipStream_t side, hipEvent_t wait_before,
+                              hipEvent_t* layer_ready) {
   np_status st = check_shape(s);
   if (st != NP_OK) return st;
   if (lb < 0 || le > s->layers || lb > le)
     return fail(NP_ERR_INVALID_ARG, "layer range [%d, %d) outside [0, %d)", lb, le, s->layers);
   if (!plan || !plan->counts || !plan->in_ids || !plan->in_slots)
-    return fail(NP_ERR_INVALID_ARG, "np_stage_rows: plan arrays must be non-NULL");
-  if (!host_storage || !host_staging || !aligned16(dev_resident) || !aligned16(dev_landing))
-    return fail(NP_ERR_INVALID_ARG, "np_stage_rows: buffers must be non-NULL (device: aligned)");
+    return fail(NP_ERR_INVALID_ARG, "%s: plan arrays must be non-NULL", fn);
+  if ((src.fd < 0 && !src.host) || !host_staging || !aligned16(dev_resident) ||
+      !aligned16(dev_landing))
+    return fail(NP_ERR_INVALID_ARG, "%s: buffers must be non-NULL (device: aligned)", fn);
   const size_t rec = (size_t)3 * s->d_model * dtype_size(s->wdtype);
-  const size_t half = (staging_bytes / 2) & ~(size_t)255;
-  const size_t cap_bytes = std::min(half, landing_bytes);
+  // halves on 4 KiB boundaries, so that direct file reads land aligned
+  const size_t half = (staging_bytes / 2) & ~(size_t)4095;
+  const void* read_target = src.io_buf ? (const void*)src.io_buf : host_staging;
+  if (src.fd >= 0 && file_is_direct(src.fd) &&
+      (rec % IO_ALIGN || src.file_offset % IO_ALIGN || (uintptr_t)read_target % IO_ALIGN))
+    return fail(NP_ERR_INVALID_ARG,
+                "%s: an O_DIRECT file needs records (%zu B), the file offset and the read "
+                "buffer aligned to %d bytes", fn, rec, IO_ALIGN);
+  size_t cap_bytes = std::min(half, landing_bytes);
+  if (src.fd >= 0 && src.io_buf) cap_bytes = std::min(cap_bytes, src.io_bytes);
   const size_t chunk_cap = cap_bytes / (rec + sizeof(int32_t));
   if (chunk_cap < 1)
     return fail(NP_ERR_CAPACITY,
@@ -165,25 +183,31 @@ extern "C" np_status np_stage_rows(const np_shape* s, const np_stage_plan* plan,
     if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
   }
 
-  const char* storage = (const char*)host_storage;
   std::vector<PackPool::Task> tasks;
+  std::vector<ReadRun> reads;
   std::vector<int32_t> dst_rows;
   dst_rows.reserve(chunk_cap);
   int h = 0, chunks = 0;
   char* stg = nullptr;
   size_t n_in_chunk = 0;
-  // run being extended: source start and length in records
-  const char* run_src = nullptr;
+  // run being extended: source byte offset in the storage tier and length
+  // in records
+  uint64_t run_src = 0;
   size_t run_len = 0, run_dst = 0;
   const size_t piece = (size_t)256 << 10;
 
   auto close_run = [&]() {
     if (!run_len) return;
     size_t bytes = run_len * rec, off = 0;
-    while (off < bytes) {
-      size_t n = std::min(piece, bytes - off);
-      tasks.push_back({stg + run_dst * rec + off, run_src + off, n});
-      off += n;
+    if (src.fd >= 0) {
+      char* target = src.io_buf ? src.io_buf : stg;
+      reads.push_back({target + run_dst * rec, (uint64_t)src.file_offset + run_src, bytes});
+    } else {
+      while (off < bytes) {
+        size_t n = std::min(piece, bytes - off);
+        tasks.push_back({stg + run_dst * rec + off, src.host + run_src + off, n});
+        off += n;
+      }
     }
     run_len = 0;
   };
@@ -195,6 +219,7 @@ extern "C" np_status np_stage_rows(const np_shape* s, const np_stage_plan* plan,
     }
     stg = (char*)host_staging + (size_t)h * half;
     tasks.clear();
+    reads.clear();
     dst_rows.clear();
     n_in_chunk = 0;
     return NP_OK;
@@ -203,8 +228,24 @@ extern "C" np_status np_stage_rows(const np_shape* s, const np_stage_plan* plan,
     close_run();
     if (n_in_chunk == 0) return NP_OK;
     if (fail_after >= 0 && chunks >= fail_after)
-      return fail(NP_ERR_HIP, "np_stage_rows: injected staging failure after %d chunks", chunks);
-    pack_pool()->run(tasks);
+      return fail(NP_ERR_HIP, "%s: injected staging failure after %d chunks", fn, chunks);
+    if (src.fd >= 0) {
+      // each piece read into io_buf goes on to the same offset of the pinned
+      // half as soon as it is complete, overlapping the copies with the
+      // reads still in flight
+      struct Ctx {
+        char* io;
+        char* stg;
+      } cx{src.io_buf, stg};
+      PieceDone to_staging = [](void* c, char* dst, size_t n) {
+        Ctx* x = (Ctx*)c;
+        memcpy(x->stg + (dst - x->io), dst, n);
+      };
+      np_status rs = read_runs(src.fd, reads, io_depth(), src.io_buf ? to_staging : nullptr, &cx);
+      if (rs != NP_OK) return rs;
+    } else {
+      pack_pool()->run(tasks);
+    }
     memcpy(stg + n_in_chunk * rec, dst_rows.data(), n_in_chunk * sizeof(int32_t));
     const size_t bytes = n_in_chunk * (rec + sizeof(int32_t));
     hipError_t ee = hipMemcpyAsync(dev_landing, stg, bytes, hipMemcpyHostToDevice, side);
@@ -230,12 +271,12 @@ extern "C" np_status np_stage_rows(const np_shape* s, const np_stage_plan* plan,
         if ((st = begin_chunk()) != NP_OK) return st;
         open = true;
       }
-      const char* src = storage + ((size_t)l * s->d_ffn + ids[j]) * rec;
-      if (run_len && src == run_src + run_len * rec) {
+      const uint64_t at = ((uint64_t)l * s->d_ffn + ids[j]) * rec;
+      if (run_len && at == run_src + run_len * rec) {
         ++run_len;  // adjacent id: extend the contiguous range
       } else {
         close_run();
-        run_src = src;
+        run_src = at;
         run_len = 1;
         run_dst = n_in_chunk;
       }
@@ -257,4 +298,37 @@ extern "C" np_status np_stage_rows(const np_shape* s, const np_stage_plan* plan,
   }
   if (open && (st = flush()) != NP_OK) return st;
   return NP_OK;
+}
+
+}  // namespace np
+
+using namespace np;
+
+extern "C" np_status np_stage_rows(const np_shape* s, const np_stage_plan* plan, int32_t lb,
+                                   int32_t le, const void* host_storage, void* dev_resident,
+                                   void* host_staging, size_t staging_bytes, void* dev_landing,
+                                   size_t landing_bytes, hipStream_t side, hipEvent_t wait_before,
+                                   hipEvent_t* layer_ready) {
+  if (!host_storage) return fail(NP_ERR_INVALID_ARG, "np_stage_rows: host_storage is NULL");
+  return stage_common("np_stage_rows", s, plan, lb, le,
+                      {(const char*)host_storage, -1, 0, nullptr, 0},
+                      dev_resident, host_staging, staging_bytes, dev_landing, landing_bytes, side,
+                      wait_before, layer_ready);
+}
+
+extern "C" np_status np_stage_file(const np_shape* s, const np_stage_plan* plan, int32_t lb,
+                                   int32_t le, int32_t fd, int64_t file_offset,
+                                   void* dev_resident, void* host_staging, size_t staging_bytes,
+                                   void* io_buffer, size_t io_buffer_bytes, void* dev_landing,
+                                   size_t landing_bytes, hipStream_t side,
+                                   hipEvent_t wait_before, hipEvent_t* layer_ready) {
+  if (fd < 0 || file_offset < 0)
+    return fail(NP_ERR_INVALID_ARG, "np_stage_file: fd %d / file offset %lld", fd,
+                (long long)file_offset);
+  if (io_buffer && io_buffer_bytes == 0)
+    return fail(NP_ERR_INVALID_ARG, "np_stage_file: io_buffer of 0 bytes");
+  return stage_common("np_stage_file", s, plan, lb, le,
+                      {nullptr, fd, file_offset, (char*)io_buffer, io_buffer_bytes},
+                      dev_resident, host_staging, staging_bytes, dev_landing, landing_bytes, side,
+                      wait_before, layer_ready);
 }

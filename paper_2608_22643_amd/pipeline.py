@@ -15,14 +15,20 @@ Staging modes:
             memory, the host packs coalesced records into pinned staging and
             each chunk goes over with hipMemcpyAsync on a side stream, then a
             scatter kernel places the records.  Needs the "host" tier.
+  "file"    np_stage_file: as "memcpy", but the coalesced records are read
+            from the storage tier in a file (tier "file"; O_DIRECT when the
+            record size allows) through io_uring, up to 256 reads in flight
+            (Sec. 3.5).  The file is written once at set-up (storage_path, or
+            a temporary file removed by close()).
 
 The MLP's gated form follows cfg.act (ReLU-gated or SwiGLU).  With
 thresholds (one per downstream layer, e.g. from calibrate.thresholds) every
 sparse layer applies eq. 1 to its active rows (np_sparse_mlp_t).
 
 With dense_layers = d > 0, d dense-prefix layers (all F records of each kept
-resident, Sec. 3.1) run with np_dense_mlp after staging is enqueued and
-before the sparse layers, so side-stream staging overlaps them.
+resident, Sec. 3.1) run with np_dense_mlp, enqueued right after the delta and
+before staging starts, so the GPU computes them while the host reads and
+stages the sparse layers' rows.
 
 With overlap=True staging runs in a few layer chunks (layer 0, layers 1-2,
 the rest): the first on the main stream right after np_delta, the others on a
@@ -63,7 +69,7 @@ class DecodePipeline:
                  staging: str = "gather", overlap: bool = False, tokens: int | None = None,
                  staging_mib: int = 64, landing_mib: int = 32,
                  host_storage: torch.Tensor | None = None, predictor: str = "lowrank",
-                 dense_layers: int = 0, thresholds=None):
+                 dense_layers: int = 0, thresholds=None, storage_path: str | None = None):
         if predictor not in ("lowrank", "centroid"):
             raise ValueError(f"unknown predictor {predictor!r}")
         if dense_layers < 0:
@@ -72,6 +78,9 @@ class DecodePipeline:
         self.dense_layers = dense_layers
         if staging == "memcpy" and tier != "host":
             raise ValueError("memcpy staging reads a pinned host storage tier")
+        if (staging == "file") != (tier == "file"):
+            raise ValueError("the file tier is staged with staging='file' and only so")
+        self.storage_fd, self.storage_path, self._own_file = -1, None, False
         self.cfg, self.device, self.tier, self.staging, self.overlap = cfg, device, tier, staging, overlap
         torch.cuda.set_device(device)
         L, d, F, r, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.rank, cfg.k, cfg.capacity
@@ -100,6 +109,9 @@ class DecodePipeline:
             else:
                 self.storage = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
                 W.fill_storage(cfg, self.storage.data_ptr())
+        elif tier == "file":
+            self.storage = None
+            self._open_storage_file(storage_path, host_storage)
         else:
             self.storage = torch.empty(cfg.storage_bytes, dtype=torch.uint8, device=dev)
             if host_storage is not None:
@@ -161,13 +173,16 @@ class DecodePipeline:
         # staging chunks of the overlapped gather path: [0,1), [1,3), [3,L)
         cuts = sorted({0, min(1, L), min(3, L), L})
         self.chunks = list(zip(cuts[:-1], cuts[1:]))
-        if staging == "memcpy":
+        if staging in ("memcpy", "file"):
             self.plan_counts = torch.empty(L * 4, dtype=torch.int32, pin_memory=True)
             self.plan_ids = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
             self.plan_slots = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
             self.plan = B.np_stage_plan(self.plan_counts.data_ptr(), self.plan_ids.data_ptr(),
                                         self.plan_slots.data_ptr())
             self.staging_buf = torch.empty(staging_mib << 20, dtype=torch.uint8, pin_memory=True)
+            # file reads land in ordinary host memory (a direct read cannot
+            # target pinned memory), one staging half at a time
+            self.io_buf = B.HostBuffer((staging_mib << 20) // 2) if staging == "file" else None
             self.landing = torch.empty(landing_mib << 20, dtype=torch.uint8, device=dev)
             self.ev_plan = torch.cuda.Event()
             # events handed to the library must exist: record them once
@@ -245,6 +260,12 @@ class DecodePipeline:
             B.np_select(s, self.scores, self.mask, self.active_ids, self.ws, main)
             B.np_delta(s, token, self.active_ids, self.state, self.out, self.ws, main)
         ready = None  # ready[l]: the event layer l's MLP waits for
+        slots = self.lists["active_slots"]
+        ybytes = cfg.d_model * W.ITEMSIZE[cfg.adtype]
+        # the dense prefix: on the GPU while the host stages the sparse rows
+        for l in range(self.dense_layers):
+            B.np_dense_mlp(s, self.dense_w.data_ptr() + l * self.dense_layer_bytes, x_ptr,
+                           self.y_dense.data_ptr() + l * ybytes, self.ws, main)
         if self.staging == "gather":
             if self.overlap:
                 # the first chunk on the main stream (the first MLP follows it
@@ -269,23 +290,23 @@ class DecodePipeline:
             self.ev_plan.record(main)
             self.ev_plan.synchronize()  # the host reads the plan
             t0 = time.perf_counter()
-            B.np_stage_rows(s, self.plan, 0, L, self.storage, self.resident, self.staging_buf,
-                            self.staging_buf.numel(), self.landing, self.landing.numel(),
-                            self.side, self.ev_plan if self.overlap else None,
-                            self.layer_ready)
+            if self.staging == "file":
+                B.np_stage_file(s, self.plan, 0, L, self.storage_fd, 0, self.resident,
+                                self.staging_buf, self.staging_buf.numel(), self.io_buf,
+                                self.io_buf.nbytes, self.landing, self.landing.numel(),
+                                self.side, self.ev_plan if self.overlap else None,
+                                self.layer_ready)
+            else:
+                B.np_stage_rows(s, self.plan, 0, L, self.storage, self.resident,
+                                self.staging_buf, self.staging_buf.numel(), self.landing,
+                                self.landing.numel(), self.side,
+                                self.ev_plan if self.overlap else None, self.layer_ready)
             if self.stage_log is not None:  # staging alone: host packing + copies + scatter
                 self.side.synchronize()
                 n_rec = int(self.plan_counts.view(L, 4)[:, 0].sum())
                 self.stage_log.append((n_rec * cfg.record_bytes, time.perf_counter() - t0))
             if self.overlap:
                 ready = self.layer_ready
-        slots = self.lists["active_slots"]
-        ybytes = cfg.d_model * W.ITEMSIZE[cfg.adtype]
-        # the dense prefix runs while the sparse layers' rows are staged (on the
-        # side stream when overlapping)
-        for l in range(self.dense_layers):
-            B.np_dense_mlp(s, self.dense_w.data_ptr() + l * self.dense_layer_bytes, x_ptr,
-                           self.y_dense.data_ptr() + l * ybytes, self.ws, main)
         if mlp_block_events is not None:
             if ready is not None:  # time the MLP block, not the wait for staging
                 for e in ready:
@@ -308,6 +329,51 @@ class DecodePipeline:
                                 self.y.data_ptr() + l * ybytes, self.ws, main)
         if mlp_block_events is not None:
             mlp_block_events[1].record(main)
+
+    def _open_storage_file(self, path, host_storage) -> None:
+        """Writes the storage tier ([L'][F][3d] records, layer-major: the
+        neuron-centric file layout of Sec. 3.5) to `path` (a temporary file
+        when None) and opens it for np_stage_file, with O_DIRECT when the
+        record size is a multiple of 512 bytes."""
+        import os
+        import tempfile
+
+        cfg = self.cfg
+        if path is None:
+            d = os.environ.get("NP_STORAGE_DIR") or tempfile.gettempdir()
+            fd, path = tempfile.mkstemp(prefix="np_storage_", suffix=".bin", dir=d)
+            os.close(fd)
+            self._own_file = True
+        self.storage_path = path
+        if not (os.path.exists(path) and os.path.getsize(path) == cfg.storage_bytes):
+            layer_bytes = cfg.d_ffn * cfg.record_bytes
+            with open(path, "wb") as f:
+                if host_storage is not None:
+                    f.write(memoryview(host_storage.numpy()))
+                else:
+                    buf = np.empty(layer_bytes, dtype=np.uint8)
+                    for l in range(cfg.layers):
+                        W.fill_storage(cfg, buf.ctypes.data, l, 1)
+                        f.write(memoryview(buf))
+        direct = cfg.record_bytes % 512 == 0
+        self.storage_fd = os.open(path, os.O_RDONLY | (os.O_DIRECT if direct else 0))
+        self.storage_direct = direct
+
+    def close(self) -> None:
+        """Closes the storage file (and removes it if the pipeline made it)."""
+        import os
+
+        if self.storage_fd >= 0:
+            os.close(self.storage_fd)
+            self.storage_fd = -1
+            if self._own_file and self.storage_path:
+                os.remove(self.storage_path)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
     def set_thresholds(self, thresholds) -> None:
         """Eq. 1 thresholds of the downstream layers (float32 [L'], host or

@@ -28,7 +28,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 20, names
+    assert len(names) == 22, names
     for n in names:
         assert hasattr(lib, n), f"missing export {n}"
     assert set(names) == set(B.EXPORTS)

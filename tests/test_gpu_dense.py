@@ -38,7 +38,8 @@ def test_dense_mlp(name):
 
 
 @pytest.mark.parametrize("tier,staging,overlap", [("device", "gather", False),
-                                                  ("host", "memcpy", True)])
+                                                  ("host", "memcpy", True),
+                                                  ("file", "file", True)])
 def test_dense_prefix_pipeline(tier, staging, overlap):
     from paper_2608_22643_amd.pipeline import DecodePipeline
 

@@ -1,0 +1,57 @@
+"""The storage tier as a file at the 7B record shape (d 4096, F 11008, fp16:
+24 KiB records, O_DIRECT, io_uring at queue depth 256), four downstream
+layers to keep the file at 1.1 GB: the decode path with file staging against
+the oracle token by token -- delta lists and slot maps bit for bit, resident
+records byte-equal to the file's on sampled slots, MLP outputs within the
+fp16 tolerance on every layer."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_2608_22643_amd import workload as W
+from gpu_util import compare_delta, decode_y, mlp_tolerance, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("overlap", [True, False])
+def test_file_tier_7b_records(overlap, tmp_path):
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get("7b").with_(layers=4)
+    L, d, F, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.k, cfg.capacity
+    T = 4
+    say(f"[file tier] 7b records, {L} layers, overlap={overlap}")
+    store = W.storage(cfg)
+    path = str(tmp_path / "storage.bin")
+    host = torch.from_numpy(store.view(np.uint8).reshape(-1)).pin_memory()
+    pipe = DecodePipeline(cfg, tier="file", staging="file", overlap=overlap, tokens=T,
+                          host_storage=host, storage_path=path)
+    assert pipe.storage_direct
+    h = W.hidden(cfg, T)
+    A, Bm = W.predictor(cfg)
+    st = orc.State(L, F, C)
+    rng = np.random.default_rng(3)
+    for t in range(T):
+        pipe.step(t)
+        torch.cuda.synchronize()
+        scores = pipe.scores.cpu().numpy().reshape(L, F)
+        mask, ids = orc.select(scores, k)
+        assert np.array_equal(pipe.active_ids.cpu().numpy().reshape(L, k), ids)
+        ref = orc.delta(t, ids, st, C)
+        compare_delta(pipe.host_lists(), ref, L)
+        P, Q, U = pipe.host_state()
+        assert np.array_equal(P, st.slot_of) and np.array_equal(Q, st.neuron_of)
+        res = pipe.resident.view(L, C, 3 * d * 2)
+        occ = np.argwhere(st.neuron_of >= 0)
+        for l, s in occ[rng.choice(len(occ), 128, replace=False)]:
+            got = res[l, s].cpu().numpy().view(np.uint16)
+            assert np.array_equal(got, store[l, st.neuron_of[l, s]]), (t, l, s)
+        y = pipe.y.cpu().numpy().view(np.uint16).reshape(L, d)
+        for l in range(L):
+            _, ref64 = orc.sparse_mlp(cfg, l, h[t], store, ids[l], want_f64=True)
+            got = decode_y(orc, cfg.adtype, y[l])
+            assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (t, l)
+    assert pipe.device_error() == 0
+    pipe.close()

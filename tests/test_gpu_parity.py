@@ -149,10 +149,21 @@ def stage_and_check(cfg, mode, staging_records=None):
         dstore.numpy()[:] = store.view(np.uint8).reshape(-1)
     resident = torch.zeros(cfg.resident_bytes, dtype=torch.uint8, device=DEV)
     ref_res = np.zeros(cfg.resident_bytes, np.uint8)
-    if mode == "memcpy":
+    fd = -1
+    if mode == "file":  # the storage tier as a file, read with O_DIRECT when records allow
+        import os
+        import tempfile
+
+        path = os.path.join(tempfile.mkdtemp(), "storage.bin")
+        store.tofile(path)
+        direct = rec % 512 == 0
+        fd = os.open(path, os.O_RDONLY | (os.O_DIRECT if direct else 0))
+        say(f"[stage] file tier {path} direct={direct}")
+    if mode in ("memcpy", "file"):
         cap = staging_records or 64
-        staging = torch.empty(2 * cap * (rec + 4) + 512, dtype=torch.uint8, pin_memory=True)
+        staging = torch.empty(2 * cap * (rec + 4) + 8192, dtype=torch.uint8, pin_memory=True)
         landing = torch.empty(cap * (rec + 4), dtype=torch.uint8, device=DEV)
+        io = B.HostBuffer(cap * (rec + 4))  # direct reads land in ordinary host memory
         pc = torch.empty(L * 4, dtype=torch.int32, pin_memory=True)
         pi = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
         ps = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
@@ -164,13 +175,19 @@ def stage_and_check(cfg, mode, staging_records=None):
         A = np.stack([seqs[l][t] for l in range(L)]).astype(np.int32)
         bufs.ids.copy_(torch.from_numpy(A.reshape(-1)))
         B.np_delta(bufs.shape, t, bufs.ids, bufs.state, bufs.out, bufs.ws)
-        if mode == "memcpy":
+        if mode in ("memcpy", "file"):
             torch.cuda.synchronize()
             pc.copy_(bufs.counts)
             pi.copy_(bufs.lists["in_ids"])
             ps.copy_(bufs.lists["in_slots"])
-            B.np_stage_rows(bufs.shape, plan, 0, L, dstore, resident, staging, staging.numel(),
-                            landing, landing.numel(), torch.cuda.current_stream())
+            if mode == "memcpy":
+                B.np_stage_rows(bufs.shape, plan, 0, L, dstore, resident, staging,
+                                staging.numel(), landing, landing.numel(),
+                                torch.cuda.current_stream())
+            else:
+                B.np_stage_file(bufs.shape, plan, 0, L, fd, 0, resident, staging,
+                                staging.numel(), io, io.nbytes, landing, landing.numel(),
+                                torch.cuda.current_stream())
         else:
             B.np_stage_gather(bufs.shape, bufs.out, 0, L, dstore, resident, bufs.ws)
         torch.cuda.synchronize()
@@ -180,11 +197,16 @@ def stage_and_check(cfg, mode, staging_records=None):
         got = resident.cpu().numpy()
         assert np.array_equal(got, ref_res), f"resident bytes differ at token {t}"
     assert B.np_device_error(bufs.ws) == 0
+    if fd >= 0:
+        import os
+
+        os.close(fd)
+        os.remove(path)
     return bufs, resident, store, st
 
 
 @pytest.mark.parametrize("name", ["tiny", "ragged_f16", "ragged_bf16", "k_eq_c"])
-@pytest.mark.parametrize("mode", ["gather_device", "gather_host", "memcpy"])
+@pytest.mark.parametrize("mode", ["gather_device", "gather_host", "memcpy", "file"])
 def test_stage(name, mode):
     cfg = SHAPES[name]
     say(f"[stage] {name} {mode}")
@@ -192,10 +214,11 @@ def test_stage(name, mode):
 
 
 @pytest.mark.parametrize("records", [1, 3, 1000])
-def test_stage_memcpy_chunk_invariance(records):
-    cfg = SHAPES["ragged_f16"]
-    say(f"[stage chunks] records per chunk {records}")
-    stage_and_check(cfg, "memcpy", staging_records=records)
+@pytest.mark.parametrize("mode", ["memcpy", "file"])
+def test_stage_chunk_invariance(records, mode):
+    cfg = SHAPES["ragged_f16"] if mode == "memcpy" else SHAPES["wide_f16"]
+    say(f"[stage chunks] {mode} records per chunk {records}")
+    stage_and_check(cfg, mode, staging_records=records)
 
 
 def test_stage_rows_rejects_small_staging():
@@ -326,7 +349,9 @@ def test_dyadic_end_to_end_bit_exact():
                                                   ("device", "gather", True),
                                                   ("host", "gather", True),
                                                   ("host", "memcpy", True),
-                                                  ("host", "memcpy", False)])
+                                                  ("host", "memcpy", False),
+                                                  ("file", "file", True),
+                                                  ("file", "file", False)])
 def test_lockstep_tiny(tier, staging, overlap):
     from paper_2608_22643_amd.pipeline import DecodePipeline
 
