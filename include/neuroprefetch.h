@@ -38,7 +38,8 @@
  *  - extern "C"; plain pointers and sizes only.  All memory is owned by the
  *    caller; no call allocates or frees device or host memory.  The staging
  *    path keeps two HIP events and a small worker-thread pool per process,
- *    created on first use (see np_stage_rows).
+ *    created on first use (see np_stage_rows), and the file tier one io_uring
+ *    ring of 256 entries per process (see np_stage_file).
  *  - "device" pointers point into memory of the current HIP device.  Device
  *    pointers must be 16-byte aligned.  Every call is asynchronous on the HIP
  *    stream it is given (0 = the null stream) unless stated otherwise.
