@@ -42,11 +42,11 @@ HBM_PEAK_GBPS = 8000.0
 MLP_COUNTERS = {
     "config": "7b",
     "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
-    "sha256": "86079bd0606453ea17c25e7a6262e164648136024a77024d10eb3721df52ec1b"
-              "753eac23b781ed50788521c47469bf5e9c3fb1e925f19d8a10eea91c62a914a9",
-    "fetch_kib": {"rows": 19919.4, "reduce": 4119.5},
+    "sha256": "f78a1bb2f21f7e232d47df4e719b6cd4785946437d9f14d8d532f4fa39b02447"
+              "e7c091e9cb927d79cad3826398857f00b7e26d440bcaac25904b88684aa49c3f",
+    "fetch_kib": {"rows": 19930.4, "reduce": 4119.5},
     "write_kib": {"rows": 4096.0, "reduce": 8.0},
-    "copy_fetch_kib": 131087.4, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+    "copy_fetch_kib": 131086.6, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
 }
 
 
@@ -586,6 +586,8 @@ def main():
     ap.add_argument("--dense-prefixes", default="0,8,16",
                     help="comma-separated dense-prefix lengths for the split sweep ('' to skip)")
     ap.add_argument("--dense-steps", type=int, default=10)
+    ap.add_argument("--dense-reps", type=int, default=3,
+                    help="timed passes of the dense-MLP roofline over all layers (0: skip)")
     ap.add_argument("--centroid-steps", type=int, default=30,
                     help="steps with the centroid-ID predictor (0: skip)")
     ap.add_argument("--file-tier-steps", type=int, default=10,
@@ -715,8 +717,9 @@ def main():
     if args.file_tier_steps > 0:
         file_tier = file_tier_run(cfg, host_storage, args.file_tier_steps)
         log(f"[bench] file tier: {file_tier}")
-    dense = dense_mlp_roofline(cfg, host_storage)
-    log(f"[bench] dense MLP: {dense}")
+    dense = dense_mlp_roofline(cfg, host_storage, args.dense_reps) if args.dense_reps > 0 else None
+    if dense:
+        log(f"[bench] dense MLP: {dense}")
     sweep = None
     prefixes = [int(v) for v in args.dense_prefixes.split(",") if v]
     if prefixes:
