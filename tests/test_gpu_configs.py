@@ -1,0 +1,79 @@
+"""Parity at the full per-layer shapes of the other workload configurations:
+13B (d 5120, F 13824, r 512, 12% active, 40% resident, fp16) and 70B (d 8192,
+F 28672, r 768, 10% active, 35% resident, bf16) with the storage tier in
+pinned host memory staged per token, as those configurations state, and the
+points of the 7B sweep (activity 5 / 30%, persistence 70 / 95%, residency 25 /
+75%) with the tier in HBM.  Each runs four downstream layers of the real
+shape (the layer count only repeats the same work) for four tokens against
+the oracle: every score within the predictor's fp32 bound; masks, ids, delta
+lists and slot maps bit for bit; resident records byte-equal to the storage
+rows on sampled slots; MLP outputs within the tolerance of the type on every
+layer."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_2608_22643_amd import workload as W
+from gpu_util import compare_delta, decode_y, mlp_tolerance, say, score_bound
+
+pytestmark = pytest.mark.gpu
+
+LAYERS = 4
+
+
+def run_lockstep(cfg, tier, staging, overlap, T=4):
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    L, d, F, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.k, cfg.capacity
+    say(f"[config] {cfg.name}: L'={L} d={d} F={F} r={cfg.rank} k={k} C={C} {cfg.wdtype} "
+        f"tier={tier} staging={staging}")
+    store = W.storage(cfg)
+    host = torch.from_numpy(store.view(np.uint8).reshape(-1)).pin_memory()
+    pipe = DecodePipeline(cfg, tier=tier, staging=staging, overlap=overlap, tokens=T,
+                          host_storage=host)
+    h = W.hidden(cfg, T)
+    A, Bm = W.predictor(cfg)
+    st = orc.State(L, F, C)
+    rng = np.random.default_rng(5)
+    esz = W.ITEMSIZE[cfg.wdtype]
+    for t in range(T):
+        pipe.step(t)
+        torch.cuda.synchronize()
+        scores = pipe.scores.cpu().numpy().reshape(L, F)
+        ref_s = orc.predict(cfg, h[t], A, Bm).astype(np.float64)
+        tol = score_bound(cfg, A, Bm, h[t]) + np.abs(ref_s) * 2.0 ** -23
+        assert np.all(np.abs(scores.astype(np.float64) - ref_s) <= tol), t
+        mask, ids = orc.select(scores, k)
+        assert np.array_equal(pipe.mask.cpu().numpy().view(np.uint32).reshape(L, -1), mask), t
+        assert np.array_equal(pipe.active_ids.cpu().numpy().reshape(L, k), ids), t
+        ref = orc.delta(t, ids, st, C)
+        compare_delta(pipe.host_lists(), ref, L)
+        P, Q, U = pipe.host_state()
+        assert np.array_equal(P, st.slot_of) and np.array_equal(Q, st.neuron_of), t
+        assert np.array_equal(U, st.last_used), t
+        res = pipe.resident.view(L, C, 3 * d * esz)
+        occ = np.argwhere(st.neuron_of >= 0)
+        for l, s in occ[rng.choice(len(occ), 64, replace=False)]:
+            got = res[l, s].cpu().numpy().view(np.uint16 if esz == 2 else np.float32)
+            assert np.array_equal(got, store[l, st.neuron_of[l, s]]), (t, l, s)
+        ybits = pipe.y.cpu().view(torch.uint8).numpy()
+        y = ybits.view(np.uint16 if esz == 2 else np.float32).reshape(L, d)
+        for l in range(L):
+            _, ref64 = orc.sparse_mlp(cfg, l, h[t], store, ids[l], want_f64=True)
+            got = decode_y(orc, cfg.adtype, y[l])
+            assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (t, l)
+    assert pipe.device_error() == 0
+
+
+@pytest.mark.parametrize("name", ["13b", "70b"])
+def test_large_configs_host_tier(name):
+    cfg = W.get(name).with_(layers=LAYERS)
+    run_lockstep(cfg, "host", "memcpy", True)
+
+
+@pytest.mark.parametrize("name", ["7b_act5", "7b_act30", "7b_pers70", "7b_pers95", "7b_res25",
+                                  "7b_res75"])
+def test_sweep_points(name):
+    cfg = W.get(name).with_(layers=LAYERS)
+    run_lockstep(cfg, "device", "gather", False)
