@@ -459,6 +459,45 @@ def swiglu_run(steps: int, calib_tokens: int = 128, alpha: float = 61.6) -> dict
     return res
 
 
+def sweep_run(host_storage, steps: int) -> dict:
+    """The 7B sweep (activity 5/15/30%, persistence 70/82/85/95%, residency
+    25/50/75%, one factor at a time around 15% / 83.5% / 50%): per point the
+    step rate, incoming rows and staged bytes per token, the hit share, and
+    the sparse MLP's per-call time and HBM rate.  The records are the same at
+    every point (same shapes and seed), so the 7B storage tier is reused."""
+    import numpy as np
+    import torch
+
+    from paper_2608_22643_amd import workload as W
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    out = {}
+    warm = 120  # the resident set fills for ~C / (incoming per layer) tokens
+    for cfg in W.sweep_configs():
+        T = warm + 2 * steps + 8
+        pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T,
+                              host_storage=host_storage)
+        for i in range(warm):
+            pipe.step(i)
+        wall, mlp_us = timed_steps(pipe, warm, steps)
+        _, per_tok = breakdown(pipe, warm + steps, max(3, steps // 2))
+        if pipe.device_error():
+            raise RuntimeError(f"sweep {cfg.name}: device error word {pipe.device_error():#x}")
+        n_in = float(np.mean([c[:, 0].sum() for c in per_tok]))
+        n_hit = float(np.mean([c[:, 1].sum() for c in per_tok]))
+        b = mlp_bytes_per_launch(cfg)
+        out[cfg.name] = {"k": cfg.k, "C": cfg.capacity, "persistence": cfg.persistence,
+                         "tok_s": round(steps / wall, 1),
+                         "incoming_rows_per_token": round(n_in, 1),
+                         "staged_MB_per_token": round(n_in * cfg.record_bytes / 1e6, 2),
+                         "reuse_pct": round(100.0 * n_hit / (cfg.k * cfg.layers), 2),
+                         "mlp_us_per_call": round(mlp_us, 2),
+                         "mlp_GBps": round(b / (mlp_us * 1e-6) / 1e9, 1)}
+        del pipe
+        torch.cuda.empty_cache()
+    return out
+
+
 def dense_mlp_roofline(cfg, host_storage, reps: int = 3) -> dict:
     """np_dense_mlp over every layer of the storage tier (all F records of a
     layer: the dense prefix's MLP), back to back, against the HBM roofline."""
@@ -590,6 +629,8 @@ def main():
                     help="timed passes of the dense-MLP roofline over all layers (0: skip)")
     ap.add_argument("--centroid-steps", type=int, default=30,
                     help="steps with the centroid-ID predictor (0: skip)")
+    ap.add_argument("--sweep-steps", type=int, default=10,
+                    help="steps per point of the 7B sweep (0: skip; 7B configuration only)")
     ap.add_argument("--file-tier-steps", type=int, default=10,
                     help="steps with the storage tier in a local file (0: skip)")
     ap.add_argument("--swiglu-steps", type=int, default=30,
@@ -713,6 +754,10 @@ def main():
         host.update(staging_rates(hp, 4 + args.host_tier_steps, max(3, args.host_tier_steps // 4)))
         log(f"[bench] host tier: {host}")
         del hp, hg
+    sweep7b = None
+    if args.sweep_steps > 0 and cfg.name == "7b":
+        sweep7b = sweep_run(host_storage, args.sweep_steps)
+        log(f"[bench] 7B sweep: {sweep7b}")
     file_tier = None
     if args.file_tier_steps > 0:
         file_tier = file_tier_run(cfg, host_storage, args.file_tier_steps)
@@ -781,6 +826,7 @@ def main():
         "delta": stats,
         "host_tier": host,
         "file_tier": file_tier,
+        "sweep_7b": sweep7b,
         "cpu_baseline": cpu,
         "dense_mlp": dense,
         "dense_prefix_sweep": sweep,
