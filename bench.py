@@ -42,11 +42,11 @@ HBM_PEAK_GBPS = 8000.0
 MLP_COUNTERS = {
     "config": "7b",
     "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
-    "sha256": "f78a1bb2f21f7e232d47df4e719b6cd4785946437d9f14d8d532f4fa39b02447"
+    "sha256": "fe692c6038a177b6991d8546e9ce20abff0dc03ee996f64e5f3379b99e64a23b"
               "e7c091e9cb927d79cad3826398857f00b7e26d440bcaac25904b88684aa49c3f",
-    "fetch_kib": {"rows": 19930.4, "reduce": 4119.5},
+    "fetch_kib": {"rows": 19933.4, "reduce": 4119.5},
     "write_kib": {"rows": 4096.0, "reduce": 8.0},
-    "copy_fetch_kib": 131086.6, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+    "copy_fetch_kib": 131087.7, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
 }
 
 

@@ -79,29 +79,37 @@ __device__ inline void store_y1(void* y, int col, float v) {
 // Grid barrier, then the column reduction of this workgroup's chunks.  Every
 // thread of the workgroup calls it; thread 0 holds `gen0`, the generation
 // read at entry.  red: blockDim.x float4 of LDS.
-template <class T>
-__device__ inline void fused_reduce(const MlpArgs& a, int gen0, float4* red) {
-  constexpr int V = T::V;
-  __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are complete
+// Grid barrier over the n_wg workgroups of the launch: every thread calls
+// it after its agent-scope stores; thread 0 holds `gen0`, the generation
+// read at entry.  The last workgroup to arrive resets the arrival counter and
+// advances the generation; the others poll it (bounded).
+__device__ inline void grid_barrier(void* ws, int n_wg, int gen0) {
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's stores are complete
   __syncthreads();
   if (threadIdx.x == 0) {
-    int* arrive = (int*)((char*)a.ws + WS_BAR_ARRIVE);
-    int* gen = (int*)((char*)a.ws + WS_BAR_GEN);
+    int* arrive = (int*)((char*)ws + WS_BAR_ARRIVE);
+    int* gen = (int*)((char*)ws + WS_BAR_GEN);
     const int old = __hip_atomic_fetch_add(arrive, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (old == a.n_wg - 1) {  // last to arrive: every partial is written
+    if (old == n_wg - 1) {  // last to arrive: every workgroup's stores are done
       (void)__hip_atomic_exchange(arrive, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       (void)__hip_atomic_fetch_add(gen, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     } else {
       uint32_t spins = 0;
       while (__hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gen0) {
         if (++spins == MLP_SPIN_LIMIT) {
-          raise_error(a.ws, NP_DEVERR_SPIN_LIMIT);
+          raise_error(ws, NP_DEVERR_SPIN_LIMIT);
           break;
         }
       }
     }
   }
   __syncthreads();
+}
+
+template <class T>
+__device__ inline void fused_reduce(const MlpArgs& a, int gen0, float4* red) {
+  constexpr int V = T::V;
+  grid_barrier(a.ws, a.n_wg, gen0);
   const int d = a.NV * V, nchunks = d / 16;
   const int b = blockIdx.x, t = threadIdx.x, nt = blockDim.x;
   const int q = t & 3, rsub = t >> 2, rstep = nt >> 2;
@@ -427,6 +435,151 @@ __global__ __launch_bounds__(256) void mlp_reduce_kernel(const float* __restrict
   }
 }
 
+// ---------------------------------------------------------------------------
+// Single-kernel path without partial sums (16-bit records, whole wave
+// slices).  Workgroup b owns (i) a balanced range of the active list, whose
+// gate/up dot products it computes as the rows kernel does (wave p: a fixed
+// 1 KiB column slice of gate and up; the sums meet in LDS) and turns into
+// activations a_j, and (ii) a band of 16 columns of y.  At entry every thread
+// also requests the band's 32 bytes of the down^T row of active rows t,
+// t + nt, ..., so the down projection streams together with the gate/up
+// rows instead of after them.  The activations are published with
+// agent-scope stores; after a grid barrier each workgroup reads all of them
+// and sums a_j * down_j[band] in a fixed order (thread, then wave): y needs no
+// partial sums and no second kernel, and the result is deterministic.  Bands
+// are handed out XCD by XCD (workgroups b, b + 8, ... run on one XCD and take
+// adjacent bands), so the 128-byte lines of a down^T row are filled once per
+// XCD, not once per band.  Needs the whole grid resident (checked at launch).
+constexpr int CS_BAND = 16;  // columns of y per workgroup: two 16-byte vectors
+constexpr int CS_RPT = 4;    // active rows per thread for the band (n <= 4 * threads)
+
+template <class T, int R, int MAXT>
+__global__ __launch_bounds__(MAXT) void sparse_mlp_colsplit_kernel(MlpArgs a) {
+  constexpr int V = T::V;
+  constexpr int BV = CS_BAND / V;   // vectors of a band row
+  constexpr int NVAL = 2 * R;       // g and u of each row of a round
+  constexpr int G = WAVE / NVAL;    // lanes holding one reduced value
+  __shared__ float gu[NVAL][MAXT / WAVE];  // value, wave
+  __shared__ float act_all[CS_RPT * MAXT];
+  __shared__ float red[MAXT / WAVE][CS_BAND];
+  const int lane = threadIdx.x & (WAVE - 1), p = threadIdx.x / WAVE;
+  const int nt = blockDim.x, P = a.P, b = blockIdx.x;
+  int n = a.n_active;
+  if (a.n_dev) {  // a row count produced on the device (variable-size sets)
+    n = a.n_dev[a.layer];
+    if (n < 0 || n > a.n_active) {
+      if (threadIdx.x == 0 && b == 0) raise_error(a.ws, NP_DEVERR_STATE);
+      n = n < 0 ? 0 : a.n_active;
+    }
+  }
+  const float thr = a.thr ? a.thr[a.layer] : 0.f;  // eq. 1; 0 keeps every row
+  int gen0 = 0;
+  if (threadIdx.x == 0)
+    gen0 = __hip_atomic_load((int*)((char*)a.ws + WS_BAR_GEN), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+  const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(a.res_layer, a.layer_bytes);
+  const uint32_t third = (uint32_t)a.NV * 16u;
+  // (ii) the band's piece of every active row's down^T, requested first
+  const int band = (b % 8) * (a.n_wg / 8) + b / 8;
+  const uint32_t band_off = 2u * third + (uint32_t)band * BV * 16u;
+  int drow_slot[CS_RPT];
+#pragma unroll
+  for (int j = 0; j < CS_RPT; ++j) {
+    const int row = threadIdx.x + nt * j;
+    drow_slot[j] = row < n ? a.slots[row] : -1;
+  }
+  uint4 dv[CS_RPT][BV];
+#pragma unroll
+  for (int j = 0; j < CS_RPT; ++j) {
+    const bool ok = drow_slot[j] >= 0 && drow_slot[j] < a.C;  // others reported by (i)
+    const uint32_t base = ok ? (uint32_t)drow_slot[j] * 3u * third + band_off : BUF_OOB;
+#pragma unroll
+    for (int q = 0; q < BV; ++q) dv[j][q] = buf_load16(rsrc, base, ok ? 16u * q : 0u);
+  }
+  // (i) the gate/up dot products of this workgroup's rows
+  const int row_begin = (int)(((long long)b * n) / a.n_wg);
+  const int row_end = (int)(((long long)(b + 1) * n) / a.n_wg);
+  const int v = p * WAVE + lane;  // this lane's vector of the column slice
+  const uint4 xr = a.x[v];
+  const uint32_t loff = (uint32_t)v * 16u;
+  float* avals = a.partials;  // the workspace's partial area holds the activations
+  for (int rb = row_begin; rb < row_end; rb += R) {
+    const int my_slot = (lane < R && rb + lane < row_end) ? a.slots[rb + lane] : -1;
+    int slot[R];
+    bool valid[R];
+    bool bad = false;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      slot[r] = __builtin_amdgcn_readlane(my_slot, r);
+      valid[r] = rb + r < row_end && slot[r] >= 0 && slot[r] < a.C;
+      bad |= rb + r < row_end && !valid[r];
+    }
+    if (bad && threadIdx.x == 0) raise_error(a.ws, NP_DEVERR_NOT_RESIDENT);
+    uint4 gw[R], uw[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const uint32_t roff = valid[r] ? (uint32_t)slot[r] * 3u * third + loff : BUF_OOB;
+      gw[r] = buf_load16(rsrc, roff, 0);
+      uw[r] = buf_load16(rsrc, roff, valid[r] ? third : 0u);
+    }
+    float val[NVAL];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      val[r] = T::dot(gw[r], xr, 0.f);
+      val[R + r] = T::dot(uw[r], xr, 0.f);
+    }
+    wave_reduce_scatter<NVAL>(val);  // lane l holds the wave sum of value l / G
+    if (lane % G == 0) gu[lane / G][p] = val[0];
+    __syncthreads();
+    if (threadIdx.x < R && rb + (int)threadIdx.x < row_end) {  // wave 0, lane r: row rb + r
+      const int r = threadIdx.x;
+      float g = 0.f, u = 0.f;
+      for (int w = 0; w < P; ++w) {  // waves in order
+        g += gu[r][w];
+        u += gu[R + r][w];
+      }
+      const bool ok = my_slot >= 0 && my_slot < a.C;
+      float act = ok ? gated(a.act, g, u) : 0.f;
+      if (fabsf(act) < thr) act = 0.f;
+      __hip_atomic_store((int*)(avals + rb + r), __float_as_int(act), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();  // gu is rewritten by the next round
+  }
+  grid_barrier(a.ws, a.n_wg, gen0);
+  // every activation, from the agent-coherent level
+  // whole 16-byte vectors (the area is larger; entries past n are not used)
+  const __amdgpu_buffer_rsrc_t ars = make_rsrc(avals, (uint32_t)((n + 3) / 4) * 16u);
+  for (int i = threadIdx.x; 4 * i < n; i += nt) {
+    const float4 f = buf_load16_agent(ars, 16u * (uint32_t)i);
+    act_all[4 * i] = f.x;
+    act_all[4 * i + 1] = f.y;
+    act_all[4 * i + 2] = f.z;
+    act_all[4 * i + 3] = f.w;
+  }
+  __syncthreads();
+  float acc[CS_BAND];
+#pragma unroll
+  for (int c = 0; c < CS_BAND; ++c) acc[c] = 0.f;
+#pragma unroll
+  for (int j = 0; j < CS_RPT; ++j) {
+    const int row = threadIdx.x + nt * j;
+    if (row < n && drow_slot[j] >= 0 && drow_slot[j] < a.C) {
+      const float av = act_all[row];
+#pragma unroll
+      for (int q = 0; q < BV; ++q) T::axpy(acc + q * V, av, dv[j][q]);
+    }
+  }
+  wave_reduce_scatter<CS_BAND>(acc);  // lane l: the wave's sum of column l / 4
+  if (lane % (WAVE / CS_BAND) == 0) red[p][lane / (WAVE / CS_BAND)] = acc[0];
+  __syncthreads();
+  if (threadIdx.x < CS_BAND) {
+    float y = 0.f;
+    for (int w = 0; w < P; ++w) y += red[w][threadIdx.x];
+    store_y1<T>(a.y, band * CS_BAND + threadIdx.x, y);
+  }
+}
+
 static int env_int(const char* name, int dflt) {
   const char* v = getenv(name);
   if (!v || !*v) return dflt;
@@ -526,6 +679,31 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   a.y = y;
   a.n_dev = n_dev;
   a.layer = layer;
+  // the single kernel without partial sums (opt-in, NP_MLP_COLSPLIT=1; measured
+  // 17.3 against 16.1 us per call at the 7B shape: its 32-byte down^T pieces
+  // touch 64 lines per load instruction and cost 4.5 us, the barrier 0.3 us)
+  if constexpr (V == 8) {
+    const bool on = env_int("NP_MLP_COLSPLIT", 0) == 1;
+    const int P = a.NV / WAVE, bands = s.d_model / CS_BAND, threads = P * WAVE;
+    if (on && active_slots && a.NV % WAVE == 0 && P <= 16 && bands % 8 == 0 &&
+        n_active <= CS_RPT * threads && bands <= MLP_MAX_WG) {
+      MlpArgs c = a;
+      c.P = P;
+      c.teams = 1;
+      c.n_wg = bands;
+      const void* k = threads <= 512 ? (const void*)sparse_mlp_colsplit_kernel<T, 8, 512>
+                                     : (const void*)sparse_mlp_colsplit_kernel<T, 4, 1024>;
+      if (bands <= coresident(k, threads, 0)) {
+        if (threads <= 512)
+          hipLaunchKernelGGL((sparse_mlp_colsplit_kernel<T, 8, 512>), dim3(bands), dim3(threads),
+                             0, stream, c);
+        else
+          hipLaunchKernelGGL((sparse_mlp_colsplit_kernel<T, 4, 1024>), dim3(bands),
+                             dim3(threads), 0, stream, c);
+        return hipGetLastError();
+      }
+    }
+  }
   const size_t lds = (size_t)(teams - 1) * a.NV * V * sizeof(float);
   // the single-kernel reduction adds one float4 per thread of LDS
   const size_t lds_fused = lds + (size_t)teams * a.P * WAVE * sizeof(float4);

@@ -1,0 +1,131 @@
+"""The sparse MLP's three reduction paths against the oracle, on shapes that
+each path accepts: the two-kernel path (the default), the single kernel
+with a partial-sum reduction after a grid barrier (NP_MLP_FUSED=1) and the
+single kernel without partial sums (column bands; 16-bit records with whole
+wave slices, at most four rows per thread, the grid resident;
+NP_MLP_COLSPLIT=1).  Row counts from 0 to the path's
+maximum (fewer rows than workgroups, one row per workgroup, ragged), device
+counts, SwiGLU with eq. 1 thresholds, a slot outside the buffer, and bit-for-
+bit repeatability of each path."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_2608_22643_amd import binding as B
+from paper_2608_22643_amd import workload as W
+from gpu_util import DEV, Bufs, decode_y, mlp_tolerance, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def cfg_small(name, L, d, F, r, k, C, dt, **kw):
+    return W.Config(name, L, d, F, r, k / F, C / F, dt, dt, 4, rho_given=0.9, k_override=k,
+                    c_override=C, **kw)
+
+
+# (d, F, k, C): threads = d / 8 per workgroup, bands = d / 16 workgroups,
+# at most 4 * threads rows for the column-band kernel
+SHAPES = {
+    "d512_f16": cfg_small("d512_f16", 2, 512, 3000, 8, 256, 600, "f16"),
+    "d1024_bf16": cfg_small("d1024_bf16", 3, 1024, 5000, 16, 512, 1200, "bf16"),
+    "d2048_f16": cfg_small("d2048_f16", 2, 2048, 7000, 16, 1000, 2000, "f16"),
+    "d4096_bf16": cfg_small("d4096_bf16", 2, 4096, 11008, 16, 1651, 5504, "bf16"),
+}
+PATHS = {"colsplit": {"NP_MLP_COLSPLIT": "1"}, "two_kernel": {},
+         "fused": {"NP_MLP_FUSED": "1"}}
+
+
+def resident_of(cfg, store, rng):
+    L, F, C = cfg.layers, cfg.d_ffn, cfg.capacity
+    neuron = np.stack([rng.permutation(F)[:C] for _ in range(L)]).astype(np.int32)
+    return to_dev(np.stack([store[l][neuron[l]] for l in range(L)])), neuron
+
+
+def setup(cfg, seed):
+    bufs = Bufs(cfg)
+    bufs.reset()
+    rng = np.random.default_rng(seed)
+    store = W.storage(cfg)
+    res, neuron = resident_of(cfg, store, rng)
+    h = W.hidden(cfg, 1)[0]
+    return bufs, rng, store, res, neuron, h
+
+
+@pytest.mark.parametrize("path", list(PATHS))
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_mlp_paths_row_counts(name, path, monkeypatch):
+    for k_, v_ in PATHS[path].items():
+        monkeypatch.setenv(k_, v_)
+    cfg = SHAPES[name]
+    d, k, C = cfg.d_model, cfg.k, cfg.capacity
+    bands = d // 16
+    say(f"[mlp path] {name} {path}")
+    bufs, rng, store, res, neuron, h = setup(cfg, 21)
+    x = to_dev(h)
+    esz = W.ITEMSIZE[cfg.adtype]
+    y = torch.zeros(d * esz, dtype=torch.uint8, device=DEV)
+    y2 = torch.zeros(d * esz, dtype=torch.uint8, device=DEV)
+    slots = np.sort(rng.choice(C, k, replace=False)).astype(np.int32)
+    sl = to_dev(slots)
+    for n in sorted({0, 1, 7, bands - 1, bands, bands + 1, k // 2 + 3, k}):
+        for l in range(cfg.layers):
+            B.np_sparse_mlp(bufs.shape, l, x, res, sl, n, y, bufs.ws)
+            B.np_sparse_mlp(bufs.shape, l, x, res, sl, n, y2, bufs.ws)
+            torch.cuda.synchronize()
+            assert torch.equal(y, y2), (n, l)  # repeatable bit for bit
+            _, ref64 = orc.sparse_mlp(cfg, l, h, store, neuron[l][slots[:n]].astype(np.int32),
+                                      want_f64=True)
+            got = decode_y(orc, cfg.adtype, y.cpu().numpy())
+            assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (n, l)
+    assert B.np_device_error(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("path", list(PATHS))
+@pytest.mark.parametrize("name", ["d1024_bf16", "d4096_bf16"])
+def test_mlp_paths_counts_swiglu_thresholds(name, path, monkeypatch):
+    for k_, v_ in PATHS[path].items():
+        monkeypatch.setenv(k_, v_)
+    cfg = SHAPES[name].with_(act="swiglu")
+    L, d, k, C = cfg.layers, cfg.d_model, cfg.k, cfg.capacity
+    say(f"[mlp path swiglu] {name} {path}")
+    bufs, rng, store, res, neuron, h = setup(cfg, 22)
+    x = to_dev(h)
+    esz = W.ITEMSIZE[cfg.adtype]
+    y = torch.zeros(d * esz, dtype=torch.uint8, device=DEV)
+    all_slots = [np.sort(rng.choice(C, k, replace=False)).astype(np.int32) for _ in range(L)]
+    # thresholds in the widest gap of each layer's activation magnitudes
+    T = np.zeros(L, np.float32)
+    for l in range(L):
+        rec = orc.decode(cfg.wdtype, store[l][neuron[l][all_slots[l]]])
+        xv = orc.decode(cfg.adtype, h)
+        g, u = rec[:, :d] @ xv, rec[:, d:2 * d] @ xv
+        a = np.abs(g / (1 + np.exp(-g)) * u)
+        s = np.sort(a)
+        j = int(np.argmax(np.diff(s[k // 4:k // 2]))) + k // 4
+        T[l] = np.float32((s[j] + s[j + 1]) / 2)
+    counts = torch.tensor(rng.integers(0, k + 1, size=L), dtype=torch.int32, device=DEV)
+    thr = to_dev(T)
+    for l in range(L):
+        B.np_sparse_mlp_t(bufs.shape, l, x, res, to_dev(all_slots[l]), k, counts, thr, y, bufs.ws)
+        torch.cuda.synchronize()
+        n = int(counts[l])
+        ids = neuron[l][all_slots[l][:n]].astype(np.int32)
+        _, ref64 = orc.sparse_mlp(cfg, l, h, store, ids, want_f64=True, threshold=float(T[l]))
+        got = decode_y(orc, cfg.adtype, y.cpu().numpy())
+        assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (l, n)
+    assert B.np_device_error(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("path", list(PATHS))
+def test_mlp_paths_bad_slot(path, monkeypatch):
+    for k_, v_ in PATHS[path].items():
+        monkeypatch.setenv(k_, v_)
+    cfg = SHAPES["d2048_f16"]
+    say(f"[mlp path bad slot] {path}")
+    bufs, rng, store, res, neuron, h = setup(cfg, 23)
+    y = torch.zeros(cfg.d_model, dtype=torch.float16, device=DEV)
+    bad = torch.tensor([0, cfg.capacity + 5, -1, 2] + list(range(3, 200)), dtype=torch.int32,
+                       device=DEV)
+    B.np_sparse_mlp(bufs.shape, 1, to_dev(h), res, bad, bad.numel(), y, bufs.ws)
+    assert B.np_device_error(bufs.ws) & B.NP_DEVERR_NOT_RESIDENT
