@@ -645,7 +645,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
-              "(this build runs the hot path of one GPU only)", file=sys.stderr)
+              "(the hot path here is measured on one GPU)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

@@ -87,7 +87,7 @@ typedef enum np_status {
   NP_ERR_INVALID_ARG = 1, /* null/misaligned pointer, bad size or dtype */
   NP_ERR_CAPACITY = 2,    /* k > C, staging buffer smaller than one record, ... */
   NP_ERR_HIP = 3,         /* a HIP runtime call failed; detail in np_last_error() */
-  NP_ERR_UNSUPPORTED = 4, /* valid request this build does not implement */
+  NP_ERR_UNSUPPORTED = 4, /* valid request this library does not implement */
   NP_ERR_STATE = 5,       /* reserved */
   NP_ERR_IO = 6           /* a storage-tier file read failed (detail in np_last_error()) */
 } np_status;

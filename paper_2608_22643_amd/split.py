@@ -23,7 +23,7 @@ def dense_prefix(budget_bytes: int, n_layers: int, layer_bytes: int, buffer_byte
     budget_bytes.  A dense layer holds all F records and a buffer C of them
     (C <= F), so the footprint grows with d and d* is found in closed form.
     Raises ValueError when even min_dense does not fit (the paper's
-    whole-layer fallback is outside this build)."""
+    whole-layer fallback is not implemented here)."""
     if buffer_bytes > layer_bytes or min(n_layers, layer_bytes, buffer_bytes) < 0:
         raise ValueError("need 0 <= buffer_bytes <= layer_bytes and n_layers >= 0")
     if resident_bytes(min_dense, n_layers, layer_bytes, buffer_bytes, fixed_bytes) > budget_bytes:
