@@ -355,6 +355,8 @@ class DecodePipeline:
                     for l in range(cfg.layers):
                         W.fill_storage(cfg, buf.ctypes.data, l, 1)
                         f.write(memoryview(buf))
+                f.flush()
+                os.fsync(f.fileno())  # on the device before any timed read
         direct = cfg.record_bytes % 512 == 0
         self.storage_fd = os.open(path, os.O_RDONLY | (os.O_DIRECT if direct else 0))
         self.storage_direct = direct
