@@ -24,16 +24,19 @@ namespace np {
 // accumulator layout: lane l, register r holds output row 4*(l/16) + r
 // (neuron) and column l%16 (token).
 //
-// A workgroup owns 32 neurons (two row tiles that share every token
-// fragment); its four waves split the reduction (d) into quarters and hold
-// every token tile of the launch (up to 8, 128 tokens), so each record is
-// read from HBM once per launch.  Operands come straight from memory with
-// 16-byte buffer loads (a record's row is contiguous in d; the tokens are
-// L2-resident); the quarters meet in LDS, two token tiles at a time, and wave
-// 0 applies the activation and writes acts[token][neuron].
+// A workgroup owns 32 neurons (two row tiles) and every token of the launch
+// (up to 128: eight 16-token tiles); wave w takes tiles w and w + 4 over the
+// whole reduction, so no wave needs another's sums.  The neurons' gate and up
+// rows stream through LDS in chunks of KC elements: the workgroup loads a
+// chunk with whole-line 16-byte loads (16 lanes per 256-byte row piece) into
+// one of two buffers while the waves multiply the other, and each wave reads
+// its MFMA fragments from LDS (rows padded by 16 bytes: no bank conflicts).
+// The token fragments come straight from memory (the tokens are L2-resident),
+// a chunk ahead in registers.
 constexpr int AB_WAVES = 4;
 constexpr int AB_MAX_TILES = 8;   // token tiles of 16
-constexpr int AB_UNROLL = 2;
+constexpr int AB_ROWB = 256;      // bytes of a row piece per chunk
+constexpr int AB_PITCH = AB_ROWB + 16;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
@@ -64,111 +67,126 @@ struct ActBatchArgs {
   int F, d, n, act;
 };
 
-template <class T, int NTT>
+template <class T, int TPW>
 __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs a) {
-  constexpr int V = T::V, ESZ = 16 / V, KS = 4 * V;
-  constexpr int XT = 2;  // token tiles exchanged per round
-  __shared__ f32x4 xch[AB_WAVES - 1][2][2][XT][WAVE];  // wave, g/u, row tile, tile, lane
-  const int lane = threadIdx.x & (WAVE - 1), q = threadIdx.x / WAVE;
-  const int n0 = blockIdx.x * 32, grp = lane / 16;
-  const int steps = (a.d + KS - 1) / KS;
-  const int s0 = q * steps / AB_WAVES, s1 = (q + 1) * steps / AB_WAVES;
+  constexpr int V = T::V, ESZ = 16 / V, KS = 4 * V;  // KS: reduction elements per MFMA step
+  constexpr int KC = AB_ROWB / ESZ;                  // reduction elements per chunk
+  constexpr int SPC = KC / KS;                       // MFMA steps per chunk (4)
+  constexpr int PIECES = 2 * 32 * (AB_ROWB / 16);    // 16-byte pieces of a chunk (g and u)
+  constexpr int PPT = PIECES / (AB_WAVES * WAVE);    // pieces per thread (4)
+  __shared__ __attribute__((aligned(16))) char lds[2][2][32][AB_PITCH];  // buffer, g/u, row
+  const int t = threadIdx.x, lane = t & (WAVE - 1), w = t / WAVE, grp = lane / 16;
+  const int n0 = blockIdx.x * 32;
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes), xr = make_rsrc(a.x, a.x_bytes);
-  // byte offsets of this lane's operands at reduction index 0 (OOB past the
-  // neurons / tokens of the launch)
-  const uint32_t rec = (uint32_t)(3 * a.d * ESZ), up = (uint32_t)(a.d * ESZ);
-  uint32_t r_off[2];
+  const uint32_t rec = (uint32_t)(3 * a.d * ESZ), dbytes = (uint32_t)(a.d * ESZ);
+  const int chunks = (a.d + KC - 1) / KC;
+  // this thread's pieces of every chunk: piece p -> (projection, row, 16-byte column)
+  uint32_t p_off[PPT];  // byte offset at reduction index 0, or OOB
+  int p_col[PPT];
 #pragma unroll
-  for (int m = 0; m < 2; ++m) {
-    const int row = n0 + 16 * m + (lane & 15);
-    r_off[m] = row < a.F ? (uint32_t)row * rec : BUF_OOB;
+  for (int i = 0; i < PPT; ++i) {
+    const int pc = t + AB_WAVES * WAVE * i;
+    const int proj = pc / (PIECES / 2), row = (pc / (AB_ROWB / 16)) % 32, col = pc % (AB_ROWB / 16);
+    const int neuron = n0 + row;
+    p_off[i] = neuron < a.F ? (uint32_t)neuron * rec + (uint32_t)proj * dbytes : BUF_OOB;
+    p_col[i] = col;
   }
-  uint32_t t_off[NTT];
+  auto load_chunk = [&](int c, uint4* r) {
 #pragma unroll
-  for (int t = 0; t < NTT; ++t) {
-    const int tok = t * 16 + (lane & 15);
-    t_off[t] = tok < a.n ? (uint32_t)tok * (uint32_t)(a.d * ESZ) : BUF_OOB;
+    for (int i = 0; i < PPT; ++i) {
+      const int k = c * KC + p_col[i] * V;  // first element of the piece
+      r[i] = buf_load16(wr, (p_off[i] != BUF_OOB && k < a.d) ? p_off[i] + (uint32_t)k * ESZ
+                                                             : BUF_OOB, 0);
+    }
+  };
+  auto store_chunk = [&](int buf, const uint4* r) {
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int pc = t + AB_WAVES * WAVE * i;
+      const int proj = pc / (PIECES / 2), row = (pc / (AB_ROWB / 16)) % 32, col = pc % (AB_ROWB / 16);
+      *(uint4*)&lds[buf][proj][row][col * 16] = r[i];
+    }
+  };
+  // token fragments: tile ti = w + 4j, token 16 ti + lane % 16
+  uint32_t t_off[TPW];
+#pragma unroll
+  for (int j = 0; j < TPW; ++j) {
+    const int tok = (w + AB_WAVES * j) * 16 + (lane & 15);
+    t_off[j] = tok < a.n ? (uint32_t)tok * dbytes : BUF_OOB;
   }
-  f32x4 accg[2][NTT], accu[2][NTT];
+  auto load_tokens = [&](int c, uint4 (&b)[SPC][TPW]) {
+#pragma unroll
+    for (int s = 0; s < SPC; ++s) {
+      const int k = c * KC + s * KS + grp * V;
+#pragma unroll
+      for (int j = 0; j < TPW; ++j)
+        b[s][j] = buf_load16(xr, (t_off[j] != BUF_OOB && k < a.d) ? t_off[j] + (uint32_t)k * ESZ
+                                                                 : BUF_OOB, 0);
+    }
+  };
+  f32x4 accg[2][TPW], accu[2][TPW];
 #pragma unroll
   for (int m = 0; m < 2; ++m)
 #pragma unroll
-    for (int t = 0; t < NTT; ++t)
+    for (int j = 0; j < TPW; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) accg[m][t][r] = accu[m][t][r] = 0.f;
+      for (int r = 0; r < 4; ++r) accg[m][j][r] = accu[m][j][r] = 0.f;
 
-  for (int s = s0; s < s1; s += AB_UNROLL) {
-    uint4 ag[AB_UNROLL][2], au[AB_UNROLL][2], bx[AB_UNROLL][NTT];
+  uint4 pre[PPT];
+  uint4 bcur[SPC][TPW], bnext[SPC][TPW];
+  load_chunk(0, pre);
+  load_tokens(0, bcur);
+  store_chunk(0, pre);
+  __syncthreads();
+  for (int c = 0; c < chunks; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < chunks) {  // the next chunk is in flight during this one's products
+      load_chunk(c + 1, pre);
+      load_tokens(c + 1, bnext);
+    }
 #pragma unroll
-    for (int u = 0; u < AB_UNROLL; ++u) {
-      const int k = (s + u) * KS + grp * V;  // first reduction index of the lane
-      const bool ok = s + u < s1 && k < a.d;
-      const uint32_t kb = (uint32_t)k * ESZ;
+    for (int s = 0; s < SPC; ++s) {
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
-        const bool rok = ok && r_off[m] != BUF_OOB;
-        ag[u][m] = buf_load16(wr, rok ? r_off[m] + kb : BUF_OOB, 0);
-        au[u][m] = buf_load16(wr, rok ? r_off[m] + up + kb : BUF_OOB, 0);
-      }
+        const int row = 16 * m + (lane & 15);
+        const uint4 ag = *(const uint4*)&lds[buf][0][row][s * 64 + grp * 16];
+        const uint4 au = *(const uint4*)&lds[buf][1][row][s * 64 + grp * 16];
 #pragma unroll
-      for (int t = 0; t < NTT; ++t)
-        bx[u][t] = buf_load16(xr, ok && t_off[t] != BUF_OOB ? t_off[t] + kb : BUF_OOB, 0);
-    }
-#pragma unroll
-    for (int u = 0; u < AB_UNROLL; ++u)
-#pragma unroll
-      for (int t = 0; t < NTT; ++t)
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-          accg[m][t] = mfma_step<T>(ag[u][m], bx[u][t], accg[m][t]);
-          accu[m][t] = mfma_step<T>(au[u][m], bx[u][t], accu[m][t]);
+        for (int j = 0; j < TPW; ++j) {
+          accg[m][j] = mfma_step<T>(ag, bcur[s][j], accg[m][j]);
+          accu[m][j] = mfma_step<T>(au, bcur[s][j], accu[m][j]);
         }
+      }
+    }
+    if (c + 1 < chunks) {
+      store_chunk(buf ^ 1, pre);
+#pragma unroll
+      for (int s = 0; s < SPC; ++s)
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) bcur[s][j] = bnext[s][j];
+    }
+    __syncthreads();  // the other buffer is complete; this one may be overwritten next
   }
-  // the quarters meet in LDS, XT token tiles at a time, in wave order
+  // acts[token][neuron]: lane l, register r holds neuron 16 m + 4 (l / 16) + r
 #pragma unroll
-  for (int t0 = 0; t0 < NTT; t0 += XT) {
-    if (q > 0) {
+  for (int j = 0; j < TPW; ++j) {
+    const int tok = (w + AB_WAVES * j) * 16 + (lane & 15);
+    if (tok >= a.n) continue;
+    float* dst = a.acts + (size_t)tok * a.F;
 #pragma unroll
-      for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < 2; ++m) {
+      const int nb = n0 + 16 * m + 4 * grp;  // neurons nb .. nb + 3
+      float o[4];
 #pragma unroll
-        for (int i = 0; i < XT; ++i)
-          if (t0 + i < NTT) {
-            xch[q - 1][0][m][i][lane] = accg[m][t0 + i];
-            xch[q - 1][1][m][i][lane] = accu[m][t0 + i];
-          }
-    }
-    __syncthreads();
-    if (q == 0) {
+      for (int e = 0; e < 4; ++e) o[e] = gated(a.act, accg[m][j][e], accu[m][j][e]);
+      if ((a.F & 3) == 0) {
+        if (nb < a.F) *(float4*)(dst + nb) = make_float4(o[0], o[1], o[2], o[3]);
+      } else {
 #pragma unroll
-      for (int i = 0; i < XT; ++i) {
-        if (t0 + i >= NTT) break;
-        const int tok = (t0 + i) * 16 + (lane & 15);
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-          f32x4 g = accg[m][t0 + i], u = accu[m][t0 + i];
-#pragma unroll
-          for (int w = 0; w < AB_WAVES - 1; ++w) {
-            g += xch[w][0][m][i][lane];
-            u += xch[w][1][m][i][lane];
-          }
-          const int nb = n0 + 16 * m + 4 * grp;  // neurons nb .. nb + 3
-          if (tok < a.n) {
-            float* dst = a.acts + (size_t)tok * a.F;
-            float o[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = gated(a.act, g[e], u[e]);
-            if ((a.F & 3) == 0) {
-              if (nb < a.F) *(float4*)(dst + nb) = make_float4(o[0], o[1], o[2], o[3]);
-            } else {
-#pragma unroll
-              for (int e = 0; e < 4; ++e)
-                if (nb + e < a.F) dst[nb + e] = o[e];
-            }
-          }
-        }
+        for (int e = 0; e < 4; ++e)
+          if (nb + e < a.F) dst[nb + e] = o[e];
       }
     }
-    __syncthreads();  // xch is reused by the next round
   }
 }
 
@@ -188,15 +206,13 @@ static hipError_t act_batch_t(const np_shape& s, const void* weights, const void
     a.F = s.d_ffn;
     a.d = s.d_model;
     a.act = s.act;
-    const int ntt = (a.n + 15) / 16;
-#define NP_AB_CASE(N) \
-  hipLaunchKernelGGL((act_batch_kernel<T, N>), dim3(tiles), dim3(AB_WAVES * WAVE), 0, stream, a)
-    if (ntt <= 1) NP_AB_CASE(1);
-    else if (ntt <= 2) NP_AB_CASE(2);
-    else if (ntt <= 4) NP_AB_CASE(4);
-    else if (ntt <= 6) NP_AB_CASE(6);
-    else NP_AB_CASE(8);
-#undef NP_AB_CASE
+    const int ntt = (a.n + 15) / 16;  // token tiles; wave w takes tiles w, w + 4
+    if (ntt <= AB_WAVES)
+      hipLaunchKernelGGL((act_batch_kernel<T, 1>), dim3(tiles), dim3(AB_WAVES * WAVE), 0, stream,
+                         a);
+    else
+      hipLaunchKernelGGL((act_batch_kernel<T, 2>), dim3(tiles), dim3(AB_WAVES * WAVE), 0, stream,
+                         a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
