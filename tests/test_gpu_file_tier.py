@@ -55,3 +55,49 @@ def test_file_tier_7b_records(overlap, tmp_path):
             assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (t, l)
     assert pipe.device_error() == 0
     pipe.close()
+
+
+def test_file_tier_short_file_is_an_io_error(tmp_path):
+    """A plan naming records past the end of the file: np_stage_file returns
+    NP_ERR_IO at the chunk that reads them; the chunks before it are enqueued
+    and land in their slots."""
+    import os
+
+    from paper_2608_22643_amd import binding as B
+    from gpu_util import DEV, Bufs, to_dev
+
+    cfg = W.get("tiny")
+    L, F, k, C, rec = cfg.layers, cfg.d_ffn, cfg.k, cfg.capacity, cfg.record_bytes
+    store = W.storage(cfg)
+    path = str(tmp_path / "short.bin")
+    store[:1].tofile(path)  # layer 0 only
+    say("[file tier] short file")
+    bufs = Bufs(cfg)
+    pc = torch.zeros(L * 4, dtype=torch.int32).pin_memory()
+    pi = torch.zeros(L * k, dtype=torch.int32).pin_memory()
+    ps = torch.zeros(L * k, dtype=torch.int32).pin_memory()
+    n0 = 5
+    pc[0], pc[4] = n0, 3                              # 5 records of layer 0, 3 of layer 1
+    pi[:n0] = torch.arange(10, 10 + n0)
+    ps[:n0] = torch.arange(n0)
+    pi[k:k + 3] = torch.tensor([1, 2, 3])
+    ps[k:k + 3] = torch.tensor([0, 1, 2])
+    plan = B.np_stage_plan(pc.data_ptr(), pi.data_ptr(), ps.data_ptr())
+    cap = n0  # one chunk per layer
+    staging = torch.empty(2 * cap * (rec + 4) + 8192, dtype=torch.uint8).pin_memory()
+    landing = torch.empty(cap * (rec + 4), dtype=torch.uint8, device=DEV)
+    io = B.HostBuffer(cap * (rec + 4))
+    resident = torch.zeros(cfg.resident_bytes, dtype=torch.uint8, device=DEV)
+    fd = os.open(path, os.O_RDONLY | os.O_DIRECT)
+    try:
+        with pytest.raises(B.NPError) as e:
+            B.np_stage_file(bufs.shape, plan, 0, L, fd, 0, resident, staging, staging.numel(),
+                            io, io.nbytes, landing, landing.numel(), torch.cuda.current_stream())
+        assert e.value.status == B.NP_ERR_IO and "end of file" in str(e.value)
+    finally:
+        os.close(fd)
+    torch.cuda.synchronize()
+    res = resident.cpu().numpy().view(np.float32).reshape(L, C, -1)
+    for j in range(n0):
+        assert np.array_equal(res[0, j], store[0, 10 + j]), j
+    assert not res[1].any()
