@@ -77,3 +77,53 @@ def test_fullsize_7b_graph_step():
             got = decode_y(orc, cfg.adtype, y[l])
             assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (t, l)
     assert pipe.device_error() == 0
+
+
+def test_fullsize_7b_long_sequence():
+    """64 tokens of the 7B decode replayed from a HIP graph, in lockstep with
+    the oracle's selection and delta on every token (masks, ids, every delta
+    list and the slot maps bit for bit: the resident set fills, then LRU
+    victims appear), resident records on sampled slots every 8th token, and
+    the MLP output of two layers every 16th token."""
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get("7b")
+    L, d, F, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.k, cfg.capacity
+    T = 64
+    say(f"[fullsize] 7b long sequence, {T} tokens")
+    host = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
+    W.fill_storage(cfg, host.data_ptr())
+    store = host.numpy().view(np.uint16).reshape(L, F, 3 * d)
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T, host_storage=host)
+    pipe.capture_graph()
+    h = W.hidden(cfg, T)
+    st = orc.State(L, F, C)
+    rng = np.random.default_rng(9)
+    evictions = 0
+    for t in range(T):
+        pipe.step_graph(t)
+        torch.cuda.synchronize()
+        scores = pipe.scores.cpu().numpy().reshape(L, F)
+        mask, ids = orc.select(scores, k)
+        assert np.array_equal(pipe.active_ids.cpu().numpy().reshape(L, k), ids), t
+        assert np.array_equal(pipe.mask.cpu().numpy().view(np.uint32).reshape(L, -1), mask), t
+        ref = orc.delta(t, ids, st, C)
+        compare_delta(pipe.host_lists(), ref, L)
+        evictions += int(ref["counts"][:, 2].sum())
+        P, Q, U = pipe.host_state()
+        assert np.array_equal(P, st.slot_of) and np.array_equal(Q, st.neuron_of), t
+        assert np.array_equal(U, st.last_used), t
+        if t % 8 == 7:
+            res = pipe.resident.view(L, C, 3 * d * 2)
+            occ = np.argwhere(st.neuron_of >= 0)
+            for l, s in occ[rng.choice(len(occ), 64, replace=False)]:
+                got = res[l, s].cpu().numpy().view(np.uint16)
+                assert np.array_equal(got, store[l, st.neuron_of[l, s]]), (t, l, s)
+        if t % 16 == 15:
+            y = pipe.y.cpu().numpy().view(np.uint16).reshape(L, d)
+            for l in sorted(rng.choice(L, 2, replace=False)):
+                _, ref64 = orc.sparse_mlp(cfg, l, h[t], store, ids[l], want_f64=True)
+                got = decode_y(orc, cfg.adtype, y[l])
+                assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (t, l)
+    assert evictions > 0, "the sequence never filled the resident set"
+    assert pipe.device_error() == 0
