@@ -230,3 +230,62 @@ def test_centroid_pipeline_lockstep(graph):
                                       want_f64=True)
             assert np.all(np.abs(y[l] - ref64) <= mlp_tolerance("f32", ref64))
     assert pipe.device_error() == 0
+
+
+def test_centroid_pipeline_7b_fullsize():
+    """The decode path with the centroid predictor at the full 7B shape
+    (K = 512 centroids, D = 4096 features, 2 x 31 heads), 16 eager tokens in
+    lockstep with the oracle: logits within the fp32 bound on the first
+    token; centroid ids, intersection masks, lists, counts, delta lists and
+    slot maps bit for bit on every token; MLP outputs sampled."""
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get("7b")
+    L, d, F, K, D, k, C = (cfg.layers, cfg.d_model, cfg.d_ffn, cfg.centroid_k, cfg.feat_dim,
+                           cfg.k, cfg.capacity)
+    T = 16
+    say(f"[centroid fullsize] 7b K={K} D={D}, {T} tokens")
+    host = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
+    W.fill_storage(cfg, host.data_ptr())
+    store = host.numpy().view(np.uint16).reshape(L, F, 3 * d)
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T, host_storage=host,
+                          predictor="centroid")
+    heads = W.centroid_heads(cfg)
+    feats = W.features(cfg, T)
+    bank = W.centroid_bank(cfg)
+    h = W.hidden(cfg, T)
+    st = orc.State(L, F, C)
+    rng = np.random.default_rng(4)
+    for t in range(T):
+        pipe.step(t)
+        torch.cuda.synchronize()
+        logits = pipe.logits.cpu().numpy().reshape(2 * L, K)
+        if t == 0:
+            ref = orc.centroid_logits(heads, feats[0], 2 * L, K, D, cfg.wdtype, cfg.adtype)
+            Hd = np.abs(orc.decode(cfg.wdtype, heads).reshape(2 * L * K, D))
+            fd = np.abs(orc.decode(cfg.adtype, feats[0]))
+            bound = (D + 2) * 2.0 ** -24 * (Hd @ fd).reshape(2 * L, K) + np.abs(ref) * 2.0 ** -23
+            assert np.all(np.abs(logits.astype(np.float64) - ref) <= bound)
+        o = orc.centroid_active(logits, bank, L, F, K, k)
+        n = pipe.active_counts.cpu().numpy()[:L]
+        assert np.array_equal(n, o["counts"]), t
+        assert np.array_equal(pipe.cids.cpu().numpy()[:2 * L].reshape(2, L), o["cids"]), t
+        assert np.array_equal(pipe.mask.cpu().numpy().view(np.uint32).reshape(L, -1), o["mask"])
+        ids = pipe.active_ids.cpu().numpy().reshape(L, k)
+        for l in range(L):
+            assert np.array_equal(ids[l][:n[l]], o["active_ids"][l][:n[l]]), (t, l)
+        ref_d = orc.delta_n(t, o["active_ids"], o["counts"], st, C)
+        got = pipe.host_lists()
+        for l in range(L):
+            got["active_slots"][l][n[l]:] = -1
+        compare_delta(got, ref_d, L)
+        P, Q, U = pipe.host_state()
+        assert np.array_equal(P, st.slot_of) and np.array_equal(Q, st.neuron_of), t
+        if t % 5 == 4:
+            y = pipe.y.cpu().numpy().view(np.uint16).reshape(L, d)
+            for l in sorted(rng.choice(L, 2, replace=False)):
+                _, ref64 = orc.sparse_mlp(cfg, l, h[t], store, o["active_ids"][l][:n[l]],
+                                          want_f64=True)
+                got_y = decode_y(orc, cfg.adtype, y[l])
+                assert np.all(np.abs(got_y - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (t, l)
+    assert pipe.device_error() == 0
