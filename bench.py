@@ -42,11 +42,11 @@ HBM_PEAK_GBPS = 8000.0
 MLP_COUNTERS = {
     "config": "7b",
     "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
-    "sha256": "fe692c6038a177b6991d8546e9ce20abff0dc03ee996f64e5f3379b99e64a23b"
-              "e7c091e9cb927d79cad3826398857f00b7e26d440bcaac25904b88684aa49c3f",
+    "sha256": "e1a16a7b4837026533e00b20e4ede2f6b7081ea5f7f713abaef80b0942e05aef"
+              "5a89f137f8ede14f2a3db251acb659578b978d62f554eac21f05a7cf43580852",
     "fetch_kib": {"rows": 19933.4, "reduce": 4119.5},
     "write_kib": {"rows": 4096.0, "reduce": 8.0},
-    "copy_fetch_kib": 131087.7, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+    "copy_fetch_kib": 131087.3, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
 }
 
 

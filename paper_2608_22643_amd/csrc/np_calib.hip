@@ -95,7 +95,7 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int k = c * KC + p_col[i] * V;  // first element of the piece
-      r[i] = buf_load16(wr, (p_off[i] != BUF_OOB && k < a.d) ? p_off[i] + (uint32_t)k * ESZ
+      r[i] = buf_load16_nt(wr, (p_off[i] != BUF_OOB && k < a.d) ? p_off[i] + (uint32_t)k * ESZ
                                                              : BUF_OOB, 0);
     }
   };

@@ -247,9 +247,9 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
         const uint32_t off = roff + loff[c];  // both < 2^31: no wrap
-        gw[r][c] = buf_load16(rsrc, off, 0);
-        uw[r][c] = buf_load16(rsrc, off, third);
-        dw[r][c] = buf_load16(rsrc, off, 2 * third);
+        gw[r][c] = buf_load16_nt(rsrc, off, 0);
+        uw[r][c] = buf_load16_nt(rsrc, off, third);
+        dw[r][c] = buf_load16_nt(rsrc, off, 2 * third);
       }
     }
     // next round's slots, in flight behind this round's records
@@ -494,7 +494,7 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_colsplit_kernel(MlpArgs a) {
     const bool ok = drow_slot[j] >= 0 && drow_slot[j] < a.C;  // others reported by (i)
     const uint32_t base = ok ? (uint32_t)drow_slot[j] * 3u * third + band_off : BUF_OOB;
 #pragma unroll
-    for (int q = 0; q < BV; ++q) dv[j][q] = buf_load16(rsrc, base, ok ? 16u * q : 0u);
+    for (int q = 0; q < BV; ++q) dv[j][q] = buf_load16_nt(rsrc, base, ok ? 16u * q : 0u);
   }
   // (i) the gate/up dot products of this workgroup's rows
   const int row_begin = (int)(((long long)b * n) / a.n_wg);
@@ -519,8 +519,8 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_colsplit_kernel(MlpArgs a) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const uint32_t roff = valid[r] ? (uint32_t)slot[r] * 3u * third + loff : BUF_OOB;
-      gw[r] = buf_load16(rsrc, roff, 0);
-      uw[r] = buf_load16(rsrc, roff, valid[r] ? third : 0u);
+      gw[r] = buf_load16_nt(rsrc, roff, 0);
+      uw[r] = buf_load16_nt(rsrc, roff, valid[r] ? third : 0u);
     }
     float val[NVAL];
 #pragma unroll
