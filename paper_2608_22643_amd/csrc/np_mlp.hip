@@ -188,9 +188,14 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
     }
   }
   const float thr = a.thr ? a.thr[a.layer] : 0.f;  // eq. 1; 0 keeps every row
-  // balanced contiguous ranges: workgroup b takes rows [b*n/G, (b+1)*n/G)
-  const int row_begin = (int)(((long long)b * n_active) / a.n_wg);
-  const int row_end = (int)(((long long)(b + 1) * n_active) / a.n_wg);
+  // sparse: balanced contiguous ranges of the active list, workgroup b takes
+  // [b*n/G, (b+1)*n/G).  Dense (no slot list): workgroup b takes rows b,
+  // b + G, b + 2G, ... (index i of its range is row i*G + b), so the
+  // workgroups of a round read neighbouring records together
+  const bool dense = a.slots == nullptr;
+  const int row_begin = dense ? 0 : (int)(((long long)b * n_active) / a.n_wg);
+  const int row_end = dense ? n_active / a.n_wg + (b < n_active % a.n_wg ? 1 : 0)
+                            : (int)(((long long)(b + 1) * n_active) / a.n_wg);
   const int v0 = p * WAVE * CPL;  // first vector of this wave's column slice
   int gen0 = 0;  // grid barrier generation at entry (thread 0)
   if (FUSED && threadIdx.x == 0)
@@ -202,7 +207,8 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   int my_slot = -1;
   {
     const int r0 = row_begin + team * R;
-    if (lane < R && r0 + lane < row_end) my_slot = a.slots ? a.slots[r0 + lane] : r0 + lane;
+    if (lane < R && r0 + lane < row_end)
+      my_slot = dense ? (r0 + lane) * a.n_wg + b : a.slots[r0 + lane];
   }
   // Loads below are unconditional, with no branches around them, so the
   // compiler can wait for each stage's loads alone.  Record loads are buffer
@@ -255,7 +261,9 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
     // next round's slots, in flight behind this round's records
     {
       const int rn = r0 + teams * R;
-      my_slot = (lane < R && rn + lane < row_end) ? (a.slots ? a.slots[rn + lane] : rn + lane) : -1;
+      my_slot = (lane < R && rn + lane < row_end)
+                    ? (dense ? (rn + lane) * a.n_wg + b : a.slots[rn + lane])
+                    : -1;
     }
 #pragma unroll
     for (int st = 0; st < S; ++st) {

@@ -129,3 +129,46 @@ def test_mlp_paths_bad_slot(path, monkeypatch):
                        device=DEV)
     B.np_sparse_mlp(bufs.shape, 1, to_dev(h), res, bad, bad.numel(), y, bufs.ws)
     assert B.np_device_error(bufs.ws) & B.NP_DEVERR_NOT_RESIDENT
+
+
+def test_mlp_multi_round():
+    """More active rows than one 8-row round per workgroup (2 to 3 rounds,
+    workgroups with different round counts in one launch), and SwiGLU with a
+    threshold on a second layer."""
+    cfg = cfg_small("d4096_many", 2, 4096, 6000, 16, 4200, 4500, "f16")
+    say("[mlp multi-round]")
+    bufs, rng, store, res, neuron, h = setup(cfg, 24)
+    x = to_dev(h)
+    y = torch.zeros(cfg.d_model, dtype=torch.float16, device=DEV)
+    y2 = torch.zeros_like(y)
+    slots = rng.permutation(cfg.capacity)[:cfg.k].astype(np.int32)
+    sl = to_dev(slots)
+    for n in (2048, 2049, 2304, 2560, 3000, 4100, 4200):
+        B.np_sparse_mlp(bufs.shape, 0, x, res, sl, n, y, bufs.ws)
+        B.np_sparse_mlp(bufs.shape, 0, x, res, sl, n, y2, bufs.ws)
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2), n
+        _, ref64 = orc.sparse_mlp(cfg, 0, h, store, neuron[0][slots[:n]].astype(np.int32),
+                                  want_f64=True)
+        got = decode_y(orc, cfg.adtype, y.cpu().view(torch.uint8).numpy())
+        assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), n
+    # SwiGLU with a threshold that drops about a third of the rows
+    sw = cfg.with_(act="swiglu")
+    bufs2 = Bufs(sw)
+    bufs2.reset()
+    n = 3000
+    ids = neuron[1][slots[:n]].astype(np.int32)
+    rec = orc.decode(sw.wdtype, store[1][ids])
+    xv = orc.decode(sw.adtype, h)
+    g, u = rec[:, :4096] @ xv, rec[:, 4096:8192] @ xv
+    a = np.sort(np.abs(g / (1 + np.exp(-g)) * u))
+    j = int(np.argmax(np.diff(a[n // 4:n // 2]))) + n // 4
+    T = np.float32((a[j] + a[j + 1]) / 2)
+    thr = to_dev(np.array([0.0, T], np.float32))
+    counts = to_dev(np.array([0, n], np.int32))
+    B.np_sparse_mlp_t(bufs2.shape, 1, x, res, sl, cfg.k, counts, thr, y, bufs2.ws)
+    torch.cuda.synchronize()
+    _, ref64 = orc.sparse_mlp(sw, 1, h, store, ids, want_f64=True, threshold=float(T))
+    got = decode_y(orc, sw.adtype, y.cpu().view(torch.uint8).numpy())
+    assert np.all(np.abs(got - ref64) <= mlp_tolerance(sw.adtype, ref64))
+    assert B.np_device_error(bufs.ws) == 0 and B.np_device_error(bufs2.ws) == 0
