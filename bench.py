@@ -42,11 +42,11 @@ HBM_PEAK_GBPS = 8000.0
 MLP_COUNTERS = {
     "config": "7b",
     "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
-    "sha256": "e1a16a7b4837026533e00b20e4ede2f6b7081ea5f7f713abaef80b0942e05aef"
+    "sha256": "0b1bc9ab260122154dd279eed2d6a60a75d6dceea57046cafc5af5e8e3a5e72d"
               "5a89f137f8ede14f2a3db251acb659578b978d62f554eac21f05a7cf43580852",
-    "fetch_kib": {"rows": 19933.4, "reduce": 4119.5},
+    "fetch_kib": {"rows": 19929.9, "reduce": 4118.5},
     "write_kib": {"rows": 4096.0, "reduce": 8.0},
-    "copy_fetch_kib": 131087.3, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+    "copy_fetch_kib": 131087.9, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
 }
 
 
@@ -84,6 +84,14 @@ def mlp_bytes_per_launch(cfg) -> int:
     return cfg.k * 3 * cfg.d_model * esz + cfg.k * 4 + 2 * cfg.d_model * esz
 
 
+def predict_bytes(cfg) -> int:
+    """Algorithmic bytes of one np_predict (all L' layers): A [L'][r][d] and
+    B [L'][F][r] in the weight type, h, and the fp32 scores written."""
+    esz = 4 if cfg.wdtype == "f32" else 2
+    L, d, F, r = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.rank
+    return L * r * d * esz + L * F * r * esz + d * esz + L * F * 4
+
+
 def trace_marker():
     """A one-element float fill kernel: in a kernel trace of this script, the
     only float fills bracket the steps the sparse-MLP roofline is taken on."""
@@ -106,28 +114,69 @@ def timed_graph_steps(pipe, t0, steps):
     return time.perf_counter() - t_start
 
 
-def timed_steps(pipe, t0, steps, with_mlp_events=True):
+def timed_steps(pipe, t0, steps, with_mlp_events=True, step_us=None):
     """Times `steps` decode tokens.  With with_mlp_events, one pair of HIP
     events on the main stream brackets each token's block of L' back-to-back
     np_sparse_mlp calls; the mean per call over the timed region is returned
-    (gaps between the calls included)."""
+    (gaps between the calls included).  A list passed as step_us receives
+    each token's device time, from an event before its np_predict to the end
+    of its last np_sparse_mlp (on the same stream)."""
     import torch
 
     L = pipe.cfg.layers
-    evs = None
+    evs = starts = None
     if with_mlp_events:
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(steps)]
+        if step_us is not None:
+            starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(steps):
+        if starts:
+            starts[i].record(pipe.main)
         pipe.step(t0 + i, mlp_block_events=evs[i] if evs else None)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     mlp_us = None
     if evs:
         mlp_us = sum(a.elapsed_time(b) * 1e3 for a, b in evs) / (steps * L)
+    if starts:
+        step_us.extend(a.elapsed_time(e[1]) * 1e3 for a, e in zip(starts, evs))
     return wall, mlp_us
+
+
+def read_ref_gbps(nbytes: int = 2 << 30, reps: int = 5) -> float:
+    """A read-bound library kernel of the same run for reference: torch.mv
+    (the library GEMV) of a [nbytes / 8192][4096] fp16 matrix by a vector,
+    timed with events (GB/s of matrix bytes read)."""
+    import torch
+
+    w = torch.ones(nbytes // 8192, 4096, dtype=torch.float16, device="cuda")
+    x = torch.ones(4096, dtype=torch.float16, device="cuda")
+    torch.mv(w, x)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        torch.mv(w, x)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    del w, x
+    return nbytes / (us * 1e-6) / 1e9
+
+
+def persistence_of(ids_seq):
+    """Mean over consecutive tokens and layers of |A_t & A_t-1| / k, from the
+    active-id lists of consecutive tokens ([L'][k] arrays)."""
+    import numpy as np
+
+    vals = []
+    for a, b in zip(ids_seq, ids_seq[1:]):
+        for l in range(a.shape[0]):
+            vals.append(np.intersect1d(a[l], b[l], assume_unique=True).size / a.shape[1])
+    return float(np.mean(vals)) if vals else None
 
 
 def breakdown(pipe, t0, steps):
@@ -141,7 +190,7 @@ def breakdown(pipe, t0, steps):
     L, k = cfg.layers, cfg.k
     names = ("predict", "select", "delta", "stage", "mlp")
     acc = {n: 0.0 for n in names}
-    counts = []
+    counts, ids = [], []
     ybytes = cfg.d_model * (4 if cfg.adtype == "f32" else 2)
     for i in range(steps):
         t = t0 + i
@@ -165,7 +214,8 @@ def breakdown(pipe, t0, steps):
         for j, n in enumerate(names):
             acc[n] += ev[j].elapsed_time(ev[j + 1]) * 1e3
         counts.append(delta_stats(pipe))
-    return {n: round(v / steps, 2) for n, v in acc.items()}, counts
+        ids.append(pipe.active_ids.cpu().numpy().reshape(L, k))
+    return {n: round(v / steps, 2) for n, v in acc.items()}, counts, ids
 
 
 def h2d_peak_gbps(nbytes: int = 1 << 30) -> float:
@@ -480,13 +530,14 @@ def sweep_run(host_storage, steps: int) -> dict:
         for i in range(warm):
             pipe.step(i)
         wall, mlp_us = timed_steps(pipe, warm, steps)
-        _, per_tok = breakdown(pipe, warm + steps, max(3, steps // 2))
+        _, per_tok, ids = breakdown(pipe, warm + steps, max(3, steps // 2))
         if pipe.device_error():
             raise RuntimeError(f"sweep {cfg.name}: device error word {pipe.device_error():#x}")
         n_in = float(np.mean([c[:, 0].sum() for c in per_tok]))
         n_hit = float(np.mean([c[:, 1].sum() for c in per_tok]))
         b = mlp_bytes_per_launch(cfg)
         out[cfg.name] = {"k": cfg.k, "C": cfg.capacity, "persistence": cfg.persistence,
+                         "persistence_measured": round(persistence_of(ids), 4),
                          "tok_s": round(steps / wall, 1),
                          "incoming_rows_per_token": round(n_in, 1),
                          "staged_MB_per_token": round(n_in * cfg.record_bytes / 1e6, 2),
@@ -603,7 +654,20 @@ def cpu_baseline(cfg, host_storage, seconds: float):
     return {"value": round(n / el, 4), "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"{n} whole decode tokens (cold start first) of the {cfg.name} workload: "
                       f"predict, select, delta, sparse MLP of all {cfg.layers} layers; "
-                      f"staging omitted (a byte copy); {el:.1f} s on 1 host thread"}
+                      f"staging omitted (a byte copy); {el:.1f} s on 1 host thread",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count()}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():
@@ -618,7 +682,7 @@ def main():
     ap.add_argument("--host-tier-steps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--breakdown-steps", type=int, default=10)
-    ap.add_argument("--mlp-steps", type=int, default=20)
+    ap.add_argument("--mlp-steps", type=int, default=50)
     ap.add_argument("--extra-configs", default="13b",
                     help="comma-separated further configurations measured after the main one")
     ap.add_argument("--extra-steps", type=int, default=30)
@@ -707,8 +771,12 @@ def main():
     # sparse-MLP roofline: further steps, each token's block of calls
     # bracketed by events (staging of the token finished before the block)
     trace_marker()
-    _, mlp_us = timed_steps(pipe, t1, args.mlp_steps)
+    step_list = []
+    _, mlp_us = timed_steps(pipe, t1, args.mlp_steps, step_us=step_list)
     trace_marker()
+    step_pct = {"p50": round(float(np.percentile(step_list, 50)), 2),
+                "p99": round(float(np.percentile(step_list, 99)), 2), "tokens": len(step_list),
+                "note": "device time per token, np_predict start to last np_sparse_mlp end"}
     log(f"[bench] np_sparse_mlp: {mlp_us:.2f} us per call")
     err = pipe.device_error()
     if err:
@@ -720,14 +788,19 @@ def main():
     achieved = bytes_launch / (mlp_us * 1e-6) / 1e9
     # per-phase breakdown (no overlap) and delta statistics over its tokens
     t1 += args.mlp_steps
-    bd, per_tok = breakdown(pipe, t1, max(1, args.breakdown_steps))
+    bd, per_tok, ids = breakdown(pipe, t1, max(2, args.breakdown_steps))
     log(f"[bench] breakdown us: {bd}")
+    pbytes = predict_bytes(cfg)
+    predictor = {"avg_us": bd["predict"], "bytes": pbytes,
+                 "achieved_GBps": round(pbytes / (bd["predict"] * 1e-6) / 1e9, 1)}
+    predictor["frac"] = round(predictor["achieved_GBps"] / HBM_PEAK_GBPS, 4)
     n_in = np.mean([c[:, 0].sum() for c in per_tok])
     n_hit = np.mean([c[:, 1].sum() for c in per_tok])
     rec = cfg.record_bytes
     stats = {"incoming_rows_per_token": round(float(n_in), 1),
              "staged_MB_per_token": round(float(n_in) * rec / 1e6, 2),
              "reuse_pct": round(100.0 * float(n_hit) / (cfg.k * cfg.layers), 2),
+             "persistence_pct": round(100.0 * persistence_of(ids), 2),
              "tokens": len(per_tok)}
     del pipe
     torch.cuda.empty_cache()
@@ -784,6 +857,8 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    read_ref = round(read_ref_gbps(), 1)
+    log(f"[bench] read reference: {read_ref} GB/s")
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(cfg, host_storage, args.cpu_seconds)
@@ -818,7 +893,11 @@ def main():
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "traffic_detail": traffic_detail,
-                     "bytes_per_launch": bytes_launch, "avg_launch_us": round(mlp_us, 3)},
+                     "bytes_per_launch": bytes_launch, "avg_launch_us": round(mlp_us, 3),
+                     "frac_of_read_ref": round(achieved / read_ref, 4)},
+        "step_us": step_pct,
+        "predictor": predictor,
+        "read_ref": {"GBps": read_ref, "kernel": "torch.mv (library GEMV) over a 2 GiB [262144][4096] fp16 matrix"},
         ("eager_tok_s" if graph else "graph_tok_s"): round(1e3 / other_ms, 2),
         "sparse_mlp_tok_s": round(1e6 / (mlp_us * cfg.layers), 1),
         "cold_start_ms": round(cold_ms, 2),
