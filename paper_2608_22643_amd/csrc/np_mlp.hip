@@ -393,53 +393,59 @@ __device__ inline void store_y4(void* y, int col, float4 v) {
 }
 
 // y[col] = sum over workgroups b of partials[b][col], in a fixed order.  A
-// block of 256 threads owns 16 columns; thread t loads 64 contiguous bytes
-// of each of the partial rows t, t+256, t+512, t+768 (all loads in flight at
-// once).  Each wave then reduce-scatters its 16 column sums, and one lane per
-// column adds the four waves' sums in wave order.
+// block of 256 threads owns 16 columns (64 bytes of every partial row); the
+// per-thread sums meet through a shuffle tree within each wave and then in
+// wave order through LDS.
 constexpr int RED_COLS = 16;
 
 template <class T>
 __global__ __launch_bounds__(256) void mlp_reduce_kernel(const float* __restrict__ partials,
                                                          int n_wg, int d, void* y) {
-  __shared__ float red[4][RED_COLS];
-  const int t = threadIdx.x, lane = t & (WAVE - 1), w = t / WAVE;
-  const int col = blockIdx.x * RED_COLS;
-  float4 v[4][RED_COLS / 4];
+  // thread t reads 16-byte piece q = t % 4 of the workgroup's 16 columns in
+  // partial rows t / 4, t / 4 + 64, ...: each wave instruction reads 16 whole
+  // 64-byte row pieces
+  __shared__ float4 red[4][4];  // wave, piece
+  const int t = threadIdx.x, lane = t & (WAVE - 1), w = t / WAVE, q = t & 3, rs = t >> 2;
+  const int col = blockIdx.x * RED_COLS + 4 * q;
+  const bool cok = col < d;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int r0 = rs; r0 < n_wg; r0 += 256) {  // rows in a fixed order
+    float4 v[4];
 #pragma unroll
-  for (int h = 0; h < 4; ++h) {
-    const int row = t + 256 * h;
-#pragma unroll
-    for (int q = 0; q < RED_COLS / 4; ++q)
-      v[h][q] = (row < n_wg && col + 4 * q < d)
-                    ? *(const float4*)(partials + (size_t)row * d + col + 4 * q)
-                    : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-  float s[RED_COLS];
-#pragma unroll
-  for (int q = 0; q < RED_COLS / 4; ++q) {
-    float4 a = v[0][q];
-#pragma unroll
-    for (int h = 1; h < 4; ++h) {
-      a.x += v[h][q].x;
-      a.y += v[h][q].y;
-      a.z += v[h][q].z;
-      a.w += v[h][q].w;
+    for (int h = 0; h < 4; ++h) {
+      const int row = r0 + 64 * h;
+      v[h] = (row < n_wg && cok) ? *(const float4*)(partials + (size_t)row * d + col)
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    s[4 * q] = a.x;
-    s[4 * q + 1] = a.y;
-    s[4 * q + 2] = a.z;
-    s[4 * q + 3] = a.w;
-  }
-  wave_reduce_scatter<RED_COLS>(s);  // lane l: wave sum of column l / 4
-  if (lane % (WAVE / RED_COLS) == 0) red[w][lane / (WAVE / RED_COLS)] = s[0];
-  __syncthreads();
-  if (t < RED_COLS / 4 && col + 4 * t < d) {
-    float4 o;
-    float* of = (float*)&o;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) of[j] = red[0][4 * t + j] + red[1][4 * t + j] + red[2][4 * t + j] + red[3][4 * t + j];
-    store_y4<T>(y, col + 4 * t, o);
+    for (int h = 0; h < 4; ++h) {
+      acc.x += v[h].x;
+      acc.y += v[h].y;
+      acc.z += v[h].z;
+      acc.w += v[h].w;
+    }
+  }
+  // the wave's 16 row groups of each piece: a fixed shuffle tree over lane
+  // bits 2..5, leaving lane q with piece q's wave sum
+#pragma unroll
+  for (int m = 4; m < WAVE; m <<= 1) {
+    acc.x += __shfl_xor(acc.x, m, WAVE);
+    acc.y += __shfl_xor(acc.y, m, WAVE);
+    acc.z += __shfl_xor(acc.z, m, WAVE);
+    acc.w += __shfl_xor(acc.w, m, WAVE);
+  }
+  if (lane < 4) red[w][lane] = acc;
+  __syncthreads();
+  if (t < 4 && cok) {  // waves in order
+    float4 o = red[0][t];
+#pragma unroll
+    for (int k = 1; k < 4; ++k) {
+      o.x += red[k][t].x;
+      o.y += red[k][t].y;
+      o.z += red[k][t].z;
+      o.w += red[k][t].w;
+    }
+    store_y4<T>(y, col, o);
   }
 }
 
