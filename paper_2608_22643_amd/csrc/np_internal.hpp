@@ -20,7 +20,7 @@ namespace np {
 //       +256  int32  sparse-MLP grid barrier: arrivals of the current call
 //       +384  int32  sparse-MLP grid barrier: generation (calls completed)
 //   [4096, +L'*r*4)      predictor intermediate z, fp32 [L'][r]
-//   [.., +MLP_MAX_WG*d*4) sparse-MLP per-workgroup partial sums, fp32
+//   [.., +MLP_MAX_WG*ceil16(d)*4) sparse-MLP per-workgroup partial sums, fp32
 // ---------------------------------------------------------------------------
 constexpr size_t WS_ERR = 0;
 constexpr size_t WS_TOKEN = 64;
@@ -35,7 +35,8 @@ inline size_t ws_partials_offset(const np_shape& s) {
   return align256(ws_z_offset() + (size_t)s.layers * s.rank * 4);
 }
 inline size_t ws_total(const np_shape& s) {
-  return align256(ws_partials_offset(s) + (size_t)MLP_MAX_WG * s.d_model * 4);
+  // partial rows of d rounded up to whole 16-column blocks
+  return align256(ws_partials_offset(s) + (size_t)MLP_MAX_WG * ((s.d_model + 15) / 16 * 16) * 4);
 }
 
 inline int dtype_size(int dt) { return dt == NP_F32 ? 4 : 2; }

@@ -45,7 +45,7 @@ struct MlpArgs {
   const uint4* res_layer;  // first record of the layer in the resident buffer
   const int32_t* slots;    // active_slots of the layer; nullptr: row j is slot j (dense layer)
   const uint4* x;
-  float* partials;         // [n_wg][d]
+  float* partials;         // [d/16][n_wg][16] (two kernels); fused: position order
   void* ws;
   int n_active, C, NV, n_wg, P, PP, teams;  // PP: P rounded up to a power of two
   uint32_t layer_bytes;  // resident bytes of the layer (< 2^31)
@@ -353,7 +353,6 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
     }
   }
   // this wave's column slice of the workgroup's partial y (team 0)
-  float* dst = a.partials + (size_t)b * a.NV * V;
   if (team == 0) {
     if constexpr (FUSED) {  // position order, agent-scope stores (see above)
       const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.partials, (uint32_t)a.n_wg * a.NV * V * 4u);
@@ -366,14 +365,17 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
           buf_store16_agent(prs, off, make_float4(yacc[c][4 * q], yacc[c][4 * q + 1],
                                                   yacc[c][4 * q + 2], yacc[c][4 * q + 3]));
         }
-    } else {
+    } else {  // blocks of 16 columns: [d/16][n_wg][16] (see the reduce kernel)
 #pragma unroll
       for (int c = 0; c < CPL; ++c)
         if (vok[c]) {
-          float4* d4 = (float4*)(dst + (size_t)(v0 + lane + WAVE * c) * V);
+          const int col0 = (v0 + lane + WAVE * c) * V;
 #pragma unroll
-          for (int e = 0; e < V; e += 4)
-            d4[e / 4] = make_float4(yacc[c][e], yacc[c][e + 1], yacc[c][e + 2], yacc[c][e + 3]);
+          for (int e = 0; e < V; e += 4) {
+            const int col = col0 + e;
+            float4* d4 = (float4*)(a.partials + ((size_t)(col >> 4) * a.n_wg + b) * 16 + (col & 15));
+            *d4 = make_float4(yacc[c][e], yacc[c][e + 1], yacc[c][e + 2], yacc[c][e + 3]);
+          }
         }
     }
   }
@@ -392,29 +394,30 @@ __device__ inline void store_y4(void* y, int col, float4 v) {
   }
 }
 
-// y[col] = sum over workgroups b of partials[b][col], in a fixed order.  A
-// block of 256 threads owns 16 columns (64 bytes of every partial row); the
-// per-thread sums meet through a shuffle tree within each wave and then in
-// wave order through LDS.
+// y[col] = sum over workgroups b of partial_b[col], in a fixed order.  The
+// rows kernel stores the partials in blocks of 16 columns, [d/16][n_wg][16]
+// fp32, so the block of 256 threads that owns 16 columns reads n_wg * 64
+// contiguous bytes; the per-thread sums meet through a shuffle tree within
+// each wave and then in wave order through LDS.
 constexpr int RED_COLS = 16;
 
 template <class T>
 __global__ __launch_bounds__(256) void mlp_reduce_kernel(const float* __restrict__ partials,
                                                          int n_wg, int d, void* y) {
-  // thread t reads 16-byte piece q = t % 4 of the workgroup's 16 columns in
-  // partial rows t / 4, t / 4 + 64, ...: each wave instruction reads 16 whole
-  // 64-byte row pieces
+  // thread t reads 16-byte piece q = t % 4 of partial rows t / 4, t / 4 + 64,
+  // ...: each wave instruction reads 1 KiB of contiguous memory
   __shared__ float4 red[4][4];  // wave, piece
   const int t = threadIdx.x, lane = t & (WAVE - 1), w = t / WAVE, q = t & 3, rs = t >> 2;
   const int col = blockIdx.x * RED_COLS + 4 * q;
   const bool cok = col < d;
+  const float* blk = partials + (size_t)blockIdx.x * n_wg * RED_COLS + 4 * q;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int r0 = rs; r0 < n_wg; r0 += 256) {  // rows in a fixed order
     float4 v[4];
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
       const int row = r0 + 64 * h;
-      v[h] = (row < n_wg && cok) ? *(const float4*)(partials + (size_t)row * d + col)
+      v[h] = (row < n_wg && cok) ? *(const float4*)(blk + (size_t)row * RED_COLS)
                                  : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
