@@ -45,7 +45,7 @@ struct MlpArgs {
   const uint4* res_layer;  // first record of the layer in the resident buffer
   const int32_t* slots;    // active_slots of the layer; nullptr: row j is slot j (dense layer)
   const uint4* x;
-  float* partials;         // [d/16][n_wg][16] (two kernels); fused: position order
+  float* partials;         // [d/16][n_wg][16] fp32
   void* ws;
   int n_active, C, NV, n_wg, P, PP, teams;  // PP: P rounded up to a power of two
   uint32_t layer_bytes;  // resident bytes of the layer (< 2^31)
@@ -57,18 +57,26 @@ struct MlpArgs {
 };
 
 
-// Single-kernel path.  Partial rows are stored in "position" order: float4
-// position pos = ((p*CPL + c)*(V/4) + q)*64 + lane holds columns
-// v*V + 4q .. v*V + 4q + 3 of vector v = (p*CPL + c)*64 + lane, so each wave
-// store instruction writes 1 KiB of contiguous memory.  The reduction works
-// on chunks of 4 positions (64 bytes of every partial row): workgroup b takes
-// chunks b, b + n_wg, ... (at most FUSED_CH); for each, thread t reads
-// position t % 4 of partial rows t/4, t/4 + nt/4, ... (at most FUSED_RPT),
-// the per-thread sums meet in LDS and one thread per column adds them in
-// row order.  The barrier's spin is bounded (polls of about 1 us each).
-constexpr int FUSED_CH = 4;
-constexpr int FUSED_RPT = 4;
+// Single-kernel path.  The partials use the blocked layout of the two-kernel
+// path ([d/16][n_wg][16] fp32), written with agent-scope stores; after the
+// grid barrier workgroup b reduces column blocks b, b + n_wg, ... with
+// agent-scope loads, in the reduce kernel's order (thread t: 16-byte piece
+// t % 4 of rows t/4, t/4 + nt/4, ...; a shuffle tree within each wave, then
+// the waves in order).  The barrier's spin is bounded (polls of about 1 us
+// each).
 constexpr uint32_t MLP_SPIN_LIMIT = 1u << 20;
+
+template <class T>
+__device__ inline void store_y4(void* y, int col, float4 v) {
+  if constexpr (T::dtype == NP_F32) {
+    *(float4*)((float*)y + col) = v;
+  } else {
+    uint2 o;
+    o.x = T::from_f32(v.x) | (T::from_f32(v.y) << 16);
+    o.y = T::from_f32(v.z) | (T::from_f32(v.w) << 16);
+    *(uint2*)((uint16_t*)y + col) = o;
+  }
+}
 
 template <class T>
 __device__ inline void store_y1(void* y, int col, float v) {
@@ -108,58 +116,53 @@ __device__ inline void grid_barrier(void* ws, int n_wg, int gen0) {
 
 template <class T>
 __device__ inline void fused_reduce(const MlpArgs& a, int gen0, float4* red) {
-  constexpr int V = T::V;
   grid_barrier(a.ws, a.n_wg, gen0);
-  const int d = a.NV * V, nchunks = d / 16;
-  const int b = blockIdx.x, t = threadIdx.x, nt = blockDim.x;
-  const int q = t & 3, rsub = t >> 2, rstep = nt >> 2;
-  const int rpt = (a.n_wg + rstep - 1) / rstep;  // partial rows per thread, uniform
-  const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.partials, (uint32_t)a.n_wg * d * 4u);
-  for (int chunk = b, j = 0; chunk < nchunks && j < FUSED_CH; chunk += a.n_wg, ++j) {
-    float4 v[FUSED_RPT];
+  const int d = a.NV * T::V, nblk = (d + 15) / 16;
+  const int t = threadIdx.x, nt = blockDim.x, lane = t & (WAVE - 1), w = t / WAVE;
+  const int q = t & 3, rs = t >> 2, rstep = nt >> 2, nw = nt / WAVE;
+  const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.partials, (uint32_t)a.n_wg * nblk * 64u);
+  for (int cb = blockIdx.x; cb < nblk; cb += a.n_wg) {
+    const int col = cb * 16 + 4 * q;
+    const bool cok = col < d;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int r0 = rs; r0 < a.n_wg; r0 += 4 * rstep) {  // rows in a fixed order
+      float4 v[4];
 #pragma unroll
-    for (int m = 0; m < FUSED_RPT; ++m) {
-      const int row = rsub + m * rstep;
-      const uint32_t off = (m < rpt && row < a.n_wg)
-                               ? ((uint32_t)row * d + (uint32_t)(chunk * 4 + q) * 4u) * 4u
-                               : BUF_OOB;
-      v[m] = m < rpt ? buf_load16_agent(prs, off) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    float4 s = v[0];
+      for (int h = 0; h < 4; ++h) {
+        const int row = r0 + rstep * h;
+        const uint32_t off = (row < a.n_wg && cok)
+                                 ? (((uint32_t)cb * a.n_wg + row) * 16u + 4u * q) * 4u
+                                 : BUF_OOB;
+        v[h] = buf_load16_agent(prs, off);
+      }
 #pragma unroll
-    for (int m = 1; m < FUSED_RPT; ++m) {
-      s.x += v[m].x;
-      s.y += v[m].y;
-      s.z += v[m].z;
-      s.w += v[m].w;
+      for (int h = 0; h < 4; ++h) {
+        acc.x += v[h].x;
+        acc.y += v[h].y;
+        acc.z += v[h].z;
+        acc.w += v[h].w;
+      }
     }
-    red[t] = s;
+#pragma unroll
+    for (int m = 4; m < WAVE; m <<= 1) {
+      acc.x += __shfl_xor(acc.x, m, WAVE);
+      acc.y += __shfl_xor(acc.y, m, WAVE);
+      acc.z += __shfl_xor(acc.z, m, WAVE);
+      acc.w += __shfl_xor(acc.w, m, WAVE);
+    }
+    if (lane < 4) red[w * 4 + lane] = acc;
     __syncthreads();
-    if (t < WAVE) {  // lane = (quarter, column): each quarter sums a quarter of the row groups
-      const int col = t & 15, quarter = t >> 4, pq = col >> 2, comp = col & 3;
-      const float* redf = (const float*)red + 4 * pq + comp;
-      const int r0 = quarter * rstep / 4, r1 = (quarter + 1) * rstep / 4;
-      float acc = 0.f;
-      int r = r0;
-      for (; r + 8 <= r1; r += 8) {  // eight reads in flight, added in row order
-        float f[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) f[i] = redf[16 * (r + i)];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc += f[i];
+    if (t < 4 && cok) {  // waves in order
+      float4 o = red[t];
+      for (int k = 1; k < nw; ++k) {
+        o.x += red[k * 4 + t].x;
+        o.y += red[k * 4 + t].y;
+        o.z += red[k * 4 + t].z;
+        o.w += red[k * 4 + t].w;
       }
-      for (; r < r1; ++r) acc += redf[16 * r];
-      // quarters in order: lane col gets q0 + q1 + q2 + q3
-      const float a1 = __shfl(acc, col + 16, WAVE), a2 = __shfl(acc, col + 32, WAVE),
-                  a3 = __shfl(acc, col + 48, WAVE);
-      if (quarter == 0) {
-        const int pos = chunk * 4 + pq;
-        const int tt = pos / WAVE, vq = tt % (V / 4);
-        const int vec = (tt / (V / 4)) * WAVE + pos % WAVE;
-        store_y1<T>(a.y, vec * V + 4 * vq + comp, ((acc + a1) + a2) + a3);
-      }
+      store_y4<T>(a.y, col, o);
     }
-    __syncthreads();  // red is reused by the next chunk
+    __syncthreads();  // red is reused by the next block
   }
 }
 
@@ -354,17 +357,21 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   }
   // this wave's column slice of the workgroup's partial y (team 0)
   if (team == 0) {
-    if constexpr (FUSED) {  // position order, agent-scope stores (see above)
-      const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.partials, (uint32_t)a.n_wg * a.NV * V * 4u);
+    if constexpr (FUSED) {  // the blocked layout with agent-scope stores
+      const uint32_t nblk = (uint32_t)(a.NV * V + 15) / 16u;
+      const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.partials, (uint32_t)a.n_wg * nblk * 64u);
 #pragma unroll
-      for (int c = 0; c < CPL; ++c)
+      for (int c = 0; c < CPL; ++c) {
+        const uint32_t col0 = (uint32_t)(v0 + lane + WAVE * c) * V;
 #pragma unroll
-        for (int q = 0; q < V / 4; ++q) {
-          const uint32_t pos = (uint32_t)(((p * CPL + c) * (V / 4) + q) * WAVE + lane);
-          const uint32_t off = vok[c] ? ((uint32_t)b * a.NV * V + pos * 4u) * 4u : BUF_OOB;
-          buf_store16_agent(prs, off, make_float4(yacc[c][4 * q], yacc[c][4 * q + 1],
-                                                  yacc[c][4 * q + 2], yacc[c][4 * q + 3]));
+        for (int e = 0; e < V; e += 4) {
+          const uint32_t col = col0 + e;
+          const uint32_t off =
+              vok[c] ? (((col >> 4) * (uint32_t)a.n_wg + b) * 16u + (col & 15u)) * 4u : BUF_OOB;
+          buf_store16_agent(prs, off, make_float4(yacc[c][e], yacc[c][e + 1], yacc[c][e + 2],
+                                                  yacc[c][e + 3]));
         }
+      }
     } else {  // blocks of 16 columns: [d/16][n_wg][16] (see the reduce kernel)
 #pragma unroll
       for (int c = 0; c < CPL; ++c)
@@ -382,17 +389,6 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   if constexpr (FUSED) fused_reduce<T>(a, gen0, (float4*)team_part + (size_t)(teams - 1) * a.NV * V / 4);
 }
 
-template <class T>
-__device__ inline void store_y4(void* y, int col, float4 v) {
-  if constexpr (T::dtype == NP_F32) {
-    *(float4*)((float*)y + col) = v;
-  } else {
-    uint2 o;
-    o.x = T::from_f32(v.x) | (T::from_f32(v.y) << 16);
-    o.y = T::from_f32(v.z) | (T::from_f32(v.w) << 16);
-    *(uint2*)((uint16_t*)y + col) = o;
-  }
-}
 
 // y[col] = sum over workgroups b of partial_b[col], in a fixed order.  The
 // rows kernel stores the partials in blocks of 16 columns, [d/16][n_wg][16]
@@ -724,15 +720,10 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   const size_t lds = (size_t)(teams - 1) * a.NV * V * sizeof(float);
   // the single-kernel reduction adds one float4 per thread of LDS
   const size_t lds_fused = lds + (size_t)teams * a.P * WAVE * sizeof(float4);
-  // single kernel while the reduction layout holds: whole wave slices (every
-  // lane owns a vector), at least a wave of partial rows, at most FUSED_RPT
-  // rows and FUSED_CH chunks per thread (a co-resident grid is checked at
-  // launch)
+  // single kernel on request, with at most 16 waves per workgroup (the
+  // reduction's LDS); a co-resident grid is checked at launch
   const int threads = teams * a.P * WAVE;
-  const int nchunks = s.d_model / 16;
-  const bool want_fused = env_int("NP_MLP_FUSED", 0) == 1 && a.NV % (WAVE * cpl) == 0 &&
-                          n_wg >= WAVE && n_wg <= FUSED_RPT * (threads / 4) &&
-                          nchunks <= FUSED_CH * n_wg && threads / WAVE <= 16;
+  const bool want_fused = env_int("NP_MLP_FUSED", 0) == 1 && threads / WAVE <= 16;
   bool fused = false;
   if (cpl == 1) {
     if (R == 4) launch_rows<T, 1, 4>(a, lds, lds_fused, want_fused, &fused, stream);
