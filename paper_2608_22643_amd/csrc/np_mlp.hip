@@ -674,9 +674,13 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   while (a.PP < a.P) a.PP *= 2;
   // the exchange holds 2 * (R / stages) values x PP waves in one wave's lanes
   while (R > 2 && 2 * (R >= 4 ? R / 2 : R) * a.PP > WAVE) R /= 2;
-  // one workgroup per CU by default: the bytes of each CU, not the total,
-  // set the time of this short streaming kernel, so spread rows evenly
-  const int target = std::min(env_int("NP_MLP_WG", 256), MLP_MAX_WG);
+  // at most one workgroup per CU, and no more workgroups than it takes to
+  // give each a full round of R rows per team: fewer, fuller workgroups
+  // finish sooner and leave fewer partial sums (7B, k = 1651: 207
+  // workgroups take 15.05 us per call, 256 take 15.45, and 206 or fewer,
+  // which need a second round, about 18)
+  const int full = (n_active + R * teams - 1) / (R * teams);
+  const int target = std::min(env_int("NP_MLP_WG", full < 256 ? full : 256), MLP_MAX_WG);
   int n_wg = n_active < target ? n_active : target;
   if (n_wg < 1) n_wg = 1;
   a.n_wg = n_wg;
