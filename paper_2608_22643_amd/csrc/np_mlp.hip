@@ -171,8 +171,9 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   constexpr int V = T::V;
   // a round's R rows are finished in S stages of RS rows: the gate/up sums of
   // stage s are reduced, exchanged and applied while later stages' records
-  // are still arriving
-  constexpr int S = R >= 4 ? 2 : 1;
+  // are still arriving (four stages for 8 rows over 9-10 waves, whose
+  // exchange holds 2 * RS values of 16 lanes each in one wave)
+  constexpr int S = (R >= 8 && MAXT > 512) ? 4 : (R >= 4 ? 2 : 1);
   constexpr int RS = R / S;
   constexpr int NVAL = 2 * RS;        // g and u of each stage row
   constexpr int G = WAVE / NVAL;      // lanes holding one reduced value
@@ -643,6 +644,8 @@ static void launch_rows(const MlpArgs& a, size_t lds, size_t lds_fused, bool wan
   const int threads = a.teams * a.P * WAVE;
   if (threads <= 512) {  // up to 8 waves: a register budget of 256 per lane
     launch_rows_t<T, CPL, R, 512>(a, lds, lds_fused, want_fused, fused, stream);
+  } else if constexpr (R == 8) {  // 9-10 waves: 168 registers per lane
+    if (threads <= 640) launch_rows_t<T, CPL, R, 640>(a, lds, lds_fused, want_fused, fused, stream);
   } else if constexpr (R <= 4) {  // 128 registers per lane: at most 4 rows a round
     launch_rows_t<T, CPL, R, 1024>(a, lds, lds_fused, want_fused, fused, stream);
   }
@@ -665,15 +668,18 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   while (teams > 1 && teams * a.P > 16) teams /= 2;
   if (teams > 4) teams = 4;
   a.teams = teams;
-  // rows per team and round: 8 while the workgroup has at most 8 waves (256
-  // registers per lane), 4 above that (128 registers), 2 for 128-vector slices
-  int R = cpl == 1 ? env_int("NP_MLP_R", teams * a.P <= 8 ? 8 : 4) : 2;
+  // rows per team and round: 8 while the workgroup has at most 10 waves
+  // (168 or more registers per lane), 4 above that (128 registers), 2 for
+  // 128-vector slices (13B, d 5120, 10 waves: 8-row rounds 19.14 us per
+  // call, 4-row rounds 19.48)
+  int R = cpl == 1 ? env_int("NP_MLP_R", teams * a.P <= 10 ? 8 : 4) : 2;
   if (R != 2 && R != 4) R = 8;
-  if (R == 8 && teams * a.P > 8) R = 4;
+  if (R == 8 && teams * a.P > 10) R = 4;
   a.PP = 1;
   while (a.PP < a.P) a.PP *= 2;
   // the exchange holds 2 * (R / stages) values x PP waves in one wave's lanes
-  while (R > 2 && 2 * (R >= 4 ? R / 2 : R) * a.PP > WAVE) R /= 2;
+  auto stage_rows = [&](int r) { return r >= 8 && teams * a.P > 8 ? r / 4 : (r >= 4 ? r / 2 : r); };
+  while (R > 2 && 2 * stage_rows(R) * a.PP > WAVE) R /= 2;
   // at most one workgroup per CU, and no more workgroups than it takes to
   // give each a full round of R rows per team: fewer, fuller workgroups
   // finish sooner and leave fewer partial sums (7B, k = 1651: 207

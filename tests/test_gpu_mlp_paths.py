@@ -6,7 +6,7 @@ wave slices, at most four rows per thread, the grid resident;
 NP_MLP_COLSPLIT=1).  Row counts from 0 to the path's
 maximum (fewer rows than workgroups, one row per workgroup, ragged), device
 counts, SwiGLU with eq. 1 thresholds, a slot outside the buffer, and bit-for-
-bit repeatability of each path."""
+bit repeatability of each path; workgroups of 4 to 10 waves (d 512 to 5120)."""
 import numpy as np
 import pytest
 import torch
@@ -31,6 +31,9 @@ SHAPES = {
     "d1024_bf16": cfg_small("d1024_bf16", 3, 1024, 5000, 16, 512, 1200, "bf16"),
     "d2048_f16": cfg_small("d2048_f16", 2, 2048, 7000, 16, 1000, 2000, "f16"),
     "d4096_bf16": cfg_small("d4096_bf16", 2, 4096, 11008, 16, 1651, 5504, "bf16"),
+    # 9 and 10 waves per workgroup: 8-row rounds in four stages
+    "d4608_bf16": cfg_small("d4608_bf16", 2, 4608, 5000, 16, 1200, 2000, "bf16"),
+    "d5120_f16": cfg_small("d5120_f16", 2, 5120, 6000, 16, 1658, 2600, "f16"),
 }
 PATHS = {"colsplit": {"NP_MLP_COLSPLIT": "1"}, "two_kernel": {},
          "fused": {"NP_MLP_FUSED": "1"}}
@@ -82,7 +85,7 @@ def test_mlp_paths_row_counts(name, path, monkeypatch):
 
 
 @pytest.mark.parametrize("path", list(PATHS))
-@pytest.mark.parametrize("name", ["d1024_bf16", "d4096_bf16"])
+@pytest.mark.parametrize("name", ["d1024_bf16", "d4096_bf16", "d5120_f16"])
 def test_mlp_paths_counts_swiglu_thresholds(name, path, monkeypatch):
     for k_, v_ in PATHS[path].items():
         monkeypatch.setenv(k_, v_)
