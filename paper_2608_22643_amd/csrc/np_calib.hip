@@ -24,9 +24,10 @@ namespace np {
 // accumulator layout: lane l, register r holds output row 4*(l/16) + r
 // (neuron) and column l%16 (token).
 //
-// A workgroup owns 32 neurons (two row tiles) and every token of the launch
-// (up to 128: eight 16-token tiles); wave w takes tiles w and w + 4 over the
-// whole reduction, so no wave needs another's sums.  The neurons' gate and up
+// A workgroup owns 64 neurons (four row tiles) and every token of the launch
+// (up to 128: eight 16-token tiles); wave w takes token tiles w and w + 4 of
+// every row tile over the whole reduction, so no wave needs another's sums,
+// and each token fragment a wave loads serves four row tiles.  The neurons' gate and up
 // rows stream through LDS in chunks of KC elements: the workgroup loads a
 // chunk with whole-line 16-byte loads (16 lanes per 256-byte row piece) into
 // one of two buffers while the waves multiply the other, and each wave reads
@@ -34,6 +35,7 @@ namespace np {
 // The token fragments come straight from memory (the tokens are L2-resident),
 // a chunk ahead in registers.
 constexpr int AB_WAVES = 4;
+constexpr int AB_NB = 64;         // neurons of a workgroup (AB_NB / 16 row tiles)
 constexpr int AB_MAX_TILES = 8;   // token tiles of 16
 constexpr int AB_ROWB = 256;      // bytes of a row piece per chunk
 constexpr int AB_PITCH = AB_ROWB + 16;
@@ -72,11 +74,12 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
   constexpr int V = T::V, ESZ = 16 / V, KS = 4 * V;  // KS: reduction elements per MFMA step
   constexpr int KC = AB_ROWB / ESZ;                  // reduction elements per chunk
   constexpr int SPC = KC / KS;                       // MFMA steps per chunk (4)
-  constexpr int PIECES = 2 * 32 * (AB_ROWB / 16);    // 16-byte pieces of a chunk (g and u)
-  constexpr int PPT = PIECES / (AB_WAVES * WAVE);    // pieces per thread (4)
-  __shared__ __attribute__((aligned(16))) char lds[2][2][32][AB_PITCH];  // buffer, g/u, row
+  constexpr int MT = AB_NB / 16;                      // row tiles
+  constexpr int PIECES = 2 * AB_NB * (AB_ROWB / 16);  // 16-byte pieces of a chunk (g and u)
+  constexpr int PPT = PIECES / (AB_WAVES * WAVE);    // pieces per thread (8)
+  __shared__ __attribute__((aligned(16))) char lds[2][2][AB_NB][AB_PITCH];  // buffer, g/u, row
   const int t = threadIdx.x, lane = t & (WAVE - 1), w = t / WAVE, grp = lane / 16;
-  const int n0 = blockIdx.x * 32;
+  const int n0 = blockIdx.x * AB_NB;
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes), xr = make_rsrc(a.x, a.x_bytes);
   const uint32_t rec = (uint32_t)(3 * a.d * ESZ), dbytes = (uint32_t)(a.d * ESZ);
   const int chunks = (a.d + KC - 1) / KC;
@@ -86,7 +89,7 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
 #pragma unroll
   for (int i = 0; i < PPT; ++i) {
     const int pc = t + AB_WAVES * WAVE * i;
-    const int proj = pc / (PIECES / 2), row = (pc / (AB_ROWB / 16)) % 32, col = pc % (AB_ROWB / 16);
+    const int proj = pc / (PIECES / 2), row = (pc / (AB_ROWB / 16)) % AB_NB, col = pc % (AB_ROWB / 16);
     const int neuron = n0 + row;
     p_off[i] = neuron < a.F ? (uint32_t)neuron * rec + (uint32_t)proj * dbytes : BUF_OOB;
     p_col[i] = col;
@@ -103,7 +106,7 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int pc = t + AB_WAVES * WAVE * i;
-      const int proj = pc / (PIECES / 2), row = (pc / (AB_ROWB / 16)) % 32, col = pc % (AB_ROWB / 16);
+      const int proj = pc / (PIECES / 2), row = (pc / (AB_ROWB / 16)) % AB_NB, col = pc % (AB_ROWB / 16);
       *(uint4*)&lds[buf][proj][row][col * 16] = r[i];
     }
   };
@@ -124,9 +127,9 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
                                                                  : BUF_OOB, 0);
     }
   };
-  f32x4 accg[2][TPW], accu[2][TPW];
+  f32x4 accg[MT][TPW], accu[MT][TPW];
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int m = 0; m < MT; ++m)
 #pragma unroll
     for (int j = 0; j < TPW; ++j)
 #pragma unroll
@@ -147,7 +150,7 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
 #pragma unroll
     for (int s = 0; s < SPC; ++s) {
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
+      for (int m = 0; m < MT; ++m) {
         const int row = 16 * m + (lane & 15);
         const uint4 ag = *(const uint4*)&lds[buf][0][row][s * 64 + grp * 16];
         const uint4 au = *(const uint4*)&lds[buf][1][row][s * 64 + grp * 16];
@@ -174,7 +177,7 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
     if (tok >= a.n) continue;
     float* dst = a.acts + (size_t)tok * a.F;
 #pragma unroll
-    for (int m = 0; m < 2; ++m) {
+    for (int m = 0; m < MT; ++m) {
       const int nb = n0 + 16 * m + 4 * grp;  // neurons nb .. nb + 3
       float o[4];
 #pragma unroll
@@ -194,7 +197,7 @@ template <class T>
 static hipError_t act_batch_t(const np_shape& s, const void* weights, const void* x, int n,
                               float* acts, hipStream_t stream) {
   constexpr int ESZ = 16 / T::V;
-  const int tiles = (s.d_ffn + 31) / 32;
+  const int tiles = (s.d_ffn + AB_NB - 1) / AB_NB;
   for (int i0 = 0; i0 < n; i0 += 16 * AB_MAX_TILES) {
     ActBatchArgs a;
     a.w = weights;
