@@ -27,7 +27,7 @@ constexpr size_t WS_TOKEN = 64;
 constexpr size_t WS_BAR_ARRIVE = 256;  // own cache lines: polled by every workgroup
 constexpr size_t WS_BAR_GEN = 384;
 constexpr size_t WS_CTRL_BYTES = 4096;
-constexpr int MLP_MAX_WG = 1024;  // partial rows the reduce kernel sums (4 per thread)
+constexpr int MLP_MAX_WG = 1024;  // partial rows the workspace holds (workgroups of one call)
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline size_t ws_z_offset() { return WS_CTRL_BYTES; }

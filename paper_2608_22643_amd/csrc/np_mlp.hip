@@ -20,15 +20,16 @@
 //     the workgroup's partial y to the workspace.
 // Reduction of the per-workgroup partials, one of two ways:
 //  * single kernel (opt-in with NP_MLP_FUSED=1, when the whole grid fits on
-//    the device at once; measured no faster than two kernels at 7B shape):
+//    the device at once; measured slower than two kernels at 7B shape):
 //    the rows kernel writes its partial with agent-scope stores (coherent
 //    across the XCDs' L2s without a cache write-back), meets every other
 //    workgroup in a grid barrier (an arrival counter and a generation word in
 //    the workspace; bounded spin, NP_DEVERR_SPIN_LIMIT when it runs out), and
 //    then each workgroup reduces a slice of the columns over all partials
 //    with agent-scope loads, in a fixed order, and rounds y once;
-//  * two kernels: a separate reduce kernel sums the partials of each column
-//    in workgroup order; the kernel boundary makes them visible.
+//  * two kernels (the default): the partials are stored in blocks of 16
+//    columns and a separate reduce kernel sums each column's partials in
+//    workgroup order; the kernel boundary makes them visible.
 // Both orders are fixed, so each path is deterministic.
 #include <stdlib.h>
 
