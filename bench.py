@@ -626,9 +626,47 @@ def dense_prefix_sweep(cfg, host_storage, prefixes, steps: int) -> dict:
     return out
 
 
-def cpu_baseline(cfg, host_storage, seconds: float):
+def capture_outputs(pipe) -> dict:
+    """One token's results on the host: scores, selection, delta lists, slot
+    maps and the sparse-MLP outputs of every layer (after a synchronize)."""
+    cfg = pipe.cfg
+    L, F, k, d = cfg.layers, cfg.d_ffn, cfg.k, cfg.d_model
+    out = {"scores": pipe.scores.cpu().numpy().reshape(L, F).copy(),
+           "ids": pipe.active_ids.cpu().numpy().reshape(L, k).copy(),
+           "lists": pipe.host_lists(), "state": pipe.host_state()}
+    yb = pipe.y.cpu().view(torch_uint8()).numpy()
+    out["y"] = yb.view("float32" if cfg.adtype == "f32" else "uint16").reshape(L, d).copy()
+    return out
+
+
+def torch_uint8():
+    import torch
+
+    return torch.uint8
+
+
+def mlp_tol(adtype: str, ref64):
+    """The sparse-MLP output tolerance of the GPU tests: fp16 2e-2 absolute;
+    fp32 1e-5 relative to max |y|; bf16 max(2e-2, one bf16 ulp of |y|)."""
+    import numpy as np
+
+    if adtype == "f16":
+        return np.full(ref64.shape, 2e-2)
+    if adtype == "f32":
+        return np.full(ref64.shape, 1e-5 * max(float(np.max(np.abs(ref64))), 1e-30))
+    a = np.abs(ref64)
+    ulp = np.where(a > 0, 2.0 ** (np.floor(np.log2(np.maximum(a, 1e-300))) - 7), 2.0 ** -133)
+    return np.maximum(2e-2, ulp)
+
+
+def cpu_baseline(cfg, host_storage, seconds: float, gpu_ref=()):
     """The oracle (plain C, fp64, one thread) on whole tokens of the same
-    workload until `seconds` of CPU work have run (at least one token)."""
+    workload until `seconds` of CPU work have run (at least one token, and
+    every token of gpu_ref).  For the tokens in gpu_ref (the GPU's first
+    tokens from cold start) it runs in lockstep with the GPU as the tests do:
+    its select takes the GPU's scores (fp32 rounding may move ties at the
+    k-th score), and the selection, every delta list, the slot maps and the
+    MLP outputs are compared; the verdict is returned under "parity"."""
     import numpy as np
 
     import oracle
@@ -640,22 +678,62 @@ def cpu_baseline(cfg, host_storage, seconds: float):
     store = host_storage.numpy().view(np.float32 if cfg.wdtype == "f32" else np.uint16)
     store = store.reshape(cfg.layers, cfg.d_ffn, 3 * cfg.d_model)
     st = oracle.State(cfg.layers, cfg.d_ffn, cfg.capacity)
+    L = cfg.layers
+    checks = {"tokens": 0, "scores_max_rel_diff": 0.0, "select_exact": True, "delta_exact": True,
+              "slot_maps_exact": True, "mlp_max_abs_err": 0.0, "mlp_within_tol": True}
     n, t0 = 0, time.perf_counter()
     while True:
         s = oracle.predict(cfg, h[n], A, Bm)
+        ref = gpu_ref[n] if n < len(gpu_ref) else None
+        if ref is not None:
+            gs = ref["scores"]
+            scale = max(float(np.max(np.abs(s))), 1e-30)
+            checks["scores_max_rel_diff"] = max(checks["scores_max_rel_diff"],
+                                                float(np.max(np.abs(gs.astype(np.float64) - s))) / scale)
+            s = gs
         _, ids = oracle.select(s, cfg.k)
-        oracle.delta(n, ids, st, cfg.capacity)
-        for l in range(cfg.layers):
-            oracle.sparse_mlp(cfg, l, h[n], store, ids[l])
+        dl = oracle.delta(n, ids, st, cfg.capacity)
+        ys = [oracle.sparse_mlp(cfg, l, h[n], store, ids[l], want_f64=ref is not None)
+              for l in range(L)]
+        if ref is not None:
+            checks["tokens"] += 1
+            checks["select_exact"] &= bool(np.array_equal(ids, ref["ids"]))
+            gl = ref["lists"]
+            ok = np.array_equal(gl["counts"], dl["counts"]) and np.array_equal(
+                gl["active_slots"], dl["active_slots"])
+            for l in range(L):
+                c = dl["counts"][l]
+                for name, m in (("in_ids", c[0]), ("in_slots", c[0]), ("hit_ids", c[1]),
+                                ("ev_ids", c[2]), ("ev_slots", c[2])):
+                    ok = ok and np.array_equal(gl[name][l][:m], dl[name][l][:m])
+            checks["delta_exact"] &= bool(ok)
+            P, Q, U = ref["state"]
+            checks["slot_maps_exact"] &= bool(np.array_equal(P, st.slot_of) and
+                                              np.array_equal(Q, st.neuron_of) and
+                                              np.array_equal(U, st.last_used))
+            for l in range(L):
+                ref64 = ys[l][1]
+                got = (ref["y"][l].astype(np.float64) if cfg.adtype == "f32"
+                       else oracle.decode(cfg.adtype, ref["y"][l]))
+                err = np.abs(got - ref64)
+                checks["mlp_max_abs_err"] = max(checks["mlp_max_abs_err"], float(np.max(err)))
+                checks["mlp_within_tol"] &= bool(np.all(err <= mlp_tol(cfg.adtype, ref64)))
         n += 1
         el = time.perf_counter() - t0
-        if el >= seconds or n >= 64:
+        if (el >= seconds and n >= len(gpu_ref)) or n >= 64:
             break
-    return {"value": round(n / el, 4), "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n} whole decode tokens (cold start first) of the {cfg.name} workload: "
-                      f"predict, select, delta, sparse MLP of all {cfg.layers} layers; "
-                      f"staging omitted (a byte copy); {el:.1f} s on 1 host thread",
-            "cpu_model": cpu_model(), "host_cpus": os.cpu_count()}
+    out = {"value": round(n / el, 4), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+           "sample": f"{n} whole decode tokens (cold start first) of the {cfg.name} workload: "
+                     f"predict, select, delta, sparse MLP of all {cfg.layers} layers; "
+                     f"staging omitted (a byte copy); {el:.1f} s on 1 host thread",
+           "cpu_model": cpu_model(), "host_cpus": os.cpu_count()}
+    if gpu_ref:
+        checks["scores_max_rel_diff"] = float(f"{checks['scores_max_rel_diff']:.3g}")
+        checks["mlp_max_abs_err"] = float(f"{checks['mlp_max_abs_err']:.3g}")
+        checks["ok"] = bool(checks["select_exact"] and checks["delta_exact"] and
+                            checks["slot_maps_exact"] and checks["mlp_within_tol"])
+        out["parity"] = checks
+    return out
 
 
 def cpu_model() -> str:
@@ -683,6 +761,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--breakdown-steps", type=int, default=10)
     ap.add_argument("--mlp-steps", type=int, default=50)
+    ap.add_argument("--parity-tokens", type=int, default=3,
+                    help="first tokens checked against the oracle in its leg")
     ap.add_argument("--extra-configs", default="13b",
                     help="comma-separated further configurations measured after the main one")
     ap.add_argument("--extra-steps", type=int, default=30)
@@ -736,14 +816,22 @@ def main():
         pipe.capture_graph()
         log("[bench] decode step captured as a HIP graph")
     step = pipe.step_graph if graph else pipe.step
-    # cold start, then warmup
+    # cold start, then warmup; the first tokens' outputs are kept for the
+    # parity check of the oracle leg
+    gpu_ref = []
+    keep = args.parity_tokens if args.cpu_seconds > 0 else 0
     torch.cuda.synchronize()
     c0 = time.perf_counter()
     step(0)
     torch.cuda.synchronize()
     cold_ms = (time.perf_counter() - c0) * 1e3
+    if keep > 0:
+        gpu_ref.append(capture_outputs(pipe))
     for i in range(Wm):
         step(1 + i)
+        if len(gpu_ref) < keep:
+            torch.cuda.synchronize()
+            gpu_ref.append(capture_outputs(pipe))
     torch.cuda.synchronize()
     log("[bench] warmup done")
     if graph:
@@ -861,7 +949,7 @@ def main():
     log(f"[bench] read reference: {read_ref} GB/s")
     cpu = None
     if args.cpu_seconds > 0:
-        cpu = cpu_baseline(cfg, host_storage, args.cpu_seconds)
+        cpu = cpu_baseline(cfg, host_storage, args.cpu_seconds, gpu_ref)
         log(f"[bench] cpu baseline: {cpu}")
     extra = {}
     for name in [n for n in args.extra_configs.split(",") if n]:
@@ -907,6 +995,7 @@ def main():
         "file_tier": file_tier,
         "sweep_7b": sweep7b,
         "cpu_baseline": cpu,
+        "parity": (cpu or {}).get("parity"),
         "dense_mlp": dense,
         "dense_prefix_sweep": sweep,
         "centroid_predictor": centroid,
