@@ -313,6 +313,59 @@ def delta_stats(pipe):
     return c
 
 
+def hbm_config_run(name: str, steps: int) -> tuple[dict, dict]:
+    """A configuration whose storage tier, resident set and predictor all fit
+    in one GPU's HBM at full size (the 70B shape: 111 GB + 39 GB + 4.5 GB):
+    steps launched as the main measurement, the sparse-MLP call against the
+    HBM roofline, and the delta figures.  Returns the figures and a sample of
+    the last token (two layers' scores, selection and MLP outputs) for the
+    oracle leg to check."""
+    import numpy as np
+    import torch
+
+    from paper_2608_22643_amd import workload as W
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get(name)
+    T = 4 + 2 * steps + 4
+    t = time.perf_counter()
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T)
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t
+    log(f"[bench] {name}: every tier in HBM ({torch.cuda.memory_allocated() / 1e9:.1f} GB), "
+        f"generated in {setup_s:.1f} s")
+    for i in range(4):
+        pipe.step(i)
+    wall, _ = timed_steps(pipe, 4, steps, with_mlp_events=False)
+    _, mlp_us = timed_steps(pipe, 4 + steps, steps)
+    torch.cuda.synchronize()
+    counts = delta_stats(pipe)
+    if pipe.device_error():
+        raise RuntimeError(f"{name}: device error word {pipe.device_error():#x}")
+    L, F, k, d = cfg.layers, cfg.d_ffn, cfg.k, cfg.d_model
+    last = 4 + 2 * steps - 1
+    layers = [0, L - 1]
+    scores = pipe.scores.cpu().numpy().reshape(L, F)
+    ids = pipe.active_ids.cpu().numpy().reshape(L, k)
+    yb = pipe.y.cpu().view(torch.uint8).numpy()
+    y = yb.view(np.float32 if cfg.adtype == "f32" else np.uint16).reshape(L, d)
+    sample = {"cfg": cfg, "tokens": T, "token": last, "layers": layers,
+              "scores": scores[layers].copy(), "ids": ids[layers].copy(), "y": y[layers].copy()}
+    bytes_launch = mlp_bytes_per_launch(cfg)
+    achieved = bytes_launch / (mlp_us * 1e-6) / 1e9
+    out = {"workload": f"{cfg.name}-shaped decode, every tier in HBM: {L} downstream layers, "
+                       f"d={d}, F={F}, rank {cfg.rank}, k={k}, C={cfg.capacity}, {cfg.wdtype}",
+           "hbm_GB": round(torch.cuda.memory_allocated() / 1e9, 1),
+           "tok_s": round(steps / wall, 2), "ms_per_step": round(wall * 1e3 / steps, 4),
+           "sparse_mlp": {"avg_launch_us": round(mlp_us, 3), "bytes_per_launch": bytes_launch,
+                          "achieved_GBps": round(achieved, 1),
+                          "frac": round(achieved / HBM_PEAK_GBPS, 4)},
+           "incoming_rows_per_token": int(counts[:, 0].sum())}
+    del pipe
+    torch.cuda.empty_cache()
+    return out, sample
+
+
 def extra_config(name: str, steps: int, graph: bool, overlap: bool) -> dict:
     """The same measurements, shorter, on another configuration (13B shape):
     steps with the storage tier in HBM (launched as the main measurement),
@@ -659,14 +712,18 @@ def mlp_tol(adtype: str, ref64):
     return np.maximum(2e-2, ulp)
 
 
-def cpu_baseline(cfg, host_storage, seconds: float, gpu_ref=()):
+def cpu_baseline(cfg, host_storage, seconds: float, gpu_ref=(), big_samples=()):
     """The oracle (plain C, fp64, one thread) on whole tokens of the same
     workload until `seconds` of CPU work have run (at least one token, and
     every token of gpu_ref).  For the tokens in gpu_ref (the GPU's first
     tokens from cold start) it runs in lockstep with the GPU as the tests do:
     its select takes the GPU's scores (fp32 rounding may move ties at the
     k-th score), and the selection, every delta list, the slot maps and the
-    MLP outputs are compared; the verdict is returned under "parity"."""
+    MLP outputs are compared; the verdict is returned under "parity".  Each
+    of big_samples (a few layers of the last token of a full-size
+    configuration run with every tier in HBM) is checked the same way: the
+    selection on the GPU's scores, and the MLP outputs against the oracle
+    over those layers' regenerated records."""
     import numpy as np
 
     import oracle
@@ -745,11 +802,30 @@ def cpu_baseline(cfg, host_storage, seconds: float, gpu_ref=()):
         el2 = time.perf_counter() - t1
         out["all_cores"] = {"value": round(n / el2, 4), "cores": threads,
                             "note": "the same tokens, the layers' sparse MLPs on a thread pool"}
+    for smp in big_samples:  # sampled layers of the full-size HBM configurations
+        bc = smp["cfg"]
+        hb = W.hidden(bc, smp["tokens"])[smp["token"]]
+        res = {"token": smp["token"], "layers": smp["layers"], "select_exact": True,
+               "mlp_max_abs_err": 0.0, "mlp_within_tol": True}
+        for i, l in enumerate(smp["layers"]):
+            _, ids1 = oracle.select(smp["scores"][i:i + 1], bc.k)
+            res["select_exact"] &= bool(np.array_equal(ids1[0], smp["ids"][i]))
+            rec = W.storage(bc, l, 1)  # the layer's records, regenerated
+            _, ref64 = oracle.sparse_mlp(bc, 0, hb, rec, smp["ids"][i], want_f64=True)
+            got = (smp["y"][i].astype(np.float64) if bc.adtype == "f32"
+                   else oracle.decode(bc.adtype, smp["y"][i]))
+            err = np.abs(got - ref64)
+            res["mlp_max_abs_err"] = max(res["mlp_max_abs_err"], float(np.max(err)))
+            res["mlp_within_tol"] &= bool(np.all(err <= mlp_tol(bc.adtype, ref64)))
+        res["mlp_max_abs_err"] = float(f"{res['mlp_max_abs_err']:.3g}")
+        res["ok"] = bool(res["select_exact"] and res["mlp_within_tol"])
+        checks.setdefault("sampled", {})[bc.name] = res
     if gpu_ref:
         checks["scores_max_rel_diff"] = float(f"{checks['scores_max_rel_diff']:.3g}")
         checks["mlp_max_abs_err"] = float(f"{checks['mlp_max_abs_err']:.3g}")
         checks["ok"] = bool(checks["select_exact"] and checks["delta_exact"] and
-                            checks["slot_maps_exact"] and checks["mlp_within_tol"])
+                            checks["slot_maps_exact"] and checks["mlp_within_tol"] and
+                            all(v["ok"] for v in checks.get("sampled", {}).values()))
         out["parity"] = checks
     return out
 
@@ -781,6 +857,9 @@ def main():
     ap.add_argument("--mlp-steps", type=int, default=50)
     ap.add_argument("--parity-tokens", type=int, default=3,
                     help="first tokens checked against the oracle in its leg")
+    ap.add_argument("--hbm-configs", default="70b",
+                    help="configurations run at full size with every tier in HBM")
+    ap.add_argument("--hbm-steps", type=int, default=20)
     ap.add_argument("--extra-configs", default="13b",
                     help="comma-separated further configurations measured after the main one")
     ap.add_argument("--extra-steps", type=int, default=30)
@@ -965,9 +1044,14 @@ def main():
         del src, dst
     read_ref = round(read_ref_gbps(), 1)
     log(f"[bench] read reference: {read_ref} GB/s")
+    big, big_samples = {}, []
+    for name in [n for n in args.hbm_configs.split(",") if n]:
+        big[name], smp = hbm_config_run(name, args.hbm_steps)
+        big_samples.append(smp)
+        log(f"[bench] {name}: {big[name]}")
     cpu = None
     if args.cpu_seconds > 0:
-        cpu = cpu_baseline(cfg, host_storage, args.cpu_seconds, gpu_ref)
+        cpu = cpu_baseline(cfg, host_storage, args.cpu_seconds, gpu_ref, big_samples)
         log(f"[bench] cpu baseline: {cpu}")
     extra = {}
     for name in [n for n in args.extra_configs.split(",") if n]:
@@ -1018,7 +1102,7 @@ def main():
         "dense_prefix_sweep": sweep,
         "centroid_predictor": centroid,
         "swiglu_7b": swiglu,
-        "other_configs": extra or None,
+        "other_configs": {**big, **extra} or None,
     }
     print(json.dumps(line), flush=True)
 

@@ -1,7 +1,8 @@
 """The parity verdict of bench.py's oracle leg, on the CPU: references built
-by the oracle itself (standing in for the GPU's first tokens) pass, and a
-wrong active id, a wrong delta entry, a wrong slot map or an MLP output
-outside the tolerance each turn the verdict false."""
+by the oracle itself (standing in for the GPU's first tokens, and for the
+sampled layers of a full-size run) pass, and a wrong active id, a wrong delta
+entry, a wrong slot map or an MLP output outside the tolerance each turn the
+verdict false."""
 import copy
 
 import numpy as np
@@ -33,8 +34,30 @@ def tiny():
     return cfg, host, refs
 
 
-def verdict(cfg, host, refs):
-    return bench.cpu_baseline(cfg, host, 0.0, refs)["parity"]
+def verdict(cfg, host, refs, samples=()):
+    return bench.cpu_baseline(cfg, host, 0.0, refs, samples)["parity"]
+
+
+def sample_of(cfg, refs, t=2, layers=(0, 2)):
+    """What the full-size leg keeps: a few layers of one token."""
+    r = refs[t]
+    L = list(layers)
+    return {"cfg": cfg, "tokens": 64, "token": t, "layers": L, "scores": r["scores"][L].copy(),
+            "ids": r["ids"][L].copy(), "y": r["y"][L].copy()}
+
+
+def test_sampled_layers_checked(tiny):
+    cfg, host, refs = tiny
+    good = verdict(cfg, host, refs, [sample_of(cfg, refs)])
+    assert good["ok"] and good["sampled"]["tiny"]["ok"], good
+    bad = sample_of(cfg, refs)
+    bad["y"][1, 3] = np.float32(bad["y"][1, 3] + 1.0)
+    v = verdict(cfg, host, refs, [bad])
+    assert not v["sampled"]["tiny"]["mlp_within_tol"] and not v["ok"], v
+    bad = sample_of(cfg, refs)
+    bad["ids"][0, 1] = (bad["ids"][0, 1] + 1) % cfg.d_ffn
+    v = verdict(cfg, host, refs, [bad])
+    assert not v["sampled"]["tiny"]["select_exact"] and not v["ok"], v
 
 
 def test_parity_passes_on_oracle_references(tiny):
