@@ -326,8 +326,9 @@ np_status np_stage_gather(const np_shape* shape, const np_delta_out* out,
  * NP_DEVERR_SPIN_LIMIT (y then undefined until np_state_reset) if the grid
  * never meets.  NP_MLP_COLSPLIT=1 selects a single kernel without partial
  * sums (16-bit records, d a multiple of 512, at most 4 * d / 8 rows; each
- * workgroup owns 16 columns of y) under the same barrier and conditions.  dev_ws must have been zeroed or passed to np_state_reset
- * before its first use. */
+ * workgroup owns 16 columns of y) under the same barrier and conditions.
+ * dev_ws must have been zeroed or passed to np_state_reset before its first
+ * use. */
 np_status np_sparse_mlp(const np_shape* shape, int32_t layer, const void* x,
                         const void* dev_resident, const int32_t* active_slots,
                         int32_t n_active, void* y, void* dev_ws,
