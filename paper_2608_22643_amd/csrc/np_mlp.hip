@@ -661,9 +661,10 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   a.act = s.act;
   a.thr = thr;
   a.NV = s.d_model / V;
-  // column slice per wave: 64 vectors (CPL = 1) while that needs at most 16
-  // waves, else 128 vectors (CPL = 2)
-  const int cpl = (a.NV + WAVE - 1) / WAVE <= 16 ? 1 : 2;
+  // column slice per wave: 64 vectors (CPL = 1) while that needs at most 10
+  // waves, else 128 vectors (CPL = 2; 70B, d 8192: 8 waves with 4-row rounds
+  // take 33.6 us per call, 16 waves of 64 vectors 35.1)
+  const int cpl = (a.NV + WAVE - 1) / WAVE <= 10 ? 1 : 2;
   a.P = (a.NV + WAVE * cpl - 1) / (WAVE * cpl);
   int teams = env_int("NP_MLP_TEAMS", 1);
   while (teams > 1 && teams * a.P > 16) teams /= 2;
@@ -673,7 +674,7 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   // (168 or more registers per lane), 4 above that (128 registers), 2 for
   // 128-vector slices (13B, d 5120, 10 waves: 8-row rounds 19.14 us per
   // call, 4-row rounds 19.48)
-  int R = cpl == 1 ? env_int("NP_MLP_R", teams * a.P <= 10 ? 8 : 4) : 2;
+  int R = cpl == 1 ? env_int("NP_MLP_R", teams * a.P <= 10 ? 8 : 4) : (teams * a.P <= 8 ? 4 : 2);
   if (R != 2 && R != 4) R = 8;
   if (R == 8 && teams * a.P > 10) R = 4;
   a.PP = 1;
@@ -741,7 +742,8 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
     else if (R == 2) launch_rows<T, 1, 2>(a, lds, lds_fused, want_fused, &fused, stream);
     else launch_rows<T, 1, 8>(a, lds, lds_fused, want_fused, &fused, stream);
   } else {
-    launch_rows<T, 2, 2>(a, lds, lds_fused, want_fused, &fused, stream);
+    if (R == 4) launch_rows<T, 2, 4>(a, lds, lds_fused, want_fused, &fused, stream);
+    else launch_rows<T, 2, 2>(a, lds, lds_fused, want_fused, &fused, stream);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || fused) return e;

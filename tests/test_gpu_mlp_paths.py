@@ -6,7 +6,8 @@ wave slices, at most four rows per thread, the grid resident;
 NP_MLP_COLSPLIT=1).  Row counts from 0 to the path's
 maximum (fewer rows than workgroups, one row per workgroup, ragged), device
 counts, SwiGLU with eq. 1 thresholds, a slot outside the buffer, and bit-for-
-bit repeatability of each path; workgroups of 4 to 10 waves (d 512 to 5120)."""
+bit repeatability of each path; workgroups of 4 to 10 waves of one-vector
+slices (d 512 to 5120) and of 8 waves of two-vector slices (d 8192)."""
 import numpy as np
 import pytest
 import torch
@@ -34,6 +35,8 @@ SHAPES = {
     # 9 and 10 waves per workgroup: 8-row rounds in four stages
     "d4608_bf16": cfg_small("d4608_bf16", 2, 4608, 5000, 16, 1200, 2000, "bf16"),
     "d5120_f16": cfg_small("d5120_f16", 2, 5120, 6000, 16, 1658, 2600, "f16"),
+    # 128-vector slices: 8 waves of two vectors per lane, 4-row rounds
+    "d8192_bf16": cfg_small("d8192_bf16", 2, 8192, 6000, 16, 2867, 3200, "bf16"),
 }
 PATHS = {"colsplit": {"NP_MLP_COLSPLIT": "1"}, "two_kernel": {},
          "fused": {"NP_MLP_FUSED": "1"}}
