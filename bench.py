@@ -520,6 +520,26 @@ def swiglu_run(steps: int, calib_tokens: int = 128, alpha: float = 61.6) -> dict
     pct_us = ev[1].elapsed_time(ev[2]) * 1e3
     if not torch.equal(out, thr):
         raise RuntimeError("calibration: thresholds differ between two identical runs")
+    # eq. 1 as active sets (np_threshold_active) over one token's activations
+    # of every layer, with room for 8192 ids per layer (its own workspace, so
+    # that an overflow would be reported here, not as the pipeline's error)
+    a0 = acts.view(L, calib_tokens, F)[:, 0, :].contiguous()
+    tshape = B.make_shape(L, d, F, cfg.rank, min(F, 8192), F, cfg.wdtype, act="swiglu")
+    tws = torch.zeros(B.np_workspace_size(tshape), dtype=torch.uint8, device="cuda")
+    tmask = torch.empty(L * ((F + 31) // 32), dtype=torch.int32, device="cuda")
+    tids = torch.empty(L * min(F, 8192), dtype=torch.int32, device="cuda")
+    tcnt = torch.empty(L, dtype=torch.int32, device="cuda")
+    B.np_threshold_active(tshape, a0, L, thr, tmask, tids, tcnt, tws, stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(10):
+        B.np_threshold_active(tshape, a0, L, thr, tmask, tids, tcnt, tws, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ta_us = e0.elapsed_time(e1) * 1e3 / 10
+    ta_err = B.np_device_error(tws)
+    ta_kept = float(tcnt.float().mean())
+    del a0, tmask, tids, tcnt, tws
     ab_bytes = F * 2 * d * esz + calib_tokens * d * esz + calib_tokens * F * 4
     ab_flops = 4.0 * F * d * calib_tokens
     ab_gbps = ab_bytes / (ab_us * 1e-6) / 1e9
@@ -556,7 +576,10 @@ def swiglu_run(steps: int, calib_tokens: int = 128, alpha: float = 61.6) -> dict
                                       "mfma_TFLOPs": round(ab_flops / (ab_us * 1e-6) / 1e12, 1),
                                       "mfma_peak_TFLOPs": 2500.0},
                "percentile_us": round(pct_us, 1),
-               "percentile_values": L * calib_tokens * F}}
+               "percentile_values": L * calib_tokens * F,
+               "threshold_active_us": round(ta_us, 2),
+               "threshold_active_mean_ids": round(ta_kept, 1),
+               "threshold_active_error_word": ta_err}}
     del pipe, acts
     torch.cuda.empty_cache()
     return res
