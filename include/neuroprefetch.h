@@ -88,7 +88,8 @@ typedef enum np_status {
   NP_ERR_CAPACITY = 2,    /* k > C, staging buffer smaller than one record, ... */
   NP_ERR_HIP = 3,         /* a HIP runtime call failed; detail in np_last_error() */
   NP_ERR_UNSUPPORTED = 4, /* valid request this library does not implement */
-  NP_ERR_STATE = 5,       /* reserved */
+  NP_ERR_STATE = 5,       /* a staging into this resident buffer failed part-way: calls on it
+                             fail until np_state_reset */
   NP_ERR_IO = 6           /* a storage-tier file read failed (detail in np_last_error()) */
 } np_status;
 
@@ -184,7 +185,13 @@ np_status np_workspace_size(const np_shape* shape, size_t* dev_ws_bytes);
  * previous active set"): sets every entry of slot_of, neuron_of and last_used
  * to -1 with a fill kernel on `stream`, and clears the device error word and
  * the workspace counters.  After it, np_delta on the next token gives every
- * active neuron a slot (slots 0..k-1 in ascending neuron order). */
+ * active neuron a slot (slots 0..k-1 in ascending neuron order).  It also
+ * lifts every NP_ERR_STATE mark of the process: a staging that fails at run
+ * time (NP_ERR_HIP, NP_ERR_IO or NP_ERR_UNSUPPORTED from np_stage_rows,
+ * np_stage_file or np_stage_gather) may have placed only part of a delta whose
+ * slot map np_delta had already written, so that resident buffer is marked and
+ * every later staging or sparse-MLP call on it returns NP_ERR_STATE until the
+ * decode restarts from this cold start.  Argument errors mark nothing. */
 np_status np_state_reset(const np_shape* shape, const np_state* state,
                          void* dev_ws, hipStream_t stream);
 

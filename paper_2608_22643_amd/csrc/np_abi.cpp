@@ -8,9 +8,35 @@
 
 #include <string>
 
+#include <mutex>
+#include <unordered_set>
+
 #include "np_internal.hpp"
 
 namespace np {
+
+namespace {
+std::mutex g_incomplete_mu;
+std::unordered_set<uintptr_t> g_incomplete;  // resident buffers (base pointers)
+}  // namespace
+
+void mark_resident_incomplete(const void* resident) {
+  std::lock_guard<std::mutex> g(g_incomplete_mu);
+  g_incomplete.insert((uintptr_t)resident);
+}
+
+np_status check_resident(const char* fn, const void* resident) {
+  std::lock_guard<std::mutex> g(g_incomplete_mu);
+  if (g_incomplete.count((uintptr_t)resident))
+    return fail(NP_ERR_STATE,
+                "%s: a staging into this resident buffer failed part-way; np_state_reset first", fn);
+  return NP_OK;
+}
+
+void clear_incomplete_residents() {
+  std::lock_guard<std::mutex> g(g_incomplete_mu);
+  g_incomplete.clear();
+}
 
 thread_local std::string g_last_error;
 
@@ -104,7 +130,9 @@ np_status np_state_reset(const np_shape* s, const np_state* state, void* ws, hip
     return fail(NP_ERR_INVALID_ARG, "state arrays must be non-NULL and 16-byte aligned");
   if (!aligned16(ws)) return fail(NP_ERR_INVALID_ARG, "dev_ws must be non-NULL and 16-byte aligned");
   hipError_t e = launch_fill_state(*s, *state, ws, stream);
-  return e == hipSuccess ? NP_OK : hip_fail(e, "np_state_reset launch");
+  if (e != hipSuccess) return hip_fail(e, "np_state_reset launch");
+  clear_incomplete_residents();  // a cold start: no resident row is assumed
+  return NP_OK;
 }
 
 np_status np_predict(const np_shape* s, const void* h, const void* A, const void* B,
@@ -193,6 +221,7 @@ np_status np_stage_gather(const np_shape* s, const np_delta_out* out, int32_t lb
     return fail(NP_ERR_INVALID_ARG, "np_stage_gather: plan lists must be non-NULL and aligned");
   if (!aligned16(storage) || !aligned16(resident) || !aligned16(ws))
     return fail(NP_ERR_INVALID_ARG, "np_stage_gather: pointers must be non-NULL and aligned");
+  if ((st = check_resident("np_stage_gather", resident)) != NP_OK) return st;
   if (lb == le) return NP_OK;
   // a pinned host storage tier is read through its device mapping
   hipPointerAttribute_t attr;
@@ -206,7 +235,9 @@ np_status np_stage_gather(const np_shape* s, const np_delta_out* out, int32_t lb
     storage = attr.devicePointer;
   }
   hipError_t e = launch_stage_gather(*s, *out, lb, le, storage, resident, ws, stream);
-  return e == hipSuccess ? NP_OK : hip_fail(e, "np_stage_gather launch");
+  if (e == hipSuccess) return NP_OK;
+  mark_resident_incomplete(resident);
+  return hip_fail(e, "np_stage_gather launch");
 }
 
 np_status np_sparse_mlp(const np_shape* s, int32_t layer, const void* x, const void* resident,
@@ -221,6 +252,7 @@ np_status np_sparse_mlp(const np_shape* s, int32_t layer, const void* x, const v
   if (!aligned16(x) || !aligned16(resident) || !aligned16(y) || !aligned16(ws) ||
       (n_active > 0 && !slots))
     return fail(NP_ERR_INVALID_ARG, "np_sparse_mlp: pointers must be non-NULL and aligned");
+  if ((st = check_resident("np_sparse_mlp", resident)) != NP_OK) return st;
   hipError_t e = launch_sparse_mlp(*s, layer, x, resident, slots, n_active, y, ws, stream);
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp launch");
 }
@@ -249,6 +281,7 @@ np_status np_sparse_mlp_n(const np_shape* s, int32_t layer, const void* x, const
   if (!aligned16(x) || !aligned16(resident) || !aligned16(y) || !aligned16(ws) || !slots ||
       !counts || ((uintptr_t)slots & 3) || ((uintptr_t)counts & 3))
     return fail(NP_ERR_INVALID_ARG, "np_sparse_mlp_n: pointers must be non-NULL and aligned");
+  if ((st = check_resident("np_sparse_mlp_n", resident)) != NP_OK) return st;
   hipError_t e = launch_sparse_mlp(*s, layer, x, resident, slots, s->k, y, ws, stream, counts);
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp_n launch");
 }
@@ -266,6 +299,7 @@ np_status np_sparse_mlp_t(const np_shape* s, int32_t layer, const void* x, const
       (n_active > 0 && !slots) || ((uintptr_t)slots & 3) || ((uintptr_t)counts & 3) ||
       ((uintptr_t)thr & 3))
     return fail(NP_ERR_INVALID_ARG, "np_sparse_mlp_t: pointers must be non-NULL and aligned");
+  if ((st = check_resident("np_sparse_mlp_t", resident)) != NP_OK) return st;
   hipError_t e = launch_sparse_mlp(*s, layer, x, resident, slots, n_active, y, ws, stream, counts,
                                    thr);
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp_t launch");

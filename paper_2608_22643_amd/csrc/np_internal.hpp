@@ -107,6 +107,13 @@ np_status read_runs(int fd, const std::vector<ReadRun>& runs, int qd, PieceDone 
 
 // host-side helpers shared by the ABI files (np_abi.cpp)
 np_status fail(np_status st, const char* fmt, ...);
+// Resident buffers whose staging failed after np_delta had already moved the
+// slot map: the map names records that never arrived.  Every later staging
+// or MLP call on such a buffer fails with NP_ERR_STATE until np_state_reset,
+// which clears every mark of the process.
+void mark_resident_incomplete(const void* resident);
+np_status check_resident(const char* fn, const void* resident);
+void clear_incomplete_residents();
 np_status hip_fail(hipError_t e, const char* what);
 bool aligned16(const void* p);
 np_status check_shape(const np_shape* s);

@@ -136,6 +136,7 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
   if ((src.fd < 0 && !src.host) || !host_staging || !aligned16(dev_resident) ||
       !aligned16(dev_landing))
     return fail(NP_ERR_INVALID_ARG, "%s: buffers must be non-NULL (device: aligned)", fn);
+  if ((st = check_resident(fn, dev_resident)) != NP_OK) return st;
   const size_t rec = (size_t)3 * s->d_model * dtype_size(s->wdtype);
   // halves on 4 KiB boundaries, so that direct file reads land aligned
   const size_t half = (staging_bytes / 2) & ~(size_t)4095;
@@ -300,6 +301,15 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
   return NP_OK;
 }
 
+// A staging that fails at run time (a HIP call, a file read) may have
+// placed only part of the delta: the resident buffer is marked so that later
+// calls on it report NP_ERR_STATE.  Argument errors enqueue nothing.
+static np_status staged(const void* resident, np_status st) {
+  if (st == NP_ERR_HIP || st == NP_ERR_IO || st == NP_ERR_UNSUPPORTED)
+    mark_resident_incomplete(resident);
+  return st;
+}
+
 }  // namespace np
 
 using namespace np;
@@ -310,10 +320,11 @@ extern "C" np_status np_stage_rows(const np_shape* s, const np_stage_plan* plan,
                                    size_t landing_bytes, hipStream_t side, hipEvent_t wait_before,
                                    hipEvent_t* layer_ready) {
   if (!host_storage) return fail(NP_ERR_INVALID_ARG, "np_stage_rows: host_storage is NULL");
-  return stage_common("np_stage_rows", s, plan, lb, le,
-                      {(const char*)host_storage, -1, 0, nullptr, 0},
-                      dev_resident, host_staging, staging_bytes, dev_landing, landing_bytes, side,
-                      wait_before, layer_ready);
+  return staged(dev_resident,
+                stage_common("np_stage_rows", s, plan, lb, le,
+                             {(const char*)host_storage, -1, 0, nullptr, 0}, dev_resident,
+                             host_staging, staging_bytes, dev_landing, landing_bytes, side,
+                             wait_before, layer_ready));
 }
 
 extern "C" np_status np_stage_file(const np_shape* s, const np_stage_plan* plan, int32_t lb,
@@ -327,8 +338,9 @@ extern "C" np_status np_stage_file(const np_shape* s, const np_stage_plan* plan,
                 (long long)file_offset);
   if (io_buffer && io_buffer_bytes == 0)
     return fail(NP_ERR_INVALID_ARG, "np_stage_file: io_buffer of 0 bytes");
-  return stage_common("np_stage_file", s, plan, lb, le,
-                      {nullptr, fd, file_offset, (char*)io_buffer, io_buffer_bytes},
-                      dev_resident, host_staging, staging_bytes, dev_landing, landing_bytes, side,
-                      wait_before, layer_ready);
+  return staged(dev_resident,
+                stage_common("np_stage_file", s, plan, lb, le,
+                             {nullptr, fd, file_offset, (char*)io_buffer, io_buffer_bytes},
+                             dev_resident, host_staging, staging_bytes, dev_landing,
+                             landing_bytes, side, wait_before, layer_ready));
 }

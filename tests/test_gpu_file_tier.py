@@ -60,7 +60,8 @@ def test_file_tier_7b_records(overlap, tmp_path):
 def test_file_tier_short_file_is_an_io_error(tmp_path):
     """A plan naming records past the end of the file: np_stage_file returns
     NP_ERR_IO at the chunk that reads them; the chunks before it are enqueued
-    and land in their slots."""
+    and land in their slots; the resident buffer is then refused with
+    NP_ERR_STATE until np_state_reset."""
     import os
 
     from paper_2608_22643_amd import binding as B
@@ -101,3 +102,13 @@ def test_file_tier_short_file_is_an_io_error(tmp_path):
     for j in range(n0):
         assert np.array_equal(res[0, j], store[0, 10 + j]), j
     assert not res[1].any()
+    # the failed staging marked the resident buffer: calls on it report
+    # NP_ERR_STATE until np_state_reset
+    y = torch.zeros(cfg.d_model, dtype=torch.float32, device=DEV)
+    sl = to_dev(np.arange(k, dtype=np.int32))
+    with pytest.raises(B.NPError) as e:
+        B.np_sparse_mlp(bufs.shape, 0, to_dev(W.hidden(cfg, 1)[0]), resident, sl, k, y, bufs.ws)
+    assert e.value.status == B.NP_ERR_STATE
+    bufs.reset()
+    B.np_sparse_mlp(bufs.shape, 0, to_dev(W.hidden(cfg, 1)[0]), resident, sl, k, y, bufs.ws)
+    torch.cuda.synchronize()
