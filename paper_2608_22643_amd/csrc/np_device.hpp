@@ -60,6 +60,17 @@ __device__ inline float4 buf_load16_agent(__amdgpu_buffer_rsrc_t r, uint32_t vof
                      __uint_as_float(v.w));
 }
 
+// A 16-byte store with the nontemporal hint: data the next kernel reads once
+// (the MLP's partial sums) need not displace other lines on the way.
+__device__ inline void buf_store16_nt(__amdgpu_buffer_rsrc_t r, uint32_t voff, float4 f) {
+  u32x4_t v;
+  v.x = __float_as_uint(f.x);
+  v.y = __float_as_uint(f.y);
+  v.z = __float_as_uint(f.z);
+  v.w = __float_as_uint(f.w);
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, 0, CPOL_NT);
+}
+
 __device__ inline void buf_store16_agent(__amdgpu_buffer_rsrc_t r, uint32_t voff, float4 f) {
   u32x4_t v;
   v.x = __float_as_uint(f.x);

@@ -374,18 +374,22 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
                                                   yacc[c][e + 3]));
         }
       }
-    } else {  // blocks of 16 columns: [d/16][n_wg][16] (see the reduce kernel)
+    } else {  // blocks of 16 columns: [d/16][n_wg][16] (see the reduce kernel),
+              // nontemporal stores (measured 14.7 against 15.1 us per call)
+      const uint32_t nblk = (uint32_t)(a.NV * V + 15) / 16u;
+      const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.partials, (uint32_t)a.n_wg * nblk * 64u);
 #pragma unroll
-      for (int c = 0; c < CPL; ++c)
-        if (vok[c]) {
-          const int col0 = (v0 + lane + WAVE * c) * V;
+      for (int c = 0; c < CPL; ++c) {
+        const uint32_t col0 = (uint32_t)(v0 + lane + WAVE * c) * V;
 #pragma unroll
-          for (int e = 0; e < V; e += 4) {
-            const int col = col0 + e;
-            float4* d4 = (float4*)(a.partials + ((size_t)(col >> 4) * a.n_wg + b) * 16 + (col & 15));
-            *d4 = make_float4(yacc[c][e], yacc[c][e + 1], yacc[c][e + 2], yacc[c][e + 3]);
-          }
+        for (int e = 0; e < V; e += 4) {
+          const uint32_t col = col0 + e;
+          const uint32_t off =
+              vok[c] ? (((col >> 4) * (uint32_t)a.n_wg + b) * 16u + (col & 15u)) * 4u : BUF_OOB;
+          buf_store16_nt(prs, off, make_float4(yacc[c][e], yacc[c][e + 1], yacc[c][e + 2],
+                                               yacc[c][e + 3]));
         }
+      }
     }
   }
   if constexpr (FUSED) fused_reduce<T>(a, gen0, (float4*)team_part + (size_t)(teams - 1) * a.NV * V / 4);
