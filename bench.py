@@ -42,11 +42,11 @@ HBM_PEAK_GBPS = 8000.0
 MLP_COUNTERS = {
     "config": "7b",
     "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
-    "sha256": "375f1692668081ade2d46e95d43353bacb02e89c06ec9a5352c4c64cfe1455c6"
-              "5a89f137f8ede14f2a3db251acb659578b978d62f554eac21f05a7cf43580852",
-    "fetch_kib": {"rows": 19926.5, "reduce": 1681.5},
-    "write_kib": {"rows": 3312.0, "reduce": 8.0},
-    "copy_fetch_kib": 131088.2, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+    "sha256": "f4a8e8a720e7c88c53a6b84bd40354a2af8d1c149776d9216581edfcaa5f5a05"
+              "299ac6b7372e8888986a5f931b9562140f84d9a02aa00e03289ad3bb3c43fab9",
+    "fetch_kib": {"rows": 19927.0, "reduce": 1678.5},
+    "write_kib": {"rows": 3374.4, "reduce": 8.0},
+    "copy_fetch_kib": 131087.7, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
 }
 
 

@@ -24,6 +24,17 @@ __device__ inline uint4 load_nt(const uint4* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// A 16-byte store with the nontemporal hint (written records go to memory
+// without lingering as dirty lines that later kernels would have to flush).
+__device__ inline void store_nt(uint4* p, uint4 x) {
+  u32x4_t v;
+  v.x = x.x;
+  v.y = x.y;
+  v.z = x.z;
+  v.w = x.w;
+  __builtin_nontemporal_store(v, (u32x4_t*)p);
+}
+
 // Buffer loads: a 128-bit resource (base, size) held in scalar registers plus
 // a 32-bit per-lane byte offset, so no 64-bit address arithmetic per lane.
 // The hardware range-checks the per-lane offset: an offset at or past the
