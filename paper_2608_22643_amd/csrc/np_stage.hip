@@ -5,7 +5,7 @@
 // host-link bound.  One workgroup copies one whole record per iteration with
 // 16-byte vectors, all loads of a record issued before its stores; loads and
 // stores carry the nontemporal hint (with write-back stores the step's first
-// sparse-MLP calls paid for the written lines: 7B step 1757 -> 1863 tokens/s
+// sparse-MLP calls paid for the written lines: 7B step 1755 -> 1861 tokens/s
 // with the hint).
 #include "np_device.hpp"
 
