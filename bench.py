@@ -237,18 +237,25 @@ def h2d_peak_gbps(nbytes: int = 1 << 30) -> float:
 def staging_rates(pipe, t0: int, steps: int) -> dict:
     """np_stage_rows alone (memcpy tier): staged bytes over the time from the
     call (host packing included) to the end of its copies and scatters, next
-    to a 1 GiB pinned hipMemcpyAsync measured in the same run."""
+    to a 1 GiB pinned hipMemcpyAsync measured in the same run; and the host
+    side alone: the time until the call returns, when every record has been
+    packed into pinned staging and every chunk's copy enqueued (a chunk waits
+    for a staging half to drain when one token's records fill more than
+    one)."""
     pipe.stage_log = []
     for i in range(steps):
         pipe.step(t0 + i)
     import torch
 
     torch.cuda.synchronize()
-    nb = sum(b for b, _ in pipe.stage_log)
-    sec = sum(x for _, x in pipe.stage_log)
+    nb = sum(e[0] for e in pipe.stage_log)
+    sec = sum(e[1] for e in pipe.stage_log)
+    call = sum(e[2] for e in pipe.stage_log)
     pipe.stage_log = None
     return {"staging_h2d_GBps": round(nb / sec / 1e9, 2),
             "staged_MB_per_token": round(nb / steps / 1e6, 2),
+            "staging_ms_per_token": round(sec * 1e3 / steps, 3),
+            "host_call_ms_per_token": round(call * 1e3 / steps, 3),
             "h2d_peak_GBps": round(h2d_peak_gbps(), 2)}
 
 

@@ -191,7 +191,8 @@ class DecodePipeline:
             self.ev_delta.record(self.main)
             torch.cuda.synchronize()
         # memcpy staging: when a list, each step appends (bytes staged, seconds
-        # from the call to the end of its copies) and waits for the staging
+        # from the call to the end of its copies, seconds until the call
+        # returned) and waits for the staging
         self.stage_log = None
         self.reset()
 
@@ -302,9 +303,11 @@ class DecodePipeline:
                                 self.landing.numel(), self.side,
                                 self.ev_plan if self.overlap else None, self.layer_ready)
             if self.stage_log is not None:  # staging alone: host packing + copies + scatter
+                t_call = time.perf_counter() - t0  # until the call returned: packing done
                 self.side.synchronize()
                 n_rec = int(self.plan_counts.view(L, 4)[:, 0].sum())
-                self.stage_log.append((n_rec * cfg.record_bytes, time.perf_counter() - t0))
+                self.stage_log.append((n_rec * cfg.record_bytes, time.perf_counter() - t0,
+                                       t_call))
             if self.overlap:
                 ready = self.layer_ready
         if mlp_block_events is not None:
