@@ -191,7 +191,10 @@ np_status np_workspace_size(const np_shape* shape, size_t* dev_ws_bytes);
  * np_stage_file or np_stage_gather) may have placed only part of a delta whose
  * slot map np_delta had already written, so that resident buffer is marked and
  * every later staging or sparse-MLP call on it returns NP_ERR_STATE until the
- * decode restarts from this cold start.  Argument errors mark nothing. */
+ * decode restarts from this cold start.  Argument errors mark nothing.  A
+ * mark is kept by the buffer's base address: a marked buffer that is freed
+ * leaves its mark on the address, so a new buffer allocated there is refused
+ * the same way until np_state_reset. */
 np_status np_state_reset(const np_shape* shape, const np_state* state,
                          void* dev_ws, hipStream_t stream);
 
