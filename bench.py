@@ -42,11 +42,11 @@ HBM_PEAK_GBPS = 8000.0
 MLP_COUNTERS = {
     "config": "7b",
     "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
-    "sha256": "f4a8e8a720e7c88c53a6b84bd40354a2af8d1c149776d9216581edfcaa5f5a05"
+    "sha256": "f35fb90947eabb9517382fc11d2fb20c65d8db572219326e4410c24c079f93cc"
               "299ac6b7372e8888986a5f931b9562140f84d9a02aa00e03289ad3bb3c43fab9",
     "fetch_kib": {"rows": 19927.0, "reduce": 1678.5},
-    "write_kib": {"rows": 3374.4, "reduce": 8.0},
-    "copy_fetch_kib": 131087.7, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+    "write_kib": {"rows": 3374.1, "reduce": 8.0},
+    "copy_fetch_kib": 131087.8, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
 }
 
 

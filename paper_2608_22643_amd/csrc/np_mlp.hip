@@ -686,13 +686,17 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   // the exchange holds 2 * (R / stages) values x PP waves in one wave's lanes
   auto stage_rows = [&](int r) { return r >= 8 && teams * a.P > 8 ? r / 4 : (r >= 4 ? r / 2 : r); };
   while (R > 2 && 2 * stage_rows(R) * a.PP > WAVE) R /= 2;
-  // at most one workgroup per CU, and no more workgroups than it takes to
-  // give each a full round of R rows per team: fewer, fuller workgroups
-  // finish sooner and leave fewer partial sums (7B, k = 1651: 207
-  // workgroups take 15.05 us per call, 256 take 15.45, and 206 or fewer,
-  // which need a second round, about 18)
-  const int full = (n_active + R * teams - 1) / (R * teams);
-  const int target = std::min(env_int("NP_MLP_WG", full < 256 ? full : 256), MLP_MAX_WG);
+  // at most one workgroup per CU (256), as many rounds of R rows per team
+  // as 256 workgroups would need, and the fewest workgroups that still
+  // finish in that many rounds: fewer, fuller workgroups finish sooner and
+  // leave fewer partial sums (7B, k = 1651, one round: 207 workgroups take
+  // 15.05 us per call, 256 take 15.45, and 206 or fewer, which need a second
+  // round, about 18; 70B, k = 2867, three 4-row rounds: 239 workgroups 31.7
+  // us, 256 32.0)
+  const int per = R * teams;
+  const int rounds = (n_active + per * 256 - 1) / (per * 256);
+  const int full = rounds > 0 ? (n_active + per * rounds - 1) / (per * rounds) : 1;
+  const int target = std::min(env_int("NP_MLP_WG", full), MLP_MAX_WG);
   int n_wg = n_active < target ? n_active : target;
   if (n_wg < 1) n_wg = 1;
   a.n_wg = n_wg;
