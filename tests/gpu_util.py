@@ -106,3 +106,26 @@ def score_bound(cfg, A, Bm, h):
     Bd = np.abs(Bd).reshape(L, cfg.d_ffn, cfg.rank)
     mag = np.stack([Bd[l] @ (Ad[l] @ hd) for l in range(L)])
     return (cfg.d_model + cfg.rank + 2) * 2.0 ** -24 * mag
+
+
+def check_native_mask(gpu_ids: np.ndarray, ref_scores: np.ndarray, tol: np.ndarray, k: int) -> int:
+    """The oracle's own scores (O1, independent of the GPU's) through its own
+    top-k (O2) against the GPU's active sets: every id in one set and not
+    the other must be a near-tie, its oracle score within twice the layer's
+    largest score error bound of the oracle's k-th largest score (a GPU
+    score error can move it across the threshold only then).  Returns the
+    number of such ids over all layers."""
+    import oracle as orc
+
+    _, native = orc.select(ref_scores.astype(np.float32), k)
+    n_diff = 0
+    for l in range(gpu_ids.shape[0]):
+        diff = np.setxor1d(gpu_ids[l], native[l])
+        if diff.size == 0:
+            continue
+        s = ref_scores[l].astype(np.float64)
+        kth = np.sort(s)[-k]
+        width = 2.0 * float(np.max(tol[l]))
+        assert np.all(np.abs(s[diff] - kth) <= width), (l, diff, s[diff], kth, width)
+        n_diff += diff.size
+    return n_diff

@@ -5,17 +5,18 @@ pinned host memory staged per token, as those configurations state, and the
 points of the 7B sweep (activity 5 / 30%, persistence 70 / 95%, residency 25 /
 75%) with the tier in HBM.  Each runs four downstream layers of the real
 shape (the layer count only repeats the same work) for four tokens against
-the oracle: every score within the predictor's fp32 bound; masks, ids, delta
-lists and slot maps bit for bit; resident records byte-equal to the storage
-rows on sampled slots; MLP outputs within the tolerance of the type on every
-layer."""
+the oracle: every score within the predictor's fp32 bound; the oracle's own
+scores through its own top-k differing from the GPU's sets only in near-ties;
+masks, ids, delta lists and slot maps bit for bit; resident records
+byte-equal to the storage rows on sampled slots; MLP outputs within the
+tolerance of the type on every layer."""
 import numpy as np
 import pytest
 import torch
 
 import oracle as orc
 from paper_2608_22643_amd import workload as W
-from gpu_util import compare_delta, decode_y, mlp_tolerance, say, score_bound
+from gpu_util import check_native_mask, compare_delta, decode_y, mlp_tolerance, say, score_bound
 
 pytestmark = pytest.mark.gpu
 
@@ -45,6 +46,7 @@ def run_lockstep(cfg, tier, staging, overlap, T=4):
         tol = score_bound(cfg, A, Bm, h[t]) + np.abs(ref_s) * 2.0 ** -23
         assert np.all(np.abs(scores.astype(np.float64) - ref_s) <= tol), t
         mask, ids = orc.select(scores, k)
+        check_native_mask(pipe.active_ids.cpu().numpy().reshape(L, k), ref_s, tol, k)
         assert np.array_equal(pipe.mask.cpu().numpy().view(np.uint32).reshape(L, -1), mask), t
         assert np.array_equal(pipe.active_ids.cpu().numpy().reshape(L, k), ids), t
         ref = orc.delta(t, ids, st, C)

@@ -7,6 +7,8 @@ step counter.
 Per token, against the oracle: every score within the predictor's fp32
 bound; every mask, active-id list, delta list and slot map bit for bit (the
 oracle's select runs on the GPU's scores, so both take the same decisions);
+the oracle's own scores through its own top-k against the GPU's sets, every
+difference a near-tie within the score bound;
 resident records byte-equal to the storage rows on a sample of slots; MLP
 outputs within the fp16 tolerance on every layer of one steady token and on
 sampled layers of the others.
@@ -17,7 +19,7 @@ import torch
 
 import oracle as orc
 from paper_2608_22643_amd import workload as W
-from gpu_util import compare_delta, decode_y, mlp_tolerance, say
+from gpu_util import check_native_mask, compare_delta, decode_y, mlp_tolerance, say
 
 pytestmark = pytest.mark.gpu
 
@@ -57,6 +59,8 @@ def test_fullsize_7b_graph_step():
         tol = bound(h[t]) + np.abs(ref_s) * 2.0 ** -23
         assert np.all(np.abs(scores.astype(np.float64) - ref_s) <= tol), t
         mask, ids = orc.select(scores, k)
+        n_tie = check_native_mask(pipe.active_ids.cpu().numpy().reshape(L, k), ref_s, tol, k)
+        say(f"[fullsize] token {t}: native-mask near-ties {n_tie}")
         assert np.array_equal(pipe.mask.cpu().numpy().view(np.uint32).reshape(L, -1), mask), t
         assert np.array_equal(pipe.active_ids.cpu().numpy().reshape(L, k), ids), t
         ref = orc.delta(t, ids, st, C)
