@@ -36,7 +36,10 @@
  * Conventions shared by every call
  * --------------------------------
  *  - extern "C"; plain pointers and sizes only.  All memory is owned by the
- *    caller; no call allocates or frees device or host memory.  The staging
+ *    caller; no call allocates or frees device or host memory
+ *    (np_sparse_mlp_noalloc's scratch is a device array of the library
+ *    itself, 8 MiB per device, present once the library's code is loaded on
+ *    that device).  The staging
  *    path keeps two HIP events and a small worker-thread pool per process,
  *    created on first use (see np_stage_rows), and the file tier one io_uring
  *    ring of 256 entries per process (see np_stage_file).
@@ -343,6 +346,25 @@ np_status np_sparse_mlp(const np_shape* shape, int32_t layer, const void* x,
                         const void* dev_resident, const int32_t* active_slots,
                         int32_t n_active, void* y, void* dev_ws,
                         hipStream_t stream);
+
+/* np_sparse_mlp for callers that cannot allocate device memory or hand over
+ * a workspace (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same computation, kernels, launch shape and
+ * summation order as np_sparse_mlp, so y is bit-identical to np_sparse_mlp's
+ * for the same inputs.  The per-workgroup partial sums live in the library's
+ * own device array of 8 MiB per device (at most 256 workgroups of d <= 8192
+ * fp32 columns), held from the first call on a device until the process ends;
+ * the call itself allocates nothing.  dev_error: device int32 (4-byte
+ * aligned) into which the kernels OR NP_DEVERR_* bits (the caller clears and
+ * reads it).  d_model > 8192 returns NP_ERR_CAPACITY; the opt-in
+ * single-kernel paths (NP_MLP_FUSED, NP_MLP_COLSPLIT) are never taken.  All
+ * calls on one device share that array: calls that overlap in time on one
+ * device (two streams, two threads) race and give undefined y.  Everything
+ * else as np_sparse_mlp. */
+np_status np_sparse_mlp_noalloc(const np_shape* shape, int32_t layer, const void* x,
+                                const void* dev_resident, const int32_t* active_slots,
+                                int32_t n_active, void* y, int32_t* dev_error,
+                                hipStream_t stream);
 
 /* Centroid-ID prediction and the intersected active sets (Sec. 3.3: each
  * head selects its highest-scoring centroid; Sec. 3.4: the active set of a

@@ -33,7 +33,7 @@ EXPORTS = ("np_status_str", "np_last_error", "np_shape_check", "np_workspace_siz
            "np_stage_gather", "np_sparse_mlp", "np_centroid_select", "np_delta_n",
            "np_sparse_mlp_n", "np_dense_mlp", "np_sparse_mlp_t", "np_act_batch",
            "np_percentile", "np_threshold_active", "np_stage_file", "np_read_records",
-           "np_device_error")
+           "np_device_error", "np_sparse_mlp_noalloc")
 
 
 class NPError(RuntimeError):
@@ -97,6 +97,7 @@ def lib():
         L.np_stage_gather.argtypes = [S, ctypes.POINTER(np_delta_out), i32, i32, vp, vp, vp, vp]
         L.np_sparse_mlp.argtypes = [S, i32, vp, vp, vp, i32, vp, vp, vp]
         L.np_device_error.argtypes = [vp, vp, ctypes.POINTER(i32)]
+        L.np_sparse_mlp_noalloc.argtypes = [S, i32, vp, vp, vp, i32, vp, vp, vp]
         L.np_centroid_select.argtypes = [S, ctypes.POINTER(np_centroid_model), vp, vp, vp, vp,
                                          vp, vp, vp, vp]
         L.np_delta_n.argtypes = [S, i32, vp, vp, ctypes.POINTER(np_state),
@@ -243,6 +244,13 @@ def np_sparse_mlp(shape, layer: int, x, dev_resident, active_slots, n_active: in
     _check(lib().np_sparse_mlp(ctypes.byref(shape), int(layer), _p(x), _p(dev_resident),
                                _p(active_slots), int(n_active), _p(y), _p(ws), _s(stream)),
            "np_sparse_mlp")
+
+
+def np_sparse_mlp_noalloc(shape, layer: int, x, dev_resident, active_slots, n_active: int, y,
+                          dev_error, stream=None) -> None:
+    _check(lib().np_sparse_mlp_noalloc(ctypes.byref(shape), int(layer), _p(x), _p(dev_resident),
+                                       _p(active_slots), int(n_active), _p(y), _p(dev_error),
+                                       _s(stream)), "np_sparse_mlp_noalloc")
 
 
 def np_centroid_select(shape, model: np_centroid_model, feat, logits, centroid_ids, mask,

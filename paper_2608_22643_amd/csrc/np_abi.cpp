@@ -257,6 +257,29 @@ np_status np_sparse_mlp(const np_shape* s, int32_t layer, const void* x, const v
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp launch");
 }
 
+np_status np_sparse_mlp_noalloc(const np_shape* s, int32_t layer, const void* x,
+                                const void* resident, const int32_t* slots, int32_t n_active,
+                                void* y, int32_t* dev_error, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (layer < 0 || layer >= s->layers)
+    return fail(NP_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, s->layers);
+  if (n_active < 0 || n_active > s->capacity)
+    return fail(NP_ERR_INVALID_ARG, "n_active %d outside [0, capacity]", n_active);
+  if (s->d_model > NOALLOC_MAX_D)
+    return fail(NP_ERR_CAPACITY,
+                "np_sparse_mlp_noalloc: d_model %d above the scratch maximum %d (use "
+                "np_sparse_mlp with a workspace)", s->d_model, NOALLOC_MAX_D);
+  if (!aligned16(x) || !aligned16(resident) || !aligned16(y) || (n_active > 0 && !slots) ||
+      !dev_error || ((uintptr_t)dev_error & 3))
+    return fail(NP_ERR_INVALID_ARG,
+                "np_sparse_mlp_noalloc: pointers must be non-NULL and aligned");
+  if ((st = check_resident("np_sparse_mlp_noalloc", resident)) != NP_OK) return st;
+  hipError_t e =
+      launch_sparse_mlp_noalloc(*s, layer, x, resident, slots, n_active, y, dev_error, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp_noalloc launch");
+}
+
 np_status np_dense_mlp(const np_shape* s, const void* weights, const void* x, void* y, void* ws,
                        hipStream_t stream) {
   np_status st = check_shape(s);

@@ -39,6 +39,12 @@ inline size_t ws_total(const np_shape& s) {
   return align256(ws_partials_offset(s) + (size_t)MLP_MAX_WG * ((s.d_model + 15) / 16 * 16) * 4);
 }
 
+// Scratch of the allocation-free sparse MLP: NOALLOC_MAX_WG partial rows of
+// at most NOALLOC_MAX_D fp32 columns (8 MiB per device).
+constexpr int NOALLOC_MAX_WG = 256;
+constexpr int NOALLOC_MAX_D = 8192;
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)NOALLOC_MAX_WG * NOALLOC_MAX_D * 4;
+
 inline int dtype_size(int dt) { return dt == NP_F32 ? 4 : 2; }
 // elements per 16-byte vector
 inline int vec_elems(int dt) { return 16 / dtype_size(dt); }
@@ -75,6 +81,12 @@ hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const 
                              const int32_t* active_slots, int n_active, void* y, void* ws,
                              hipStream_t stream, const int32_t* n_dev = nullptr,
                              const float* thr = nullptr);
+// np_sparse_mlp with its partial sums in the library's own device array
+// (no workspace); device errors are OR-ed into *dev_error.
+hipError_t launch_sparse_mlp_noalloc(const np_shape& s, int layer, const void* x,
+                                     const void* resident, const int32_t* active_slots,
+                                     int n_active, void* y, int32_t* dev_error,
+                                     hipStream_t stream);
 // activations of one layer over n tokens (matrix cores), acts [n][F] fp32
 hipError_t launch_act_batch(const np_shape& s, const void* weights, const void* x, int n,
                             float* acts, hipStream_t stream);

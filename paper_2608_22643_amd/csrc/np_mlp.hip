@@ -656,10 +656,23 @@ static void launch_rows(const MlpArgs& a, size_t lds, size_t lds_fused, bool wan
   }
 }
 
+// Where one call keeps its scratch.  The workspace path: partials in dev_ws
+// after the control block, opt-in single-kernel paths allowed.  The
+// allocation-free path: partials in the library's own device array, at most
+// max_wg workgroups, the error word the caller's, no opt-in path (they keep
+// barrier words in the control block).
+struct MlpScratch {
+  float* partials;
+  void* err;   // error word (raise_error target; WS_ERR is 0)
+  int max_wg;
+  bool opt_in;
+};
+
 template <class T>
 static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void* resident,
                         const int32_t* active_slots, int n_active, void* y, void* ws,
-                        hipStream_t stream, const int32_t* n_dev, const float* thr) {
+                        hipStream_t stream, const int32_t* n_dev, const float* thr,
+                        const MlpScratch* sc = nullptr) {
   constexpr int V = T::V;
   MlpArgs a;
   a.act = s.act;
@@ -696,7 +709,7 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   const int per = R * teams;
   const int rounds = (n_active + per * 256 - 1) / (per * 256);
   const int full = rounds > 0 ? (n_active + per * rounds - 1) / (per * rounds) : 1;
-  const int target = std::min(env_int("NP_MLP_WG", full), MLP_MAX_WG);
+  const int target = std::min(env_int("NP_MLP_WG", full), sc ? sc->max_wg : MLP_MAX_WG);
   int n_wg = n_active < target ? n_active : target;
   if (n_wg < 1) n_wg = 1;
   a.n_wg = n_wg;
@@ -707,8 +720,8 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   a.layer_bytes = (uint32_t)((size_t)s.capacity * rec_vecs * 16);
   a.slots = active_slots;
   a.x = (const uint4*)x;
-  a.partials = (float*)((char*)ws + ws_partials_offset(s));
-  a.ws = ws;
+  a.partials = sc ? sc->partials : (float*)((char*)ws + ws_partials_offset(s));
+  a.ws = sc ? sc->err : ws;
   a.y = y;
   a.n_dev = n_dev;
   a.layer = layer;
@@ -716,7 +729,7 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   // 17.3 against 16.1 us per call at the 7B shape: its 32-byte down^T pieces
   // touch 64 lines per load instruction and cost 4.5 us, the barrier 0.3 us)
   if constexpr (V == 8) {
-    const bool on = env_int("NP_MLP_COLSPLIT", 0) == 1;
+    const bool on = (!sc || sc->opt_in) && env_int("NP_MLP_COLSPLIT", 0) == 1;
     const int P = a.NV / WAVE, bands = s.d_model / CS_BAND, threads = P * WAVE;
     if (on && active_slots && a.NV % WAVE == 0 && P <= 16 && bands % 8 == 0 &&
         n_active <= CS_RPT * threads && bands <= MLP_MAX_WG) {
@@ -743,7 +756,8 @@ static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void*
   // single kernel on request, with at most 16 waves per workgroup (the
   // reduction's LDS); a co-resident grid is checked at launch
   const int threads = teams * a.P * WAVE;
-  const bool want_fused = env_int("NP_MLP_FUSED", 0) == 1 && threads / WAVE <= 16;
+  const bool want_fused =
+      (!sc || sc->opt_in) && env_int("NP_MLP_FUSED", 0) == 1 && threads / WAVE <= 16;
   bool fused = false;
   if (cpl == 1) {
     if (R == 4) launch_rows<T, 1, 4>(a, lds, lds_fused, want_fused, &fused, stream);
@@ -782,6 +796,57 @@ hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const 
     default:
       return mlp_t<TBF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev,
                           thr);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free sparse MLP (np_sparse_mlp_noalloc): the partial sums live in
+// `scratch`, a file-scope device array of NOALLOC_SCRATCH_BYTES (room for
+// NOALLOC_MAX_WG partial rows of NOALLOC_MAX_D fp32 columns), one copy per
+// device, held until the process ends.  Host code never passes the array's
+// name to a kernel: its device address is looked up once per device with
+// hipGetSymbolAddress (with that device current) and kept in scratch_addr.
+// Every call on a device shares that device's array; each call writes every
+// partial row it reads before reading it, so nothing needs clearing, and two
+// calls that overlap on one device race.
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+static hipError_t scratch_addr(void** out) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_sparse_mlp_noalloc(const np_shape& s, int layer, const void* x,
+                                     const void* resident, const int32_t* active_slots,
+                                     int n_active, void* y, int32_t* dev_error,
+                                     hipStream_t stream) {
+  void* base = nullptr;
+  hipError_t e = scratch_addr(&base);
+  if (e != hipSuccess) return e;
+  const MlpScratch sc{(float*)base, dev_error, NOALLOC_MAX_WG, false};
+  switch (s.wdtype) {
+    case NP_F32:
+      return mlp_t<TF32>(s, layer, x, resident, active_slots, n_active, y, nullptr, stream,
+                         nullptr, nullptr, &sc);
+    case NP_F16:
+      return mlp_t<TF16>(s, layer, x, resident, active_slots, n_active, y, nullptr, stream,
+                         nullptr, nullptr, &sc);
+    default:
+      return mlp_t<TBF16>(s, layer, x, resident, active_slots, n_active, y, nullptr, stream,
+                          nullptr, nullptr, &sc);
   }
 }
 

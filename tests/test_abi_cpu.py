@@ -28,7 +28,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 22, names
+    assert len(names) == 23, names
     for n in names:
         assert hasattr(lib, n), f"missing export {n}"
     assert set(names) == set(B.EXPORTS)
@@ -175,3 +175,17 @@ def test_threshold_calls_validate_before_enqueueing(lib):
     with pytest.raises(B.NPError) as e:
         B.np_act_batch(big, 16, 16, 1, 16)
     assert e.value.status == B.NP_ERR_UNSUPPORTED
+
+
+def test_noalloc_rejects_rows_wider_than_its_scratch(lib):
+    """The allocation-free MLP keeps partial rows of at most 8192 columns: a
+    wider shape is refused before anything is enqueued."""
+    s = B.make_shape(1, 16384, 2000, 16, 100, 200, "f16")
+    with pytest.raises(B.NPError) as e:
+        B.np_sparse_mlp_noalloc(s, 0, 256, 256, 256, 1, 256, 256)
+    assert e.value.status == B.NP_ERR_CAPACITY
+    assert "8192" in str(e.value)
+    ok = B.make_shape(1, 8192, 2000, 16, 100, 200, "bf16")
+    with pytest.raises(B.NPError) as e:  # passes the size check, fails on the error word
+        B.np_sparse_mlp_noalloc(ok, 0, 256, 256, 256, 1, 256, None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
