@@ -197,7 +197,9 @@ int orc_predict(int L, int d, int F, int r, int wdtype, int adtype,
 /* Sec. 3.4: every active set has the same size.  The active set is the k
  * neurons with the largest score; a tie at the k-th score goes to the
  * smaller id; -0 and +0 are equal; a NaN score is an error. */
-static const float* g_sort_scores;
+/* The comparator's scores: qsort passes no context, so the array is handed
+ * over in a thread-local pointer (calls from several threads stay apart). */
+static _Thread_local const float* g_sort_scores;
 
 static int by_score_desc_id_asc(const void* pa, const void* pb) {
   int32_t a = *(const int32_t*)pa, b = *(const int32_t*)pb;
@@ -251,7 +253,7 @@ int orc_select(int L, int F, int k, const float* scores, uint32_t* mask,
  * Outputs are [L][k] lists (first counts entries defined) and counts [L][4].
  * Returns 0, or 2 if a precondition fails (A not strictly ascending or out
  * of range, P and Q not mutual inverses, k > C). */
-static const int32_t* g_sort_lastused;
+static _Thread_local const int32_t* g_sort_lastused;  /* as g_sort_scores */
 
 static int by_lastused_then_id(const void* pa, const void* pb) {
   int32_t a = *(const int32_t*)pa, b = *(const int32_t*)pb;

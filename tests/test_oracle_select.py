@@ -63,3 +63,40 @@ def test_select_nan_is_error(orc):
     s = np.array([[1.0, np.nan, 0.5]], dtype=np.float32)
     with pytest.raises(orc.OracleError):
         orc.select(s, 1)
+
+
+def test_select_and_delta_from_several_threads(orc):
+    """O2 and O3 sort through comparators that read their keys from a
+    pointer set by the call; calls from several host threads at once (as in
+    the tests that run two decode pipelines side by side) must give exactly
+    what one thread gives."""
+    import threading
+
+    rng = np.random.default_rng(3)
+    L, F, k, C = 3, 5000, 700, 1500
+    scores = [rng.standard_normal((L, F)).astype(np.float32) for _ in range(6)]
+    ref_sel = [orc.select(s, k)[1] for s in scores]
+
+    def delta_run(ids):
+        st = orc.State(L, F, C)
+        return [orc.delta(t, ids[t], st, C)["in_slots"] for t in range(len(ids))]
+
+    seqs = [[np.sort(rng.choice(F, k, replace=False)).reshape(1, k).repeat(L, 0).astype(np.int32)
+             for _ in range(4)] for _ in range(6)]
+    ref_delta = [delta_run(s) for s in seqs]
+    bad = []
+
+    def work(i):
+        for _ in range(10):
+            if not np.array_equal(orc.select(scores[i], k)[1], ref_sel[i]):
+                bad.append(("select", i))
+            got = delta_run(seqs[i])
+            if not all(np.array_equal(a, b) for a, b in zip(got, ref_delta[i])):
+                bad.append(("delta", i))
+
+    th = [threading.Thread(target=work, args=(i,)) for i in range(6)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    assert not bad, bad[:5]
