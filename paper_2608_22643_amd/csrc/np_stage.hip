@@ -83,14 +83,16 @@ __global__ __launch_bounds__(STAGE_NT) void stage_gather_kernel(
   }
 }
 
-// Scatter: a landing chunk holds n records followed by n int32 destination
-// rows (row = layer * C + slot, checked on the host when the chunk is packed).
-__global__ __launch_bounds__(STAGE_NT) void stage_scatter_kernel(const uint4* __restrict__ landing,
-                                                                 int n, int rec_vecs,
-                                                                 uint4* __restrict__ resident) {
-  const int32_t* dst_rows = (const int32_t*)(landing + (size_t)n * rec_vecs);
+// Scatter: n landed records and their int32 destination rows (row = layer *
+// C + slot, checked on the host when the records are packed; a row outside
+// [0, n_rows) is skipped all the same, so no record lands outside the
+// resident buffer).
+__global__ __launch_bounds__(STAGE_NT) void stage_scatter_kernel(
+    const uint4* __restrict__ landing, const int32_t* __restrict__ dst_rows, int n, int rec_vecs,
+    uint4* __restrict__ resident, int n_rows) {
   for (int r = blockIdx.x; r < n; r += gridDim.x) {
     const int row = dst_rows[r];
+    if (row < 0 || row >= n_rows) continue;
     copy_record(resident + (size_t)row * rec_vecs, landing + (size_t)r * rec_vecs, rec_vecs);
   }
 }
@@ -108,13 +110,14 @@ hipError_t launch_stage_gather(const np_shape& s, const np_delta_out& out, int l
   return hipGetLastError();
 }
 
-hipError_t launch_stage_scatter(const np_shape& s, const void* landing, int n_records,
-                                void* resident, hipStream_t stream) {
+hipError_t launch_stage_scatter(const np_shape& s, const void* landing, const int32_t* rows,
+                                int n_records, void* resident, hipStream_t stream) {
   const int rec_vecs = 3 * s.d_model * dtype_size(s.wdtype) / 16;
-  int grid = n_records < 1024 ? n_records : 1024;
+  int grid = n_records < 2048 ? n_records : 2048;
   if (grid < 1) return hipSuccess;
   hipLaunchKernelGGL(stage_scatter_kernel, dim3(grid), dim3(STAGE_NT), 0, stream,
-                     (const uint4*)landing, n_records, rec_vecs, (uint4*)resident);
+                     (const uint4*)landing, rows, n_records, rec_vecs, (uint4*)resident,
+                     s.layers * s.capacity);
   return hipGetLastError();
 }
 

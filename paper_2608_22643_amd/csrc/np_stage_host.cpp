@@ -1,19 +1,22 @@
 // np_stage_host.cpp -- staging through pinned host memory (Sec. 3.5, I/O
 // path): incoming ids are walked layer by layer in ascending order, adjacent
 // ids are coalesced into one contiguous source range, records are packed
-// into a capacity-bounded pinned staging area, and each chunk goes to the
-// device with one hipMemcpyAsync on the side stream, followed by a kernel
-// that scatters the chunk's records into their slots.  The staging area is
-// used as two halves so that packing one chunk overlaps the copy of the
-// previous one; a delta larger than a chunk runs as several independent
-// submit-and-scatter chunks.  The source is the storage tier in host memory
-// (np_stage_rows: the ranges are copied by a thread pool) or in a file
-// (np_stage_file: the ranges are read through io_uring, np_file.cpp).
+// into a capacity-bounded pinned staging area, and each packed piece goes to
+// the device with one hipMemcpyAsync on the side stream; a kernel then
+// scatters the landed records into their slots.  The staging area is a ring
+// of pieces so that packing one piece overlaps the copy of the previous
+// ones, and every piece of a landing round lands in its own part of the
+// landing area, so the copies run back to back with one scatter per round; a
+// delta larger than the landing area runs as several rounds.  The source is
+// the storage tier in host memory (np_stage_rows: the ranges are copied by a
+// thread pool) or in a file (np_stage_file: the ranges are read through
+// io_uring, np_file.cpp).
 #include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
 #include <atomic>
+#include <map>
 #include <condition_variable>
 #include <mutex>
 #include <thread>
@@ -23,7 +26,9 @@
 
 namespace np {
 
-// Persistent worker pool for the host pack (memcpy of coalesced runs).
+// Persistent worker pool for the host pack (memcpy of coalesced runs).  One
+// pool per process; concurrent callers take turns (run() holds a lock), so
+// two pipelines staging at once share the packing threads.
 class PackPool {
  public:
   struct Task {
@@ -41,6 +46,7 @@ class PackPool {
       for (const Task& t : tasks) memcpy(t.dst, t.src, t.n);
       return;
     }
+    std::lock_guard<std::mutex> turn(run_mu_);
     {
       std::lock_guard<std::mutex> lk(mu_);
       tasks_ = &tasks;
@@ -78,6 +84,7 @@ class PackPool {
   }
 
   std::vector<std::thread> workers_;
+  std::mutex run_mu_;
   std::mutex mu_;
   std::condition_variable cv_start_, cv_done_;
   const std::vector<Task>* tasks_ = nullptr;
@@ -87,6 +94,9 @@ class PackPool {
 };
 
 // Created on first use and kept for the life of the process (never joined).
+// 8 threads including the caller: on the MI355X host, 8 packing threads
+// (87 GB/s) leave the DMA engine its pinned-memory bandwidth; 16 packed
+// faster alone (105 GB/s) but slowed the overlapped copies.
 static PackPool* pack_pool() {
   static PackPool* pool = [] {
     int n = 8;
@@ -100,15 +110,39 @@ static PackPool* pack_pool() {
   return pool;
 }
 
-struct DeviceStaging {
+// State of one pinned staging buffer (keyed by device and base address):
+// an event per staging piece (its copies have finished reading the piece)
+// and the scatter stream with its events.  Copies
+// run on the caller's side stream back to back; each landing round's
+// scatter runs on the buffer's own scatter stream (default priority) once
+// the round's copies are done (ev_copied), so the copy engine never waits for
+// a kernel between two copies.  ev_scattered marks the last scatter: the side
+// stream waits on it before copies reuse the landing area and at the end of
+// each call, so work the caller puts on `side` later follows the scatters.
+// Calls on different staging buffers share nothing but the packing threads;
+// calls on one buffer are serialised by its lock.
+constexpr int MAX_PIECES = 8;
+struct StageCtx {
   std::mutex mu;
-  hipEvent_t ev[2] = {nullptr, nullptr};
-  bool pending[2] = {false, false};
+  hipEvent_t ev[MAX_PIECES] = {};
+  bool pending[MAX_PIECES] = {};
+  int next_piece = 0;  // the piece ring continues across calls
+  hipStream_t scat = nullptr;
+  hipEvent_t ev_copied = nullptr, ev_scattered = nullptr;
+  bool scattered = false;  // ev_scattered has been recorded
+  // the landing area is a ring: rounds follow one another in it across
+  // calls, and the copies wait for the scatters only when the ring wraps
+  const void* land_ptr = nullptr;
+  size_t land_cap = 0, land_pos = 0;
 };
 
-static DeviceStaging* device_staging(int dev) {
-  static DeviceStaging slots[64];
-  return (dev >= 0 && dev < 64) ? &slots[dev] : nullptr;
+static StageCtx* stage_ctx(int dev, const void* staging) {
+  static std::mutex mu;
+  static std::map<std::pair<int, uintptr_t>, StageCtx*> ctx;
+  std::lock_guard<std::mutex> g(mu);
+  StageCtx*& c = ctx[{dev, (uintptr_t)staging}];
+  if (!c) c = new StageCtx();
+  return c;
 }
 
 // Where the records come from: host memory (`host`) or a file (`fd` >= 0,
@@ -122,6 +156,18 @@ struct StageSource {
   size_t io_bytes;
 };
 
+// Layout of the areas (rec = record bytes):
+//   landing:  [cap_land records | cap_land int32 destination rows], a ring
+//   staging:  n_pieces pieces, each [piece_cap records | piece_cap int32 rows]
+// A token's records are packed piece by piece (the pieces form a ring: a
+// piece is reused once its copies have finished), and each piece is copied
+// to the next free positions of the landing ring with two hipMemcpyAsync on
+// `side`, its records and their destination rows (layer * C + slot).  At the
+// end of the call, when the ring wraps, or (with layer_ready) at a layer
+// boundary once a group of layers holds enough bytes, the round of landed
+// records is scattered into the slots by one kernel on the scatter stream.
+// Pieces start small and double (2 MiB, 4, 8, ...) so the first copy starts
+// after little packing; packing piece i + 1 overlaps the copy of piece i.
 static np_status stage_common(const char* fn, const np_shape* s, const np_stage_plan* plan,
                               int32_t lb, int32_t le, const StageSource& src, void* dev_resident,
                               void* host_staging, size_t staging_bytes, void* dev_landing,
@@ -134,25 +180,29 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
   if (!plan || !plan->counts || !plan->in_ids || !plan->in_slots)
     return fail(NP_ERR_INVALID_ARG, "%s: plan arrays must be non-NULL", fn);
   if ((src.fd < 0 && !src.host) || !host_staging || !aligned16(dev_resident) ||
-      !aligned16(dev_landing))
-    return fail(NP_ERR_INVALID_ARG, "%s: buffers must be non-NULL (device: aligned)", fn);
+      !aligned16(dev_landing) || !aligned16(host_staging))
+    return fail(NP_ERR_INVALID_ARG, "%s: buffers must be non-NULL and 16-byte aligned", fn);
   if ((st = check_resident(fn, dev_resident)) != NP_OK) return st;
   const size_t rec = (size_t)3 * s->d_model * dtype_size(s->wdtype);
-  // halves on 4 KiB boundaries, so that direct file reads land aligned
-  const size_t half = (staging_bytes / 2) & ~(size_t)4095;
+  const size_t cap_land = landing_bytes / (rec + sizeof(int32_t));
+  // pieces on 4 KiB boundaries, so that direct file reads land aligned
+  int n_pieces = 4;
+  while (n_pieces > 1 && ((staging_bytes / n_pieces) & ~(size_t)4095) < rec + sizeof(int32_t))
+    --n_pieces;
+  const size_t piece_bytes = (staging_bytes / n_pieces) & ~(size_t)4095;
+  size_t piece_cap = piece_bytes / (rec + sizeof(int32_t));
+  if (src.fd >= 0 && src.io_buf) piece_cap = std::min(piece_cap, src.io_bytes / rec);
+  if (cap_land < 1 || piece_cap < 1)
+    return fail(NP_ERR_CAPACITY,
+                "%s: the landing area (%zu B) or a staging piece (%zu B of %zu B) holds no "
+                "record of %zu B and its row index", fn, landing_bytes, piece_bytes,
+                staging_bytes, rec);
   const void* read_target = src.io_buf ? (const void*)src.io_buf : host_staging;
   if (src.fd >= 0 && file_is_direct(src.fd) &&
       (rec % IO_ALIGN || src.file_offset % IO_ALIGN || (uintptr_t)read_target % IO_ALIGN))
     return fail(NP_ERR_INVALID_ARG,
                 "%s: an O_DIRECT file needs records (%zu B), the file offset and the read "
                 "buffer aligned to %d bytes", fn, rec, IO_ALIGN);
-  size_t cap_bytes = std::min(half, landing_bytes);
-  if (src.fd >= 0 && src.io_buf) cap_bytes = std::min(cap_bytes, src.io_bytes);
-  const size_t chunk_cap = cap_bytes / (rec + sizeof(int32_t));
-  if (chunk_cap < 1)
-    return fail(NP_ERR_CAPACITY,
-                "staging half (%zu B) or landing area (%zu B) holds no record of %zu B", half,
-                landing_bytes, rec + sizeof(int32_t));
   // validate the whole plan before enqueueing anything
   for (int l = lb; l < le; ++l) {
     const int n = plan->counts[(size_t)l * 4];
@@ -168,97 +218,173 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  DeviceStaging* ds = device_staging(dev);
-  if (!ds) return fail(NP_ERR_UNSUPPORTED, "device index %d", dev);
-  std::lock_guard<std::mutex> guard(ds->mu);
-  for (int i = 0; i < 2; ++i)
-    if (!ds->ev[i]) {
-      e = hipEventCreateWithFlags(&ds->ev[i], hipEventDisableTiming);
+  StageCtx* cx = stage_ctx(dev, host_staging);
+  std::lock_guard<std::mutex> guard(cx->mu);
+  for (int i = 0; i < MAX_PIECES; ++i)
+    if (!cx->ev[i]) {
+      e = hipEventCreateWithFlags(&cx->ev[i], hipEventDisableTiming);
       if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
     }
-  int fail_after = -1;  // test hook: fail after this many chunks
+  for (hipEvent_t* ev : {&cx->ev_copied, &cx->ev_scattered})
+    if (!*ev) {
+      e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+      if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+    }
+  if (!cx->scat) {
+    e = hipStreamCreateWithFlags(&cx->scat, hipStreamNonBlocking);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags (scatter stream)");
+  }
+  int fail_after = -1;  // test hook: fail after this many pieces
   if (const char* v = getenv("NP_TEST_FAIL_STAGE_AFTER")) fail_after = atoi(v);
+  // with layer_ready: a landing round closes at a layer boundary once it
+  // holds this many bytes (NP_STAGE_GROUP_MIB, default 8 MiB)
+  size_t group_bytes = (size_t)8 << 20;
+  if (const char* v = getenv("NP_STAGE_GROUP_MIB"))
+    if (atoi(v) > 0) group_bytes = (size_t)atoi(v) << 20;
 
+  // scatters write the resident buffer: they wait for wait_before; copies
+  // into the landing area wait for the previous call's last scatter
   if (wait_before) {
-    e = hipStreamWaitEvent(side, wait_before, 0);
+    e = hipStreamWaitEvent(cx->scat, wait_before, 0);
     if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
   }
+  if (cx->land_ptr != dev_landing || cx->land_cap != cap_land) {
+    // another landing area (or size): start its ring at 0 after every
+    // scatter that may still read the previous one
+    if (cx->scattered) {
+      e = hipStreamWaitEvent(side, cx->ev_scattered, 0);
+      if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+    }
+    cx->land_ptr = dev_landing;
+    cx->land_cap = cap_land;
+    cx->land_pos = 0;
+  }
 
+  char* const landing = (char*)dev_landing;
+  int32_t* const land_rows = (int32_t*)(landing + cap_land * rec);
   std::vector<PackPool::Task> tasks;
   std::vector<ReadRun> reads;
-  std::vector<int32_t> dst_rows;
-  dst_rows.reserve(chunk_cap);
-  int h = 0, chunks = 0;
+  int32_t* piece_rows = nullptr;  // the open piece's destination rows
+  int h = cx->next_piece % n_pieces, pieces = 0;
   char* stg = nullptr;
-  size_t n_in_chunk = 0;
-  // run being extended: source byte offset in the storage tier and length
-  // in records
+  // the current round occupies ring positions [land_base, land_base + land_n)
+  size_t n_piece = 0, land_n = 0, land_base = cx->land_pos;
+  size_t cur_cap = std::min(piece_cap, std::max<size_t>(1, ((size_t)2 << 20) / rec));
+  // run being extended: source byte offset in the storage tier, length in
+  // records, first record's index in the piece
   uint64_t run_src = 0;
   size_t run_len = 0, run_dst = 0;
-  const size_t piece = (size_t)256 << 10;
+  const size_t chunk = (size_t)256 << 10;
+  int ready_from = lb;  // first layer whose layer_ready event is not recorded yet
 
   auto close_run = [&]() {
     if (!run_len) return;
-    size_t bytes = run_len * rec, off = 0;
+    const size_t bytes = run_len * rec;
     if (src.fd >= 0) {
       char* target = src.io_buf ? src.io_buf : stg;
       reads.push_back({target + run_dst * rec, (uint64_t)src.file_offset + run_src, bytes});
     } else {
-      while (off < bytes) {
-        size_t n = std::min(piece, bytes - off);
-        tasks.push_back({stg + run_dst * rec + off, src.host + run_src + off, n});
-        off += n;
-      }
+      for (size_t off = 0; off < bytes; off += chunk)
+        tasks.push_back({stg + run_dst * rec + off, src.host + run_src + off,
+                         std::min(chunk, bytes - off)});
     }
     run_len = 0;
   };
-  auto begin_chunk = [&]() -> np_status {
-    if (ds->pending[h]) {
-      hipError_t ee = hipEventSynchronize(ds->ev[h]);
+  auto begin_piece = [&]() -> np_status {
+    if (cx->pending[h]) {
+      hipError_t ee = hipEventSynchronize(cx->ev[h]);
       if (ee != hipSuccess) return hip_fail(ee, "hipEventSynchronize (staging reuse)");
-      ds->pending[h] = false;
+      cx->pending[h] = false;
     }
-    stg = (char*)host_staging + (size_t)h * half;
+    stg = (char*)host_staging + (size_t)h * piece_bytes;
+    piece_rows = (int32_t*)(stg + piece_cap * rec);
     tasks.clear();
     reads.clear();
-    dst_rows.clear();
-    n_in_chunk = 0;
+    n_piece = 0;
     return NP_OK;
   };
-  auto flush = [&]() -> np_status {
+  // packs (or reads) the open piece and copies it to the landing area
+  auto flush_piece = [&]() -> np_status {
     close_run();
-    if (n_in_chunk == 0) return NP_OK;
-    if (fail_after >= 0 && chunks >= fail_after)
-      return fail(NP_ERR_HIP, "%s: injected staging failure after %d chunks", fn, chunks);
+    if (n_piece == 0) return NP_OK;
+    if (fail_after >= 0 && pieces >= fail_after)
+      return fail(NP_ERR_HIP, "%s: injected staging failure after %d pieces", fn, pieces);
     if (src.fd >= 0) {
       // each piece read into io_buf goes on to the same offset of the pinned
-      // half as soon as it is complete, overlapping the copies with the
+      // piece as soon as it is complete, overlapping the copies with the
       // reads still in flight
       struct Ctx {
         char* io;
         char* stg;
-      } cx{src.io_buf, stg};
-      PieceDone to_staging = [](void* c, char* dst, size_t n) {
-        Ctx* x = (Ctx*)c;
+      } c{src.io_buf, stg};
+      PieceDone to_staging = [](void* p, char* dst, size_t n) {
+        Ctx* x = (Ctx*)p;
         memcpy(x->stg + (dst - x->io), dst, n);
       };
-      np_status rs = read_runs(src.fd, reads, io_depth(), src.io_buf ? to_staging : nullptr, &cx);
+      np_status rs = read_runs(src.fd, reads, io_depth(), src.io_buf ? to_staging : nullptr, &c);
       if (rs != NP_OK) return rs;
     } else {
       pack_pool()->run(tasks);
     }
-    memcpy(stg + n_in_chunk * rec, dst_rows.data(), n_in_chunk * sizeof(int32_t));
-    const size_t bytes = n_in_chunk * (rec + sizeof(int32_t));
-    hipError_t ee = hipMemcpyAsync(dev_landing, stg, bytes, hipMemcpyHostToDevice, side);
-    if (ee != hipSuccess) return hip_fail(ee, "hipMemcpyAsync (staging chunk)");
-    ee = hipEventRecord(ds->ev[h], side);
+    hipError_t ee = hipMemcpyAsync(landing + (land_base + land_n) * rec, stg, n_piece * rec,
+                                   hipMemcpyHostToDevice, side);
+    if (ee == hipSuccess)
+      ee = hipMemcpyAsync(land_rows + land_base + land_n, piece_rows, n_piece * sizeof(int32_t),
+                          hipMemcpyHostToDevice, side);
+    if (ee != hipSuccess) return hip_fail(ee, "hipMemcpyAsync (staging piece)");
+    ee = hipEventRecord(cx->ev[h], side);
     if (ee != hipSuccess) return hip_fail(ee, "hipEventRecord");
-    ds->pending[h] = true;
-    ee = launch_stage_scatter(*s, dev_landing, (int)n_in_chunk, dev_resident, side);
+    cx->pending[h] = true;
+    ++pieces;
+    h = (h + 1) % n_pieces;
+    cx->next_piece = h;
+    land_n += n_piece;
+    n_piece = 0;
+    cur_cap = std::min(piece_cap, 2 * cur_cap);
+    return NP_OK;
+  };
+  // one scatter of the round's landed records, after their copies
+  auto close_round = [&]() -> np_status {
+    if (land_n == 0) return NP_OK;
+    hipError_t ee = hipEventRecord(cx->ev_copied, side);
+    if (ee == hipSuccess) ee = hipStreamWaitEvent(cx->scat, cx->ev_copied, 0);
+    if (ee != hipSuccess) return hip_fail(ee, "scatter stream ordering");
+    ee = launch_stage_scatter(*s, landing + land_base * rec, land_rows + land_base, (int)land_n,
+                              dev_resident, cx->scat);
     if (ee != hipSuccess) return hip_fail(ee, "scatter launch");
-    ++chunks;
-    h ^= 1;
-    n_in_chunk = 0;
+    ee = hipEventRecord(cx->ev_scattered, cx->scat);
+    if (ee != hipSuccess) return hip_fail(ee, "hipEventRecord");
+    cx->scattered = true;
+    land_base += land_n;
+    land_n = 0;
+    cx->land_pos = land_base;
+    return NP_OK;
+  };
+  // before a piece is packed: wrap the ring when the rest of it cannot hold
+  // one more record; copies into it then wait (on the side stream) for every
+  // scatter that may still read it
+  auto ring_room = [&]() -> np_status {
+    if (land_base + land_n < cap_land) return NP_OK;
+    np_status r = close_round();
+    if (r != NP_OK) return r;
+    hipError_t ee = hipStreamWaitEvent(side, cx->ev_scattered, 0);
+    if (ee != hipSuccess) return hip_fail(ee, "hipStreamWaitEvent (landing ring)");
+    land_base = 0;
+    cx->land_pos = 0;
+    return NP_OK;
+  };
+  // a piece that fails (a HIP call, a read) ends the call; the records of
+  // the pieces already copied are still scattered, so what was enqueued
+  // lands (the caller marks the resident buffer in any case)
+  auto bail = [&](np_status err) -> np_status {
+    (void)close_round();
+    return err;
+  };
+  auto record_ready = [&](int upto) -> np_status {  // layers [ready_from, upto)
+    for (; ready_from < upto; ++ready_from) {
+      hipError_t ee = hipEventRecord(layer_ready[ready_from], cx->scat);
+      if (ee != hipSuccess) return hip_fail(ee, "hipEventRecord (layer_ready)");
+    }
     return NP_OK;
   };
 
@@ -269,7 +395,8 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
     const int32_t* slots = plan->in_slots + (size_t)l * s->k;
     for (int j = 0; j < n; ++j) {
       if (!open) {
-        if ((st = begin_chunk()) != NP_OK) return st;
+        if ((st = ring_room()) != NP_OK) return bail(st);
+        if ((st = begin_piece()) != NP_OK) return st;
         open = true;
       }
       const uint64_t at = ((uint64_t)l * s->d_ffn + ids[j]) * rec;
@@ -279,25 +406,32 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
         close_run();
         run_src = at;
         run_len = 1;
-        run_dst = n_in_chunk;
+        run_dst = n_piece;
       }
-      dst_rows.push_back(l * s->capacity + slots[j]);
-      ++n_in_chunk;
-      if (n_in_chunk == chunk_cap) {
-        if ((st = flush()) != NP_OK) return st;
+      piece_rows[n_piece] = l * s->capacity + slots[j];
+      ++n_piece;
+      if (n_piece == cur_cap || land_base + land_n + n_piece == cap_land) {
+        if ((st = flush_piece()) != NP_OK) return bail(st);
         open = false;
       }
     }
-    if (layer_ready) {
+    if (layer_ready && (l == le - 1 || (land_n + n_piece) * rec >= group_bytes)) {
       if (open) {
-        if ((st = flush()) != NP_OK) return st;
+        if ((st = flush_piece()) != NP_OK) return bail(st);
         open = false;
       }
-      e = hipEventRecord(layer_ready[l], side);
-      if (e != hipSuccess) return hip_fail(e, "hipEventRecord (layer_ready)");
+      if ((st = close_round()) != NP_OK) return st;
+      if ((st = record_ready(l + 1)) != NP_OK) return st;
     }
   }
-  if (open && (st = flush()) != NP_OK) return st;
+  if (open && (st = flush_piece()) != NP_OK) return bail(st);
+  if ((st = close_round()) != NP_OK) return st;
+  if (layer_ready) return record_ready(le);
+  // without layer events, later work on `side` follows the whole staging
+  if (cx->scattered) {
+    e = hipStreamWaitEvent(side, cx->ev_scattered, 0);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+  }
   return NP_OK;
 }
 

@@ -30,13 +30,16 @@ resident, Sec. 3.1) run with np_dense_mlp, enqueued right after the delta and
 before staging starts, so the GPU computes them while the host reads and
 stages the sparse layers' rows.
 
-With overlap=True staging runs in a few layer chunks (layer 0, layers 1-2,
-the rest): the first on the main stream right after np_delta, the others on a
-side stream, each followed by an event, and layer l's MLP waits only for the
-chunk holding layer l: staging later layers overlaps the MLP of earlier ones
-with three staging launches per token, not one per layer.  The side stream waits for np_delta of the same token,
-which itself follows the previous token's MLP on the main stream, so a victim
-slot is never overwritten while the previous token still reads it.
+With overlap=True staging runs in layer groups (layer 0, layers 1-2, then
+four layers at a time) on a side stream, each group followed by events, and
+layer l's MLP waits only for the group holding layer l: staging later layers
+overlaps the MLPs of earlier ones.  Gather staging puts the first group on the
+main stream; host staging (memcpy, file) calls np_stage_rows / np_stage_file
+once per group and enqueues that group's MLPs right after the call, so they
+run while the host packs the next group.  The side stream waits for np_delta
+of the same token, which itself follows the previous token's MLP on the main
+stream, so a victim slot is never overwritten while the previous token still
+reads it.
 
 Graph mode (capture_graph / step_graph): one decode step is captured once as
 a HIP graph and replayed per token.  The step then has no per-token argument:
@@ -67,7 +70,7 @@ def _i32(n, device):
 class DecodePipeline:
     def __init__(self, cfg: W.Config, device: str = "cuda:0", tier: str = "device",
                  staging: str = "gather", overlap: bool = False, tokens: int | None = None,
-                 staging_mib: int = 64, landing_mib: int = 32,
+                 staging_mib: float = 64, landing_mib: float = 128,
                  host_storage: torch.Tensor | None = None, predictor: str = "lowrank",
                  dense_layers: int = 0, thresholds=None, storage_path: str | None = None):
         if predictor not in ("lowrank", "centroid"):
@@ -171,7 +174,10 @@ class DecodePipeline:
         self.ev_delta = torch.cuda.Event()
         self.layer_ready = [torch.cuda.Event() for _ in range(L)] if overlap else None
         # staging chunks of the overlapped gather path: [0,1), [1,3), [3,L)
-        cuts = sorted({0, min(1, L), min(3, L), L})
+        # staging groups of the overlapped paths: layer 0, layers 1-2, then
+        # four layers at a time, so the first MLPs start early and each later
+        # group's MLPs run while the next group is staged
+        cuts = sorted({0, min(1, L), min(3, L), L} | set(range(3, L, 4)))
         self.chunks = list(zip(cuts[:-1], cuts[1:]))
         if staging in ("memcpy", "file"):
             self.plan_counts = torch.empty(L * 4, dtype=torch.int32, pin_memory=True)
@@ -179,17 +185,23 @@ class DecodePipeline:
             self.plan_slots = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
             self.plan = B.np_stage_plan(self.plan_counts.data_ptr(), self.plan_ids.data_ptr(),
                                         self.plan_slots.data_ptr())
-            self.staging_buf = torch.empty(staging_mib << 20, dtype=torch.uint8, pin_memory=True)
+            self.staging_buf = torch.empty(int(staging_mib * (1 << 20)), dtype=torch.uint8,
+                                           pin_memory=True)
             # file reads land in ordinary host memory (a direct read cannot
             # target pinned memory), one staging half at a time
-            self.io_buf = B.HostBuffer((staging_mib << 20) // 2) if staging == "file" else None
-            self.landing = torch.empty(landing_mib << 20, dtype=torch.uint8, device=dev)
+            self.io_buf = (B.HostBuffer(int(staging_mib * (1 << 20)) // 2) if staging == "file"
+                           else None)
+            self.landing = torch.empty(int(landing_mib * (1 << 20)), dtype=torch.uint8, device=dev)
             self.ev_plan = torch.cuda.Event()
             # events handed to the library must exist: record them once
             for e in (self.layer_ready or []):
                 e.record(self.side)
             self.ev_delta.record(self.main)
             torch.cuda.synchronize()
+        # test hooks: callables run with a stream, to enqueue a fixed-length
+        # delay on the side stream just before a token's staging
+        # (delay_side) or on the main stream just before its MLPs (delay_main)
+        self.delay_side = self.delay_main = None
         # memcpy staging: when a list, each step appends (bytes staged, seconds
         # from the call to the end of its copies, seconds until the call
         # returned) and waits for the staging
@@ -200,7 +212,7 @@ class DecodePipeline:
     def reset(self) -> None:
         """Cold start: every slot map entry -1 (the next token loads its
         whole active set)."""
-        B.np_state_reset(self.shape, self.state, self.ws, self.main)
+        B.np_state_reset(self.shape, self.state, self.ws, self.main, self.resident)
         self.main.synchronize()
 
     def x_ptr(self, t: int) -> int:
@@ -267,58 +279,7 @@ class DecodePipeline:
         for l in range(self.dense_layers):
             B.np_dense_mlp(s, self.dense_w.data_ptr() + l * self.dense_layer_bytes, x_ptr,
                            self.y_dense.data_ptr() + l * ybytes, self.ws, main)
-        if self.staging == "gather":
-            if self.overlap:
-                # the first chunk on the main stream (the first MLP follows it
-                # in stream order), the others on the side stream
-                lb0, le0 = self.chunks[0]
-                B.np_stage_gather(s, self.out, lb0, le0, self.storage, self.resident, self.ws, main)
-                self.ev_delta.record(main)
-                self.side.wait_event(self.ev_delta)
-                ready = [None] * L
-                for lb, le in self.chunks[1:]:
-                    B.np_stage_gather(s, self.out, lb, le, self.storage, self.resident,
-                                      self.ws, self.side)
-                    self.layer_ready[lb].record(self.side)
-                    ready[lb] = self.layer_ready[lb]
-            else:
-                B.np_stage_gather(s, self.out, 0, L, self.storage, self.resident, self.ws, main)
-        else:
-            with torch.cuda.stream(main):
-                self.plan_counts.copy_(self.counts, non_blocking=True)
-                self.plan_ids.copy_(self.lists["in_ids"], non_blocking=True)
-                self.plan_slots.copy_(self.lists["in_slots"], non_blocking=True)
-            self.ev_plan.record(main)
-            self.ev_plan.synchronize()  # the host reads the plan
-            t0 = time.perf_counter()
-            if self.staging == "file":
-                B.np_stage_file(s, self.plan, 0, L, self.storage_fd, 0, self.resident,
-                                self.staging_buf, self.staging_buf.numel(), self.io_buf,
-                                self.io_buf.nbytes, self.landing, self.landing.numel(),
-                                self.side, self.ev_plan if self.overlap else None,
-                                self.layer_ready)
-            else:
-                B.np_stage_rows(s, self.plan, 0, L, self.storage, self.resident,
-                                self.staging_buf, self.staging_buf.numel(), self.landing,
-                                self.landing.numel(), self.side,
-                                self.ev_plan if self.overlap else None, self.layer_ready)
-            if self.stage_log is not None:  # staging alone: host packing + copies + scatter
-                t_call = time.perf_counter() - t0  # until the call returned: packing done
-                self.side.synchronize()
-                n_rec = int(self.plan_counts.view(L, 4)[:, 0].sum())
-                self.stage_log.append((n_rec * cfg.record_bytes, time.perf_counter() - t0,
-                                       t_call))
-            if self.overlap:
-                ready = self.layer_ready
-        if mlp_block_events is not None:
-            if ready is not None:  # time the MLP block, not the wait for staging
-                for e in ready:
-                    if e is not None:
-                        main.wait_event(e)
-            mlp_block_events[0].record(main)
-        for l in range(L):
-            if ready is not None and ready[l] is not None:
-                main.wait_event(ready[l])
+        def mlp(l):
             if self.thr is not None:
                 B.np_sparse_mlp_t(s, l, x_ptr, self.resident, slots.data_ptr() + l * k * 4, k,
                                   self.active_counts if centroid else None, self.thr,
@@ -330,6 +291,90 @@ class DecodePipeline:
             else:
                 B.np_sparse_mlp(s, l, x_ptr, self.resident, slots.data_ptr() + l * k * 4, k,
                                 self.y.data_ptr() + l * ybytes, self.ws, main)
+
+        if self.staging == "gather":
+            if self.overlap:
+                # the first chunk on the main stream (the first MLP follows it
+                # in stream order), the others on the side stream
+                lb0, le0 = self.chunks[0]
+                B.np_stage_gather(s, self.out, lb0, le0, self.storage, self.resident, self.ws, main)
+                self.ev_delta.record(main)
+                self.side.wait_event(self.ev_delta)
+                if self.delay_side is not None:
+                    self.delay_side(self.side)
+                ready = [None] * L
+                for lb, le in self.chunks[1:]:
+                    B.np_stage_gather(s, self.out, lb, le, self.storage, self.resident,
+                                      self.ws, self.side)
+                    self.layer_ready[lb].record(self.side)
+                    ready[lb] = self.layer_ready[lb]
+            else:
+                B.np_stage_gather(s, self.out, 0, L, self.storage, self.resident, self.ws, main)
+            if mlp_block_events is not None:
+                for e in (ready or []):  # time the MLP block, not the wait for staging
+                    if e is not None:
+                        main.wait_event(e)
+                mlp_block_events[0].record(main)
+            if self.delay_main is not None:
+                self.delay_main(main)
+            for l in range(L):
+                if ready is not None and ready[l] is not None:
+                    main.wait_event(ready[l])
+                mlp(l)
+            if mlp_block_events is not None:
+                mlp_block_events[1].record(main)
+            return
+        # staging through the host: the plan is read on the host first
+        with torch.cuda.stream(main):
+            self.plan_counts.copy_(self.counts, non_blocking=True)
+            self.plan_ids.copy_(self.lists["in_ids"], non_blocking=True)
+            self.plan_slots.copy_(self.lists["in_slots"], non_blocking=True)
+        self.ev_plan.record(main)
+        self.ev_plan.synchronize()  # the host reads the plan
+        t0 = time.perf_counter()
+        t_call = 0.0
+        # with overlap, staging runs on the side stream one layer group at a
+        # time and each group's MLPs are enqueued right after its staging
+        # call, so they run while the host packs the next groups
+        groups = self.chunks if self.overlap else [(0, L)]
+        if self.delay_side is not None:
+            self.delay_side(self.side)
+        if self.delay_main is not None:
+            self.delay_main(main)
+        for gi, (lb, le) in enumerate(groups):
+            wait = self.ev_plan if (self.overlap and gi == 0) else None
+            tc = time.perf_counter()
+            if self.staging == "file":
+                B.np_stage_file(s, self.plan, lb, le, self.storage_fd, 0, self.resident,
+                                self.staging_buf, self.staging_buf.numel(), self.io_buf,
+                                self.io_buf.nbytes, self.landing, self.landing.numel(),
+                                self.side, wait, self.layer_ready)
+            else:
+                B.np_stage_rows(s, self.plan, lb, le, self.storage, self.resident,
+                                self.staging_buf, self.staging_buf.numel(), self.landing,
+                                self.landing.numel(), self.side, wait, self.layer_ready)
+            t_call += time.perf_counter() - tc
+            if self.stage_log is not None:
+                continue  # staging alone: the MLPs follow the whole staging
+            for l in range(lb, le):
+                if self.overlap:
+                    main.wait_event(self.layer_ready[l])
+                if l == 0 and mlp_block_events is not None:
+                    mlp_block_events[0].record(main)
+                mlp(l)
+        if self.stage_log is not None:  # staging alone: host packing + copies + scatter
+            if self.overlap:  # the scatters run on the library's scatter stream
+                self.layer_ready[L - 1].synchronize()
+            else:
+                self.side.synchronize()
+            n_rec = int(self.plan_counts.view(L, 4)[:, 0].sum())
+            self.stage_log.append((n_rec * cfg.record_bytes, time.perf_counter() - t0, t_call))
+            for l in range(L):
+                if self.overlap:
+                    main.wait_event(self.layer_ready[l])
+                if l == 0 and mlp_block_events is not None:
+                    mlp_block_events[0].record(main)
+                mlp(l)
         if mlp_block_events is not None:
             mlp_block_events[1].record(main)
 
