@@ -39,8 +39,8 @@
  *    caller; no call allocates or frees device or host memory
  *    (np_sparse_mlp_noalloc's scratch is a device array of the library
  *    itself, 8 MiB per device, present once the library's code is loaded on
- *    that device).  The staging
- *    path keeps two HIP events and a small worker-thread pool per process,
+ *    that device).  The staging path keeps a few HIP events per pinned
+ *    staging buffer it is given and one pool of packing threads per process,
  *    created on first use (see np_stage_rows), and the file tier one io_uring
  *    ring of 256 entries per process (see np_stage_file).
  *  - "device" pointers point into memory of the current HIP device.  Device
@@ -180,26 +180,34 @@ const char* np_last_error(void);
 /* Validates a shape (the requirements listed above).  Host only. */
 np_status np_shape_check(const np_shape* shape);
 
-/* Bytes of device workspace ("dev_ws") the calls below need for this shape.
- * One workspace serves all calls of one decode stream.  Host only. */
-np_status np_workspace_size(const np_shape* shape, size_t* dev_ws_bytes);
+/* Bytes of device workspace ("dev_ws") the calls below need for this shape
+ * (one workspace serves all calls of one decode stream), and, in
+ * *pinned_host_bytes (nullable), the pinned host memory one decode stream
+ * uses to stage from a host or file tier: the plan copy (counts, in_ids,
+ * in_slots: L' (4 + 2k) int32, rounded up to 4 KiB) plus the staging area
+ * np_stage_rows is tuned for: four pieces of 16 MiB (at least one record and
+ * its row index each, in 4 KiB pages).  Host only. */
+np_status np_workspace_size(const np_shape* shape, size_t* dev_ws_bytes,
+                            size_t* pinned_host_bytes);
 
 /* Cold start (Sec. 3.1 last paragraph; Sec. 3.4 "the first token has no
  * previous active set"): sets every entry of slot_of, neuron_of and last_used
  * to -1 with a fill kernel on `stream`, and clears the device error word and
  * the workspace counters.  After it, np_delta on the next token gives every
- * active neuron a slot (slots 0..k-1 in ascending neuron order).  It also
- * lifts every NP_ERR_STATE mark of the process: a staging that fails at run
- * time (NP_ERR_HIP, NP_ERR_IO or NP_ERR_UNSUPPORTED from np_stage_rows,
- * np_stage_file or np_stage_gather) may have placed only part of a delta whose
- * slot map np_delta had already written, so that resident buffer is marked and
- * every later staging or sparse-MLP call on it returns NP_ERR_STATE until the
- * decode restarts from this cold start.  Argument errors mark nothing.  A
- * mark is kept by the buffer's base address: a marked buffer that is freed
- * leaves its mark on the address, so a new buffer allocated there is refused
- * the same way until np_state_reset. */
+ * active neuron a slot (slots 0..k-1 in ascending neuron order).
+ * dev_resident (nullable): the resident buffer this state describes; its
+ * NP_ERR_STATE mark is lifted.  A staging that fails at run time
+ * (NP_ERR_HIP, NP_ERR_IO or NP_ERR_UNSUPPORTED from np_stage_rows,
+ * np_stage_file or np_stage_gather) may have placed only part of a delta
+ * whose slot map np_delta had already written, so that resident buffer is
+ * marked and every later staging or sparse-MLP call on it returns
+ * NP_ERR_STATE until the decode restarts from a cold start that names it.
+ * Marks of other resident buffers are left alone.  Argument errors mark
+ * nothing.  A mark is kept by the buffer's base address: a marked buffer
+ * that is freed leaves its mark on the address, so a new buffer allocated
+ * there is refused the same way until a reset names it. */
 np_status np_state_reset(const np_shape* shape, const np_state* state,
-                         void* dev_ws, hipStream_t stream);
+                         const void* dev_resident, void* dev_ws, hipStream_t stream);
 
 /* Activity predictor (Sec. 3.1 step 2, Sec. 3.3 role: one pass after layer 0
  * scores every downstream layer).  Low-rank form per downstream layer l:
@@ -252,18 +260,37 @@ np_status np_delta(const np_shape* shape, int32_t token,
  *   resident[l][in_slots[l][j]] <- storage[l][in_ids[l][j]],  j < counts[l][0].
  * plan: host copy of np_delta's counts/in_ids/in_slots (read synchronously).
  * host_storage: [L'][F][3d] records, pinned host memory (hipHostMalloc).
- * dev_resident: [L'][C][3d] device.  host_staging / staging_bytes: pinned
- * host area, used as two halves (double buffer).  dev_landing /
- * landing_bytes: device area that receives each chunk before the scatter
- * kernel moves its records into their slots.  A chunk holds at most
- * min(staging_bytes/2, landing_bytes) / (3d*sizeof(w) + 4) records.
- * `side`: stream that runs the copies and the scatter kernels.
- * wait_before (nullable): `side` waits on it before the first write into
- * dev_resident (orders the write after the previous token's MLP reads).
- * layer_ready (nullable, [L'] events): event l is recorded on `side` once
- * layer l's rows are in place.  The host blocks only to reuse a staging half
- * whose previous copy has not finished.  Returns NP_ERR_CAPACITY if the
- * staging or landing area is smaller than one chunk of one record. */
+ * dev_resident: [L'][C][3d] device.
+ * dev_landing / landing_bytes (device, 16-byte aligned): holds
+ * cap = landing_bytes / (rec + 4) records (rec = 3d*sizeof(w)) and their
+ * int32 destination rows; a delta of more than cap records is staged in
+ * several landing rounds.
+ * host_staging / staging_bytes (pinned host, 16-byte aligned): a ring of up
+ * to 4 pieces (4 KiB multiples) into which the host packs records (8
+ * threads) and their int32 destination rows (layer * C + slot); each piece
+ * is copied with hipMemcpyAsync on `side` (records, then rows) to the next
+ * free positions of the landing area.  The landing area is a ring too: a
+ * round of landed records (closed at the end of the call, when the ring
+ * wraps, or at layer groups, below) is moved into its slots by one scatter
+ * kernel.  The scatters
+ * run on a stream the library keeps per staging buffer (default priority),
+ * ordered after their round's copies by events, so the copies run back to
+ * back; copies into a wrapped ring wait for the scatters before them.
+ * wait_before (nullable): the scatters of this call wait on it (orders the
+ * writes into dev_resident after the previous token's MLP reads).
+ * layer_ready (nullable, [L'] events): a round also closes at the end of a
+ * layer once it holds 8 MiB (NP_STAGE_GROUP_MIB), and event l is recorded
+ * after the scatter that places layer l's last record; these events are
+ * then the call's completion signal.  Without layer_ready, `side` is made to
+ * wait for the call's last scatter, so later work on `side` follows the whole
+ * staging.  The host blocks only to reuse a staging piece (or the row area)
+ * whose copy has not finished.  State kept between calls (pending copies,
+ * the rings' positions, the scatter stream) is per staging buffer: calls
+ * with different staging buffers are independent; calls with the same one
+ * must come from one thread at a time.  On a failure after some pieces were
+ * copied, those records are still scattered before the call returns the
+ * error.  Returns NP_ERR_CAPACITY if the landing area or a staging piece
+ * holds no record (with its row index). */
 np_status np_stage_rows(const np_shape* shape, const np_stage_plan* plan,
                         int32_t layer_begin, int32_t layer_end,
                         const void* host_storage, void* dev_resident,
@@ -275,12 +302,12 @@ np_status np_stage_rows(const np_shape* shape, const np_stage_plan* plan,
 /* np_stage_rows with the storage tier in a file (Sec. 3.5, I/O path): the
  * file holds the [L'][F][3d] records starting at byte file_offset (the
  * neuron-centric, layer-major layout).  The coalesced record ranges of each
- * chunk are read through Linux io_uring with up to 256 reads in flight
- * (NP_IO_QD lowers it) into io_buffer, copied into the pinned staging half
- * by the worker threads, then sent and scattered as in np_stage_rows.
- * io_buffer: ordinary host memory of io_buffer_bytes (a chunk holds at most
- * io_buffer_bytes of records), owned by the caller; NULL reads straight into
- * host_staging.  Memory pinned through the HIP runtime cannot be the target
+ * staging piece are read through Linux io_uring with up to 256 reads in
+ * flight (NP_IO_QD lowers it) into io_buffer, each finished read copied into
+ * the pinned piece while the others are in flight, then sent and scattered
+ * as in np_stage_rows.  io_buffer: ordinary host memory of io_buffer_bytes
+ * (a piece holds at most io_buffer_bytes of records), owned by the caller;
+ * NULL reads straight into the pinned pieces of host_staging.  Memory pinned through the HIP runtime cannot be the target
  * of a direct (O_DIRECT) read on this platform (the read fails with EFAULT),
  * so a direct-I/O descriptor needs io_buffer.  fd: a readable descriptor
  * owned by the caller; opened with O_DIRECT, the reads bypass the page cache
@@ -365,6 +392,21 @@ np_status np_sparse_mlp_noalloc(const np_shape* shape, int32_t layer, const void
                                 const void* dev_resident, const int32_t* active_slots,
                                 int32_t n_active, void* y, int32_t* dev_error,
                                 hipStream_t stream);
+
+/* np_sparse_mlp in the form of the paper's statement (Sec. 3.4: the slot map
+ * locates each active row): row j is slot slot_of[active_ids[j]] of layer
+ * `layer`.  active_ids: the layer's n_active active neuron ids (np_select's
+ * row for the layer); slot_of: the layer's row of the slot map
+ * (state.slot_of + layer * F), both device int32 with 4-byte alignment.  An
+ * id outside [0, F) or a slot outside [0, C) sets NP_DEVERR_NOT_RESIDENT and
+ * the row is skipped.  The kernels look the slot up themselves (one more
+ * dependent load than np_sparse_mlp, which takes np_delta's active_slots,
+ * the same lookup already applied); for the same rows in the same order both
+ * give the same bits.  Everything else as np_sparse_mlp. */
+np_status np_sparse_mlp_ids(const np_shape* shape, int32_t layer, const void* x,
+                            const void* dev_resident, const int32_t* active_ids,
+                            const int32_t* slot_of, int32_t n_active, void* y, void* dev_ws,
+                            hipStream_t stream);
 
 /* Centroid-ID prediction and the intersected active sets (Sec. 3.3: each
  * head selects its highest-scoring centroid; Sec. 3.4: the active set of a

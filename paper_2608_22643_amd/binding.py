@@ -33,7 +33,7 @@ EXPORTS = ("np_status_str", "np_last_error", "np_shape_check", "np_workspace_siz
            "np_stage_gather", "np_sparse_mlp", "np_centroid_select", "np_delta_n",
            "np_sparse_mlp_n", "np_dense_mlp", "np_sparse_mlp_t", "np_act_batch",
            "np_percentile", "np_threshold_active", "np_stage_file", "np_read_records",
-           "np_device_error", "np_sparse_mlp_noalloc")
+           "np_device_error", "np_sparse_mlp_noalloc", "np_sparse_mlp_ids")
 
 
 class NPError(RuntimeError):
@@ -86,8 +86,8 @@ def lib():
         L.np_last_error.argtypes = []
         L.np_last_error.restype = ctypes.c_char_p
         L.np_shape_check.argtypes = [S]
-        L.np_workspace_size.argtypes = [S, ctypes.POINTER(sz)]
-        L.np_state_reset.argtypes = [S, ctypes.POINTER(np_state), vp, vp]
+        L.np_workspace_size.argtypes = [S, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+        L.np_state_reset.argtypes = [S, ctypes.POINTER(np_state), vp, vp, vp]
         L.np_predict.argtypes = [S, vp, vp, vp, vp, vp, vp]
         L.np_select.argtypes = [S, vp, vp, vp, vp, vp]
         L.np_delta.argtypes = [S, i32, vp, ctypes.POINTER(np_state), ctypes.POINTER(np_delta_out),
@@ -98,6 +98,7 @@ def lib():
         L.np_sparse_mlp.argtypes = [S, i32, vp, vp, vp, i32, vp, vp, vp]
         L.np_device_error.argtypes = [vp, vp, ctypes.POINTER(i32)]
         L.np_sparse_mlp_noalloc.argtypes = [S, i32, vp, vp, vp, i32, vp, vp, vp]
+        L.np_sparse_mlp_ids.argtypes = [S, i32, vp, vp, vp, vp, i32, vp, vp, vp]
         L.np_centroid_select.argtypes = [S, ctypes.POINTER(np_centroid_model), vp, vp, vp, vp,
                                          vp, vp, vp, vp]
         L.np_delta_n.argtypes = [S, i32, vp, vp, ctypes.POINTER(np_state),
@@ -158,14 +159,21 @@ def np_shape_check(shape: np_shape) -> None:
 
 
 def np_workspace_size(shape: np_shape) -> int:
-    n = ctypes.c_size_t(0)
-    _check(lib().np_workspace_size(ctypes.byref(shape), ctypes.byref(n)), "np_workspace_size")
-    return n.value
+    """Device workspace bytes (np_workspace_sizes gives the pinned host size too)."""
+    return np_workspace_sizes(shape)[0]
 
 
-def np_state_reset(shape, state: np_state, ws, stream=None) -> None:
-    _check(lib().np_state_reset(ctypes.byref(shape), ctypes.byref(state), _p(ws), _s(stream)),
-           "np_state_reset")
+def np_workspace_sizes(shape: np_shape) -> tuple[int, int]:
+    """(device workspace bytes, pinned host bytes for host staging)."""
+    n, h = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    _check(lib().np_workspace_size(ctypes.byref(shape), ctypes.byref(n), ctypes.byref(h)),
+           "np_workspace_size")
+    return n.value, h.value
+
+
+def np_state_reset(shape, state: np_state, ws, stream=None, dev_resident=None) -> None:
+    _check(lib().np_state_reset(ctypes.byref(shape), ctypes.byref(state), _p(dev_resident),
+                                _p(ws), _s(stream)), "np_state_reset")
 
 
 def np_predict(shape, h, A, B, scores, ws, stream=None) -> None:
@@ -251,6 +259,13 @@ def np_sparse_mlp_noalloc(shape, layer: int, x, dev_resident, active_slots, n_ac
     _check(lib().np_sparse_mlp_noalloc(ctypes.byref(shape), int(layer), _p(x), _p(dev_resident),
                                        _p(active_slots), int(n_active), _p(y), _p(dev_error),
                                        _s(stream)), "np_sparse_mlp_noalloc")
+
+
+def np_sparse_mlp_ids(shape, layer: int, x, dev_resident, active_ids, slot_of, n_active: int, y,
+                      ws, stream=None) -> None:
+    _check(lib().np_sparse_mlp_ids(ctypes.byref(shape), int(layer), _p(x), _p(dev_resident),
+                                   _p(active_ids), _p(slot_of), int(n_active), _p(y), _p(ws),
+                                   _s(stream)), "np_sparse_mlp_ids")
 
 
 def np_centroid_select(shape, model: np_centroid_model, feat, logits, centroid_ids, mask,

@@ -1,6 +1,7 @@
 // np_abi.cpp -- host side of the C ABI: argument validation, status text,
 // workspace sizing and dispatch to the kernel launchers.  Validation runs
 // before anything is enqueued.
+#include <algorithm>
 #include <cmath>
 #include <stdarg.h>
 #include <stdio.h>
@@ -33,9 +34,9 @@ np_status check_resident(const char* fn, const void* resident) {
   return NP_OK;
 }
 
-void clear_incomplete_residents() {
+void clear_incomplete_resident(const void* resident) {
   std::lock_guard<std::mutex> g(g_incomplete_mu);
-  g_incomplete.clear();
+  g_incomplete.erase((uintptr_t)resident);
 }
 
 thread_local std::string g_last_error;
@@ -114,15 +115,24 @@ np_status np_shape_check(const np_shape* s) {
   return st;
 }
 
-np_status np_workspace_size(const np_shape* s, size_t* bytes) {
+np_status np_workspace_size(const np_shape* s, size_t* bytes, size_t* pinned_host_bytes) {
   np_status st = check_shape(s);
   if (st != NP_OK) return st;
   if (!bytes) return fail(NP_ERR_INVALID_ARG, "dev_ws_bytes is NULL");
   *bytes = ws_total(*s);
+  if (pinned_host_bytes) {
+    // the plan copy (counts, in_ids, in_slots), then a staging area of four
+    // pieces of 16 MiB (at least one record and its row index each)
+    const size_t rec = (size_t)3 * s->d_model * dtype_size(s->wdtype);
+    const size_t plan = ((size_t)s->layers * (4 + 2 * (size_t)s->k) * 4 + 4095) & ~(size_t)4095;
+    const size_t piece = (std::max((size_t)16 << 20, rec + 4) + 4095) & ~(size_t)4095;
+    *pinned_host_bytes = plan + 4 * piece;
+  }
   return NP_OK;
 }
 
-np_status np_state_reset(const np_shape* s, const np_state* state, void* ws, hipStream_t stream) {
+np_status np_state_reset(const np_shape* s, const np_state* state, const void* resident,
+                         void* ws, hipStream_t stream) {
   np_status st = check_shape(s);
   if (st != NP_OK) return st;
   if (!state || !aligned16(state->slot_of) || !aligned16(state->neuron_of) ||
@@ -131,7 +141,7 @@ np_status np_state_reset(const np_shape* s, const np_state* state, void* ws, hip
   if (!aligned16(ws)) return fail(NP_ERR_INVALID_ARG, "dev_ws must be non-NULL and 16-byte aligned");
   hipError_t e = launch_fill_state(*s, *state, ws, stream);
   if (e != hipSuccess) return hip_fail(e, "np_state_reset launch");
-  clear_incomplete_residents();  // a cold start: no resident row is assumed
+  if (resident) clear_incomplete_resident(resident);  // a cold start: no resident row is assumed
   return NP_OK;
 }
 
@@ -278,6 +288,25 @@ np_status np_sparse_mlp_noalloc(const np_shape* s, int32_t layer, const void* x,
   hipError_t e =
       launch_sparse_mlp_noalloc(*s, layer, x, resident, slots, n_active, y, dev_error, stream);
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp_noalloc launch");
+}
+
+np_status np_sparse_mlp_ids(const np_shape* s, int32_t layer, const void* x, const void* resident,
+                            const int32_t* active_ids, const int32_t* slot_of, int32_t n_active,
+                            void* y, void* ws, hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (layer < 0 || layer >= s->layers)
+    return fail(NP_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, s->layers);
+  if (n_active < 0 || n_active > s->capacity)
+    return fail(NP_ERR_INVALID_ARG, "n_active %d outside [0, capacity]", n_active);
+  if (!aligned16(x) || !aligned16(resident) || !aligned16(y) || !aligned16(ws) ||
+      (n_active > 0 && (!active_ids || !slot_of)) || ((uintptr_t)active_ids & 3) ||
+      ((uintptr_t)slot_of & 3))
+    return fail(NP_ERR_INVALID_ARG, "np_sparse_mlp_ids: pointers must be non-NULL and aligned");
+  if ((st = check_resident("np_sparse_mlp_ids", resident)) != NP_OK) return st;
+  hipError_t e = launch_sparse_mlp(*s, layer, x, resident, nullptr, n_active, y, ws, stream,
+                                   nullptr, nullptr, active_ids, slot_of);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_sparse_mlp_ids launch");
 }
 
 np_status np_dense_mlp(const np_shape* s, const void* weights, const void* x, void* y, void* ws,

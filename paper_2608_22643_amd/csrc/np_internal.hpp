@@ -70,17 +70,20 @@ hipError_t launch_centroid_active(const np_shape& s, const np_centroid_model& m,
 hipError_t launch_stage_gather(const np_shape& s, const np_delta_out& out, int layer_begin,
                                int layer_end, const void* storage, void* resident, void* ws,
                                hipStream_t stream);
-hipError_t launch_stage_scatter(const np_shape& s, const void* landing, int n_records,
-                                void* resident, hipStream_t stream);
+hipError_t launch_stage_scatter(const np_shape& s, const void* landing, const int32_t* rows,
+                                int n_records, void* resident, hipStream_t stream);
 hipError_t launch_dense_mlp(const np_shape& s, const void* weights, const void* x, void* y,
                             void* ws, hipStream_t stream);
 // n_dev: nullptr for n_active rows, else the row count is n_dev[layer]
 // (device), at most n_active.  thr: nullptr, or the eq. 1 threshold of each
 // layer (device fp32 [L']).
+// ids/slot_map: with active_slots == nullptr, row j is slot slot_map[ids[j]]
+// (the layer's active ids and its row of the slot map).
 hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const void* resident,
                              const int32_t* active_slots, int n_active, void* y, void* ws,
                              hipStream_t stream, const int32_t* n_dev = nullptr,
-                             const float* thr = nullptr);
+                             const float* thr = nullptr, const int32_t* ids = nullptr,
+                             const int32_t* slot_map = nullptr);
 // np_sparse_mlp with its partial sums in the library's own device array
 // (no workspace); device errors are OR-ed into *dev_error.
 hipError_t launch_sparse_mlp_noalloc(const np_shape& s, int layer, const void* x,
@@ -121,11 +124,11 @@ np_status read_runs(int fd, const std::vector<ReadRun>& runs, int qd, PieceDone 
 np_status fail(np_status st, const char* fmt, ...);
 // Resident buffers whose staging failed after np_delta had already moved the
 // slot map: the map names records that never arrived.  Every later staging
-// or MLP call on such a buffer fails with NP_ERR_STATE until np_state_reset,
-// which clears every mark of the process.
+// or MLP call on such a buffer fails with NP_ERR_STATE until np_state_reset
+// is given that buffer, which clears its mark (and no other).
 void mark_resident_incomplete(const void* resident);
 np_status check_resident(const char* fn, const void* resident);
-void clear_incomplete_residents();
+void clear_incomplete_resident(const void* resident);
 np_status hip_fail(hipError_t e, const char* what);
 bool aligned16(const void* p);
 np_status check_shape(const np_shape* s);

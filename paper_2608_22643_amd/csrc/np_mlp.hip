@@ -55,7 +55,22 @@ struct MlpArgs {
   int layer;
   int act;               // np_act
   const float* thr;      // nullptr, or the eq. 1 threshold of each layer at thr[layer]
+  const int32_t* ids;    // with slots == nullptr: row j is slot slot_map[ids[j]]
+  const int32_t* slot_map;
+  int F;
 };
+
+// Slot of row r of the call: the active-slot list, the slot map of the
+// active ids (an id outside [0, F) gives -1, reported as not resident), or
+// the identity order of a dense layer.
+__device__ inline int row_slot(const MlpArgs& a, int r, int b) {
+  if (a.slots) return a.slots[r];
+  if (a.ids) {
+    const int id = a.ids[r];
+    return (id >= 0 && id < a.F) ? a.slot_map[id] : -1;
+  }
+  return r * a.n_wg + b;
+}
 
 
 // Single-kernel path.  The partials use the blocked layout of the two-kernel
@@ -197,7 +212,7 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   // [b*n/G, (b+1)*n/G).  Dense (no slot list): workgroup b takes rows b,
   // b + G, b + 2G, ... (index i of its range is row i*G + b), so the
   // workgroups of a round read neighbouring records together
-  const bool dense = a.slots == nullptr;
+  const bool dense = a.slots == nullptr && a.ids == nullptr;
   const int row_begin = dense ? 0 : (int)(((long long)b * n_active) / a.n_wg);
   const int row_end = dense ? n_active / a.n_wg + (b < n_active % a.n_wg ? 1 : 0)
                             : (int)(((long long)(b + 1) * n_active) / a.n_wg);
@@ -212,8 +227,7 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
   int my_slot = -1;
   {
     const int r0 = row_begin + team * R;
-    if (lane < R && r0 + lane < row_end)
-      my_slot = dense ? (r0 + lane) * a.n_wg + b : a.slots[r0 + lane];
+    if (lane < R && r0 + lane < row_end) my_slot = row_slot(a, r0 + lane, b);
   }
   // Loads below are unconditional, with no branches around them, so the
   // compiler can wait for each stage's loads alone.  Record loads are buffer
@@ -266,9 +280,7 @@ __global__ __launch_bounds__(MAXT) void sparse_mlp_rows_kernel(MlpArgs a) {
     // next round's slots, in flight behind this round's records
     {
       const int rn = r0 + teams * R;
-      my_slot = (lane < R && rn + lane < row_end)
-                    ? (dense ? (rn + lane) * a.n_wg + b : a.slots[rn + lane])
-                    : -1;
+      my_slot = (lane < R && rn + lane < row_end) ? row_slot(a, rn + lane, b) : -1;
     }
 #pragma unroll
     for (int st = 0; st < S; ++st) {
@@ -672,9 +684,13 @@ template <class T>
 static hipError_t mlp_t(const np_shape& s, int layer, const void* x, const void* resident,
                         const int32_t* active_slots, int n_active, void* y, void* ws,
                         hipStream_t stream, const int32_t* n_dev, const float* thr,
-                        const MlpScratch* sc = nullptr) {
+                        const MlpScratch* sc = nullptr, const int32_t* ids = nullptr,
+                        const int32_t* slot_map = nullptr) {
   constexpr int V = T::V;
   MlpArgs a;
+  a.ids = active_slots ? nullptr : ids;
+  a.slot_map = slot_map;
+  a.F = s.d_ffn;
   a.act = s.act;
   a.thr = thr;
   a.NV = s.d_model / V;
@@ -787,15 +803,18 @@ hipError_t launch_dense_mlp(const np_shape& s, const void* weights, const void* 
 
 hipError_t launch_sparse_mlp(const np_shape& s, int layer, const void* x, const void* resident,
                              const int32_t* active_slots, int n_active, void* y, void* ws,
-                             hipStream_t stream, const int32_t* n_dev, const float* thr) {
+                             hipStream_t stream, const int32_t* n_dev, const float* thr,
+                             const int32_t* ids, const int32_t* slot_map) {
   switch (s.wdtype) {
     case NP_F32:
-      return mlp_t<TF32>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev, thr);
+      return mlp_t<TF32>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev, thr,
+                         nullptr, ids, slot_map);
     case NP_F16:
-      return mlp_t<TF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev, thr);
+      return mlp_t<TF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev, thr,
+                         nullptr, ids, slot_map);
     default:
       return mlp_t<TBF16>(s, layer, x, resident, active_slots, n_active, y, ws, stream, n_dev,
-                          thr);
+                          thr, nullptr, ids, slot_map);
   }
 }
 

@@ -50,8 +50,8 @@ class Bufs:
         self.ws = torch.zeros(B.np_workspace_size(self.shape), dtype=torch.uint8, device=DEV)
         self.stream = torch.cuda.current_stream()
 
-    def reset(self):
-        B.np_state_reset(self.shape, self.state, self.ws, self.stream)
+    def reset(self, resident=None):
+        B.np_state_reset(self.shape, self.state, self.ws, self.stream, resident)
 
     def host_lists(self):
         L, k = self.cfg.layers, self.cfg.k

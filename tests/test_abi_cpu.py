@@ -28,7 +28,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 23, names
+    assert len(names) == 24, names
     for n in names:
         assert hasattr(lib, n), f"missing export {n}"
     assert set(names) == set(B.EXPORTS)
@@ -189,3 +189,17 @@ def test_noalloc_rejects_rows_wider_than_its_scratch(lib):
     with pytest.raises(B.NPError) as e:  # passes the size check, fails on the error word
         B.np_sparse_mlp_noalloc(ok, 0, 256, 256, 256, 1, 256, None)
     assert e.value.status == B.NP_ERR_INVALID_ARG
+
+
+def test_pinned_host_size(lib):
+    """The pinned host size covers the plan copy and a staging area of at
+    least four records with their row indices, in whole 4 KiB pages, for a
+    small record and for the largest one (d 16384, fp16: 96 KiB)."""
+    for kw in (GOOD, dict(GOOD, d_model=16384, capacity=4000)):
+        shape = B.make_shape(**kw)
+        dev, pinned = B.np_workspace_sizes(shape)
+        assert dev == B.np_workspace_size(shape)
+        rec = 3 * kw["d_model"] * 2
+        plan = kw["layers"] * (4 + 2 * kw["k"]) * 4
+        assert pinned % 4096 == 0
+        assert pinned >= plan + 4 * rec + 4 * 4

@@ -109,6 +109,10 @@ def test_file_tier_short_file_is_an_io_error(tmp_path):
     with pytest.raises(B.NPError) as e:
         B.np_sparse_mlp(bufs.shape, 0, to_dev(W.hidden(cfg, 1)[0]), resident, sl, k, y, bufs.ws)
     assert e.value.status == B.NP_ERR_STATE
-    bufs.reset()
+    bufs.reset()  # a reset of another buffer's state leaves the mark
+    with pytest.raises(B.NPError) as e:
+        B.np_sparse_mlp(bufs.shape, 0, to_dev(W.hidden(cfg, 1)[0]), resident, sl, k, y, bufs.ws)
+    assert e.value.status == B.NP_ERR_STATE
+    bufs.reset(resident)
     B.np_sparse_mlp(bufs.shape, 0, to_dev(W.hidden(cfg, 1)[0]), resident, sl, k, y, bufs.ws)
     torch.cuda.synchronize()

@@ -178,3 +178,41 @@ def test_mlp_multi_round():
     got = decode_y(orc, sw.adtype, y.cpu().view(torch.uint8).numpy())
     assert np.all(np.abs(got - ref64) <= mlp_tolerance(sw.adtype, ref64))
     assert B.np_device_error(bufs.ws) == 0 and B.np_device_error(bufs2.ws) == 0
+
+
+@pytest.mark.parametrize("name", ["d512_f16", "d4096_bf16", "d5120_f16", "d8192_bf16"])
+def test_mlp_ids_form_matches_slots_form(name):
+    """np_sparse_mlp_ids (active ids and the layer's slot map, the lookup done
+    in the kernel) against np_sparse_mlp on the slots that lookup gives: the
+    same rows in the same order, so the same bits; and the oracle.  An id
+    outside [0, F) or an id whose slot is -1 is reported as not resident."""
+    cfg = SHAPES[name]
+    L, d, F, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.k, cfg.capacity
+    say(f"[mlp ids form] {name}")
+    bufs, rng, store, res, neuron, h = setup(cfg, 25)
+    x = to_dev(h)
+    esz = W.ITEMSIZE[cfg.adtype]
+    y = torch.zeros(d * esz, dtype=torch.uint8, device=DEV)
+    y2 = torch.full((d * esz,), 0x5A, dtype=torch.uint8, device=DEV)
+    for l in range(L):
+        slot_of = np.full(F, -1, np.int32)
+        slot_of[neuron[l]] = np.arange(C, dtype=np.int32)
+        ids = np.sort(rng.choice(neuron[l], k, replace=False)).astype(np.int32)
+        for n in sorted({0, 1, 9, k // 3, k}):
+            B.np_sparse_mlp(bufs.shape, l, x, res, to_dev(slot_of[ids]), n, y, bufs.ws)
+            B.np_sparse_mlp_ids(bufs.shape, l, x, res, to_dev(ids), to_dev(slot_of), n, y2,
+                                bufs.ws)
+            torch.cuda.synchronize()
+            assert torch.equal(y, y2), (l, n)
+            _, ref64 = orc.sparse_mlp(cfg, l, h, store, ids[:n], want_f64=True)
+            got = decode_y(orc, cfg.adtype, y2.cpu().numpy())
+            assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (l, n)
+    assert B.np_device_error(bufs.ws) == 0
+    slot_of = np.full(F, -1, np.int32)
+    slot_of[neuron[0]] = np.arange(C, dtype=np.int32)
+    absent = np.setdiff1d(np.arange(F), neuron[0])[:1]
+    for bad in (np.array([0, F + 3], np.int32), absent.astype(np.int32)):
+        bufs.reset()
+        B.np_sparse_mlp_ids(bufs.shape, 0, x, res, to_dev(bad), to_dev(slot_of), bad.size, y2,
+                            bufs.ws)
+        assert B.np_device_error(bufs.ws) & B.NP_DEVERR_NOT_RESIDENT

@@ -58,3 +58,42 @@ def test_failed_staging_marks_resident(overlap, monkeypatch):
             _, ref64 = orc.sparse_mlp(cfg, l, h[t], store, ids[l], want_f64=True)
             assert np.all(np.abs(y[l] - ref64) <= mlp_tolerance("f32", ref64)), (t, l)
     assert pipe.device_error() == 0
+
+
+def test_reset_lifts_only_its_own_mark(monkeypatch):
+    """Two decode pipelines, each with its own resident buffer: a failed
+    staging into the first marks only that buffer; the second keeps staging
+    and computing; a reset that names the second buffer leaves the first's
+    mark; the first pipeline's own cold start lifts it."""
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    cfg = W.get("tiny")
+    k = cfg.k
+    a = DecodePipeline(cfg, tier="host", staging="memcpy", overlap=False, tokens=4)
+    b = DecodePipeline(cfg, tier="host", staging="memcpy", overlap=False, tokens=4)
+    a.step(0)
+    b.step(0)
+    torch.cuda.synchronize()
+    monkeypatch.setenv("NP_TEST_FAIL_STAGE_AFTER", "0")
+    with pytest.raises(B.NPError):
+        a.step(1)
+    monkeypatch.delenv("NP_TEST_FAIL_STAGE_AFTER")
+    torch.cuda.synchronize()
+
+    def mlp(p):
+        B.np_sparse_mlp(p.shape, 0, p.x_ptr(1), p.resident, p.lists["active_slots"].data_ptr(), k,
+                        p.y.data_ptr(), p.ws, p.main)
+
+    with pytest.raises(B.NPError) as e:
+        mlp(a)
+    assert e.value.status == B.NP_ERR_STATE
+    b.step(1)  # the other pipeline is not affected
+    mlp(b)
+    b.reset()  # names b's resident buffer only
+    with pytest.raises(B.NPError) as e:
+        mlp(a)
+    assert e.value.status == B.NP_ERR_STATE
+    a.reset()
+    mlp(a)
+    torch.cuda.synchronize()
+    assert a.device_error() == 0 and b.device_error() == 0
