@@ -40,27 +40,6 @@ constexpr int AB_MAX_TILES = 8;   // token tiles of 16
 constexpr int AB_ROWB = 256;      // bytes of a row piece per chunk
 constexpr int AB_PITCH = AB_ROWB + 16;
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-
-template <class T>
-__device__ inline f32x4 mfma_step(uint4 a, uint4 b, f32x4 c) {
-  if constexpr (T::dtype == NP_F16) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
-                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
-  } else if constexpr (T::dtype == NP_BF16) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-  } else {
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0,
-                                                0);
-  }
-}
-
 struct ActBatchArgs {
   const void* w;    // one layer's [F][3d] records
   const void* x;    // [n][d] tokens of this launch

@@ -209,6 +209,35 @@ struct TBF16 {
 };
 
 // ---------------------------------------------------------------------------
+// matrix cores: one "step" of a 16 x 16 fp32 tile over 4*V reduction elements
+// (one v_mfma_f32_16x16x32 for 16-bit types, four v_mfma_f32_16x16x4f32 for
+// fp32).  Lane l holds row l%16 of the A operand and column l%16 of the B
+// operand, each as the V consecutive elements starting at V*(l/16) of the
+// step; the accumulator's register i of lane l is output row 4*(l/16) + i,
+// column l%16.
+// ---------------------------------------------------------------------------
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+template <class T>
+__device__ inline f32x4 mfma_step(uint4 a, uint4 b, f32x4 c) {
+  if constexpr (T::dtype == NP_F16) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  } else if constexpr (T::dtype == NP_BF16) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  } else {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0,
+                                                0);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // wave / workgroup reductions and scans
 // ---------------------------------------------------------------------------
 __device__ inline float wave_sum(float v) {

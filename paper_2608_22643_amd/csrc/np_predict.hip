@@ -6,6 +6,8 @@
 // multiply-add, so they are bound by HBM bandwidth.  Weight rows are streamed
 // with 16-byte loads that cover whole contiguous 1 KiB spans per wave
 // instruction; there is no data reuse for matrix cores to exploit.
+#include <stdlib.h>
+
 #include "np_device.hpp"
 
 namespace np {
@@ -107,6 +109,151 @@ __global__ __launch_bounds__(256) void predict_scores_kernel(const uint4* __rest
   }
 }
 
+// ---------------------------------------------------------------------------
+// The same two products on the matrix cores (selected with NP_PREDICT_MFMA=1,
+// or by the caller's default, see launch_predict).  A batch-1 product uses
+// one column of a 16 x 16 tile; the matrix unit replaces the per-lane dot
+// products and the cross-lane sums (every row's sum comes out whole).
+// ---------------------------------------------------------------------------
+
+// z = A h: a workgroup of 4 waves owns a tile of 16 rows of the stacked
+// [L'*r][d] matrix; wave w multiplies the tile over its quarter of the
+// reduction steps (4V elements each; lane l loads 16 bytes of row l%16), h
+// in column 0 of the B operand; the four waves' sums meet in LDS in wave
+// order.  Out-of-range rows and elements are buffer loads with an
+// out-of-range offset (zeros, no memory access).
+template <class T, int UNR>
+__global__ __launch_bounds__(256) void predict_z_mfma_kernel(const char* __restrict__ A,
+                                                             const char* __restrict__ h,
+                                                             float* __restrict__ z, int rows,
+                                                             int d) {
+  constexpr int V = T::V, KS = 4 * V, ES = 16 / V;
+  __shared__ float part[4][16];
+  const int lane = threadIdx.x & (WAVE - 1), w = threadIdx.x >> 6;
+  const int row0 = blockIdx.x * 16, r = lane & 15, q = lane >> 4;
+  const uint32_t row_bytes = (uint32_t)d * ES;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + (size_t)row0 * row_bytes, 16u * row_bytes);
+  const __amdgpu_buffer_rsrc_t rh = make_rsrc(h, row_bytes);
+  const int steps = (d + KS - 1) / KS;
+  const int s_begin = w * steps / 4, s_end = (w + 1) * steps / 4;
+  const bool row_ok = row0 + r < rows;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = s_begin; s0 < s_end; s0 += UNR) {
+    uint4 a[UNR], b[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int kk = (s0 + u) * KS + V * q;
+      const bool ok = s0 + u < s_end && kk < d;
+      a[u] = buf_load16_nt(ra, (ok && row_ok) ? (uint32_t)r * row_bytes + (uint32_t)kk * ES : BUF_OOB, 0);
+      b[u] = buf_load16(rh, (ok && r == 0) ? (uint32_t)kk * ES : BUF_OOB, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) acc = mfma_step<T>(a[u], b[u], acc);
+  }
+  if (r == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[w][4 * q + i] = acc[i];
+  }
+  __syncthreads();
+  if (threadIdx.x < 16 && row0 + (int)threadIdx.x < rows) {
+    const int t = threadIdx.x;
+    z[row0 + t] = ((part[0][t] + part[1][t]) + part[2][t]) + part[3][t];
+  }
+}
+
+// scores_l = B_l z_l: a workgroup of 4 waves owns SC_ROWS rows of one layer,
+// a 16-row tile per wave.  z is fp32 while the matrix unit takes 16-bit
+// operands, so z_l is split into three 16-bit parts, z = hi + mid + lo
+// (hi = z rounded, mid = the rest rounded, lo = what remains; 3 x 11 or
+// 3 x 8 significand bits cover fp32's 24), placed in columns 0, 1, 2 of the
+// B operand: the tile's products are exact in fp32 and the row's score is
+// D[.][0] + D[.][1] + D[.][2].  For binary16 the layer's z is first scaled
+// by 2^e (e from the largest |z|, so the parts stay in range; exact, undone
+// on the result).  fp32 weights take z itself in column 0.
+template <class T, int UNR>
+__global__ __launch_bounds__(256) void predict_scores_mfma_kernel(const char* __restrict__ B,
+                                                                  const float* __restrict__ z,
+                                                                  float* __restrict__ scores,
+                                                                  int F, int r) {
+  constexpr int V = T::V, KS = 4 * V, ES = 16 / V;
+  constexpr int NP = T::dtype == NP_F32 ? 1 : 3;
+  constexpr int MAXK = 1024;  // r <= 1024 (16-bit) or 512 (fp32): whole steps
+  __shared__ uint4 zp[NP][MAXK / V];
+  __shared__ float wmax[4];
+  const int lane = threadIdx.x & (WAVE - 1), w = threadIdx.x >> 6;
+  const int rr = lane & 15, q = lane >> 4;
+  const int l = blockIdx.y;
+  const float* zl = z + (size_t)l * r;
+  const int steps = (r + KS - 1) / KS;
+  // the layer's scale (binary16 only)
+  int e = 0;
+  if constexpr (T::dtype == NP_F16) {
+    float m = 0.f;
+    for (int k = threadIdx.x; k < r; k += 256) m = fmaxf(m, fabsf(zl[k]));
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, WAVE));
+    if (lane == 0) wmax[w] = m;
+    __syncthreads();
+    m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+    if (m > 0.f && m <= 3.0e38f) e = 14 - ilogbf(m);
+  }
+  // the parts of z_l (zero past r), V elements per 16-byte vector
+  for (int v = threadIdx.x; v < steps * 4; v += 256) {
+    uint32_t pb[NP][V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const int k = v * V + j;
+      float x = k < r ? ldexpf(zl[k], e) : 0.f;
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        pb[p][j] = T::from_f32(x);
+        if constexpr (NP > 1) x -= T::lo(pb[p][j]);
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      if constexpr (V == 8)
+        zp[p][v] = make_uint4(pb[p][0] | (pb[p][1] << 16), pb[p][2] | (pb[p][3] << 16),
+                              pb[p][4] | (pb[p][5] << 16), pb[p][6] | (pb[p][7] << 16));
+      else
+        zp[p][v] = make_uint4(pb[p][0], pb[p][1], pb[p][2], pb[p][3]);
+    }
+  }
+  __syncthreads();
+  const int n0 = blockIdx.x * SC_ROWS + 16 * w;
+  const uint32_t row_bytes = (uint32_t)r * ES;
+  const __amdgpu_buffer_rsrc_t rb =
+      make_rsrc(B + ((size_t)l * F + n0) * row_bytes, 16u * row_bytes);
+  const bool row_ok = n0 + rr < F;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < steps; s0 += UNR) {
+    uint4 a[UNR], b[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int kk = (s0 + u) * KS + V * q;
+      const bool ok = s0 + u < steps;
+      a[u] = buf_load16_nt(rb, (ok && row_ok && kk < r) ? (uint32_t)rr * row_bytes + (uint32_t)kk * ES
+                                                       : BUF_OOB, 0);
+      b[u] = (ok && rr < NP) ? zp[rr < NP ? rr : 0][(s0 + u) * 4 + q] : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) acc = mfma_step<T>(a[u], b[u], acc);
+  }
+  // column c of row i sits in lane 16 * (i / 4) + c: add columns 1 and 2
+  // into column 0 (lo and mid first), undo the scale
+  const float unscale = ldexpf(1.f, -e);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float v = acc[i];
+    if constexpr (NP > 1) {
+      const float c1 = __shfl_down(acc[i], 1, 16), c2 = __shfl_down(acc[i], 2, 16);
+      v = (c2 + c1) + v;
+    }
+    const int n = n0 + 4 * q + i;
+    if (rr == 0 && n < F) scores[(size_t)l * F + n] = v * unscale;
+  }
+}
+
 // Row dot products out[i] = A[i] . x over rows of nv 16-byte vectors (the
 // first stage of the predictor; also the centroid heads).
 template <class T>
@@ -128,10 +275,31 @@ hipError_t launch_centroid_logits(const np_shape& s, const np_centroid_model& m,
   }
 }
 
+static bool predict_mfma_requested() {
+  const char* v = getenv("NP_PREDICT_MFMA");
+  return v && atoi(v) == 1;
+}
+
+template <class T>
+static hipError_t predict_mfma_t(const np_shape& s, const void* h, const void* A, const void* B,
+                                 float* scores, void* ws, hipStream_t stream) {
+  const int rows = s.layers * s.rank;
+  float* z = (float*)((char*)ws + ws_z_offset());
+  hipLaunchKernelGGL((predict_z_mfma_kernel<T, 8>), dim3((rows + 15) / 16), dim3(256), 0, stream,
+                     (const char*)A, (const char*)h, z, rows, s.d_model);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 grid((s.d_ffn + SC_ROWS - 1) / SC_ROWS, s.layers);
+  hipLaunchKernelGGL((predict_scores_mfma_kernel<T, 8>), grid, dim3(256), 0, stream,
+                     (const char*)B, (const float*)z, scores, s.d_ffn, s.rank);
+  return hipGetLastError();
+}
+
 template <class T>
 static hipError_t predict_t(const np_shape& s, const void* h, const void* A, const void* B,
                             float* scores, void* ws, hipStream_t stream) {
   constexpr int V = T::V;
+  if (predict_mfma_requested()) return predict_mfma_t<T>(s, h, A, B, scores, ws, stream);
   const int nv = s.d_model / V;
   const int rows = s.layers * s.rank;
   float* z = (float*)((char*)ws + ws_z_offset());

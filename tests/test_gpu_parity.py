@@ -41,10 +41,16 @@ SHAPES = {
 }
 
 
+@pytest.mark.parametrize("mfma", ["0", "1"])
 @pytest.mark.parametrize("name", list(SHAPES))
-def test_predict(name):
+def test_predict(name, mfma, monkeypatch):
+    """Both predictor paths: the per-lane dot products (default) and the
+    matrix-core kernels (NP_PREDICT_MFMA=1), against O1 within the fp32
+    accumulation bound; ragged d and r (tails of the 32-element steps)."""
+    monkeypatch.setenv("NP_PREDICT_MFMA", mfma)
     cfg = SHAPES[name]
-    say(f"[predict] {name} L'={cfg.layers} d={cfg.d_model} F={cfg.d_ffn} r={cfg.rank}")
+    say(f"[predict] {name} mfma={mfma} L'={cfg.layers} d={cfg.d_model} F={cfg.d_ffn} "
+        f"r={cfg.rank}")
     bufs = Bufs(cfg)
     A, Bm = W.predictor(cfg)
     h = W.hidden(cfg, 2)
@@ -57,6 +63,26 @@ def test_predict(name):
         ref = orc.predict(cfg, h[t], A, Bm).astype(np.float64)
         tol = score_bound(cfg, A, Bm, h[t]) + np.abs(ref) * 2.0 ** -23
         assert np.all(np.abs(got - ref) <= tol), np.max(np.abs(got - ref) / tol)
+
+
+@pytest.mark.parametrize("scale", [3e2, 1e-4])
+@pytest.mark.parametrize("name", ["ragged_f16", "ragged_bf16", "wide_f16"])
+def test_predict_mfma_z_range(name, scale, monkeypatch):
+    """The matrix-core scores kernel splits the fp32 z into three 16-bit parts
+    after scaling each layer by a power of two (binary16): inputs scaled so
+    that z is far above and far below 1 keep the scores within the bound."""
+    monkeypatch.setenv("NP_PREDICT_MFMA", "1")
+    cfg = SHAPES[name]
+    say(f"[predict z range] {name} scale={scale}")
+    bufs = Bufs(cfg)
+    A, Bm = W.predictor(cfg)
+    h = orc.encode(cfg.adtype, orc.decode(cfg.adtype, W.hidden(cfg, 1)[0]) * scale)
+    B.np_predict(bufs.shape, to_dev(h), to_dev(A), to_dev(Bm), bufs.scores, bufs.ws)
+    torch.cuda.synchronize()
+    got = from_dev(bufs.scores, np.float32, (cfg.layers, cfg.d_ffn)).astype(np.float64)
+    ref = orc.predict(cfg, h, A, Bm).astype(np.float64)
+    tol = score_bound(cfg, A, Bm, h) + np.abs(ref) * 2.0 ** -23
+    assert np.all(np.abs(got - ref) <= tol), np.max(np.abs(got - ref) / tol)
 
 
 def run_select(bufs, scores_np):
