@@ -244,7 +244,8 @@ np_status np_stage_gather(const np_shape* s, const np_delta_out* out, int32_t lb
       return fail(NP_ERR_INVALID_ARG, "np_stage_gather: host storage is not mapped to the device");
     storage = attr.devicePointer;
   }
-  hipError_t e = launch_stage_gather(*s, *out, lb, le, storage, resident, ws, stream);
+  hipError_t e = launch_stage_gather(*s, *out, lb, le, storage, resident, ws, stream,
+                                     attr.type == hipMemoryTypeHost);
   if (e == hipSuccess) return NP_OK;
   mark_resident_incomplete(resident);
   return hip_fail(e, "np_stage_gather launch");

@@ -67,9 +67,10 @@ hipError_t launch_centroid_active(const np_shape& s, const np_centroid_model& m,
                                   const float* logits, int32_t* centroid_ids, uint32_t* mask,
                                   int32_t* active_ids, int32_t* active_counts, void* ws,
                                   hipStream_t stream);
+// host_storage: the storage is pinned host memory read over the host link
 hipError_t launch_stage_gather(const np_shape& s, const np_delta_out& out, int layer_begin,
                                int layer_end, const void* storage, void* resident, void* ws,
-                               hipStream_t stream);
+                               hipStream_t stream, bool host_storage = false);
 hipError_t launch_stage_scatter(const np_shape& s, const void* landing, const int32_t* rows,
                                 int n_records, void* resident, hipStream_t stream);
 hipError_t launch_dense_mlp(const np_shape& s, const void* weights, const void* x, void* y,

@@ -99,10 +99,13 @@ __global__ __launch_bounds__(STAGE_NT) void stage_scatter_kernel(
 
 hipError_t launch_stage_gather(const np_shape& s, const np_delta_out& out, int lb, int le,
                                const void* storage, void* resident, void* ws,
-                               hipStream_t stream) {
+                               hipStream_t stream, bool host_storage) {
   const int rec_vecs = 3 * s.d_model * dtype_size(s.wdtype) / 16;
   int grid = 128 * (le - lb);
-  if (grid > 2048) grid = 2048;
+  // over the host link 256 workgroups keep enough records in flight (the
+  // same rate as 2048 on the MI355X host) and leave the CUs to the MLPs
+  // that run beside a side-stream gather
+  if (grid > (host_storage ? 256 : 2048)) grid = host_storage ? 256 : 2048;
   if (grid < 64) grid = 64;
   hipLaunchKernelGGL(stage_gather_kernel, dim3(grid), dim3(STAGE_NT), 0, stream, out.counts,
                      out.in_ids, out.in_slots, s.k, s.d_ffn, s.capacity, lb, le,

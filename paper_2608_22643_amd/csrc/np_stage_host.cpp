@@ -28,7 +28,10 @@ namespace np {
 
 // Persistent worker pool for the host pack (memcpy of coalesced runs).  One
 // pool per process; concurrent callers take turns (run() holds a lock), so
-// two pipelines staging at once share the packing threads.
+// two pipelines staging at once share the packing threads.  Between jobs the
+// workers spin on the job counter for a while before they sleep, so the next
+// piece's job starts within a microsecond instead of a thread wake-up (a
+// token's staging runs a few dozen jobs in quick succession).
 class PackPool {
  public:
   struct Task {
@@ -47,21 +50,26 @@ class PackPool {
       return;
     }
     std::lock_guard<std::mutex> turn(run_mu_);
+    tasks_ = &tasks;
+    next_.store(0);
+    active_.store((int)workers_.size());
     {
-      std::lock_guard<std::mutex> lk(mu_);
-      tasks_ = &tasks;
-      next_.store(0);
-      active_ = (int)workers_.size();
-      ++gen_;
+      std::lock_guard<std::mutex> lk(mu_);  // a worker about to sleep sees the new job
+      gen_.fetch_add(1, std::memory_order_release);
     }
     cv_start_.notify_all();
     drain();
-    std::unique_lock<std::mutex> lk(mu_);
-    cv_done_.wait(lk, [this] { return active_ == 0; });
+    for (int i = 0; active_.load(std::memory_order_acquire) != 0 && i < kSpin; ++i) relax();
+    if (active_.load(std::memory_order_acquire) != 0) {
+      std::unique_lock<std::mutex> lk(mu_);
+      cv_done_.wait(lk, [this] { return active_.load(std::memory_order_acquire) == 0; });
+    }
     tasks_ = nullptr;
   }
 
  private:
+  static constexpr int kSpin = 1 << 16;  // polls before sleeping (a few hundred us)
+  static void relax() { __builtin_ia32_pause(); }
   void drain() {
     const std::vector<Task>& t = *tasks_;
     for (;;) {
@@ -73,13 +81,22 @@ class PackPool {
   void loop() {
     uint64_t seen = 0;
     for (;;) {
-      std::unique_lock<std::mutex> lk(mu_);
-      cv_start_.wait(lk, [&] { return gen_ != seen; });
-      seen = gen_;
-      lk.unlock();
+      uint64_t g = gen_.load(std::memory_order_acquire);
+      for (int i = 0; g == seen && i < kSpin; ++i) {
+        relax();
+        g = gen_.load(std::memory_order_acquire);
+      }
+      if (g == seen) {
+        std::unique_lock<std::mutex> lk(mu_);
+        cv_start_.wait(lk, [&] { return gen_.load(std::memory_order_acquire) != seen; });
+        g = gen_.load(std::memory_order_acquire);
+      }
+      seen = g;
       drain();
-      lk.lock();
-      if (--active_ == 0) cv_done_.notify_all();
+      if (active_.fetch_sub(1, std::memory_order_acq_rel) == 1) {
+        std::lock_guard<std::mutex> lk(mu_);
+        cv_done_.notify_all();
+      }
     }
   }
 
@@ -89,8 +106,8 @@ class PackPool {
   std::condition_variable cv_start_, cv_done_;
   const std::vector<Task>* tasks_ = nullptr;
   std::atomic<size_t> next_{0};
-  int active_ = 0;
-  uint64_t gen_ = 0;
+  std::atomic<int> active_{0};
+  std::atomic<uint64_t> gen_{0};
 };
 
 // Created on first use and kept for the life of the process (never joined).
@@ -269,7 +286,14 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
   char* stg = nullptr;
   // the current round occupies ring positions [land_base, land_base + land_n)
   size_t n_piece = 0, land_n = 0, land_base = cx->land_pos;
+  // the first piece is small (2 MiB) so that the copy engine starts early,
+  // unless it is still busy with the previous call's pieces
   size_t cur_cap = std::min(piece_cap, std::max<size_t>(1, ((size_t)2 << 20) / rec));
+  {
+    const int ph = (h + n_pieces - 1) % n_pieces;
+    if (cx->pending[ph] && hipEventQuery(cx->ev[ph]) == hipErrorNotReady) cur_cap = piece_cap;
+    (void)hipGetLastError();
+  }
   // run being extended: source byte offset in the storage tier, length in
   // records, first record's index in the piece
   uint64_t run_src = 0;
