@@ -16,8 +16,11 @@ Extra measurements in the same run:
     token's block of back-to-back calls on their stream, against the HBM
     roofline;
   * a per-step breakdown (predict / select / delta / stage / mlp);
-  * the same step with the storage tier in pinned host memory (staging over
-    the host link) -- reported under "host_tier", never as `value`;
+  * the same step with the storage tier in pinned host memory (np_stage_rows
+    staging over the host link, the stated tier of the 13B and 70B
+    configurations) for 7B, 13B and 70B -- "end_to_end_pinned_host" and
+    "host_tier", PCIe-inclusive, never `value`;
+  * np_predict on both of its paths (per-lane dot products and matrix cores);
   * the CPU oracle on a bounded sample, on the host cores.
 """
 from __future__ import annotations
@@ -93,8 +96,11 @@ def predict_bytes(cfg) -> int:
 
 
 def trace_marker():
-    """A one-element float fill kernel: in a kernel trace of this script, the
-    only float fills bracket the steps the sparse-MLP roofline is taken on."""
+    """A one-element float fill kernel.  In a kernel trace of this script the
+    only float fills are these markers; in run order they bracket the steps
+    the sparse-MLP roofline is taken on, the empty np_sparse_mlp calls, and
+    each np_stage_rows staging window of the host-tier legs (7B, then 70B,
+    then 13B; the overlapped mode first)."""
     import torch
 
     torch.cuda.synchronize()
@@ -144,6 +150,48 @@ def timed_steps(pipe, t0, steps, with_mlp_events=True, step_us=None):
     if starts:
         step_us.extend(a.elapsed_time(e[1]) * 1e3 for a, e in zip(starts, evs))
     return wall, mlp_us
+
+
+def mlp_dispatch_floor(pipe, blocks: int = 10) -> dict:
+    """np_sparse_mlp with no active rows, L' calls back to back: each call is
+    the rows kernel on one workgroup (it writes a zero partial) and the reduce
+    kernel, so the span per call is the fixed cost of a call -- two dispatches
+    and the boundaries between them.  Each block of calls is queued behind a
+    sleep kernel on the calls' stream so that the host's enqueue rate does not
+    set the pace; events on that stream bracket the block.  In a kernel trace
+    of this script the blocks sit between the third and fourth one-element
+    float fills, so the durations the profiler records for the same empty
+    dispatches can be set beside this span."""
+    import numpy as np
+    import torch
+
+    from paper_2608_22643_amd import binding as B
+    from paper_2608_22643_amd import workload as W
+
+    cfg, m = pipe.cfg, pipe.main
+    L, k = cfg.layers, cfg.k
+    ybytes = cfg.d_model * W.ITEMSIZE[cfg.adtype]
+    slots = pipe.lists["active_slots"].data_ptr()
+    spans = []
+    trace_marker()
+    for _ in range(blocks):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(m):
+            torch.cuda._sleep(2_000_000)  # about 1 ms: the block is queued before it ends
+        e0.record(m)
+        for l in range(L):
+            B.np_sparse_mlp(pipe.shape, l, pipe.x_ptr(0), pipe.resident, slots + l * k * 4, 0,
+                            pipe.y.data_ptr() + l * ybytes, pipe.ws, m)
+        e1.record(m)
+        e1.synchronize()
+        spans.append(e0.elapsed_time(e1) * 1e3 / L)
+    trace_marker()
+    if pipe.device_error():
+        raise RuntimeError(f"empty np_sparse_mlp calls: device error word {pipe.device_error():#x}")
+    return {"us_per_call": round(float(np.median(spans)), 3),
+            "min_us_per_call": round(float(np.min(spans)), 3), "calls": L * blocks,
+            "note": "np_sparse_mlp with 0 active rows (one rows workgroup + the reduce kernel), "
+                    "L' calls back to back behind a sleep kernel: the fixed cost of a call"}
 
 
 def read_ref_gbps(nbytes: int = 2 << 30, reps: int = 5) -> float:
@@ -218,6 +266,42 @@ def breakdown(pipe, t0, steps):
     return {n: round(v / steps, 2) for n, v in acc.items()}, counts, ids
 
 
+def predictor_paths(pipe, t: int, pbytes: int, reps: int = 20) -> dict:
+    """np_predict alone, back to back on its stream, on both of its paths:
+    per-lane dot products ("vgpr", the default unless NP_PREDICT_MFMA=1) and
+    the matrix cores ("mfma").  Bytes: A, B, h and the fp32 scores."""
+    import torch
+
+    from paper_2608_22643_amd import binding as B
+
+    saved = os.environ.get("NP_PREDICT_MFMA")
+    out = {"bytes": pbytes}
+    try:
+        for name, flag in (("vgpr", "0"), ("mfma", "1")):
+            os.environ["NP_PREDICT_MFMA"] = flag
+            m = pipe.main
+            for _ in range(3):
+                B.np_predict(pipe.shape, pipe.x_ptr(t), pipe.A, pipe.B, pipe.scores, pipe.ws, m)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(m)
+            for _ in range(reps):
+                B.np_predict(pipe.shape, pipe.x_ptr(t), pipe.A, pipe.B, pipe.scores, pipe.ws, m)
+            e1.record(m)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            gbps = pbytes / (us * 1e-6) / 1e9
+            out[name] = {"avg_us": round(us, 2), "achieved_GBps": round(gbps, 1),
+                         "frac": round(gbps / HBM_PEAK_GBPS, 4)}
+    finally:
+        if saved is None:
+            os.environ.pop("NP_PREDICT_MFMA", None)
+        else:
+            os.environ["NP_PREDICT_MFMA"] = saved
+    out["default"] = "mfma" if saved == "1" else "vgpr"
+    out.update(out[out["default"]])
+    return out
+
+
 def h2d_peak_gbps(nbytes: int = 1 << 30) -> float:
     """One pinned host -> device hipMemcpyAsync of `nbytes`, timed with events."""
     import torch
@@ -243,20 +327,66 @@ def staging_rates(pipe, t0: int, steps: int) -> dict:
     for a staging half to drain when one token's records fill more than
     one)."""
     pipe.stage_log = []
+    trace_marker()  # a kernel trace shows this window's copies between two markers
     for i in range(steps):
         pipe.step(t0 + i)
     import torch
 
     torch.cuda.synchronize()
+    trace_marker()
     nb = sum(e[0] for e in pipe.stage_log)
     sec = sum(e[1] for e in pipe.stage_log)
     call = sum(e[2] for e in pipe.stage_log)
     pipe.stage_log = None
     return {"staging_h2d_GBps": round(nb / sec / 1e9, 2),
-            "staged_MB_per_token": round(nb / steps / 1e6, 2),
+            "staged_MB_per_token": round(nb / steps / 1e6, 2), "tokens": steps,
+            "staged_bytes": int(nb),
             "staging_ms_per_token": round(sec * 1e3 / steps, 3),
             "host_call_ms_per_token": round(call * 1e3 / steps, 3),
             "h2d_peak_GBps": round(h2d_peak_gbps(), 2)}
+
+
+def pinned_host_run(cfg, host_storage, steps: int, tokens: int, t0: int = 0) -> dict:
+    """The spec step with the storage tier in pinned host memory:
+    np_predict, np_select, np_delta, np_stage_rows (the plan read on the host,
+    records packed into pinned staging and sent with hipMemcpyAsync, then
+    scattered) and the sparse MLPs, per token, for the step with staging on a
+    side stream in layer groups (each group's MLPs run while the next group
+    is staged) and on the main stream; then the mapped-memory gather of the
+    same tier (np_stage_gather, the GPU reading pinned memory over the host
+    link).  Reports tokens/s of each, the staging rate of np_stage_rows alone
+    against a 1 GiB pinned hipMemcpyAsync of the same run, and the host's
+    share (packing and enqueueing)."""
+    import torch
+
+    from paper_2608_22643_amd.pipeline import DecodePipeline
+
+    out = {}
+    best = None
+    for staging, overlap in (("memcpy", True), ("memcpy", False), ("gather", True)):
+        key = f"{'np_stage_rows' if staging == 'memcpy' else 'np_stage_gather'}" + \
+              ("_overlap" if overlap else "")
+        p = DecodePipeline(cfg, tier="host", staging=staging, overlap=overlap, tokens=tokens,
+                           host_storage=host_storage)
+        for i in range(4):
+            p.step(t0 + i)
+        torch.cuda.synchronize()
+        wall, _ = timed_steps(p, t0 + 4, steps, with_mlp_events=False)
+        rec = {"tok_s": round(steps / wall, 2), "ms_per_token": round(wall * 1e3 / steps, 3)}
+        if staging == "memcpy":
+            rec.update(staging_rates(p, t0 + 4 + steps, max(3, steps // 2)))
+            if best is None or rec["tok_s"] > out[best]["tok_s"]:
+                best = key
+        if p.device_error():
+            raise RuntimeError(f"{cfg.name} host tier: device error word {p.device_error():#x}")
+        out[key] = rec
+        del p
+        torch.cuda.empty_cache()
+    out["tok_s"] = out[best]["tok_s"]
+    out["staging_GBps"] = out[best]["staging_h2d_GBps"]
+    out["h2d_peak_GBps"] = out[best]["h2d_peak_GBps"]
+    out["mode"] = best
+    return out
 
 
 def file_tier_run(cfg, host_storage, steps: int) -> dict:
@@ -334,9 +464,19 @@ def hbm_config_run(name: str, steps: int) -> tuple[dict, dict]:
     from paper_2608_22643_amd.pipeline import DecodePipeline
 
     cfg = W.get(name)
-    T = 4 + 2 * steps + 4
+    T = 4 + 2 * steps + 4 + 8 * steps + 16
     t = time.perf_counter()
-    pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T)
+    # the storage tier generated once into pinned host memory: copied to HBM
+    # for the HBM leg, read over the host link in the stated tier's leg
+    host_storage = None
+    try:
+        host_storage = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
+        W.fill_storage(cfg, host_storage.data_ptr())
+    except RuntimeError as e:  # not enough pinnable host memory: generate per layer
+        log(f"[bench] {name}: no pinned copy of the storage tier ({str(e).splitlines()[0]})")
+        host_storage = None
+    pipe = DecodePipeline(cfg, tier="device", staging="gather", tokens=T,
+                          host_storage=host_storage)
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t
     log(f"[bench] {name}: every tier in HBM ({torch.cuda.memory_allocated() / 1e9:.1f} GB), "
@@ -370,6 +510,34 @@ def hbm_config_run(name: str, steps: int) -> tuple[dict, dict]:
            "incoming_rows_per_token": int(counts[:, 0].sum())}
     del pipe
     torch.cuda.empty_cache()
+    # the stated tier: resident set in HBM, the rest in pinned host memory.
+    # When the host cannot pin the whole storage tier, the leg runs on the
+    # first layers only (the same per-layer shapes; halved until it fits) and
+    # says so.
+    host_cfg = cfg
+    n = cfg.layers
+    while host_storage is None and n > 8:
+        n //= 2
+        host_cfg = cfg.with_(name=f"{cfg.name}-first{n}", layers=n)
+        try:
+            host_storage = torch.empty(host_cfg.storage_bytes, dtype=torch.uint8,
+                                       pin_memory=True)
+            W.fill_storage(host_cfg, host_storage.data_ptr())
+            log(f"[bench] {name}: host tier on the first {n} of {cfg.layers} layers "
+                f"({host_cfg.storage_bytes / 1e9:.1f} GB pinned)")
+        except RuntimeError as e:
+            log(f"[bench] {name}: {n} layers not pinnable ({str(e).splitlines()[0]})")
+            host_storage = None
+    if host_storage is not None:
+        ht = pinned_host_run(host_cfg, host_storage, steps, T, 4 + 2 * steps + 4)
+        ht["layers"] = host_cfg.layers
+        ht["pinned_GB"] = round(host_cfg.storage_bytes / 1e9, 1)
+        ht["ms_per_layer"] = round(1e3 / ht["tok_s"] / host_cfg.layers, 4)
+        if host_cfg.layers != cfg.layers:
+            ht["note"] = (f"first {host_cfg.layers} of {cfg.layers} downstream layers: the host "
+                          f"could not pin the whole {cfg.storage_bytes / 1e9:.0f} GB storage tier")
+        out["host_tier"] = ht
+        del host_storage
     return out, sample
 
 
@@ -385,7 +553,7 @@ def extra_config(name: str, steps: int, graph: bool, overlap: bool) -> dict:
     from paper_2608_22643_amd.pipeline import DecodePipeline
 
     cfg = W.get(name)
-    T = 1 + 3 + 3 * steps + 8
+    T = 1 + 3 + 8 * steps + 16
     t = time.perf_counter()
     host_storage = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
     W.fill_storage(cfg, host_storage.data_ptr())
@@ -417,14 +585,8 @@ def extra_config(name: str, steps: int, graph: bool, overlap: bool) -> dict:
            "incoming_rows_per_token": int(counts[:, 0].sum())}
     del pipe
     torch.cuda.empty_cache()
-    hp = DecodePipeline(cfg, tier="host", staging="memcpy", overlap=True, tokens=T,
-                        host_storage=host_storage)
-    for i in range(4):
-        hp.step(i)
-    hw, _ = timed_steps(hp, 4, steps, with_mlp_events=False)
-    out["host_tier"] = {"memcpy_staging_tok_s": round(steps / hw, 2)}
-    out["host_tier"].update(staging_rates(hp, 4 + steps, max(3, steps // 4)))
-    del hp, host_storage
+    out["host_tier"] = pinned_host_run(cfg, host_storage, steps, T)
+    del host_storage
     torch.cuda.empty_cache()
     return out
 
@@ -769,8 +931,11 @@ def cpu_baseline(cfg, host_storage, seconds: float, gpu_ref=(), big_samples=()):
     checks = {"tokens": 0, "scores_max_rel_diff": 0.0, "select_exact": True, "delta_exact": True,
               "slot_maps_exact": True, "mlp_max_abs_err": 0.0, "mlp_within_tol": True}
     n, t0 = 0, time.perf_counter()
+    step_s = {"predict": 0.0, "select": 0.0, "delta": 0.0, "sparse_mlp": 0.0}
     while True:
+        ta = time.perf_counter()
         s = oracle.predict(cfg, h[n], A, Bm)
+        step_s["predict"] += time.perf_counter() - ta
         ref = gpu_ref[n] if n < len(gpu_ref) else None
         if ref is not None:
             gs = ref["scores"]
@@ -778,10 +943,16 @@ def cpu_baseline(cfg, host_storage, seconds: float, gpu_ref=(), big_samples=()):
             checks["scores_max_rel_diff"] = max(checks["scores_max_rel_diff"],
                                                 float(np.max(np.abs(gs.astype(np.float64) - s))) / scale)
             s = gs
+        ta = time.perf_counter()
         _, ids = oracle.select(s, cfg.k)
+        tb = time.perf_counter()
         dl = oracle.delta(n, ids, st, cfg.capacity)
+        tc = time.perf_counter()
         ys = [oracle.sparse_mlp(cfg, l, h[n], store, ids[l], want_f64=ref is not None)
               for l in range(L)]
+        step_s["select"] += tb - ta
+        step_s["delta"] += tc - tb
+        step_s["sparse_mlp"] += time.perf_counter() - tc
         if ref is not None:
             checks["tokens"] += 1
             checks["select_exact"] &= bool(np.array_equal(ids, ref["ids"]))
@@ -813,7 +984,8 @@ def cpu_baseline(cfg, host_storage, seconds: float, gpu_ref=(), big_samples=()):
            "sample": f"{n} whole decode tokens (cold start first) of the {cfg.name} workload: "
                      f"predict, select, delta, sparse MLP of all {cfg.layers} layers; "
                      f"staging omitted (a byte copy); {el:.1f} s on 1 host thread",
-           "cpu_model": cpu_model(), "host_cpus": os.cpu_count()}
+           "cpu_model": cpu_model(), "cpu_detail": cpu_detail(), "host_cpus": os.cpu_count(),
+           "per_step_ms_per_token": {k: round(v * 1e3 / n, 2) for k, v in step_s.items()}}
     # the same tokens again with the layers' sparse MLPs spread over the host
     # threads (the oracle's C calls release the interpreter lock; predict,
     # select and delta stay single calls)
@@ -857,6 +1029,46 @@ def cpu_baseline(cfg, host_storage, seconds: float, gpu_ref=(), big_samples=()):
                             checks["slot_maps_exact"] and checks["mlp_within_tol"] and
                             all(v["ok"] for v in checks.get("sampled", {}).values()))
         out["parity"] = checks
+    return out
+
+
+def pinned_host_summary(main_name, host, big, extra) -> dict | None:
+    """The end-to-end rate of the decode step with the storage tier in pinned
+    host memory and np_stage_rows staging (the step's stated tier for 13B and
+    70B, where only part of the rows fits the resident buffer), per
+    configuration: tokens/s of the faster np_stage_rows mode, its staging
+    rate and the same run's pinned-copy peak.  PCIe-inclusive; the headline
+    `value` keeps the storage tier in HBM."""
+    rows = {}
+    for name, h in [(main_name, host)] + [(n, (v or {}).get("host_tier"))
+                                          for n, v in {**big, **extra}.items()]:
+        if h:
+            rows[name] = {"tok_s": h["tok_s"], "staging_GBps": h["staging_GBps"],
+                          "h2d_peak_GBps": h["h2d_peak_GBps"], "mode": h["mode"]}
+            for key in ("layers", "ms_per_layer", "note"):
+                if key in h:
+                    rows[name][key] = h[key]
+    return rows or None
+
+
+def cpu_detail() -> dict:
+    """Family, model, stepping, clock and cache of the first host CPU (from
+    /proc/cpuinfo), and the CPUs this process may run on."""
+    keys = {"cpu family": "family", "model": "model", "stepping": "stepping",
+            "cpu MHz": "mhz", "cache size": "cache"}
+    out = {}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if not line.strip():
+                    break
+                k, _, v = line.partition(":")
+                if k.strip() in keys:
+                    out[keys[k.strip()]] = v.strip()
+    except OSError:
+        pass
+    if hasattr(os, "sched_getaffinity"):
+        out["usable_cpus"] = len(os.sched_getaffinity(0))
     return out
 
 
@@ -993,6 +1205,8 @@ def main():
                 "p99": round(float(np.percentile(step_list, 99)), 2), "tokens": len(step_list),
                 "note": "device time per token, np_predict start to last np_sparse_mlp end"}
     log(f"[bench] np_sparse_mlp: {mlp_us:.2f} us per call")
+    floor = mlp_dispatch_floor(pipe)
+    log(f"[bench] np_sparse_mlp with no rows: {floor}")
     err = pipe.device_error()
     if err:
         log(f"[bench] device error word {err:#x}")
@@ -1006,9 +1220,8 @@ def main():
     bd, per_tok, ids = breakdown(pipe, t1, max(2, args.breakdown_steps))
     log(f"[bench] breakdown us: {bd}")
     pbytes = predict_bytes(cfg)
-    predictor = {"avg_us": bd["predict"], "bytes": pbytes,
-                 "achieved_GBps": round(pbytes / (bd["predict"] * 1e-6) / 1e9, 1)}
-    predictor["frac"] = round(predictor["achieved_GBps"] / HBM_PEAK_GBPS, 4)
+    predictor = predictor_paths(pipe, t1, pbytes)
+    log(f"[bench] predictor: {predictor}")
     n_in = np.mean([c[:, 0].sum() for c in per_tok])
     n_hit = np.mean([c[:, 1].sum() for c in per_tok])
     rec = cfg.record_bytes
@@ -1022,26 +1235,9 @@ def main():
     # storage tier in pinned host memory: the PCIe-inclusive rate
     host = None
     if args.host_tier_steps > 0:
-        hp = DecodePipeline(cfg, tier="host", staging="memcpy", overlap=True, tokens=T,
-                            host_storage=host_storage)
-        hp.step(0)
-        for i in range(3):
-            hp.step(1 + i)
-        torch.cuda.synchronize()
-        hw, _ = timed_steps(hp, 4, args.host_tier_steps, with_mlp_events=False)
-        hg = DecodePipeline(cfg, tier="host", staging="gather", overlap=True, tokens=T,
-                            host_storage=host_storage)
-        hg.step(0)
-        for i in range(3):
-            hg.step(1 + i)
-        torch.cuda.synchronize()
-        gw, _ = timed_steps(hg, 4, args.host_tier_steps, with_mlp_events=False)
-        host = {"memcpy_staging_tok_s": round(args.host_tier_steps / hw, 2),
-                "mapped_gather_tok_s": round(args.host_tier_steps / gw, 2),
-                "note": "storage tier in pinned host memory; staging crosses the host link"}
-        host.update(staging_rates(hp, 4 + args.host_tier_steps, max(3, args.host_tier_steps // 4)))
+        host = pinned_host_run(cfg, host_storage, args.host_tier_steps, T)
+        host["note"] = "storage tier in pinned host memory; staging crosses the host link"
         log(f"[bench] host tier: {host}")
-        del hp, hg
     sweep7b = None
     if args.sweep_steps > 0 and cfg.name == "7b":
         sweep7b = sweep_run(host_storage, args.sweep_steps)
@@ -1114,7 +1310,8 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "traffic_detail": traffic_detail,
                      "bytes_per_launch": bytes_launch, "avg_launch_us": round(mlp_us, 3),
-                     "frac_of_read_ref": round(achieved / read_ref, 4)},
+                     "frac_of_read_ref": round(achieved / read_ref, 4),
+                     "empty_call": floor},
         "step_us": step_pct,
         "predictor": predictor,
         "read_ref": {"GBps": read_ref, "kernel": "torch.mv (library GEMV) over a 2 GiB [262144][4096] fp16 matrix"},
@@ -1123,6 +1320,7 @@ def main():
         "cold_start_ms": round(cold_ms, 2),
         "breakdown_us": bd,
         "delta": stats,
+        "end_to_end_pinned_host": pinned_host_summary(cfg.name, host, big, extra),
         "host_tier": host,
         "file_tier": file_tier,
         "sweep_7b": sweep7b,

@@ -357,8 +357,12 @@ class DecodePipeline:
             if self.stage_log is not None:
                 continue  # staging alone: the MLPs follow the whole staging
             for l in range(lb, le):
-                if self.overlap:
-                    main.wait_event(self.layer_ready[l])
+                # one wait per group, on its last layer's event: a group's
+                # layers land in one or two rounds, and each wait costs the
+                # main stream several microseconds (7B: 460 against 405
+                # tokens/s with a wait per layer)
+                if self.overlap and l == lb:
+                    main.wait_event(self.layer_ready[le - 1])
                 if l == 0 and mlp_block_events is not None:
                     mlp_block_events[0].record(main)
                 mlp(l)
@@ -369,9 +373,9 @@ class DecodePipeline:
                 self.side.synchronize()
             n_rec = int(self.plan_counts.view(L, 4)[:, 0].sum())
             self.stage_log.append((n_rec * cfg.record_bytes, time.perf_counter() - t0, t_call))
+            if self.overlap:  # every layer is staged: one wait
+                main.wait_event(self.layer_ready[L - 1])
             for l in range(L):
-                if self.overlap:
-                    main.wait_event(self.layer_ready[l])
                 if l == 0 and mlp_block_events is not None:
                     mlp_block_events[0].record(main)
                 mlp(l)
