@@ -228,28 +228,42 @@ def persistence_of(ids_seq):
 
 
 def breakdown(pipe, t0, steps):
-    """Per-phase device time (µs, mean over steps) from events on the main
-    stream, one phase at a time (no overlap)."""
+    """Per-phase device time (µs, median over its tokens) from events on the
+    main stream, one phase at a time (no overlap).  Even tokens run the
+    active-set selection and the delta as the step runs them, in one call
+    (np_select_delta: "select_delta"); odd tokens run them as the two calls
+    np_select and np_delta ("select", "delta"), for comparison.  Both give the
+    same results bit for bit, so the state evolves the same either way."""
+    import numpy as np
     import torch
 
     from paper_2608_22643_amd import binding as B
 
     s, cfg = pipe.shape, pipe.cfg
     L, k = cfg.layers, cfg.k
-    names = ("predict", "select", "delta", "stage", "mlp")
-    acc = {n: 0.0 for n in names}
+    acc = {}
     counts, ids = [], []
     ybytes = cfg.d_model * (4 if cfg.adtype == "f32" else 2)
+
+    def add(name, a, b):
+        acc.setdefault(name, []).append(a.elapsed_time(b) * 1e3)
+
     for i in range(steps):
         t = t0 + i
+        fused = i % 2 == 0
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
         m = pipe.main
         ev[0].record(m)
         B.np_predict(s, pipe.x_ptr(t), pipe.A, pipe.B, pipe.scores, pipe.ws, m)
         ev[1].record(m)
-        B.np_select(s, pipe.scores, pipe.mask, pipe.active_ids, pipe.ws, m)
-        ev[2].record(m)
-        B.np_delta(s, t, pipe.active_ids, pipe.state, pipe.out, pipe.ws, m)
+        if fused:
+            B.np_select_delta(s, t, pipe.scores, pipe.mask, pipe.active_ids, pipe.state,
+                              pipe.out, pipe.ws, m)
+            ev[2].record(m)
+        else:
+            B.np_select(s, pipe.scores, pipe.mask, pipe.active_ids, pipe.ws, m)
+            ev[2].record(m)
+            B.np_delta(s, t, pipe.active_ids, pipe.state, pipe.out, pipe.ws, m)
         ev[3].record(m)
         B.np_stage_gather(s, pipe.out, 0, L, pipe.storage, pipe.resident, pipe.ws, m)
         ev[4].record(m)
@@ -259,11 +273,18 @@ def breakdown(pipe, t0, steps):
                             pipe.y.data_ptr() + l * ybytes, pipe.ws, m)
         ev[5].record(m)
         torch.cuda.synchronize()
-        for j, n in enumerate(names):
-            acc[n] += ev[j].elapsed_time(ev[j + 1]) * 1e3
+        add("predict", ev[0], ev[1])
+        if fused:
+            add("select_delta", ev[1], ev[3])
+        else:
+            add("select", ev[1], ev[2])
+            add("delta", ev[2], ev[3])
+        add("stage", ev[3], ev[4])
+        add("mlp", ev[4], ev[5])
         counts.append(delta_stats(pipe))
         ids.append(pipe.active_ids.cpu().numpy().reshape(L, k))
-    return {n: round(v / steps, 2) for n, v in acc.items()}, counts, ids
+    out = {n: round(float(np.median(v)), 2) for n, v in acc.items()}
+    return out, counts, ids
 
 
 def predictor_paths(pipe, t: int, pbytes: int, reps: int = 20) -> dict:

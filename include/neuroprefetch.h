@@ -10,6 +10,7 @@
  *   np_select      top-k of the scores -> one fixed-size active set per layer
  *   np_delta       active set vs. the GPU-resident row buffer -> incoming rows,
  *                  evicted slots, hits; updates the slot map (Sec. 3.4, eqs. 2-3)
+ *                  (np_select_delta: both in one call)
  *   np_stage_rows  incoming neuron records, storage tier -> their device slots
  *                  (np_stage_file: the storage tier in a file, read with io_uring)
  *   np_sparse_mlp  ReLU-gated MLP over the resident active rows of one layer
@@ -252,6 +253,20 @@ np_status np_select(const np_shape* shape, const float* scores, uint32_t* mask,
 np_status np_delta(const np_shape* shape, int32_t token,
                    const int32_t* active_ids, const np_state* state,
                    const np_delta_out* out, void* dev_ws, hipStream_t stream);
+
+/* np_select followed by np_delta (Sec. 3.4: the fixed-size active set and
+ * its delta against the resident set) in one call: the same arguments as the
+ * two calls, the same results bit for bit (mask, active_ids, the state and
+ * every `out` list), the same error reporting (NP_DEVERR_NAN_SCORE,
+ * NP_DEVERR_STATE).  Where the layer fits one workgroup's local memory
+ * (F <= 16384, C <= 8192, k <= 4096) both steps run in one kernel per layer
+ * that reads slot_of and neuron_of once into local memory at entry, together
+ * with the scores; other shapes run np_select's and np_delta's kernels.  With
+ * token == NP_TOKEN_AUTO a second kernel advances the step counter, as in
+ * np_delta. */
+np_status np_select_delta(const np_shape* shape, int32_t token, const float* scores,
+                          uint32_t* mask, int32_t* active_ids, const np_state* state,
+                          const np_delta_out* out, void* dev_ws, hipStream_t stream);
 
 /* Staging through pinned host memory and hipMemcpyAsync (Sec. 3.5: incoming
  * ids sorted and coalesced into contiguous ranges, one token-level batch for

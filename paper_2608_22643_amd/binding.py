@@ -33,7 +33,7 @@ EXPORTS = ("np_status_str", "np_last_error", "np_shape_check", "np_workspace_siz
            "np_stage_gather", "np_sparse_mlp", "np_centroid_select", "np_delta_n",
            "np_sparse_mlp_n", "np_dense_mlp", "np_sparse_mlp_t", "np_act_batch",
            "np_percentile", "np_threshold_active", "np_stage_file", "np_read_records",
-           "np_device_error", "np_sparse_mlp_noalloc", "np_sparse_mlp_ids")
+           "np_device_error", "np_sparse_mlp_noalloc", "np_sparse_mlp_ids", "np_select_delta")
 
 
 class NPError(RuntimeError):
@@ -99,6 +99,8 @@ def lib():
         L.np_device_error.argtypes = [vp, vp, ctypes.POINTER(i32)]
         L.np_sparse_mlp_noalloc.argtypes = [S, i32, vp, vp, vp, i32, vp, vp, vp]
         L.np_sparse_mlp_ids.argtypes = [S, i32, vp, vp, vp, vp, i32, vp, vp, vp]
+        L.np_select_delta.argtypes = [S, i32, vp, vp, vp, ctypes.POINTER(np_state),
+                                      ctypes.POINTER(np_delta_out), vp, vp]
         L.np_centroid_select.argtypes = [S, ctypes.POINTER(np_centroid_model), vp, vp, vp, vp,
                                          vp, vp, vp, vp]
         L.np_delta_n.argtypes = [S, i32, vp, vp, ctypes.POINTER(np_state),
@@ -190,6 +192,13 @@ def np_delta(shape, token: int, active_ids, state: np_state, out: np_delta_out, 
              stream=None) -> None:
     _check(lib().np_delta(ctypes.byref(shape), int(token), _p(active_ids), ctypes.byref(state),
                           ctypes.byref(out), _p(ws), _s(stream)), "np_delta")
+
+
+def np_select_delta(shape, token: int, scores, mask, active_ids, state: np_state,
+                    out: np_delta_out, ws, stream=None) -> None:
+    _check(lib().np_select_delta(ctypes.byref(shape), int(token), _p(scores), _p(mask),
+                                 _p(active_ids), ctypes.byref(state), ctypes.byref(out), _p(ws),
+                                 _s(stream)), "np_select_delta")
 
 
 def np_stage_rows(shape, plan: np_stage_plan, layer_begin: int, layer_end: int, host_storage,

@@ -187,6 +187,26 @@ np_status np_delta(const np_shape* s, int32_t token, const int32_t* ids, const n
   return delta_common("np_delta", s, token, ids, nullptr, state, out, ws, stream);
 }
 
+np_status np_select_delta(const np_shape* s, int32_t token, const float* scores, uint32_t* mask,
+                          int32_t* ids, const np_state* state, const np_delta_out* out, void* ws,
+                          hipStream_t stream) {
+  np_status st = check_shape(s);
+  if (st != NP_OK) return st;
+  if (token < NP_TOKEN_AUTO) return fail(NP_ERR_INVALID_ARG, "token %d < 0", token);
+  if (!aligned16(scores) || !aligned16(mask) || !aligned16(ids) || !aligned16(ws) || !state ||
+      !aligned16(state->slot_of) || !aligned16(state->neuron_of) ||
+      !aligned16(state->last_used))
+    return fail(NP_ERR_INVALID_ARG,
+                "np_select_delta: pointers must be non-NULL and 16-byte aligned");
+  if (!out || !aligned16(out->in_ids) || !aligned16(out->in_slots) || !aligned16(out->ev_ids) ||
+      !aligned16(out->ev_slots) || !aligned16(out->hit_ids) || !aligned16(out->active_slots) ||
+      !aligned16(out->counts))
+    return fail(NP_ERR_INVALID_ARG,
+                "np_select_delta: output lists must be non-NULL and 16-byte aligned");
+  hipError_t e = launch_select_delta(*s, token, scores, mask, ids, *state, *out, ws, stream);
+  return e == hipSuccess ? NP_OK : hip_fail(e, "np_select_delta launch");
+}
+
 np_status np_delta_n(const np_shape* s, int32_t token, const int32_t* ids, const int32_t* counts,
                      const np_state* state, const np_delta_out* out, void* ws,
                      hipStream_t stream) {

@@ -361,10 +361,14 @@ __device__ inline void raise_error(void* ws, int bits) {
 // are taken only when fewer than kk keys are nonzero (then in id order).
 // Radix select from the top over the nonzero keys on an LDS histogram of up
 // to 12 bits per pass, starting at the highest bit in which the nonzero keys
-// differ: fp32 score keys need three passes, least-recently-used keys (a
-// narrow range of token indices under a common prefix) usually one, and no
-// pass piles every key onto one histogram bin.  Then an ordered scan of the
-// ties.  hist: 4096 uint32 of LDS; scan: 3*NT/64 + 1 uint32; res: 2 uint32.
+// differ: fp32 score keys need at most three passes, least-recently-used
+// keys (a narrow range of token indices under a common prefix) usually one,
+// and no pass piles every key onto one histogram bin.  A pass whose bin holds
+// exactly the keys still needed ends the search: every key of the bin is
+// selected, so the kk-th key is the bin's smallest, found by one reduction
+// instead of further passes (fp32 scores: usually after the second pass).
+// Then an ordered scan of the ties.  hist: 4096 uint32 of LDS; scan:
+// 3*NT/64 + 1 uint32; res: 3 uint32.
 // ---------------------------------------------------------------------------
 template <int NT, int WPT>
 __device__ inline void block_select_largest(const uint32_t (&key)[WPT][32], uint32_t kk,
@@ -447,6 +451,7 @@ __device__ inline void block_select_largest(const uint32_t (&key)[WPT][32], uint
           if (c + hist[bin] >= rem) {
             res[0] = bin;
             res[1] = rem - c;
+            res[2] = hist[bin] == rem - c;  // the whole bin is needed
             break;
           }
           c += hist[bin];
@@ -457,7 +462,33 @@ __device__ inline void block_select_largest(const uint32_t (&key)[WPT][32], uint
       pmask |= (nb - 1) << shift;
       rem = res[1];
       hi = shift - 1;
+      const bool whole = res[2] != 0u && hi >= 0;
       __syncthreads();
+      if (whole) {
+        // every key of the bin is taken: the kk-th largest is its smallest
+        // key, and every key equal to it is taken too (rem: no limit)
+        uint32_t kmn = 0xFFFFFFFFu;
+#pragma unroll
+        for (int i = 0; i < WPT; ++i)
+#pragma unroll
+          for (int b = 0; b < 32; ++b) {
+            const uint32_t kv = key[i][b];
+            if (kv != 0u && (kv & pmask) == prefix && kv < kmn) kmn = kv;
+          }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+          const uint32_t c = __shfl_xor(kmn, off, WAVE);
+          kmn = c < kmn ? c : kmn;
+        }
+        if (lane == 0) scan[w] = kmn;
+        __syncthreads();
+        kmn = scan[0];
+        for (int i = 1; i < NW; ++i) kmn = scan[i] < kmn ? scan[i] : kmn;
+        __syncthreads();  // scan is reused below
+        prefix = kmn;
+        rem = 0xFFFFFFFFu;
+        break;
+      }
     }
   }
   // prefix is the kk-th largest key; take all larger keys and the first `rem`

@@ -61,6 +61,9 @@ hipError_t launch_select(const np_shape& s, const float* scores, uint32_t* mask,
 hipError_t launch_delta(const np_shape& s, int32_t token, const int32_t* active_ids,
                         const np_state& st, const np_delta_out& out, void* ws,
                         hipStream_t stream, const int32_t* active_counts = nullptr);
+hipError_t launch_select_delta(const np_shape& s, int32_t token, const float* scores,
+                               uint32_t* mask, int32_t* active_ids, const np_state& st,
+                               const np_delta_out& out, void* ws, hipStream_t stream);
 hipError_t launch_centroid_logits(const np_shape& s, const np_centroid_model& m,
                                   const void* feat, float* logits, hipStream_t stream);
 hipError_t launch_centroid_active(const np_shape& s, const np_centroid_model& m,

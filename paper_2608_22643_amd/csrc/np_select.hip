@@ -4,6 +4,8 @@
 // that set membership, ordering and compaction are bit operations, popcounts
 // and workgroup prefix sums.  Both share the radix k-selection primitive of
 // np_device.hpp (top-k of the scores; least-recently-used victims).
+#include <stdlib.h>
+
 #include "np_device.hpp"
 
 namespace np {
@@ -21,24 +23,13 @@ __device__ inline uint32_t score_key(float f, bool* nan) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// One workgroup of NT threads per layer; thread t owns id words
-// [t*WPT, t*WPT+WPT).  V4: the layer's scores are 16-byte aligned (F a
-// multiple of 4) and are read as float4.
-template <int NT, int WPT, bool V4>
-__global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ scores,
-                                                    uint32_t* __restrict__ mask,
-                                                    int32_t* __restrict__ active_ids, int F,
-                                                    int k, void* ws) {
-  __shared__ uint32_t hist[4096];
-  __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
-  __shared__ uint32_t res[2];
-  const int l = blockIdx.x, tid = threadIdx.x;
-  const int words = (F + 31) / 32;
-  const float* s = scores + (size_t)l * F;
-  // Loads are unconditional (clamped index) so that all of them are in
-  // flight together; the range test only picks the key.
-  uint32_t key[WPT][32];
-  bool nan = false;
+// Keys of thread tid's id words [tid*WPT, tid*WPT+WPT) of one layer's
+// scores (0 past F).  Loads are unconditional (clamped index) so that all of
+// them are in flight together; the range test only picks the key.  V4: the
+// layer's scores are 16-byte aligned (F a multiple of 4) and read as float4.
+template <int WPT, bool V4>
+__device__ inline void load_score_keys(const float* __restrict__ s, int F, int tid,
+                                       uint32_t (&key)[WPT][32], bool* nan) {
   if (32 * WPT * tid < F) {
 #pragma unroll
     for (int w = 0; w < WPT; ++w) {
@@ -61,7 +52,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ sc
       }
 #pragma unroll
       for (int b = 0; b < 32; ++b) {
-        const uint32_t kv = score_key(v[b], &nan);
+        const uint32_t kv = score_key(v[b], nan);
         key[w][b] = (32 * word + b < F) ? kv : 0u;
       }
     }
@@ -71,68 +62,97 @@ __global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ sc
 #pragma unroll
       for (int b = 0; b < 32; ++b) key[w][b] = 0u;
   }
-  if (nan) raise_error(ws, NP_DEVERR_NAN_SCORE);
-  uint32_t sel[WPT];
-  block_select_largest<NT, WPT>(key, (uint32_t)k, sel, hist, scan, res);
+}
+
+// The selected words of one layer out: the mask, and the ids in ascending
+// order (a workgroup prefix sum of the words' popcounts) to `ids` and, when
+// non-null, to `ids_lds` as well.
+template <int NT, int WPT>
+__device__ inline void write_selection(const uint32_t (&sel)[WPT], int tid, int words, int k,
+                                       uint32_t* __restrict__ mask_l, int32_t* __restrict__ ids,
+                                       int32_t* ids_lds, uint32_t* scan) {
   uint32_t cnt = 0;
 #pragma unroll
   for (int w = 0; w < WPT; ++w) cnt += __builtin_popcount(sel[w]);
   uint32_t tot;
   uint32_t pos = block_excl_scan<NT>(cnt, scan, &tot);
-  int32_t* ids = active_ids + (size_t)l * k;
 #pragma unroll
   for (int w = 0; w < WPT; ++w) {
     const int word = tid * WPT + w;
-    if (word < words) mask[(size_t)l * words + word] = sel[w];
+    if (word < words) mask_l[word] = sel[w];
     uint32_t bits = sel[w];
     while (bits) {
       const int b = __builtin_ctz(bits);
       bits &= bits - 1;
-      if (pos < (uint32_t)k) ids[pos] = 32 * word + b;
+      if (pos < (uint32_t)k) {
+        ids[pos] = 32 * word + b;
+        if (ids_lds) ids_lds[pos] = 32 * word + b;
+      }
       ++pos;
     }
   }
 }
 
-// One workgroup per layer.  Thread t owns: actives j in [t*JPT, t*JPT+JPT),
-// id words [t*WPT, t*WPT+WPT) and slot words [t*spt, t*spt+spt), so every
-// list below comes out in ascending order from a prefix sum in thread order.
+// One workgroup of NT threads per layer; thread t owns id words
+// [t*WPT, t*WPT+WPT).
+template <int NT, int WPT, bool V4>
+__global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ scores,
+                                                    uint32_t* __restrict__ mask,
+                                                    int32_t* __restrict__ active_ids, int F,
+                                                    int k, void* ws) {
+  __shared__ uint32_t hist[4096];
+  __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
+  __shared__ uint32_t res[3];
+  const int l = blockIdx.x, tid = threadIdx.x;
+  const int words = (F + 31) / 32;
+  uint32_t key[WPT][32];
+  bool nan = false;
+  load_score_keys<WPT, V4>(scores + (size_t)l * F, F, tid, key, &nan);
+  if (nan) raise_error(ws, NP_DEVERR_NAN_SCORE);
+  uint32_t sel[WPT];
+  block_select_largest<NT, WPT>(key, (uint32_t)k, sel, hist, scan, res);
+  write_selection<NT, WPT>(sel, tid, words, k, mask + (size_t)l * words,
+                           active_ids + (size_t)l * k, nullptr, scan);
+}
+
+// Limits of the fused selection + delta kernel (below): one id word per
+// thread at 512 threads, and the layer's slot_of and neuron_of in LDS.
+constexpr int SD_NT = 512;
+constexpr int SD_MAX_F = 32 * SD_NT;  // 16384
+constexpr int SD_MAX_C = 8192;
+constexpr int SD_MAX_K = 4096;
+constexpr int SD_PF = SD_MAX_F / SD_NT;  // slot_of loads per thread
+constexpr int SD_QF = SD_MAX_C / SD_NT;  // neuron_of loads per thread
+
+// The delta of one layer, run by all NT threads of its workgroup.  Thread t
+// owns: actives j in [t*JPT, t*JPT+JPT), id words [t*WPT, t*WPT+WPT) and slot
+// words [t*spt, t*spt+spt), so every list below comes out in ascending order
+// from a prefix sum in thread order.
+//   A: the layer's active ids (na of them, ascending); Pr, Qr: its slot_of
+//   and neuron_of as they were at entry, read from global memory or from
+//   copies in LDS; P, Q, U: the global slot_of, neuron_of and last_used,
+//   which the delta updates (Pr and Qr may be P and Q themselves: no
+//   restrict, and a thread reads an entry before any thread writes it).
+//   LDS_STATE: Pr and Qr are in LDS, where the free-slot and residency scans
+//   run as wave-wide passes (below); V4U: U's rows are 16-byte aligned (F a
+//   multiple of 4) and the victim keys are read as int4; PRE_U: they were
+//   read earlier, into upre (thread t: last_used of its id words).
+//   amask, rmask: >= ceil(F/32) words, smask: >= ceil(C/32) words of LDS;
+//   pool: >= na entries of LDS (it may share hist's storage: it is written
+//   only after the last use of hist).
 // Every global gather of a phase is issued unconditionally (clamped index)
 // so that the phase costs one memory round trip, not one per element.
-template <int NT, int WPT, int JPT>
-__global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
-                                                        const int32_t* __restrict__ active_ids,
-                                                        int32_t* __restrict__ slot_of,
-                                                        int32_t* __restrict__ neuron_of,
-                                                        int32_t* __restrict__ last_used,
-                                                        np_delta_out out, int F, int C, int k,
-                                                        int spt, void* ws,
-                                                        const int32_t* __restrict__ counts) {
-  __shared__ uint32_t amask[2048];  // active set, bit n of the layer
-  __shared__ uint32_t smask[2048];  // slot pool: free slots, then victims' slots
-  __shared__ uint32_t rmask[2048];  // resident rows (neurons held by some slot)
-  __shared__ uint32_t hist[4096];
-  __shared__ int32_t pool[8192];    // the first nI pool slots, ascending
-  __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
-  __shared__ uint32_t res[2];
-  const int l = blockIdx.x, tid = threadIdx.x;
-  if (token == NP_TOKEN_AUTO) token = *(const int32_t*)((const char*)ws + WS_TOKEN);
+template <int NT, int WPT, int JPT, bool LDS_STATE, bool V4U, bool PRE_U>
+__device__ __attribute__((always_inline)) inline void delta_layer(int l, int32_t token, const int32_t* A, int na, bool bad_count,
+                                   const int32_t* Pr, const int32_t* Qr, int32_t* P, int32_t* Q,
+                                   int32_t* U, const uint32_t (&upre)[WPT][32],
+                                   const np_delta_out& out, int F, int C, int k, int spt,
+                                   void* ws, uint32_t* amask, uint32_t* smask, uint32_t* rmask,
+                                   uint32_t* hist, int32_t* pool, uint32_t* scan,
+                                   uint32_t* res) {
+  const int tid = threadIdx.x, lane = tid & (WAVE - 1), wv = tid / WAVE;
   const int idwords = (F + 31) / 32, slotwords = (C + 31) / 32;
-  int32_t* P = slot_of + (size_t)l * F;
-  int32_t* Q = neuron_of + (size_t)l * C;
-  int32_t* U = last_used + (size_t)l * F;
-  const int32_t* A = active_ids + (size_t)l * k;
   const size_t lo = (size_t)l * k;
-  // active neurons of this layer: k, or a device count in [0, k]
-  int na = k;
-  bool bad_count = false;
-  if (counts) {
-    na = counts[l];
-    if (na < 0 || na > k) {
-      bad_count = true;
-      na = na < 0 ? 0 : k;
-    }
-  }
 
   for (int i = tid; i < idwords; i += NT) {
     amask[i] = 0;
@@ -150,11 +170,11 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
     const bool ok = nj[q] >= 0 && nj[q] < F;  // else not a neuron id: counted as a miss
     if (tid * JPT + q < na) bad |= !ok;
     if (!ok) nj[q] = -1;
-    pj[q] = P[nj[q] >= 0 ? nj[q] : 0];
+    pj[q] = Pr[nj[q] >= 0 ? nj[q] : 0];
   }
   int qb[JPT];  // a hit's slot must hold it
 #pragma unroll
-  for (int q = 0; q < JPT; ++q) qb[q] = Q[(pj[q] >= 0 && pj[q] < C) ? pj[q] : 0];
+  for (int q = 0; q < JPT; ++q) qb[q] = Qr[(pj[q] >= 0 && pj[q] < C) ? pj[q] : 0];
 #pragma unroll
   for (int q = 0; q < JPT; ++q) {
     const int j = tid * JPT + q;
@@ -179,12 +199,41 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
   // 2. free slots and resident rows, and a consistency check of the slot
   //    map: a used slot's neuron must map back to it
   uint32_t nfree_local = 0;
+  if constexpr (LDS_STATE) {
+    // wave-wide passes over the slots: lane i takes slot base + i of 64
+    // consecutive ones, a ballot gives two words of free slots; a used
+    // slot's neuron must map back to it.
+    static_assert(NT == SD_NT, "the LDS path runs at SD_NT threads");
+    constexpr int NS = SD_MAX_C / SD_NT;
+    // the ballots stay in registers: lane 2j + h keeps word h of pass j and
+    // stores it after the loop.  A used slot whose neuron maps back to it
+    // marks that neuron resident.
+    uint32_t word = 0;
+    const int passes = (C - wv * WAVE + NT - 1) / NT;  // this wave's passes (<= NS)
+#pragma unroll 4
+    for (int j = 0; j < passes; ++j) {
+      const int sl = wv * WAVE + j * NT + lane;
+      const int qv = Qr[min(sl, C - 1)];
+      const int back = Pr[(uint32_t)qv < (uint32_t)F ? qv : 0];
+      const bool in = sl < C, used = in & (qv != -1);
+      const bool pair = ((uint32_t)qv < (uint32_t)F) & (back == sl);
+      bad |= used & !pair;
+      if (used & pair) atomicOr(&rmask[qv >> 5], 1u << (qv & 31));
+      const uint64_t fm = __ballot(in & (qv == -1));
+      word = lane == 2 * j ? (uint32_t)fm : (lane == 2 * j + 1 ? (uint32_t)(fm >> 32) : word);
+      nfree_local += lane == 0 ? __popcll(fm) : 0;
+    }
+    {
+      const int wi = 2 * wv + (NT / 32) * (lane / 2) + (lane & 1);
+      if (lane < 2 * NS && wi < slotwords) smask[wi] = word;
+    }
+  } else
   for (int q = 0; q < spt; ++q) {
     const int sw = tid * spt + q;
     if (sw >= slotwords) break;
     int qn[32];
 #pragma unroll
-    for (int b = 0; b < 32; ++b) qn[b] = Q[min(32 * sw + b, C - 1)];
+    for (int b = 0; b < 32; ++b) qn[b] = Qr[min(32 * sw + b, C - 1)];
     uint32_t bits = 0;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {  // halves: 16 back-gathers in flight
@@ -192,7 +241,7 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int qv = qn[16 * h + i];
-        back[i] = P[(qv >= 0 && qv < F) ? qv : 0];
+        back[i] = Pr[(qv >= 0 && qv < F) ? qv : 0];
       }
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
@@ -227,8 +276,24 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
 #pragma unroll
       for (int w = 0; w < WPT; ++w) {
         const int word = tid * WPT + w;
+        if constexpr (PRE_U) {
 #pragma unroll
-        for (int b = 0; b < 32; ++b) key[w][b] = (uint32_t)U[min(32 * word + b, F - 1)];
+          for (int b = 0; b < 32; ++b) key[w][b] = upre[w][b];
+        } else if constexpr (V4U) {
+          const int4* u4 = reinterpret_cast<const int4*>(U);
+          const int last = F / 4 - 1;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int4 q = u4[min(8 * word + i, last)];
+            key[w][4 * i] = (uint32_t)q.x;
+            key[w][4 * i + 1] = (uint32_t)q.y;
+            key[w][4 * i + 2] = (uint32_t)q.z;
+            key[w][4 * i + 3] = (uint32_t)q.w;
+          }
+        } else {
+#pragma unroll
+          for (int b = 0; b < 32; ++b) key[w][b] = (uint32_t)U[min(32 * word + b, F - 1)];
+        }
         // resident, not active, and inside the layer (rmask has no bits past F)
         const uint32_t cm = word < idwords ? (rmask[word] & ~amask[word]) : 0u;
 #pragma unroll
@@ -250,9 +315,28 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
     for (int w = 0; w < WPT; ++w) {
       if (!vsel[w]) continue;
       const int word = tid * WPT + w;
+      if constexpr (LDS_STATE) {  // LDS: only the victims' entries, one by one
+        uint32_t bits = vsel[w];
+        while (bits) {
+          const int b = __builtin_ctz(bits);
+          bits &= bits - 1;
+          const int n = 32 * word + b, old = Pr[n];
+          if (old < 0 || old >= C || vpos >= (uint32_t)k) {  // only with a corrupted state
+            bad = 1;
+            continue;
+          }
+          out.ev_ids[lo + vpos] = n;
+          out.ev_slots[lo + vpos] = old;
+          ++vpos;
+          atomicOr(&smask[old >> 5], 1u << (old & 31));
+          Q[old] = -1;
+          P[n] = -1;
+        }
+        continue;
+      }
       int pn[32];
 #pragma unroll
-      for (int b = 0; b < 32; ++b) pn[b] = P[min(32 * word + b, F - 1)];
+      for (int b = 0; b < 32; ++b) pn[b] = Pr[min(32 * word + b, F - 1)];
 #pragma unroll
       for (int b = 0; b < 32; ++b) {
         if (!((vsel[w] >> b) & 1u)) continue;
@@ -332,6 +416,130 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
     out.counts[(size_t)l * 4 + 2] = (int32_t)m;
     out.counts[(size_t)l * 4 + 3] = (int32_t)(nI - m);
   }
+}
+
+// np_delta: one workgroup per layer, the state read from global memory.
+template <int NT, int WPT, int JPT>
+__global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
+                                                   const int32_t* __restrict__ active_ids,
+                                                   int32_t* __restrict__ slot_of,
+                                                   int32_t* __restrict__ neuron_of,
+                                                   int32_t* __restrict__ last_used,
+                                                   np_delta_out out, int F, int C, int k,
+                                                   int spt, void* ws,
+                                                   const int32_t* __restrict__ counts) {
+  __shared__ uint32_t amask[2048];  // active set, bit n of the layer
+  __shared__ uint32_t smask[2048];  // slot pool: free slots, then victims' slots
+  __shared__ uint32_t rmask[2048];  // resident rows (neurons held by some slot)
+  __shared__ uint32_t hist[4096];
+  __shared__ int32_t pool[8192];    // the first nI pool slots, ascending
+  __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
+  __shared__ uint32_t res[3];
+  const int l = blockIdx.x;
+  if (token == NP_TOKEN_AUTO) token = *(const int32_t*)((const char*)ws + WS_TOKEN);
+  int32_t* P = slot_of + (size_t)l * F;
+  int32_t* Q = neuron_of + (size_t)l * C;
+  // active neurons of this layer: k, or a device count in [0, k]
+  int na = k;
+  bool bad_count = false;
+  if (counts) {
+    na = counts[l];
+    if (na < 0 || na > k) {
+      bad_count = true;
+      na = na < 0 ? 0 : k;
+    }
+  }
+  const uint32_t none[WPT][32] = {};
+  delta_layer<NT, WPT, JPT, false, false, false>(l, token, active_ids + (size_t)l * k, na,
+                                                 bad_count, P, Q, P, Q, last_used + (size_t)l * F,
+                                                 none, out, F, C, k, spt, ws, amask, smask, rmask,
+                                                 hist, pool, scan, res);
+}
+
+// np_select followed by np_delta in one workgroup per layer.  At entry every
+// thread issues all of its loads at once: the scores of its id word (the
+// selection keys), the last_used values of the same word (the victim keys)
+// and a share of the layer's slot_of and neuron_of, which go to LDS; the delta then finds every slot and back-reference there instead
+// of in global memory, scans the slots and neurons wave by wave, and needs no
+// second launch.  For F <= SD_MAX_F, C <= SD_MAX_C and
+// k <= SD_MAX_K (one id word per thread at 512 threads); the slot pool of the
+// delta shares the selection's histogram.
+
+template <int JPT, bool V4>
+__global__ __launch_bounds__(SD_NT) void select_delta_kernel(
+    const float* __restrict__ scores, uint32_t* __restrict__ mask,
+    int32_t* __restrict__ active_ids, int32_t token, int32_t* __restrict__ slot_of,
+    int32_t* __restrict__ neuron_of, int32_t* __restrict__ last_used, np_delta_out out, int F,
+    int C, int k, void* ws) {
+  constexpr int NT = SD_NT;
+  __shared__ __attribute__((aligned(16))) int32_t Ps[SD_MAX_F];  // slot_of of the layer at entry
+  __shared__ int32_t Qs[SD_MAX_C];  // neuron_of of the layer at entry
+  __shared__ int32_t ids_s[SD_MAX_K];
+  __shared__ uint32_t amask[SD_MAX_F / 32], rmask[SD_MAX_F / 32], smask[SD_MAX_C / 32];
+  __shared__ uint32_t hist[4096];  // both selections; then the delta's slot pool
+  __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
+  __shared__ uint32_t res[3];
+  const int l = blockIdx.x, tid = threadIdx.x;
+  if (token == NP_TOKEN_AUTO) token = *(const int32_t*)((const char*)ws + WS_TOKEN);
+  const int words = (F + 31) / 32;
+  int32_t* P = slot_of + (size_t)l * F;
+  int32_t* Q = neuron_of + (size_t)l * C;
+  int32_t* U = last_used + (size_t)l * F;
+  // all loads first: slot_of (int4 when its rows are 16-byte aligned), the
+  // selection keys, neuron_of and the victim keys' last_used values.  Loads
+  // complete in order: slot_of goes to LDS as soon as it is in, the
+  // selection waits only for the keys, and neuron_of goes to LDS after it.
+  // (A clamped index loads and stores the last entry again, with the same
+  // value: the loops have no branch, so they unroll and stay in registers.)
+  constexpr int PV = V4 ? SD_PF / 4 : SD_PF;
+  int4 pv4[V4 ? PV : 1];
+  int pv1[V4 ? 1 : PV];
+  if constexpr (V4) {
+    const int4* P4 = reinterpret_cast<const int4*>(P);
+#pragma unroll
+    for (int i = 0; i < PV; ++i) pv4[i] = P4[min(tid + NT * i, F / 4 - 1)];
+  } else {
+#pragma unroll
+    for (int i = 0; i < PV; ++i) pv1[i] = P[min(tid + NT * i, F - 1)];
+  }
+  uint32_t key[1][32];
+  bool nan = false;
+  load_score_keys<1, V4>(scores + (size_t)l * F, F, tid, key, &nan);
+  int qv[SD_QF];
+#pragma unroll
+  for (int i = 0; i < SD_QF; ++i) qv[i] = Q[min(tid + NT * i, C - 1)];
+  uint32_t ukey[1][32] = {};  // with unaligned rows the delta reads them itself
+  if constexpr (V4) {
+    const int4* u4 = reinterpret_cast<const int4*>(U);
+    const int last = F / 4 - 1;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int4 q = u4[min(8 * tid + i, last)];
+      ukey[0][4 * i] = (uint32_t)q.x;
+      ukey[0][4 * i + 1] = (uint32_t)q.y;
+      ukey[0][4 * i + 2] = (uint32_t)q.z;
+      ukey[0][4 * i + 3] = (uint32_t)q.w;
+    }
+  }
+  if constexpr (V4) {
+#pragma unroll
+    for (int i = 0; i < PV; ++i)
+      reinterpret_cast<int4*>(Ps)[min(tid + NT * i, F / 4 - 1)] = pv4[i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < PV; ++i) Ps[min(tid + NT * i, F - 1)] = pv1[i];
+  }
+  if (nan) raise_error(ws, NP_DEVERR_NAN_SCORE);
+  uint32_t sel[1];
+  block_select_largest<NT, 1>(key, (uint32_t)k, sel, hist, scan, res);
+#pragma unroll
+  for (int i = 0; i < SD_QF; ++i) Qs[min(tid + NT * i, C - 1)] = qv[i];
+  write_selection<NT, 1>(sel, tid, words, k, mask + (size_t)l * words,
+                         active_ids + (size_t)l * k, ids_s, scan);
+  __syncthreads();  // ids_s, Ps and Qs complete
+  delta_layer<NT, 1, JPT, true, V4, V4>(l, token, ids_s, k, false, Ps, Qs, P, Q, U, ukey, out, F,
+                                        C, k, 1, ws, amask, smask, rmask, hist, (int32_t*)hist,
+                                        scan, res);
 }
 
 // Centroid choice and the intersected active set (Sec. 3.3-3.4), one
@@ -503,6 +711,33 @@ hipError_t launch_delta(const np_shape& s, int32_t token, const int32_t* active_
   if (words <= 512 && s.k <= 2048) e = delta_w<512, 1>(s, token, active_ids, st, out, ws, stream, counts);
   else if (words <= 1024) e = delta_w<1024, 1>(s, token, active_ids, st, out, ws, stream, counts);
   else e = delta_w<1024, 2>(s, token, active_ids, st, out, ws, stream, counts);
+  if (e != hipSuccess || token != NP_TOKEN_AUTO) return e;
+  hipLaunchKernelGGL(token_advance_kernel, dim3(1), dim3(64), 0, stream, ws);
+  return hipGetLastError();
+}
+
+// np_select then np_delta: the fused kernel where the layer fits it (unless
+// NP_SELECT_DELTA_FUSED=0), else the two kernels.
+hipError_t launch_select_delta(const np_shape& s, int32_t token, const float* scores,
+                               uint32_t* mask, int32_t* active_ids, const np_state& st,
+                               const np_delta_out& out, void* ws, hipStream_t stream) {
+  const char* env = getenv("NP_SELECT_DELTA_FUSED");
+  const bool fused = !(env && env[0] == '0') && s.d_ffn <= SD_MAX_F &&
+                     s.capacity <= SD_MAX_C && s.k <= SD_MAX_K;
+  if (!fused) {
+    hipError_t e = launch_select(s, scores, mask, active_ids, ws, stream);
+    if (e != hipSuccess) return e;
+    return launch_delta(s, token, active_ids, st, out, ws, stream, nullptr);
+  }
+  const bool v4 = s.d_ffn % 4 == 0;
+  const int jpt = (s.k + SD_NT - 1) / SD_NT;
+#define NP_SD_CASE(J)                                                                            do {                                                                                             if (v4)                                                                                          hipLaunchKernelGGL((select_delta_kernel<J, true>), dim3(s.layers), dim3(SD_NT), 0,                                stream, scores, mask, active_ids, token, st.slot_of, st.neuron_of,                             st.last_used, out, s.d_ffn, s.capacity, s.k, ws);                         else                                                                                             hipLaunchKernelGGL((select_delta_kernel<J, false>), dim3(s.layers), dim3(SD_NT), 0,                               stream, scores, mask, active_ids, token, st.slot_of, st.neuron_of,                             st.last_used, out, s.d_ffn, s.capacity, s.k, ws);                       } while (0)
+  if (jpt <= 1) NP_SD_CASE(1);
+  else if (jpt <= 2) NP_SD_CASE(2);
+  else if (jpt <= 4) NP_SD_CASE(4);
+  else NP_SD_CASE(8);
+#undef NP_SD_CASE
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess || token != NP_TOKEN_AUTO) return e;
   hipLaunchKernelGGL(token_advance_kernel, dim3(1), dim3(64), 0, stream, ws);
   return hipGetLastError();

@@ -270,8 +270,8 @@ class DecodePipeline:
                          self.ws, main)
         else:
             B.np_predict(s, x_ptr, self.A, self.B, self.scores, self.ws, main)
-            B.np_select(s, self.scores, self.mask, self.active_ids, self.ws, main)
-            B.np_delta(s, token, self.active_ids, self.state, self.out, self.ws, main)
+            B.np_select_delta(s, token, self.scores, self.mask, self.active_ids, self.state,
+                              self.out, self.ws, main)
         ready = None  # ready[l]: the event layer l's MLP waits for
         slots = self.lists["active_slots"]
         ybytes = cfg.d_model * W.ITEMSIZE[cfg.adtype]

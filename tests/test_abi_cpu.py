@@ -28,7 +28,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 24, names
+    assert len(names) == 25, names
     for n in names:
         assert hasattr(lib, n), f"missing export {n}"
     assert set(names) == set(B.EXPORTS)
@@ -94,6 +94,18 @@ def test_null_and_misaligned_pointers_rejected(lib):
     assert e.value.status == B.NP_ERR_INVALID_ARG
     with pytest.raises(B.NPError) as e:
         B.np_delta(shape, -2, 16, B.np_state(16, 16, 16), B.np_delta_out(*([16] * 7)), 16, None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    with pytest.raises(B.NPError) as e:  # np_select_delta: token below NP_TOKEN_AUTO
+        B.np_select_delta(shape, -2, 16, 16, 16, B.np_state(16, 16, 16),
+                          B.np_delta_out(*([16] * 7)), 16, None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    with pytest.raises(B.NPError) as e:  # np_select_delta: misaligned scores
+        B.np_select_delta(shape, 0, 18, 16, 16, B.np_state(16, 16, 16),
+                          B.np_delta_out(*([16] * 7)), 16, None)
+    assert e.value.status == B.NP_ERR_INVALID_ARG
+    with pytest.raises(B.NPError) as e:  # np_select_delta: a NULL output list
+        B.np_select_delta(shape, 0, 16, 16, 16, B.np_state(16, 16, 16),
+                          B.np_delta_out(*([16] * 6), None), 16, None)
     assert e.value.status == B.NP_ERR_INVALID_ARG
     with pytest.raises(B.NPError) as e:
         B.np_stage_gather(shape, B.np_delta_out(*([16] * 7)), 3, 2, 16, 16, 16, None)
