@@ -45,11 +45,11 @@ HBM_PEAK_GBPS = 8000.0
 MLP_COUNTERS = {
     "config": "7b",
     "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
-    "sha256": "f35fb90947eabb9517382fc11d2fb20c65d8db572219326e4410c24c079f93cc"
-              "299ac6b7372e8888986a5f931b9562140f84d9a02aa00e03289ad3bb3c43fab9",
-    "fetch_kib": {"rows": 19927.0, "reduce": 1678.5},
-    "write_kib": {"rows": 3374.1, "reduce": 8.0},
-    "copy_fetch_kib": 131087.8, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+    "sha256": "1a66cf3d0105bd0d9c4855f481fee9c9a79f3c6ca78b6985abbe9af97c537ec4"
+              "bfd84964fb66a6cf5e28948cb78637cddabc402c69d7a8a6c996726a88dffbd9",
+    "fetch_kib": {"rows": 19930.0, "reduce": 1681.5},
+    "write_kib": {"rows": 3374.4, "reduce": 8.0},
+    "copy_fetch_kib": 131088.4, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
 }
 
 
@@ -367,7 +367,8 @@ def staging_rates(pipe, t0: int, steps: int) -> dict:
             "h2d_peak_GBps": round(h2d_peak_gbps(), 2)}
 
 
-def pinned_host_run(cfg, host_storage, steps: int, tokens: int, t0: int = 0) -> dict:
+def pinned_host_run(cfg, host_storage, steps: int, tokens: int, t0: int = 0,
+                    fill: int = 0) -> dict:
     """The spec step with the storage tier in pinned host memory:
     np_predict, np_select, np_delta, np_stage_rows (the plan read on the host,
     records packed into pinned staging and sent with hipMemcpyAsync, then
@@ -377,7 +378,9 @@ def pinned_host_run(cfg, host_storage, steps: int, tokens: int, t0: int = 0) -> 
     same tier (np_stage_gather, the GPU reading pinned memory over the host
     link).  Reports tokens/s of each, the staging rate of np_stage_rows alone
     against a 1 GiB pinned hipMemcpyAsync of the same run, and the host's
-    share (packing and enqueueing)."""
+    share (packing and enqueueing).  Each pipeline starts cold and runs 4 +
+    `fill` untimed tokens first (with fill, the resident buffer is full and
+    every timed token evicts)."""
     import torch
 
     from paper_2608_22643_amd.pipeline import DecodePipeline
@@ -389,13 +392,13 @@ def pinned_host_run(cfg, host_storage, steps: int, tokens: int, t0: int = 0) -> 
               ("_overlap" if overlap else "")
         p = DecodePipeline(cfg, tier="host", staging=staging, overlap=overlap, tokens=tokens,
                            host_storage=host_storage)
-        for i in range(4):
+        for i in range(4 + fill):
             p.step(t0 + i)
         torch.cuda.synchronize()
-        wall, _ = timed_steps(p, t0 + 4, steps, with_mlp_events=False)
+        wall, _ = timed_steps(p, t0 + 4 + fill, steps, with_mlp_events=False)
         rec = {"tok_s": round(steps / wall, 2), "ms_per_token": round(wall * 1e3 / steps, 3)}
         if staging == "memcpy":
-            rec.update(staging_rates(p, t0 + 4 + steps, max(3, steps // 2)))
+            rec.update(staging_rates(p, t0 + 4 + fill + steps, max(3, steps // 2)))
             if best is None or rec["tok_s"] > out[best]["tok_s"]:
                 best = key
         if p.device_error():
@@ -471,7 +474,7 @@ def delta_stats(pipe):
     return c
 
 
-def hbm_config_run(name: str, steps: int) -> tuple[dict, dict]:
+def hbm_config_run(name: str, steps: int, fill: int = 0) -> tuple[dict, dict]:
     """A configuration whose storage tier, resident set and predictor all fit
     in one GPU's HBM at full size (the 70B shape: 111 GB + 39 GB + 4.5 GB):
     steps launched as the main measurement, the sparse-MLP call against the
@@ -485,7 +488,7 @@ def hbm_config_run(name: str, steps: int) -> tuple[dict, dict]:
     from paper_2608_22643_amd.pipeline import DecodePipeline
 
     cfg = W.get(name)
-    T = 4 + 2 * steps + 4 + 8 * steps + 16
+    T = 4 + fill + 2 * steps + 4 + 4 + fill + 3 * steps + 16
     t = time.perf_counter()
     # the storage tier generated once into pinned host memory: copied to HBM
     # for the HBM leg, read over the host link in the stated tier's leg
@@ -502,16 +505,16 @@ def hbm_config_run(name: str, steps: int) -> tuple[dict, dict]:
     setup_s = time.perf_counter() - t
     log(f"[bench] {name}: every tier in HBM ({torch.cuda.memory_allocated() / 1e9:.1f} GB), "
         f"generated in {setup_s:.1f} s")
-    for i in range(4):
+    for i in range(4 + fill):
         pipe.step(i)
-    wall, _ = timed_steps(pipe, 4, steps, with_mlp_events=False)
-    _, mlp_us = timed_steps(pipe, 4 + steps, steps)
+    wall, _ = timed_steps(pipe, 4 + fill, steps, with_mlp_events=False)
+    _, mlp_us = timed_steps(pipe, 4 + fill + steps, steps)
     torch.cuda.synchronize()
     counts = delta_stats(pipe)
     if pipe.device_error():
         raise RuntimeError(f"{name}: device error word {pipe.device_error():#x}")
     L, F, k, d = cfg.layers, cfg.d_ffn, cfg.k, cfg.d_model
-    last = 4 + 2 * steps - 1
+    last = 4 + fill + 2 * steps - 1
     layers = [0, L - 1]
     scores = pipe.scores.cpu().numpy().reshape(L, F)
     ids = pipe.active_ids.cpu().numpy().reshape(L, k)
@@ -550,7 +553,7 @@ def hbm_config_run(name: str, steps: int) -> tuple[dict, dict]:
             log(f"[bench] {name}: {n} layers not pinnable ({str(e).splitlines()[0]})")
             host_storage = None
     if host_storage is not None:
-        ht = pinned_host_run(host_cfg, host_storage, steps, T, 4 + 2 * steps + 4)
+        ht = pinned_host_run(host_cfg, host_storage, steps, T, 4 + fill + 2 * steps + 4, fill)
         ht["layers"] = host_cfg.layers
         ht["pinned_GB"] = round(host_cfg.storage_bytes / 1e9, 1)
         ht["ms_per_layer"] = round(1e3 / ht["tok_s"] / host_cfg.layers, 4)
@@ -562,7 +565,7 @@ def hbm_config_run(name: str, steps: int) -> tuple[dict, dict]:
     return out, sample
 
 
-def extra_config(name: str, steps: int, graph: bool, overlap: bool) -> dict:
+def extra_config(name: str, steps: int, graph: bool, overlap: bool, fill: int = 0) -> dict:
     """The same measurements, shorter, on another configuration (13B shape):
     steps with the storage tier in HBM (launched as the main measurement),
     the sparse-MLP call against the HBM roofline, and the step with the
@@ -574,7 +577,7 @@ def extra_config(name: str, steps: int, graph: bool, overlap: bool) -> dict:
     from paper_2608_22643_amd.pipeline import DecodePipeline
 
     cfg = W.get(name)
-    T = 1 + 3 + 8 * steps + 16
+    T = 4 + fill + 2 * steps + 4 + fill + 3 * steps + 16
     t = time.perf_counter()
     host_storage = torch.empty(cfg.storage_bytes, dtype=torch.uint8, pin_memory=True)
     W.fill_storage(cfg, host_storage.data_ptr())
@@ -584,14 +587,14 @@ def extra_config(name: str, steps: int, graph: bool, overlap: bool) -> dict:
                           host_storage=host_storage)
     if graph:
         pipe.capture_graph()
-        for i in range(4):
+        for i in range(4 + fill):
             pipe.step_graph(i)
-        wall = timed_graph_steps(pipe, 4, steps)
+        wall = timed_graph_steps(pipe, 4 + fill, steps)
     else:
-        for i in range(4):
+        for i in range(4 + fill):
             pipe.step(i)
-        wall, _ = timed_steps(pipe, 4, steps, with_mlp_events=False)
-    _, mlp_us = timed_steps(pipe, 4 + steps, steps)
+        wall, _ = timed_steps(pipe, 4 + fill, steps, with_mlp_events=False)
+    _, mlp_us = timed_steps(pipe, 4 + fill + steps, steps)
     counts = delta_stats(pipe)
     if pipe.device_error():
         raise RuntimeError(f"{name}: device error word {pipe.device_error():#x}")
@@ -606,7 +609,7 @@ def extra_config(name: str, steps: int, graph: bool, overlap: bool) -> dict:
            "incoming_rows_per_token": int(counts[:, 0].sum())}
     del pipe
     torch.cuda.empty_cache()
-    out["host_tier"] = pinned_host_run(cfg, host_storage, steps, T)
+    out["host_tier"] = pinned_host_run(cfg, host_storage, steps, T, 0, fill)
     del host_storage
     torch.cuda.empty_cache()
     return out
@@ -1115,6 +1118,9 @@ def main():
                     help="stage on a side stream in layer chunks (measured slower: each "
                          "cross-stream event costs about 10 us on the GPU)")
     ap.add_argument("--host-tier-steps", type=int, default=20)
+    ap.add_argument("--fill-tokens", type=int, default=64,
+                    help="untimed tokens after the warmup that fill the resident buffer, so "
+                         "that every timed token of the decode step evicts (steady state)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--breakdown-steps", type=int, default=10)
     ap.add_argument("--mlp-steps", type=int, default=50)
@@ -1160,7 +1166,9 @@ def main():
 
     cfg = W.get(args.config)
     K, Wm = args.steps, args.warmup
-    T = 1 + Wm + 2 * K + args.mlp_steps + args.breakdown_steps + 2 * args.host_tier_steps + 8
+    Fl = args.fill_tokens
+    T = (1 + Wm + Fl + 2 * K + args.mlp_steps + args.breakdown_steps +
+         4 + Fl + 2 * args.host_tier_steps + 8)
     log(f"[bench] config {cfg.name}: L'={cfg.layers} d={cfg.d_model} F={cfg.d_ffn} r={cfg.rank} "
         f"k={cfg.k} C={cfg.capacity} {cfg.wdtype}; tokens {T}")
     t = time.perf_counter()
@@ -1192,14 +1200,19 @@ def main():
         if len(gpu_ref) < keep:
             torch.cuda.synchronize()
             gpu_ref.append(capture_outputs(pipe))
+    # the resident buffer filled to steady state before the timed steps (with
+    # the default fill every timed token evicts, as in a long decode)
+    for i in range(Fl):
+        step(1 + Wm + i)
     torch.cuda.synchronize()
-    log("[bench] warmup done")
+    log(f"[bench] warmup done ({Wm} warmup + {Fl} fill tokens)")
+    t0 = 1 + Wm + Fl
     if graph:
-        wall = timed_graph_steps(pipe, 1 + Wm, K)
+        wall = timed_graph_steps(pipe, t0, K)
     else:
-        wall, _ = timed_steps(pipe, 1 + Wm, K, with_mlp_events=False)
+        wall, _ = timed_steps(pipe, t0, K, with_mlp_events=False)
     log(f"[bench] timed {K} steps ({'graph' if graph else 'eager'}): {wall * 1e3 / K:.3f} ms/step")
-    t1 = 1 + Wm + K
+    t1 = t0 + K
     other_ms = None
     if graph:  # the same steps launched one call at a time, for comparison
         ew, _ = timed_steps(pipe, t1, K, with_mlp_events=False)
@@ -1210,9 +1223,9 @@ def main():
         gp = DecodePipeline(cfg, tier="device", staging="gather", overlap=bool(args.overlap),
                             tokens=T, host_storage=host_storage)
         gp.capture_graph()
-        for i in range(1 + Wm):
+        for i in range(t0):
             gp.step_graph(i)
-        other_ms = timed_graph_steps(gp, 1 + Wm, K) * 1e3 / K
+        other_ms = timed_graph_steps(gp, t0, K) * 1e3 / K
         log(f"[bench] graph replay: {other_ms:.3f} ms/step")
         del gp
         torch.cuda.empty_cache()
@@ -1256,7 +1269,7 @@ def main():
     # storage tier in pinned host memory: the PCIe-inclusive rate
     host = None
     if args.host_tier_steps > 0:
-        host = pinned_host_run(cfg, host_storage, args.host_tier_steps, T)
+        host = pinned_host_run(cfg, host_storage, args.host_tier_steps, T, 0, Fl)
         host["note"] = "storage tier in pinned host memory; staging crosses the host link"
         log(f"[bench] host tier: {host}")
     sweep7b = None
@@ -1293,7 +1306,7 @@ def main():
     log(f"[bench] read reference: {read_ref} GB/s")
     big, big_samples = {}, []
     for name in [n for n in args.hbm_configs.split(",") if n]:
-        big[name], smp = hbm_config_run(name, args.hbm_steps)
+        big[name], smp = hbm_config_run(name, args.hbm_steps, Fl)
         big_samples.append(smp)
         log(f"[bench] {name}: {big[name]}")
     cpu = None
@@ -1304,7 +1317,7 @@ def main():
     for name in [n for n in args.extra_configs.split(",") if n]:
         del host_storage
         host_storage = None
-        extra[name] = extra_config(name, args.extra_steps, graph, bool(args.overlap))
+        extra[name] = extra_config(name, args.extra_steps, graph, bool(args.overlap), Fl)
         log(f"[bench] {name}: {extra[name]}")
     line = {
         "metric": "sparse-MLP decode tokens/sec + achieved HBM GB/s (% peak), 7B-shaped, batch 1",
@@ -1324,6 +1337,9 @@ def main():
                                f"({cfg.active_frac:.0%}), C={cfg.capacity} "
                                f"({cfg.resident_frac:.0%}), {cfg.wdtype}, batch 1",
                    "storage_tier": "HBM", "staging": "np_stage_gather",
+                   "resident_buffer": f"full: {Fl} untimed fill tokens after the warmup, so "
+                                      f"every timed token evicts" if Fl >= 64 else
+                                      f"{Fl} untimed fill tokens after the warmup",
                    "overlap": bool(args.overlap),
                    "launch": "hip_graph" if graph else "eager"},
         "roofline": {"bound": "hbm", "kernel": "np_sparse_mlp",
