@@ -376,10 +376,14 @@ np_status np_stage_gather(const np_shape* shape, const np_delta_out* out,
  * n_active = 0 gives y = 0.
  * With the environment variable NP_MLP_FUSED=1 the reduction runs inside the
  * rows kernel after a grid-wide barrier (one kernel) when the whole grid fits
- * on the device at once.  That path must not run concurrently with another
- * np_sparse_mlp on the same device; its wait is bounded and sets
- * NP_DEVERR_SPIN_LIMIT (y then undefined until np_state_reset) if the grid
- * never meets.  NP_MLP_COLSPLIT=1 selects a single kernel without partial
+ * on the device at once (an occupancy query at launch).  The barrier needs
+ * every workgroup of the grid resident together, so nothing else may hold
+ * compute units while it runs: no other np_sparse_mlp on the device, no
+ * staging kernel on another stream (np_stage_gather or np_stage_rows'
+ * scatter of an overlapped step), no kernel of the caller's.  Its wait is
+ * bounded and sets NP_DEVERR_SPIN_LIMIT (y then undefined until
+ * np_state_reset) if the grid never meets.  The default two-kernel path has
+ * no such condition.  NP_MLP_COLSPLIT=1 selects a single kernel without partial
  * sums (16-bit records, d a multiple of 512, at most 4 * d / 8 rows; each
  * workgroup owns 16 columns of y) under the same barrier and conditions.
  * dev_ws must have been zeroed or passed to np_state_reset before its first
