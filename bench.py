@@ -46,10 +46,10 @@ MLP_COUNTERS = {
     "config": "7b",
     "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
     "sha256": "1a66cf3d0105bd0d9c4855f481fee9c9a79f3c6ca78b6985abbe9af97c537ec4"
-              "bfd84964fb66a6cf5e28948cb78637cddabc402c69d7a8a6c996726a88dffbd9",
-    "fetch_kib": {"rows": 19930.0, "reduce": 1681.5},
-    "write_kib": {"rows": 3374.4, "reduce": 8.0},
-    "copy_fetch_kib": 131088.4, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+              "9e0e1f0b7a61ef93b9be1fc993a31341e591454ab40b4db720567ea646fc39f8",
+    "fetch_kib": {"rows": 19929.9, "reduce": 1681.5},
+    "write_kib": {"rows": 3374.6, "reduce": 8.0},
+    "copy_fetch_kib": 131087.9, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
 }
 
 
@@ -285,6 +285,49 @@ def breakdown(pipe, t0, steps):
         ids.append(pipe.active_ids.cpu().numpy().reshape(L, k))
     out = {n: round(float(np.median(v)), 2) for n, v in acc.items()}
     return out, counts, ids
+
+
+def select_delta_calls(pipe, t0: int, n: int = 8) -> dict:
+    """The active-set selection and the delta per call, without the event
+    overhead of timing one call: np_predict first writes the scores of n
+    consecutive tokens into n buffers, then the n tokens' np_select_delta
+    calls run back to back between two events (and, for n further tokens,
+    np_select + np_delta), queued behind a sleep kernel so that the host's
+    enqueue rate does not set the pace.  Each call advances the residency
+    state as in the decode step.  Used last on a pipeline: the tokens' rows
+    are not staged and their MLPs are not run."""
+    import numpy as np
+    import torch
+
+    from paper_2608_22643_amd import binding as B
+
+    s, cfg, m = pipe.shape, pipe.cfg, pipe.main
+    sc = torch.empty((2 * n, pipe.scores.numel()), dtype=torch.float32, device=pipe.scores.device)
+    for i in range(2 * n):
+        B.np_predict(s, pipe.x_ptr(t0 + i), pipe.A, pipe.B, sc[i], pipe.ws, m)
+    out = {}
+    for name, base in (("fused", 0), ("two_calls", n)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(m):
+            torch.cuda._sleep(2_000_000)
+        e0.record(m)
+        for i in range(n):
+            t = t0 + base + i
+            if name == "fused":
+                B.np_select_delta(s, t, sc[base + i], pipe.mask, pipe.active_ids, pipe.state,
+                                  pipe.out, pipe.ws, m)
+            else:
+                B.np_select(s, sc[base + i], pipe.mask, pipe.active_ids, pipe.ws, m)
+                B.np_delta(s, t, pipe.active_ids, pipe.state, pipe.out, pipe.ws, m)
+        e1.record(m)
+        e1.synchronize()
+        out[name + "_us"] = round(e0.elapsed_time(e1) * 1e3 / n, 2)
+    if pipe.device_error():
+        raise RuntimeError(f"select/delta calls: device error word {pipe.device_error():#x}")
+    out["tokens"] = n
+    out["note"] = ("per token, the calls of consecutive tokens back to back between two events "
+                   "(np_select_delta; np_select + np_delta)")
+    return out
 
 
 def predictor_paths(pipe, t: int, pbytes: int, reps: int = 20) -> dict:
@@ -1167,7 +1210,7 @@ def main():
     cfg = W.get(args.config)
     K, Wm = args.steps, args.warmup
     Fl = args.fill_tokens
-    T = (1 + Wm + Fl + 2 * K + args.mlp_steps + args.breakdown_steps +
+    T = (1 + Wm + Fl + 2 * K + args.mlp_steps + args.breakdown_steps + 16 +
          4 + Fl + 2 * args.host_tier_steps + 8)
     log(f"[bench] config {cfg.name}: L'={cfg.layers} d={cfg.d_model} F={cfg.d_ffn} r={cfg.rank} "
         f"k={cfg.k} C={cfg.capacity} {cfg.wdtype}; tokens {T}")
@@ -1256,6 +1299,8 @@ def main():
     pbytes = predict_bytes(cfg)
     predictor = predictor_paths(pipe, t1, pbytes)
     log(f"[bench] predictor: {predictor}")
+    sd_calls = select_delta_calls(pipe, t1 + max(2, args.breakdown_steps))
+    log(f"[bench] select/delta per call: {sd_calls}")
     n_in = np.mean([c[:, 0].sum() for c in per_tok])
     n_hit = np.mean([c[:, 1].sum() for c in per_tok])
     rec = cfg.record_bytes
@@ -1356,6 +1401,7 @@ def main():
         "sparse_mlp_tok_s": round(1e6 / (mlp_us * cfg.layers), 1),
         "cold_start_ms": round(cold_ms, 2),
         "breakdown_us": bd,
+        "select_delta_per_call": sd_calls,
         "delta": stats,
         "end_to_end_pinned_host": pinned_host_summary(cfg.name, host, big, extra),
         "host_tier": host,

@@ -363,13 +363,17 @@ __device__ inline void raise_error(void* ws, int bits) {
 // to 12 bits per pass, starting at the highest bit in which the nonzero keys
 // differ: fp32 score keys need at most three passes, least-recently-used
 // keys (a narrow range of token indices under a common prefix) usually one,
-// and no pass piles every key onto one histogram bin.  A pass whose bin holds
-// exactly the keys still needed ends the search: every key of the bin is
-// selected, so the kk-th key is the bin's smallest, found by one reduction
-// instead of further passes (fp32 scores: usually after the second pass).
-// Then an ordered scan of the ties.  hist: 4096 uint32 of LDS; scan:
-// 3*NT/64 + 1 uint32; res: 3 uint32.
+// and no pass piles every key onto one histogram bin.  Once at most
+// SEL_SMALL_CAND keys remain under the prefix, or at most 8 bits, passes
+// take 8 bits and wave 0 alone finds the bin among 256.  A pass whose bin holds exactly the keys
+// still needed ends the search: every key of the bin is selected, so the
+// kk-th key is the bin's smallest, found by one reduction instead of further
+// passes (fp32 scores: usually after the second pass).  Then an ordered scan
+// of the ties.  hist: 4096 uint32 of LDS; scan: 3*NT/64 + 1 uint32; res: 4
+// uint32.
 // ---------------------------------------------------------------------------
+constexpr uint32_t SEL_SMALL_CAND = 1024;  // at most this many keys left: 8-bit passes
+
 template <int NT, int WPT>
 __device__ inline void block_select_largest(const uint32_t (&key)[WPT][32], uint32_t kk,
                                             uint32_t (&sel)[WPT], uint32_t* hist,
@@ -421,8 +425,13 @@ __device__ inline void block_select_largest(const uint32_t (&key)[WPT][32], uint
     prefix = kmax & ~low;  // bits above hi are common to all nonzero keys
     uint32_t pmask = ~low;
     rem = kk;
+    uint32_t ncand = nz;  // keys under the prefix so far
     while (hi >= 0) {  // uniform: every thread runs the same passes
-      const int nbits = hi + 1 < 12 ? hi + 1 : 12;
+      // few keys left: an 8-bit digit, whose 256 bins wave 0 scans alone;
+      // otherwise 12 bits and a workgroup scan over the 4096 bins
+      const bool small = ncand <= SEL_SMALL_CAND || hi + 1 <= 8;
+      const int maxbits = small ? 8 : 12;
+      const int nbits = hi + 1 < maxbits ? hi + 1 : maxbits;
       const int shift = hi + 1 - nbits;
       const uint32_t nb = 1u << nbits;
       for (uint32_t i = tid; i < nb; i += NT) hist[i] = 0;
@@ -435,32 +444,61 @@ __device__ inline void block_select_largest(const uint32_t (&key)[WPT][32], uint
           if (kv != 0u && (kv & pmask) == prefix) atomicAdd(&hist[(kv >> shift) & (nb - 1)], 1u);
         }
       __syncthreads();
-      // thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top
-      const uint32_t bpt = nb >= (uint32_t)NT ? nb / NT : 1u;
-      const bool owner = (uint32_t)tid * bpt < nb;
-      const uint32_t hi_bin = nb - (uint32_t)tid * bpt;  // exclusive
-      uint32_t local = 0;
-      if (owner)
-        for (uint32_t i = 0; i < bpt; ++i) local += hist[hi_bin - 1 - i];
-      uint32_t tot;
-      const uint32_t above = block_excl_scan<NT>(local, scan, &tot);
-      if (owner && above < rem && above + local >= rem) {
-        uint32_t c = above;
-        for (uint32_t i = 0; i < bpt; ++i) {
-          const uint32_t bin = hi_bin - 1 - i;
-          if (c + hist[bin] >= rem) {
-            res[0] = bin;
-            res[1] = rem - c;
-            res[2] = hist[bin] == rem - c;  // the whole bin is needed
-            break;
+      if (small) {
+        if (w == 0) {  // lane L: bins [nb - 4(L+1), nb - 4L), from the top
+          uint32_t local = 0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int bin = (int)nb - 4 * lane - 1 - i;
+            if (bin >= 0) local += hist[bin];
           }
-          c += hist[bin];
+          const uint32_t incl = wave_incl_scan(local), above = incl - local;
+          if (above < rem && incl >= rem) {
+            uint32_t c = above;
+            for (int i = 0; i < 4; ++i) {
+              const int bin = (int)nb - 4 * lane - 1 - i;
+              const uint32_t h = hist[bin];
+              if (c + h >= rem) {
+                res[0] = (uint32_t)bin;
+                res[1] = rem - c;
+                res[2] = h == rem - c;  // the whole bin is needed
+                res[3] = h;
+                break;
+              }
+              c += h;
+            }
+          }
+        }
+      } else {
+        // thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top
+        const uint32_t bpt = nb >= (uint32_t)NT ? nb / NT : 1u;
+        const bool owner = (uint32_t)tid * bpt < nb;
+        const uint32_t hi_bin = nb - (uint32_t)tid * bpt;  // exclusive
+        uint32_t local = 0;
+        if (owner)
+          for (uint32_t i = 0; i < bpt; ++i) local += hist[hi_bin - 1 - i];
+        uint32_t tot;
+        const uint32_t above = block_excl_scan<NT>(local, scan, &tot);
+        if (owner && above < rem && above + local >= rem) {
+          uint32_t c = above;
+          for (uint32_t i = 0; i < bpt; ++i) {
+            const uint32_t bin = hi_bin - 1 - i;
+            if (c + hist[bin] >= rem) {
+              res[0] = bin;
+              res[1] = rem - c;
+              res[2] = hist[bin] == rem - c;  // the whole bin is needed
+              res[3] = hist[bin];
+              break;
+            }
+            c += hist[bin];
+          }
         }
       }
       __syncthreads();
       prefix |= res[0] << shift;
       pmask |= (nb - 1) << shift;
       rem = res[1];
+      ncand = res[3];
       hi = shift - 1;
       const bool whole = res[2] != 0u && hi >= 0;
       __syncthreads();

@@ -102,7 +102,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ sc
                                                     int k, void* ws) {
   __shared__ uint32_t hist[4096];
   __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
-  __shared__ uint32_t res[3];
+  __shared__ uint32_t res[4];
   const int l = blockIdx.x, tid = threadIdx.x;
   const int words = (F + 31) / 32;
   uint32_t key[WPT][32];
@@ -434,7 +434,7 @@ __global__ __launch_bounds__(NT) void delta_kernel(int32_t token,
   __shared__ uint32_t hist[4096];
   __shared__ int32_t pool[8192];    // the first nI pool slots, ascending
   __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
-  __shared__ uint32_t res[3];
+  __shared__ uint32_t res[4];
   const int l = blockIdx.x;
   if (token == NP_TOKEN_AUTO) token = *(const int32_t*)((const char*)ws + WS_TOKEN);
   int32_t* P = slot_of + (size_t)l * F;
@@ -478,7 +478,7 @@ __global__ __launch_bounds__(SD_NT) void select_delta_kernel(
   __shared__ uint32_t amask[SD_MAX_F / 32], rmask[SD_MAX_F / 32], smask[SD_MAX_C / 32];
   __shared__ uint32_t hist[4096];  // both selections; then the delta's slot pool
   __shared__ uint32_t scan[3 * (NT / WAVE) + 1];
-  __shared__ uint32_t res[3];
+  __shared__ uint32_t res[4];
   const int l = blockIdx.x, tid = threadIdx.x;
   if (token == NP_TOKEN_AUTO) token = *(const int32_t*)((const char*)ws + WS_TOKEN);
   const int words = (F + 31) / 32;
