@@ -26,7 +26,9 @@ constexpr size_t WS_ERR = 0;
 constexpr size_t WS_TOKEN = 64;
 constexpr size_t WS_BAR_ARRIVE = 256;  // own cache lines: polled by every workgroup
 constexpr size_t WS_BAR_GEN = 384;
+constexpr size_t WS_SEL_HINT = 512;     // per layer: the last k-th score key and a window half-width
 constexpr size_t WS_CTRL_BYTES = 4096;
+constexpr int WS_SEL_HINT_LAYERS = (int)((WS_CTRL_BYTES - WS_SEL_HINT) / 8);
 constexpr int MLP_MAX_WG = 1024;  // partial rows the workspace holds (workgroups of one call)
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }

@@ -115,6 +115,211 @@ __global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ sc
                            active_ids + (size_t)l * k, nullptr, scan);
 }
 
+// The rest of a radix select over `n` candidate keys gathered in LDS (all
+// nonzero and under `prefix`/`pmask`): 8-bit passes from bit `hi` down over
+// a histogram of 256 words at hist[0..], the bin placed by wave 0 (lane L
+// sums the 4 bins L-th from the top, a wave prefix sum finds the rem-th key).
+// Ends as block_select_largest's passes do: `prefix` the k-th key and `rem`
+// the keys equal to it still to take, or at a bin needed whole (prefix its
+// smallest key, rem no limit).  Every thread calls it.
+template <int NT>
+__device__ inline void select_candidates(const uint32_t* cand, uint32_t n, uint32_t* hist,
+                                         uint32_t* scan, uint32_t* res, int hi,
+                                         uint32_t& prefix, uint32_t& pmask, uint32_t& rem) {
+  constexpr int NW = NT / WAVE;
+  const int tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
+  while (hi >= 0) {
+    const int nbits = hi + 1 < 8 ? hi + 1 : 8;
+    const int shift = hi + 1 - nbits;
+    const uint32_t nb = 1u << nbits;
+    if ((uint32_t)tid < nb) hist[tid] = 0;
+    __syncthreads();
+    for (uint32_t c = tid; c < n; c += NT) {
+      const uint32_t kv = cand[c];
+      if ((kv & pmask) == prefix) atomicAdd(&hist[(kv >> shift) & (nb - 1)], 1u);
+    }
+    __syncthreads();
+    if (w == 0) {
+      uint32_t local = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int bin = (int)nb - 4 * lane - 1 - i;
+        if (bin >= 0) local += hist[bin];
+      }
+      const uint32_t incl = wave_incl_scan(local), above = incl - local;
+      if (above < rem && incl >= rem) {
+        uint32_t c = above;
+        for (int i = 0; i < 4; ++i) {
+          const int bin = (int)nb - 4 * lane - 1 - i;
+          const uint32_t h = hist[bin];
+          if (c + h >= rem) {
+            res[0] = (uint32_t)bin;
+            res[1] = rem - c;
+            res[2] = h == rem - c;
+            break;
+          }
+          c += h;
+        }
+      }
+    }
+    __syncthreads();
+    prefix |= res[0] << shift;
+    pmask |= (nb - 1) << shift;
+    rem = res[1];
+    hi = shift - 1;
+    const bool whole = res[2] != 0u && hi >= 0;
+    __syncthreads();  // hist and res are reused
+    if (whole) {
+      uint32_t kmn = 0xFFFFFFFFu;
+      for (uint32_t c = tid; c < n; c += NT) {
+        const uint32_t kv = cand[c];
+        if ((kv & pmask) == prefix && kv < kmn) kmn = kv;
+      }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        const uint32_t o = __shfl_xor(kmn, off, WAVE);
+        kmn = o < kmn ? o : kmn;
+      }
+      if (lane == 0) scan[w] = kmn;
+      __syncthreads();
+      kmn = scan[0];
+      for (int i = 1; i < NW; ++i) kmn = scan[i] < kmn ? scan[i] : kmn;
+      __syncthreads();
+      prefix = kmn;
+      rem = 0xFFFFFFFFu;
+      return;
+    }
+  }
+}
+
+// The k largest score keys of one layer (ties to the smaller id), as
+// block_select_largest, starting from a hint: the previous token's k-th key
+// and a window half-width, kept per layer in the workspace.  Scores change
+// little from one token to the next, so the new k-th key usually lies in
+// [key - half, key + half].  One pass counts the keys above the window and
+// the keys in it; if the k-th key is inside (fewer than k above it, at least
+// k above its lower end) and the window holds at most SEL_HINT_CAP keys,
+// those keys go to LDS and the search finishes on them alone; otherwise the
+// full radix select runs.  Either way the result is the same, and the hint
+// is updated: the new k-th key, the window halved when it held many keys,
+// quadrupled when the k-th key fell outside it.  hist: 4096 words of LDS.
+constexpr uint32_t SEL_HINT_CAP = 4096 - 256;  // candidates kept after hist's first 256 words
+constexpr uint32_t SEL_HINT_HALF0 = 1u << 20;  // first window half-width (fp32 keys: 0.125 at 1.0)
+
+template <int NT>
+__device__ inline void select_largest_hinted(const uint32_t (&key)[1][32], uint32_t kk,
+                                             uint32_t (&sel)[1], uint32_t* hist, uint32_t* scan,
+                                             uint32_t* res, uint32_t* hint) {
+  constexpr int NW = NT / WAVE;
+  const int tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
+  const uint32_t hkey = hint ? hint[0] : 0u, hhalf = hint ? hint[1] : 0u;
+  const uint32_t lo = hkey > hhalf ? hkey - hhalf : 1u;
+  const uint32_t hi_w = hkey < 0xFFFFFFFFu - hhalf ? hkey + hhalf : 0xFFFFFFFFu;
+  // nonzero keys, keys above the window, keys in it
+  uint32_t nz = 0, above = 0, inside = 0;
+#pragma unroll
+  for (int b = 0; b < 32; ++b) {
+    const uint32_t kv = key[0][b];
+    nz += kv != 0u;
+    above += kv > hi_w;
+    inside += kv >= lo && kv <= hi_w;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    nz += __shfl_xor(nz, off, WAVE);
+    above += __shfl_xor(above, off, WAVE);
+    inside += __shfl_xor(inside, off, WAVE);
+  }
+  if (lane == 0) {
+    scan[w] = nz;
+    scan[NW + w] = above;
+    scan[2 * NW + w] = inside;
+  }
+  __syncthreads();
+  nz = above = inside = 0;
+  for (int i = 0; i < NW; ++i) {
+    nz += scan[i];
+    above += scan[NW + i];
+    inside += scan[2 * NW + i];
+  }
+  __syncthreads();  // scan is reused below
+  const bool use = hkey != 0u && hhalf != 0u && kk < nz && above < kk && kk <= above + inside &&
+                   inside <= SEL_HINT_CAP;
+  uint32_t prefix = 0, rem = 0;
+  if (use) {
+    // the window's keys, in LDS after hist's first 256 words
+    uint32_t* cand = hist + 256;
+    uint32_t mine = 0;
+#pragma unroll
+    for (int b = 0; b < 32; ++b) mine += key[0][b] >= lo && key[0][b] <= hi_w;
+    uint32_t total;
+    uint32_t at = block_excl_scan<NT>(mine, scan, &total);
+#pragma unroll
+    for (int b = 0; b < 32; ++b)
+      if (key[0][b] >= lo && key[0][b] <= hi_w) cand[at++] = key[0][b];
+    // bits above the highest one in which lo and hi_w differ are common to
+    // every key of the window
+    const uint32_t diff = lo ^ hi_w;
+    const int hb = diff ? 31 - __builtin_clz(diff) : -1;
+    const uint32_t low = hb >= 0 ? (uint32_t)((2ull << hb) - 1ull) : 0u;
+    prefix = lo & ~low;
+    uint32_t pmask = ~low;
+    rem = kk - above;
+    __syncthreads();  // cand complete
+    select_candidates<NT>(cand, inside, hist, scan, res, hb, prefix, pmask, rem);
+    sel[0] = 0;
+  } else {
+    uint32_t s0[1];
+    block_select_largest<NT, 1>(key, kk, s0, hist, scan, res);
+    sel[0] = s0[0];
+  }
+  uint32_t kth = 0;  // the k-th key: the smallest selected one
+  if (use) {
+    // take every key above the k-th and the first `rem` equal ones in id order
+    uint32_t gt = 0, eq = 0;
+#pragma unroll
+    for (int b = 0; b < 32; ++b) {
+      gt |= (key[0][b] > prefix ? 1u : 0u) << b;
+      eq |= (key[0][b] == prefix ? 1u : 0u) << b;
+    }
+    uint32_t tot;
+    uint32_t before = block_excl_scan<NT>(__builtin_popcount(eq), scan, &tot);
+    while (eq && before < rem) {
+      const uint32_t lowbit = eq & (0u - eq);
+      gt |= lowbit;
+      eq ^= lowbit;
+      ++before;
+    }
+    sel[0] = gt;
+    kth = prefix;
+  } else if (hint && kk < nz) {
+    uint32_t mn = 0xFFFFFFFFu;
+#pragma unroll
+    for (int b = 0; b < 32; ++b)
+      if (((sel[0] >> b) & 1u) && key[0][b] < mn) mn = key[0][b];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const uint32_t o = __shfl_xor(mn, off, WAVE);
+      mn = o < mn ? o : mn;
+    }
+    if (lane == 0) scan[w] = mn;
+    __syncthreads();
+    kth = scan[0];
+    for (int i = 1; i < NW; ++i) kth = scan[i] < kth ? scan[i] : kth;
+    __syncthreads();
+  }
+  if (hint && tid == 0) {
+    uint32_t half = hhalf ? hhalf : SEL_HINT_HALF0;
+    if (use) {
+      if (inside > SEL_HINT_CAP / 4 && half > 1u) half >>= 1;
+    } else if (hkey != 0u && hhalf != 0u) {
+      half = half < (1u << 29) ? half << 2 : half;
+    }
+    hint[0] = kk < nz ? kth : 0u;
+    hint[1] = half;
+  }
+}
+
 // Limits of the fused selection + delta kernel (below): one id word per
 // thread at 512 threads, and the layer's slot_of and neuron_of in LDS.
 constexpr int SD_NT = 512;
@@ -210,7 +415,6 @@ __device__ __attribute__((always_inline)) inline void delta_layer(int l, int32_t
     // marks that neuron resident.
     uint32_t word = 0;
     const int passes = (C - wv * WAVE + NT - 1) / NT;  // this wave's passes (<= NS)
-#pragma unroll 4
     for (int j = 0; j < passes; ++j) {
       const int sl = wv * WAVE + j * NT + lane;
       const int qv = Qr[min(sl, C - 1)];
@@ -531,7 +735,8 @@ __global__ __launch_bounds__(SD_NT) void select_delta_kernel(
   }
   if (nan) raise_error(ws, NP_DEVERR_NAN_SCORE);
   uint32_t sel[1];
-  block_select_largest<NT, 1>(key, (uint32_t)k, sel, hist, scan, res);
+  uint32_t* hint = l < WS_SEL_HINT_LAYERS ? (uint32_t*)((char*)ws + WS_SEL_HINT) + 2 * l : nullptr;
+  select_largest_hinted<NT>(key, (uint32_t)k, sel, hist, scan, res, hint);
 #pragma unroll
   for (int i = 0; i < SD_QF; ++i) Qs[min(tid + NT * i, C - 1)] = qv[i];
   write_selection<NT, 1>(sel, tid, words, k, mask + (size_t)l * words,

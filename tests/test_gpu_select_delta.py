@@ -133,3 +133,42 @@ def test_select_delta_nan_and_corrupt_state(name):
     a, b = run_pair(cfg, seq, corrupt_at=3)
     assert B.np_device_error(b.ws) & B.NP_DEVERR_NAN_SCORE
     assert B.np_device_error(b.ws) & B.NP_DEVERR_STATE
+
+
+def test_select_delta_hint_misses_and_stale_hints():
+    """The fused kernel starts each layer's selection from the previous
+    token's k-th key (a window kept in the workspace) and falls back to the
+    full radix select when the k-th key lies outside it.  Scores that jump in
+    scale and offset from token to token force the fallback; hints
+    overwritten with arbitrary values (the workspace's control block holds
+    them from byte 512, two words per layer) must not change any result."""
+    cfg = SHAPES["7b_layers"]
+    say("[select_delta] hint misses and stale hints")
+    rng = np.random.default_rng(9)
+    seq = score_sequence(rng, cfg.layers, cfg.d_ffn, 8)
+    for t in range(1, 8, 2):  # every other token far from the previous one
+        seq[t] = (seq[t] * np.float32(37.0) + np.float32(5.0)).astype(np.float32)
+    run_pair(cfg, seq)
+
+    L, F, C, k = cfg.layers, cfg.d_ffn, cfg.capacity, cfg.k
+    a, b = Bufs(cfg), Bufs(cfg)
+    a.reset()
+    b.reset()
+    st = orc.State(L, F, C)
+    for t, sc in enumerate(score_sequence(np.random.default_rng(10), L, F, 6)):
+        junk = rng.integers(0, 2**32, size=2 * L, dtype=np.uint64).astype(np.uint32)
+        if t == 3:
+            junk[1::2] = 0  # zero half-widths: no window
+        b.ws[512: 512 + 8 * L].copy_(torch.from_numpy(junk.view(np.uint8)).cuda())
+        dev = torch.from_numpy(sc.reshape(-1)).cuda()
+        a.scores.copy_(dev)
+        b.scores.copy_(dev)
+        B.np_select(a.shape, a.scores, a.mask, a.ids, a.ws)
+        B.np_delta(a.shape, t, a.ids, a.state, a.out, a.ws)
+        B.np_select_delta(b.shape, t, b.scores, b.mask, b.ids, b.state, b.out, b.ws)
+        torch.cuda.synchronize()
+        assert torch.equal(a.mask, b.mask) and torch.equal(a.ids, b.ids), t
+        _, ids = orc.select(sc, k)
+        assert np.array_equal(from_dev(b.ids, np.int32, (L, k)), ids), t
+        compare_delta(b.host_lists(), orc.delta(t, ids, st, C), L)
+    assert B.np_device_error(b.ws) == 0
