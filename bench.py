@@ -194,6 +194,66 @@ def mlp_dispatch_floor(pipe, blocks: int = 10) -> dict:
                     "L' calls back to back behind a sleep kernel: the fixed cost of a call"}
 
 
+def mlp_same_layer(pipe, blocks: int = 5) -> dict:
+    """L' back-to-back np_sparse_mlp calls on one layer's k rows, behind a
+    sleep kernel: after the first call every record has been read once, so
+    this is the call with its records as cache-resident as the hardware
+    keeps them -- the most that fetching layer l+1's records ahead of its
+    call could save."""
+    import numpy as np
+    import torch
+
+    from paper_2608_22643_amd import binding as B
+
+    cfg, m = pipe.cfg, pipe.main
+    L, k = cfg.layers, cfg.k
+    slots = pipe.lists["active_slots"].data_ptr()
+    spans = []
+    for _ in range(blocks):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(m):
+            torch.cuda._sleep(2_000_000)
+        e0.record(m)
+        for _l in range(L):
+            B.np_sparse_mlp(pipe.shape, 0, pipe.x_ptr(0), pipe.resident, slots, k,
+                            pipe.y.data_ptr(), pipe.ws, m)
+        e1.record(m)
+        e1.synchronize()
+        spans.append(e0.elapsed_time(e1) * 1e3 / L)
+    return {"us_per_call": round(float(np.median(spans)), 3), "calls": L * blocks,
+            "note": "layer 0's k rows, L' calls back to back behind a sleep kernel"}
+
+
+def read_ref_per_call(nbytes: int, calls: int, blocks: int = 5) -> dict:
+    """The library GEMV (torch.mv) at one sparse-MLP call's byte count: calls
+    back to back, each on its own [nbytes / 8192][4096] fp16 matrix (distinct
+    bytes, as the layers' records are), behind a sleep kernel; the span per
+    call is a library kernel's rate for one launch of this size."""
+    import numpy as np
+    import torch
+
+    rows = (nbytes + 8191) // 8192
+    ws = [torch.ones(rows, 4096, dtype=torch.float16, device="cuda") for _ in range(calls)]
+    x = torch.ones(4096, dtype=torch.float16, device="cuda")
+    for w in ws:
+        torch.mv(w, x)
+    spans = []
+    for _ in range(blocks):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(2_000_000)
+        e0.record()
+        for w in ws:
+            torch.mv(w, x)
+        e1.record()
+        e1.synchronize()
+        spans.append(e0.elapsed_time(e1) * 1e3 / calls)
+    us = float(np.median(spans))
+    del ws, x
+    return {"us_per_call": round(us, 3), "bytes_per_call": rows * 8192,
+            "GBps": round(rows * 8192 / (us * 1e-6) / 1e9, 1), "calls": calls * blocks,
+            "kernel": f"torch.mv over {calls} distinct [{rows}][4096] fp16 matrices"}
+
+
 def read_ref_gbps(nbytes: int = 2 << 30, reps: int = 5) -> float:
     """A read-bound library kernel of the same run for reference: torch.mv
     (the library GEMV) of a [nbytes / 8192][4096] fp16 matrix by a vector,
@@ -1284,6 +1344,8 @@ def main():
     log(f"[bench] np_sparse_mlp: {mlp_us:.2f} us per call")
     floor = mlp_dispatch_floor(pipe)
     log(f"[bench] np_sparse_mlp with no rows: {floor}")
+    same_layer = mlp_same_layer(pipe)
+    log(f"[bench] np_sparse_mlp on one layer repeated: {same_layer}")
     err = pipe.device_error()
     if err:
         log(f"[bench] device error word {err:#x}")
@@ -1349,6 +1411,8 @@ def main():
         del src, dst
     read_ref = round(read_ref_gbps(), 1)
     log(f"[bench] read reference: {read_ref} GB/s")
+    read_call = read_ref_per_call(mlp_bytes_per_launch(cfg), cfg.layers)
+    log(f"[bench] read reference per call: {read_call}")
     big, big_samples = {}, []
     for name in [n for n in args.hbm_configs.split(",") if n]:
         big[name], smp = hbm_config_run(name, args.hbm_steps, Fl)
@@ -1393,7 +1457,9 @@ def main():
                      "traffic_detail": traffic_detail,
                      "bytes_per_launch": bytes_launch, "avg_launch_us": round(mlp_us, 3),
                      "frac_of_read_ref": round(achieved / read_ref, 4),
-                     "empty_call": floor},
+                     "empty_call": floor, "same_layer": same_layer,
+                     "read_ref_per_call": read_call,
+                     "speedup_vs_read_ref_per_call": round(read_call["us_per_call"] / mlp_us, 3)},
         "step_us": step_pct,
         "predictor": predictor,
         "read_ref": {"GBps": read_ref, "kernel": "torch.mv (library GEMV) over a 2 GiB [262144][4096] fp16 matrix"},
