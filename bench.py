@@ -809,7 +809,7 @@ def swiglu_run(steps: int, calib_tokens: int = 128, alpha: float = 61.6) -> dict
                        acts.data_ptr() + l * calib_tokens * F * 4, pipe.ws, stream)
     ev[1].record(stream)
     out = torch.empty(L, dtype=torch.float32, device="cuda")
-    B.np_percentile(acts, L, calib_tokens * F, alpha, out, pipe.ws, stream)
+    B.np_percentile(acts, L, calib_tokens * F, alpha, out, pipe.ws, pipe.ws.numel(), stream)
     ev[2].record(stream)
     torch.cuda.synchronize()
     ab_us = ev[0].elapsed_time(ev[1]) * 1e3 / L

@@ -510,11 +510,17 @@ np_status np_act_batch(const np_shape* shape, const void* weights, const void* x
  * on the host and clamped to [1, n], so out[r] is one of the magnitudes and
  * eq. 1 zeroes fewer than m of them.  alpha in [0, 100]; 1 <= rows <= 65535;
  * 1 <= n < 2^31; rows * n * 4 bytes of values.  out: device fp32 [rows].  A
- * NaN value sets NP_DEVERR_NAN_SCORE (out[r] is then undefined).  One
- * workgroup per row, radix selection on the magnitude bits; dev_ws holds
- * only the error word. */
+ * NaN value sets NP_DEVERR_NAN_SCORE (out[r] is then undefined).  Radix
+ * selection on the magnitude bits, three passes over each row.
+ * dev_ws_bytes: the size of dev_ws (at least 64: the error word).  With at
+ * least NP_PERCENTILE_WS_BYTES(rows) bytes, n > 32768 and rows < 1024, every
+ * row is spread over several workgroups (per-row histograms and selection
+ * state in dev_ws past its first 4096 bytes, which the call overwrites;
+ * seven kernels on `stream`); otherwise one workgroup per row (one kernel)
+ * and dev_ws holds only the error word.  Either way the result is the same. */
+#define NP_PERCENTILE_WS_BYTES(rows) (4352 + 8208 * (size_t)(rows))
 np_status np_percentile(const float* values, int32_t rows, int64_t n, double alpha, float* out,
-                        void* dev_ws, hipStream_t stream);
+                        void* dev_ws, size_t dev_ws_bytes, hipStream_t stream);
 
 /* Eq. 1 as an active set, in np_select's layout: for each row r of acts
  * ([rows][F] fp32, device) with threshold thresholds[r] (device fp32

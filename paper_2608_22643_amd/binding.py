@@ -109,7 +109,8 @@ def lib():
         L.np_dense_mlp.argtypes = [S, vp, vp, vp, vp, vp]
         L.np_sparse_mlp_t.argtypes = [S, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp]
         L.np_act_batch.argtypes = [S, vp, vp, i32, vp, vp, vp]
-        L.np_percentile.argtypes = [vp, i32, ctypes.c_int64, ctypes.c_double, vp, vp, vp]
+        L.np_percentile.argtypes = [vp, i32, ctypes.c_int64, ctypes.c_double, vp, vp,
+                                    ctypes.c_size_t, vp]
         L.np_threshold_active.argtypes = [S, vp, i32, vp, vp, vp, vp, vp, vp]
         i64 = ctypes.c_int64
         L.np_stage_file.argtypes = [S, ctypes.POINTER(np_stage_plan), i32, i32, i32, i64, vp, vp,
@@ -315,9 +316,15 @@ def np_act_batch(shape, weights, x, n: int, acts, ws=None, stream=None) -> None:
                               _s(stream)), "np_act_batch")
 
 
-def np_percentile(values, rows: int, n: int, alpha: float, out, ws, stream=None) -> None:
+def percentile_ws_bytes(rows: int) -> int:
+    """NP_PERCENTILE_WS_BYTES(rows) of the header."""
+    return 4352 + 8208 * int(rows)
+
+
+def np_percentile(values, rows: int, n: int, alpha: float, out, ws, ws_bytes: int,
+                  stream=None) -> None:
     _check(lib().np_percentile(_p(values), int(rows), int(n), float(alpha), _p(out), _p(ws),
-                               _s(stream)), "np_percentile")
+                               int(ws_bytes), _s(stream)), "np_percentile")
 
 
 def np_threshold_active(shape, acts, rows: int, thresholds, mask, active_ids, active_counts, ws,

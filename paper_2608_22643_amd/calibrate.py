@@ -3,7 +3,7 @@
 For each downstream layer l the activations A(i, l) = act(G_l x_i, U_l x_i)
 of a batch of calibration tokens are computed on the matrix cores
 (np_act_batch), and T(l, alpha) is the nearest-rank alpha-th percentile of
-their magnitudes (np_percentile, all layers in one launch).  Eq. 1 then
+their magnitudes (np_percentile, all layers in one call).  Eq. 1 then
 zeroes activations with |a| < T(l, alpha): a fraction just under alpha/100
 of the calibration activations.  Every step runs in the HIP library; this
 module only sizes buffers and sequences the calls.
@@ -35,5 +35,5 @@ def thresholds(cfg: W.Config, storage: torch.Tensor, x: torch.Tensor, n_tokens: 
         B.np_act_batch(shape, storage.data_ptr() + l * layer_bytes, x, n_tokens,
                        acts.data_ptr() + l * n_tokens * F * 4, ws, stream)
     out = torch.empty(L, dtype=torch.float32, device=dev)
-    B.np_percentile(acts, L, n_tokens * F, alpha, out, ws, stream)
+    B.np_percentile(acts, L, n_tokens * F, alpha, out, ws, ws.numel() * ws.element_size(), stream)
     return out

@@ -395,7 +395,7 @@ np_status np_act_batch(const np_shape* s, const void* weights, const void* x, in
 }
 
 np_status np_percentile(const float* values, int32_t rows, int64_t n, double alpha, float* out,
-                        void* ws, hipStream_t stream) {
+                        void* ws, size_t ws_bytes, hipStream_t stream) {
   if (rows < 1 || rows > 65535) return fail(NP_ERR_INVALID_ARG, "rows %d outside [1, 65535]", rows);
   if (n < 1 || n >= ((int64_t)1 << 31))
     return fail(NP_ERR_INVALID_ARG, "n %lld outside [1, 2^31)", (long long)n);
@@ -403,10 +403,13 @@ np_status np_percentile(const float* values, int32_t rows, int64_t n, double alp
     return fail(NP_ERR_INVALID_ARG, "alpha %g outside [0, 100]", alpha);
   if (!aligned16(values) || ((uintptr_t)out & 3) || !out || !aligned16(ws))
     return fail(NP_ERR_INVALID_ARG, "np_percentile: pointers must be non-NULL and aligned");
+  if (ws_bytes < 64)
+    return fail(NP_ERR_INVALID_ARG, "np_percentile: dev_ws of %zu bytes holds no error word",
+                ws_bytes);
   // nearest rank: the m-th smallest magnitude, m = ceil(alpha n / 100) in [1, n]
   double md = std::ceil(alpha * (double)n / 100.0);
   int64_t m = md < 1.0 ? 1 : (md > (double)n ? n : (int64_t)md);
-  hipError_t e = launch_percentile(values, rows, n, m, out, ws, stream);
+  hipError_t e = launch_percentile(values, rows, n, m, out, ws, ws_bytes, stream);
   return e == hipSuccess ? NP_OK : hip_fail(e, "np_percentile launch");
 }
 

@@ -1,8 +1,9 @@
 // np_calib.hip -- the magnitude-threshold sparsity of Sec. 3.2 (eq. 1):
 //  * act_batch_kernel: activations A(i, l) = act(G x_i, U x_i) of one layer
 //    over a batch of calibration tokens, on the matrix cores;
-//  * percentile_kernel: per layer, the nearest-rank alpha-th percentile of
-//    |A| (the threshold T(l, alpha)) by radix selection;
+//  * pct_hist_kernel / pct_select_kernel (percentile_kernel for short rows):
+//    per layer, the nearest-rank alpha-th percentile of |A| (the threshold
+//    T(l, alpha)) by radix selection;
 //  * threshold_active_kernel: eq. 1 as an active set, |a| >= T, in the
 //    selection's mask + ascending-id layout.
 #include "np_device.hpp"
@@ -288,8 +289,149 @@ __global__ __launch_bounds__(PCT_NT) void percentile_kernel(const float* __restr
   if (tid == 0) out[blockIdx.x] = __uint_as_float(prefix);
 }
 
+// The same selection spread over many workgroups per row, for long rows:
+// each pass is a histogram kernel over (slice, row) workgroups, which count
+// their slice of the row into LDS and add the nonzero bins to the row's
+// histogram in dev_ws, and a selection kernel with one workgroup per row,
+// which scans that histogram, narrows the row's (prefix, known bits, rank)
+// state and clears the histogram for the next pass.  The kernel boundaries
+// order the passes.  dev_ws layout past the control block: state [rows][4]
+// uint32, then histograms [rows][PCT_BINS] uint32.
+constexpr int PCT_HNT = 512;
+constexpr int PCT_HCOPIES = 4;  // LDS histogram copies, by wave
+
+__host__ __device__ inline size_t pct_hist_offset(int rows) {
+  return (WS_CTRL_BYTES + (size_t)rows * 16 + 255) & ~(size_t)255;
+}
+size_t percentile_ws_bytes(int rows) {
+  return pct_hist_offset(rows) + (size_t)rows * PCT_BINS * 4;
+}
+
+__global__ __launch_bounds__(256) void pct_init_kernel(int64_t m, void* ws) {
+  const int row = blockIdx.x;
+  uint32_t* st = (uint32_t*)((char*)ws + WS_CTRL_BYTES) + 4 * (size_t)row;
+  uint32_t* h = (uint32_t*)((char*)ws + pct_hist_offset(gridDim.x)) + (size_t)row * PCT_BINS;
+  if (threadIdx.x == 0) {
+    st[0] = 0u;  // decided high bits
+    st[1] = 0u;  // their mask
+    st[2] = (uint32_t)m;  // 1-based rank within the matching values
+    st[3] = 0u;
+  }
+  for (int i = threadIdx.x; i < PCT_BINS; i += blockDim.x) h[i] = 0u;
+}
+
+// grid (slices, rows); slice s of a row covers values [s*chunk, min(n, (s+1)*chunk))
+template <bool V4>
+__global__ __launch_bounds__(PCT_HNT) void pct_hist_kernel(const float* __restrict__ values,
+                                                           int64_t n, int64_t chunk, int pass,
+                                                           int rows, void* ws) {
+  __shared__ uint32_t hist[PCT_HCOPIES][PCT_BINS];
+  const int tid = threadIdx.x, copy = (tid / WAVE) % PCT_HCOPIES;
+  const int row = blockIdx.y;
+  const uint32_t* st = (const uint32_t*)((const char*)ws + WS_CTRL_BYTES) + 4 * (size_t)row;
+  const uint32_t prefix = st[0], known = st[1];
+  const int sh = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+  const uint32_t nb = pass == 0 ? 2048u : 1024u;
+  for (int i = tid; i < PCT_HCOPIES * PCT_BINS; i += PCT_HNT) (&hist[0][0])[i] = 0u;
+  __syncthreads();
+  const float* rowp = values + (size_t)row * (size_t)n;
+  const int64_t lo = (int64_t)blockIdx.x * chunk, hi = lo + chunk < n ? lo + chunk : n;
+  bool nan = false;
+  auto count = [&](float v) {
+    const uint32_t key = __float_as_uint(v) & 0x7FFFFFFFu;
+    if (pass == 0 && key > 0x7F800000u) nan = true;
+    if ((key & known) == prefix) atomicAdd(&hist[copy][(key >> sh) & (nb - 1)], 1u);
+  };
+  if constexpr (V4) {  // chunk and n are multiples of 4
+    const float4* r4 = (const float4*)(rowp + lo);
+    const int64_t n4 = (hi - lo) / 4;
+    for (int64_t i = tid; i < n4; i += PCT_HNT) {
+      const float4 v = r4[i];
+      count(v.x);
+      count(v.y);
+      count(v.z);
+      count(v.w);
+    }
+  } else {
+    for (int64_t i = lo + tid; i < hi; i += PCT_HNT) count(rowp[i]);
+  }
+  if (nan) raise_error(ws, NP_DEVERR_NAN_SCORE);
+  __syncthreads();
+  uint32_t* h = (uint32_t*)((char*)ws + pct_hist_offset(rows)) + (size_t)row * PCT_BINS;
+  for (int b = tid; b < (int)nb; b += PCT_HNT) {
+    uint32_t c = 0u;
+#pragma unroll
+    for (int cp = 0; cp < PCT_HCOPIES; ++cp) c += hist[cp][b];
+    if (c) atomicAdd(&h[b], c);
+  }
+}
+
+// one workgroup per row: the digit of this pass that holds the rank
+__global__ __launch_bounds__(PCT_NT) void pct_select_kernel(int pass, int rows, float* out,
+                                                            void* ws) {
+  __shared__ uint32_t scan[PCT_NT / WAVE + 1];
+  __shared__ uint32_t sel[2];
+  const int tid = threadIdx.x, row = blockIdx.x;
+  uint32_t* st = (uint32_t*)((char*)ws + WS_CTRL_BYTES) + 4 * (size_t)row;
+  uint32_t* h = (uint32_t*)((char*)ws + pct_hist_offset(rows)) + (size_t)row * PCT_BINS;
+  const int sh = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+  const int nb = pass == 0 ? 2048 : 1024;
+  const uint32_t rank = st[2];
+  uint32_t c[2];  // thread t owns bins 2t, 2t + 1
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int b = 2 * tid + j;
+    c[j] = b < nb ? h[b] : 0u;
+  }
+  if (tid == 0) {  // a rank beyond the count (NaN rows only) keeps digit 0
+    sel[0] = 0u;
+    sel[1] = rank;
+  }
+  uint32_t tot;
+  const uint32_t before = block_excl_scan<PCT_NT>(c[0] + c[1], scan, &tot);
+  if (before < rank && rank <= before + c[0]) {
+    sel[0] = 2 * tid;
+    sel[1] = rank - before;
+  } else if (before + c[0] < rank && rank <= before + c[0] + c[1]) {
+    sel[0] = 2 * tid + 1;
+    sel[1] = rank - before - c[0];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 2; ++j) h[2 * tid + j] = 0u;  // PCT_BINS = 2 * PCT_NT
+  if (tid == 0) {
+    const uint32_t prefix = st[0] | (sel[0] << sh);
+    st[0] = prefix;
+    st[1] |= (uint32_t)(nb - 1) << sh;
+    st[2] = sel[1];
+    if (pass == 2) out[row] = __uint_as_float(prefix);
+  }
+}
+
 hipError_t launch_percentile(const float* values, int rows, int64_t n, int64_t m, float* out,
-                             void* ws, hipStream_t stream) {
+                             void* ws, size_t ws_bytes, hipStream_t stream) {
+  // slices per row: about four workgroups per compute unit in all, each over
+  // at least 32K values
+  const int64_t want = ((int64_t)1024 + rows - 1) / rows;
+  int64_t slices = std::min<int64_t>(want, (n + 32767) / 32768);
+  if (slices > 65535) slices = 65535;
+  if (slices >= 2 && ws_bytes >= percentile_ws_bytes(rows)) {
+    int64_t chunk = (n + slices - 1) / slices;
+    chunk = (chunk + 3) / 4 * 4;  // whole float4 vectors
+    slices = (n + chunk - 1) / chunk;
+    hipLaunchKernelGGL(pct_init_kernel, dim3(rows), dim3(256), 0, stream, m, ws);
+    for (int pass = 0; pass < 3; ++pass) {
+      if (n % 4 == 0)
+        hipLaunchKernelGGL(pct_hist_kernel<true>, dim3((unsigned)slices, rows), dim3(PCT_HNT), 0,
+                           stream, values, n, chunk, pass, rows, ws);
+      else
+        hipLaunchKernelGGL(pct_hist_kernel<false>, dim3((unsigned)slices, rows), dim3(PCT_HNT),
+                           0, stream, values, n, chunk, pass, rows, ws);
+      hipLaunchKernelGGL(pct_select_kernel, dim3(rows), dim3(PCT_NT), 0, stream, pass, rows, out,
+                         ws);
+    }
+    return hipGetLastError();
+  }
   if (n % 4 == 0)
     hipLaunchKernelGGL(percentile_kernel<true>, dim3(rows), dim3(PCT_NT), 0, stream, values, n,
                        m, out, ws);

@@ -100,8 +100,9 @@ hipError_t launch_sparse_mlp_noalloc(const np_shape& s, int layer, const void* x
 hipError_t launch_act_batch(const np_shape& s, const void* weights, const void* x, int n,
                             float* acts, hipStream_t stream);
 // per row: the m-th smallest magnitude of n values (1 <= m <= n)
+size_t percentile_ws_bytes(int rows);
 hipError_t launch_percentile(const float* values, int rows, int64_t n, int64_t m, float* out,
-                             void* ws, hipStream_t stream);
+                             void* ws, size_t ws_bytes, hipStream_t stream);
 // eq. 1 masks and ascending ids of rows x F activations
 hipError_t launch_threshold_active(const np_shape& s, const float* acts, int rows,
                                    const float* thr, uint32_t* mask, int32_t* active_ids,

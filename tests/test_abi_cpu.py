@@ -168,12 +168,14 @@ def test_threshold_calls_validate_before_enqueueing(lib):
         lambda: B.np_act_batch(shape, 16, 16, 0, 16),
         lambda: B.np_act_batch(shape, 16, 16, 70000, 16),
         lambda: B.np_act_batch(shape, 16, 24, 8, 16),
-        # np_percentile: alpha outside [0, 100], no rows, NULL output
-        lambda: B.np_percentile(16, 1, 100, 100.5, 16, 16),
-        lambda: B.np_percentile(16, 1, 100, float("nan"), 16, 16),
-        lambda: B.np_percentile(16, 0, 100, 50.0, 16, 16),
-        lambda: B.np_percentile(16, 1, 0, 50.0, 16, 16),
-        lambda: B.np_percentile(16, 1, 100, 50.0, None, 16),
+        # np_percentile: alpha outside [0, 100], no rows, NULL output, a
+        # workspace without room for the error word
+        lambda: B.np_percentile(16, 1, 100, 100.5, 16, 16, 4096),
+        lambda: B.np_percentile(16, 1, 100, float("nan"), 16, 16, 4096),
+        lambda: B.np_percentile(16, 0, 100, 50.0, 16, 16, 4096),
+        lambda: B.np_percentile(16, 1, 0, 50.0, 16, 16, 4096),
+        lambda: B.np_percentile(16, 1, 100, 50.0, None, 16, 4096),
+        lambda: B.np_percentile(16, 1, 100, 50.0, 16, 16, 63),
         # np_threshold_active: no thresholds, no rows
         lambda: B.np_threshold_active(shape, 16, 1, None, 16, 16, 16, 16),
         lambda: B.np_threshold_active(shape, 16, 0, 16, 16, 16, 16, 16),

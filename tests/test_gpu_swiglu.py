@@ -180,9 +180,13 @@ def test_act_batch(name, n, act):
 
 # ---------------- O10: percentile -------------------------------------------------
 
-@pytest.mark.parametrize("n", [1, 5, 1000, 1001, 65536 + 3])
-def test_percentile_bit_exact(n):
-    say(f"[percentile] n={n}")
+@pytest.mark.parametrize("n", [1, 5, 1000, 1001, 32768, 32769, 65536 + 3, 200000, (1 << 20) + 2])
+@pytest.mark.parametrize("spread", [False, True])
+def test_percentile_bit_exact(n, spread):
+    """One workgroup per row (a workspace with only the error word), and rows
+    spread over several workgroups (a workspace with room for the per-row
+    histograms: taken for n > 32768)."""
+    say(f"[percentile] n={n} spread={spread}")
     rng = np.random.default_rng(n)
     rows = 3
     v = rng.normal(size=(rows, n)).astype(np.float32)
@@ -193,14 +197,15 @@ def test_percentile_bit_exact(n):
         v[2, 2] = np.float32(1e-40)          # a subnormal
     dv = to_dev(v)
     out = torch.zeros(rows, dtype=torch.float32, device=DEV)
-    ws = torch.zeros(4096, dtype=torch.uint8, device=DEV)
+    wsb = B.percentile_ws_bytes(rows) if spread else 4096
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=DEV)
     for alpha in (0.0, 12.5, 50.0, 61.6, 99.0, 100.0):
-        B.np_percentile(dv, rows, n, alpha, out, ws)
+        B.np_percentile(dv, rows, n, alpha, out, ws, wsb)
         torch.cuda.synchronize()
         assert np.array_equal(out.cpu().numpy(), orc.percentile(v, alpha)), alpha
     assert int(ws[:4].view(torch.int32)[0]) == 0
     v[0, n // 2] = np.nan
-    B.np_percentile(to_dev(v), rows, n, 50.0, out, ws)
+    B.np_percentile(to_dev(v), rows, n, 50.0, out, ws, wsb)
     assert B.np_device_error(ws) & B.NP_DEVERR_NAN_SCORE
 
 
@@ -266,7 +271,7 @@ def test_calibration_chain_7b_swiglu():
     # T(alpha) over the whole batch, bit for bit on the GPU's activations
     ws = torch.zeros(B.np_workspace_size(shape), dtype=torch.uint8, device=DEV)
     T = torch.zeros(1, dtype=torch.float32, device=DEV)
-    B.np_percentile(acts, 1, n * F, 61.6, T, ws)
+    B.np_percentile(acts, 1, n * F, 61.6, T, ws, ws.numel())
     torch.cuda.synchronize()
     assert T.cpu().numpy()[0] == orc.percentile(got.reshape(1, -1), 61.6)[0]
     # eq. 1 on the next token's activations (bit for bit on the GPU's values)
