@@ -1113,24 +1113,42 @@ def cpu_baseline(cfg, host_storage, seconds: float, gpu_ref=(), big_samples=()):
                      f"staging omitted (a byte copy); {el:.1f} s on 1 host thread",
            "cpu_model": cpu_model(), "cpu_detail": cpu_detail(), "host_cpus": os.cpu_count(),
            "per_step_ms_per_token": {k: round(v * 1e3 / n, 2) for k, v in step_s.items()}}
-    # the same tokens again with the layers' sparse MLPs spread over the host
-    # threads (the oracle's C calls release the interpreter lock; predict,
-    # select and delta stay single calls)
+    # the same tokens again with the work of each step spread over the host
+    # threads layer by layer (the oracle's C calls release the interpreter
+    # lock): O1 and O2 on one layer per call, the sparse MLPs one layer per
+    # call; O3 stays one call over all layers (its state is the whole buffer)
     threads = min(len(os.sched_getaffinity(0)), L) if hasattr(os, "sched_getaffinity") else 1
     if threads > 1:
         from concurrent.futures import ThreadPoolExecutor
+        from types import SimpleNamespace
 
+        one = SimpleNamespace(layers=1, d_model=cfg.d_model, d_ffn=cfg.d_ffn, rank=cfg.rank,
+                              wdtype=cfg.wdtype, adtype=cfg.adtype)
         st2 = oracle.State(cfg.layers, cfg.d_ffn, cfg.capacity)
+        step2 = {"predict": 0.0, "select": 0.0, "delta": 0.0, "sparse_mlp": 0.0}
         t1 = time.perf_counter()
         with ThreadPoolExecutor(threads) as ex:
             for i in range(n):
-                s2 = oracle.predict(cfg, h[i], A, Bm)
-                _, ids2 = oracle.select(s2, cfg.k)
+                ta = time.perf_counter()
+                s2 = np.concatenate(list(ex.map(
+                    lambda l: oracle.predict(one, h[i], A[l], Bm[l]), range(L))))
+                tb = time.perf_counter()
+                ids2 = np.concatenate(list(ex.map(
+                    lambda l: oracle.select(s2[l:l + 1], cfg.k)[1], range(L))))
+                tc = time.perf_counter()
                 oracle.delta(i, ids2, st2, cfg.capacity)
+                td = time.perf_counter()
                 list(ex.map(lambda l: oracle.sparse_mlp(cfg, l, h[i], store, ids2[l]), range(L)))
+                te = time.perf_counter()
+                for k2, v2 in (("predict", tb - ta), ("select", tc - tb), ("delta", td - tc),
+                               ("sparse_mlp", te - td)):
+                    step2[k2] += v2
         el2 = time.perf_counter() - t1
         out["all_cores"] = {"value": round(n / el2, 4), "cores": threads,
-                            "note": "the same tokens, the layers' sparse MLPs on a thread pool"}
+                            "per_step_ms_per_token": {k2: round(v2 * 1e3 / n, 2)
+                                                      for k2, v2 in step2.items()},
+                            "note": "the same tokens, O1, O2 and the sparse MLPs one layer per "
+                                    "call on a thread pool, O3 one call"}
     for smp in big_samples:  # sampled layers of the full-size HBM configurations
         bc = smp["cfg"]
         hb = W.hidden(bc, smp["tokens"])[smp["token"]]
