@@ -38,6 +38,11 @@ SHAPES = {
     "f_11001": cfg_small("f_11001", 2, 64, 11001, 8, 1650, 5000, "f16"),
     "f_20000": cfg_small("f_20000", 2, 64, 20000, 16, 2500, 6000, "bf16"),
     "f_max": cfg_small("f_max", 1, 64, 65535, 8, 8192, 8192, "f32"),
+    # the largest d and r the shape check accepts: 16-bit d 16384 with r 1024
+    # (the sparse MLP on 16 waves of two-vector slices, 2-row rounds), fp32
+    # d 8192 with r 512
+    "d_max_f16": cfg_small("d_max_f16", 2, 16384, 1000, 1024, 100, 200, "f16"),
+    "d_max_f32": cfg_small("d_max_f32", 2, 8192, 700, 512, 64, 150, "f32"),
 }
 
 
