@@ -276,30 +276,32 @@ np_status np_select_delta(const np_shape* shape, int32_t token, const float* sco
  * plan: host copy of np_delta's counts/in_ids/in_slots (read synchronously).
  * host_storage: [L'][F][3d] records, pinned host memory (hipHostMalloc).
  * dev_resident: [L'][C][3d] device.
- * dev_landing / landing_bytes (device, 16-byte aligned): holds
- * cap = landing_bytes / (rec + 4) records (rec = 3d*sizeof(w)) and their
- * int32 destination rows; a delta of more than cap records is staged in
- * several landing rounds.
  * host_staging / staging_bytes (pinned host, 16-byte aligned): a ring of up
  * to 4 pieces (4 KiB multiples) into which the host packs records (8
- * threads) and their int32 destination rows (layer * C + slot); each piece
- * is copied with hipMemcpyAsync on `side` (records, then rows) to the next
- * free positions of the landing area.  The landing area is a ring too: a
- * round of landed records (closed at the end of the call, when the ring
- * wraps, or at layer groups, below) is moved into its slots by one scatter
- * kernel.  The scatters
- * run on a stream the library keeps per staging buffer (default priority),
- * ordered after their round's copies by events, so the copies run back to
- * back; copies into a wrapped ring wait for the scatters before them.
+ * threads), rec = 3d*sizeof(w) bytes each, followed by their int32
+ * destination rows (layer * C + slot); a piece of n records is sent as one
+ * block of n * (rec + 4) bytes with one hipMemcpyAsync on `side` into the
+ * landing area, and one scatter kernel then moves its records into their
+ * slots.
+ * dev_landing / landing_bytes (device, 16-byte aligned): a ring of landed
+ * blocks, each at a 16-byte boundary; it must hold one record and its row
+ * (landing_bytes >= rec + 4); a piece holds at most what the whole ring
+ * holds, and the ring wraps to its start when what is left of it cannot
+ * hold the next piece.  The scatters run on a stream the library keeps per staging
+ * buffer (default priority), each ordered after its block's copy by an
+ * event, so the copies run back to back on the copy engine; copies into a
+ * wrapped ring wait for the scatters before them.
  * wait_before (nullable): the scatters of this call wait on it (orders the
  * writes into dev_resident after the previous token's MLP reads).
- * layer_ready (nullable, [L'] events): a round also closes at the end of a
- * layer once it holds 8 MiB (NP_STAGE_GROUP_MIB), and event l is recorded
- * after the scatter that places layer l's last record; these events are
- * then the call's completion signal.  Without layer_ready, `side` is made to
+ * layer_ready (nullable, [L'] events): at the end of a layer, once the
+ * layers since the last recorded event hold 8 MiB of records
+ * (NP_STAGE_GROUP_MIB), the open piece is sent, and events of those layers
+ * are recorded after its scatter; event l thus follows the scatter that
+ * places layer l's last record, and these events are the call's completion
+ * signal.  Without layer_ready, `side` is made to
  * wait for the call's last scatter, so later work on `side` follows the whole
- * staging.  The host blocks only to reuse a staging piece (or the row area)
- * whose copy has not finished.  State kept between calls (pending copies,
+ * staging.  The host blocks only to reuse a staging piece whose copy has not
+ * finished.  State kept between calls (pending copies,
  * the rings' positions, the scatter stream) is per staging buffer: calls
  * with different staging buffers are independent; calls with the same one
  * must come from one thread at a time.  On a failure after some pieces were

@@ -1,13 +1,14 @@
 // np_stage_host.cpp -- staging through pinned host memory (Sec. 3.5, I/O
 // path): incoming ids are walked layer by layer in ascending order, adjacent
 // ids are coalesced into one contiguous source range, records are packed
-// into a capacity-bounded pinned staging area, and each packed piece goes to
-// the device with one hipMemcpyAsync on the side stream; a kernel then
+// into a capacity-bounded pinned staging area, and each packed piece (its
+// records followed by their destination rows) goes to the device with one
+// hipMemcpyAsync on the side stream; a kernel on another stream then
 // scatters the landed records into their slots.  The staging area is a ring
 // of pieces so that packing one piece overlaps the copy of the previous
-// ones, and every piece of a landing round lands in its own part of the
-// landing area, so the copies run back to back with one scatter per round; a
-// delta larger than the landing area runs as several rounds.  The source is
+// ones, and the landing area is a ring of landed pieces, so the copies run
+// back to back on the copy engine, with no kernel between two of them; a
+// delta larger than the landing area wraps the ring.  The source is
 // the storage tier in host memory (np_stage_rows: the ranges are copied by a
 // thread pool) or in a file (np_stage_file: the ranges are read through
 // io_uring, np_file.cpp).
@@ -128,14 +129,14 @@ static PackPool* pack_pool() {
 }
 
 // State of one pinned staging buffer (keyed by device and base address):
-// an event per staging piece (its copies have finished reading the piece)
-// and the scatter stream with its events.  Copies
-// run on the caller's side stream back to back; each landing round's
-// scatter runs on the buffer's own scatter stream (default priority) once
-// the round's copies are done (ev_copied), so the copy engine never waits for
-// a kernel between two copies.  ev_scattered marks the last scatter: the side
-// stream waits on it before copies reuse the landing area and at the end of
-// each call, so work the caller puts on `side` later follows the scatters.
+// an event per staging piece (its copy has finished reading the piece) and
+// the scatter stream with its events.  Copies run on the caller's side
+// stream back to back; each landed piece's scatter runs on the buffer's own
+// scatter stream (default priority) once its copy is done (ev_copied), so the
+// copy engine never waits for a kernel between two copies.  ev_scattered
+// marks the last scatter: the side stream waits on it before copies reuse
+// the landing area and at the end of each call, so work the caller puts on
+// `side` later follows the scatters.
 // Calls on different staging buffers share nothing but the packing threads;
 // calls on one buffer are serialised by its lock.
 constexpr int MAX_PIECES = 8;
@@ -147,10 +148,11 @@ struct StageCtx {
   hipStream_t scat = nullptr;
   hipEvent_t ev_copied = nullptr, ev_scattered = nullptr;
   bool scattered = false;  // ev_scattered has been recorded
-  // the landing area is a ring: rounds follow one another in it across
-  // calls, and the copies wait for the scatters only when the ring wraps
+  // the landing area is a ring of landed pieces (byte positions, each piece
+  // at a 16-byte boundary) that continues across calls; the copies wait for
+  // the scatters only when the ring wraps
   const void* land_ptr = nullptr;
-  size_t land_cap = 0, land_pos = 0;
+  size_t land_bytes = 0, land_pos = 0;
 };
 
 static StageCtx* stage_ctx(int dev, const void* staging) {
@@ -174,17 +176,23 @@ struct StageSource {
 };
 
 // Layout of the areas (rec = record bytes):
-//   landing:  [cap_land records | cap_land int32 destination rows], a ring
-//   staging:  n_pieces pieces, each [piece_cap records | piece_cap int32 rows]
+//   staging:  n_pieces pieces; a piece of n records is packed as [n records]
+//             with the rows gathered at [piece_cap records ...] and moved to
+//             just after the records when the piece is sent:
+//             [n records | n int32 destination rows]
+//   landing:  a ring of such landed pieces, each at a 16-byte boundary
 // A token's records are packed piece by piece (the pieces form a ring: a
-// piece is reused once its copies have finished), and each piece is copied
-// to the next free positions of the landing ring with two hipMemcpyAsync on
-// `side`, its records and their destination rows (layer * C + slot).  At the
-// end of the call, when the ring wraps, or (with layer_ready) at a layer
-// boundary once a group of layers holds enough bytes, the round of landed
-// records is scattered into the slots by one kernel on the scatter stream.
-// Pieces start small and double (2 MiB, 4, 8, ...) so the first copy starts
-// after little packing; packing piece i + 1 overlaps the copy of piece i.
+// piece is reused once its copy has finished), and each piece goes to the
+// next free position of the landing ring with ONE hipMemcpyAsync on `side`
+// (a second, small copy for the rows would be sent as a kernel, and every
+// switch between the copy engine and a kernel on `side` costs tens of
+// microseconds), then one scatter kernel on the scatter stream moves its
+// records into their slots (layer * C + slot).  With layer_ready, at a layer
+// boundary once the layers since the last event hold enough bytes, the open
+// piece is sent and the events of those layers are recorded behind its
+// scatter.  Pieces start small and double (2 MiB, 4, 8, ...) so the first
+// copy starts after little packing; packing piece i + 1 overlaps the copy of
+// piece i.
 static np_status stage_common(const char* fn, const np_shape* s, const np_stage_plan* plan,
                               int32_t lb, int32_t le, const StageSource& src, void* dev_resident,
                               void* host_staging, size_t staging_bytes, void* dev_landing,
@@ -201,7 +209,7 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
     return fail(NP_ERR_INVALID_ARG, "%s: buffers must be non-NULL and 16-byte aligned", fn);
   if ((st = check_resident(fn, dev_resident)) != NP_OK) return st;
   const size_t rec = (size_t)3 * s->d_model * dtype_size(s->wdtype);
-  const size_t cap_land = landing_bytes / (rec + sizeof(int32_t));
+  const size_t rec_row = rec + sizeof(int32_t);  // landing bytes per record
   // pieces on 4 KiB boundaries, so that direct file reads land aligned
   int n_pieces = 4;
   while (n_pieces > 1 && ((staging_bytes / n_pieces) & ~(size_t)4095) < rec + sizeof(int32_t))
@@ -209,7 +217,7 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
   const size_t piece_bytes = (staging_bytes / n_pieces) & ~(size_t)4095;
   size_t piece_cap = piece_bytes / (rec + sizeof(int32_t));
   if (src.fd >= 0 && src.io_buf) piece_cap = std::min(piece_cap, src.io_bytes / rec);
-  if (cap_land < 1 || piece_cap < 1)
+  if (landing_bytes < rec_row || piece_cap < 1)
     return fail(NP_ERR_CAPACITY,
                 "%s: the landing area (%zu B) or a staging piece (%zu B of %zu B) holds no "
                 "record of %zu B and its row index", fn, landing_bytes, piece_bytes,
@@ -265,7 +273,7 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
     e = hipStreamWaitEvent(cx->scat, wait_before, 0);
     if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
   }
-  if (cx->land_ptr != dev_landing || cx->land_cap != cap_land) {
+  if (cx->land_ptr != dev_landing || cx->land_bytes != landing_bytes) {
     // another landing area (or size): start its ring at 0 after every
     // scatter that may still read the previous one
     if (cx->scattered) {
@@ -273,19 +281,20 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
       if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
     cx->land_ptr = dev_landing;
-    cx->land_cap = cap_land;
+    cx->land_bytes = landing_bytes;
     cx->land_pos = 0;
   }
 
   char* const landing = (char*)dev_landing;
-  int32_t* const land_rows = (int32_t*)(landing + cap_land * rec);
   std::vector<PackPool::Task> tasks;
   std::vector<ReadRun> reads;
   int32_t* piece_rows = nullptr;  // the open piece's destination rows
   int h = cx->next_piece % n_pieces, pieces = 0;
   char* stg = nullptr;
-  // the current round occupies ring positions [land_base, land_base + land_n)
-  size_t n_piece = 0, land_n = 0, land_base = cx->land_pos;
+  // the open piece lands at byte `pos` of the landing ring and holds at most
+  // piece_limit records; group_n: records sent since the last layer_ready
+  // event
+  size_t n_piece = 0, group_n = 0, pos = cx->land_pos, piece_limit = 1;
   // the first piece is small (2 MiB) so that the copy engine starts early,
   // unless it is still busy with the previous call's pieces
   size_t cur_cap = std::min(piece_cap, std::max<size_t>(1, ((size_t)2 << 20) / rec));
@@ -350,60 +359,56 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
     } else {
       pack_pool()->run(tasks);
     }
-    hipError_t ee = hipMemcpyAsync(landing + (land_base + land_n) * rec, stg, n_piece * rec,
-                                   hipMemcpyHostToDevice, side);
-    if (ee == hipSuccess)
-      ee = hipMemcpyAsync(land_rows + land_base + land_n, piece_rows, n_piece * sizeof(int32_t),
-                          hipMemcpyHostToDevice, side);
+    // the rows go right after the records: one copy carries both
+    const size_t rec_bytes = n_piece * rec, bytes = rec_bytes + n_piece * sizeof(int32_t);
+    if ((char*)piece_rows != stg + rec_bytes)
+      memmove(stg + rec_bytes, piece_rows, n_piece * sizeof(int32_t));
+    hipError_t ee = hipMemcpyAsync(landing + pos, stg, bytes, hipMemcpyHostToDevice, side);
     if (ee != hipSuccess) return hip_fail(ee, "hipMemcpyAsync (staging piece)");
     ee = hipEventRecord(cx->ev[h], side);
     if (ee != hipSuccess) return hip_fail(ee, "hipEventRecord");
     cx->pending[h] = true;
-    ++pieces;
-    h = (h + 1) % n_pieces;
-    cx->next_piece = h;
-    land_n += n_piece;
-    n_piece = 0;
-    cur_cap = std::min(piece_cap, 2 * cur_cap);
-    return NP_OK;
-  };
-  // one scatter of the round's landed records, after their copies
-  auto close_round = [&]() -> np_status {
-    if (land_n == 0) return NP_OK;
-    hipError_t ee = hipEventRecord(cx->ev_copied, side);
+    // the piece's scatter, after its copy, on the scatter stream
+    ee = hipEventRecord(cx->ev_copied, side);
     if (ee == hipSuccess) ee = hipStreamWaitEvent(cx->scat, cx->ev_copied, 0);
     if (ee != hipSuccess) return hip_fail(ee, "scatter stream ordering");
-    ee = launch_stage_scatter(*s, landing + land_base * rec, land_rows + land_base, (int)land_n,
-                              dev_resident, cx->scat);
+    ee = launch_stage_scatter(*s, landing + pos, (const int32_t*)(landing + pos + rec_bytes),
+                              (int)n_piece, dev_resident, cx->scat);
     if (ee != hipSuccess) return hip_fail(ee, "scatter launch");
     ee = hipEventRecord(cx->ev_scattered, cx->scat);
     if (ee != hipSuccess) return hip_fail(ee, "hipEventRecord");
     cx->scattered = true;
-    land_base += land_n;
-    land_n = 0;
-    cx->land_pos = land_base;
+    ++pieces;
+    h = (h + 1) % n_pieces;
+    cx->next_piece = h;
+    pos = (pos + bytes + 15) & ~(size_t)15;
+    cx->land_pos = pos;
+    group_n += n_piece;
+    n_piece = 0;
+    cur_cap = std::min(piece_cap, 2 * cur_cap);
     return NP_OK;
   };
-  // before a piece is packed: wrap the ring when the rest of it cannot hold
-  // one more record; copies into it then wait (on the side stream) for every
-  // scatter that may still read it
+  // before a piece is packed: its size (the current piece size, at most
+  // what the whole ring holds), and a wrap of the ring when the rest of it
+  // cannot hold that many records and their rows, so that a piece is never
+  // cut short at the end of the ring; copies into the wrapped ring wait (on
+  // the side stream) for every scatter that may still read it
   auto ring_room = [&]() -> np_status {
-    if (land_base + land_n < cap_land) return NP_OK;
-    np_status r = close_round();
-    if (r != NP_OK) return r;
-    hipError_t ee = hipStreamWaitEvent(side, cx->ev_scattered, 0);
-    if (ee != hipSuccess) return hip_fail(ee, "hipStreamWaitEvent (landing ring)");
-    land_base = 0;
+    piece_limit = std::min(cur_cap, landing_bytes / rec_row);
+    const size_t room = pos < landing_bytes ? (landing_bytes - pos) / rec_row : 0;
+    if (room >= piece_limit) return NP_OK;
+    if (cx->scattered) {
+      hipError_t ee = hipStreamWaitEvent(side, cx->ev_scattered, 0);
+      if (ee != hipSuccess) return hip_fail(ee, "hipStreamWaitEvent (landing ring)");
+    }
+    pos = 0;
     cx->land_pos = 0;
     return NP_OK;
   };
-  // a piece that fails (a HIP call, a read) ends the call; the records of
-  // the pieces already copied are still scattered, so what was enqueued
+  // a piece that fails (a HIP call, a read) ends the call; every piece
+  // copied before it has its scatter enqueued already, so what was enqueued
   // lands (the caller marks the resident buffer in any case)
-  auto bail = [&](np_status err) -> np_status {
-    (void)close_round();
-    return err;
-  };
+  auto bail = [&](np_status err) -> np_status { return err; };
   auto record_ready = [&](int upto) -> np_status {  // layers [ready_from, upto)
     for (; ready_from < upto; ++ready_from) {
       hipError_t ee = hipEventRecord(layer_ready[ready_from], cx->scat);
@@ -434,22 +439,21 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
       }
       piece_rows[n_piece] = l * s->capacity + slots[j];
       ++n_piece;
-      if (n_piece == cur_cap || land_base + land_n + n_piece == cap_land) {
+      if (n_piece == piece_limit) {
         if ((st = flush_piece()) != NP_OK) return bail(st);
         open = false;
       }
     }
-    if (layer_ready && (l == le - 1 || (land_n + n_piece) * rec >= group_bytes)) {
+    if (layer_ready && (l == le - 1 || (group_n + n_piece) * rec >= group_bytes)) {
       if (open) {
         if ((st = flush_piece()) != NP_OK) return bail(st);
         open = false;
       }
-      if ((st = close_round()) != NP_OK) return st;
       if ((st = record_ready(l + 1)) != NP_OK) return st;
+      group_n = 0;
     }
   }
   if (open && (st = flush_piece()) != NP_OK) return bail(st);
-  if ((st = close_round()) != NP_OK) return st;
   if (layer_ready) return record_ready(le);
   // without layer events, later work on `side` follows the whole staging
   if (cx->scattered) {

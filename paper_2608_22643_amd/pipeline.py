@@ -67,6 +67,19 @@ def _i32(n, device):
     return torch.empty(n, dtype=torch.int32, device=device)
 
 
+_MLP_POOL = None
+
+
+def _mlp_pool():
+    """One helper thread per process that enqueues MLP groups in order."""
+    global _MLP_POOL
+    if _MLP_POOL is None:
+        from concurrent.futures import ThreadPoolExecutor
+
+        _MLP_POOL = ThreadPoolExecutor(max_workers=1, thread_name_prefix="np-mlp-enqueue")
+    return _MLP_POOL
+
+
 class DecodePipeline:
     def __init__(self, cfg: W.Config, device: str = "cuda:0", tier: str = "device",
                  staging: str = "gather", overlap: bool = False, tokens: int | None = None,
@@ -146,9 +159,15 @@ class DecodePipeline:
         self.slot_of, self.neuron_of, self.last_used = _i32(L * F, dev), _i32(L * C, dev), _i32(L * F, dev)
         self.state = B.np_state(self.slot_of.data_ptr(), self.neuron_of.data_ptr(),
                                 self.last_used.data_ptr())
-        self.lists = {n: _i32(L * k, dev) for n in
-                      ("in_ids", "in_slots", "ev_ids", "ev_slots", "hit_ids", "active_slots")}
-        self.counts = _i32(L * 4, dev)
+        # the staging plan (counts, in_ids, in_slots) in one block, each part
+        # at a 16-byte boundary, so the host reads it with one copy
+        kp = (L * k + 3) // 4 * 4
+        self.plan_dev = _i32(L * 4 + 2 * kp, dev)
+        self.counts = self.plan_dev[:L * 4]
+        self.lists = {"in_ids": self.plan_dev[L * 4:L * 4 + L * k],
+                      "in_slots": self.plan_dev[L * 4 + kp:L * 4 + kp + L * k]}
+        self.lists.update({n: _i32(L * k, dev) for n in
+                           ("ev_ids", "ev_slots", "hit_ids", "active_slots")})
         self.out = B.np_delta_out(*[self.lists[n].data_ptr() for n in
                                     ("in_ids", "in_slots", "ev_ids", "ev_slots", "hit_ids",
                                      "active_slots")], self.counts.data_ptr())
@@ -180,9 +199,11 @@ class DecodePipeline:
         cuts = sorted({0, min(1, L), min(3, L), L} | set(range(3, L, 4)))
         self.chunks = list(zip(cuts[:-1], cuts[1:]))
         if staging in ("memcpy", "file"):
-            self.plan_counts = torch.empty(L * 4, dtype=torch.int32, pin_memory=True)
-            self.plan_ids = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
-            self.plan_slots = torch.empty(L * k, dtype=torch.int32, pin_memory=True)
+            self.plan_host = torch.empty(self.plan_dev.numel(), dtype=torch.int32,
+                                         pin_memory=True)
+            self.plan_counts = self.plan_host[:L * 4]
+            self.plan_ids = self.plan_host[L * 4:L * 4 + L * k]
+            self.plan_slots = self.plan_host[L * 4 + kp:L * 4 + kp + L * k]
             self.plan = B.np_stage_plan(self.plan_counts.data_ptr(), self.plan_ids.data_ptr(),
                                         self.plan_slots.data_ptr())
             self.staging_buf = torch.empty(int(staging_mib * (1 << 20)), dtype=torch.uint8,
@@ -202,6 +223,8 @@ class DecodePipeline:
         # delay on the side stream just before a token's staging
         # (delay_side) or on the main stream just before its MLPs (delay_main)
         self.delay_side = self.delay_main = None
+        # host staging with overlap: MLP groups enqueued by a helper thread
+        self.mlp_thread = True
         # memcpy staging: when a list, each step appends (bytes staged, seconds
         # from the call to the end of its copies, seconds until the call
         # returned) and waits for the staging
@@ -326,9 +349,7 @@ class DecodePipeline:
             return
         # staging through the host: the plan is read on the host first
         with torch.cuda.stream(main):
-            self.plan_counts.copy_(self.counts, non_blocking=True)
-            self.plan_ids.copy_(self.lists["in_ids"], non_blocking=True)
-            self.plan_slots.copy_(self.lists["in_slots"], non_blocking=True)
+            self.plan_host.copy_(self.plan_dev, non_blocking=True)
         self.ev_plan.record(main)
         self.ev_plan.synchronize()  # the host reads the plan
         t0 = time.perf_counter()
@@ -341,21 +362,13 @@ class DecodePipeline:
             self.delay_side(self.side)
         if self.delay_main is not None:
             self.delay_main(main)
-        for gi, (lb, le) in enumerate(groups):
-            wait = self.ev_plan if (self.overlap and gi == 0) else None
-            tc = time.perf_counter()
-            if self.staging == "file":
-                B.np_stage_file(s, self.plan, lb, le, self.storage_fd, 0, self.resident,
-                                self.staging_buf, self.staging_buf.numel(), self.io_buf,
-                                self.io_buf.nbytes, self.landing, self.landing.numel(),
-                                self.side, wait, self.layer_ready)
-            else:
-                B.np_stage_rows(s, self.plan, lb, le, self.storage, self.resident,
-                                self.staging_buf, self.staging_buf.numel(), self.landing,
-                                self.landing.numel(), self.side, wait, self.layer_ready)
-            t_call += time.perf_counter() - tc
-            if self.stage_log is not None:
-                continue  # staging alone: the MLPs follow the whole staging
+        # with overlap, a helper thread enqueues each group's MLPs while this
+        # thread packs the next groups (the library calls release the
+        # interpreter lock): packing is the host's critical path
+        helper = self.overlap and self.stage_log is None and self.mlp_thread
+        futs = []
+
+        def enqueue_group(lb, le):
             for l in range(lb, le):
                 # one wait per group, on its last layer's event: a group's
                 # layers land in one or two rounds, and each wait costs the
@@ -366,6 +379,32 @@ class DecodePipeline:
                 if l == 0 and mlp_block_events is not None:
                     mlp_block_events[0].record(main)
                 mlp(l)
+
+        try:
+            for gi, (lb, le) in enumerate(groups):
+                wait = self.ev_plan if (self.overlap and gi == 0) else None
+                tc = time.perf_counter()
+                if self.staging == "file":
+                    B.np_stage_file(s, self.plan, lb, le, self.storage_fd, 0, self.resident,
+                                    self.staging_buf, self.staging_buf.numel(), self.io_buf,
+                                    self.io_buf.nbytes, self.landing, self.landing.numel(),
+                                    self.side, wait, self.layer_ready)
+                else:
+                    B.np_stage_rows(s, self.plan, lb, le, self.storage, self.resident,
+                                    self.staging_buf, self.staging_buf.numel(), self.landing,
+                                    self.landing.numel(), self.side, wait, self.layer_ready)
+                t_call += time.perf_counter() - tc
+                if self.stage_log is not None:
+                    continue  # staging alone: the MLPs follow the whole staging
+                if helper:  # the group's layer_ready events are recorded: hand it over
+                    futs.append(_mlp_pool().submit(enqueue_group, lb, le))
+                else:
+                    enqueue_group(lb, le)
+        finally:  # the helper has finished with this token's groups
+            for fu in futs:
+                fu.exception()
+        for fu in futs:  # every MLP of this token is enqueued (errors re-raised)
+            fu.result()
         if self.stage_log is not None:  # staging alone: host packing + copies + scatter
             if self.overlap:  # the scatters run on the library's scatter stream
                 self.layer_ready[L - 1].synchronize()

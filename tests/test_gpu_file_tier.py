@@ -84,8 +84,12 @@ def test_file_tier_short_file_is_an_io_error(tmp_path):
     pi[k:k + 3] = torch.tensor([1, 2, 3])
     ps[k:k + 3] = torch.tensor([0, 1, 2])
     plan = B.np_stage_plan(pc.data_ptr(), pi.data_ptr(), ps.data_ptr())
-    cap = n0  # one chunk per layer
-    staging = torch.empty(2 * cap * (rec + 4) + 8192, dtype=torch.uint8).pin_memory()
+    # pieces of exactly one layer's five records: four 16 KiB staging pieces
+    # (five records and their rows each) and a landing ring of five, so the
+    # first piece is layer 0 whole and the failing read is in the second
+    cap = n0
+    staging = torch.empty(4 * 16384, dtype=torch.uint8).pin_memory()
+    assert (16384 // (rec + 4)) == cap
     landing = torch.empty(cap * (rec + 4), dtype=torch.uint8, device=DEV)
     io = B.HostBuffer(cap * (rec + 4))
     resident = torch.zeros(cfg.resident_bytes, dtype=torch.uint8, device=DEV)
