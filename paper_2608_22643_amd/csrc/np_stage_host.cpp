@@ -261,8 +261,9 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
   }
   int fail_after = -1;  // test hook: fail after this many pieces
   if (const char* v = getenv("NP_TEST_FAIL_STAGE_AFTER")) fail_after = atoi(v);
-  // with layer_ready: a landing round closes at a layer boundary once it
-  // holds this many bytes (NP_STAGE_GROUP_MIB, default 8 MiB)
+  // with layer_ready: at a layer boundary, once the layers since the last
+  // recorded event hold this many bytes (NP_STAGE_GROUP_MIB, default 8 MiB),
+  // the open piece is sent and their events are recorded
   size_t group_bytes = (size_t)8 << 20;
   if (const char* v = getenv("NP_STAGE_GROUP_MIB"))
     if (atoi(v) > 0) group_bytes = (size_t)atoi(v) << 20;
