@@ -29,12 +29,11 @@ namespace np {
 // (up to 128: eight 16-token tiles); wave w takes token tiles w and w + 4 of
 // every row tile over the whole reduction, so no wave needs another's sums,
 // and each token fragment a wave loads serves four row tiles.  The neurons' gate and up
-// rows stream through LDS in chunks of KC elements: the workgroup loads a
-// chunk with whole-line 16-byte loads (16 lanes per 256-byte row piece) into
-// one of two buffers while the waves multiply the other, and each wave reads
-// its MFMA fragments from LDS (rows padded by 16 bytes: no bank conflicts).
-// The token fragments come straight from memory (the tokens are L2-resident),
-// a chunk ahead in registers.
+// rows, and the chunk's token rows, stream through LDS in chunks of KC
+// elements: the workgroup loads a chunk with whole-line 16-byte loads (16
+// lanes per 256-byte row piece) into one of two buffers while the waves
+// multiply the other, and each wave reads its MFMA fragments from LDS (rows
+// padded by 16 bytes: no bank conflicts).
 constexpr int AB_WAVES = 4;
 constexpr int AB_NB = 64;         // neurons of a workgroup (AB_NB / 16 row tiles)
 constexpr int AB_MAX_TILES = 8;   // token tiles of 16
@@ -58,6 +57,9 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
   constexpr int PIECES = 2 * AB_NB * (AB_ROWB / 16);  // 16-byte pieces of a chunk (g and u)
   constexpr int PPT = PIECES / (AB_WAVES * WAVE);    // pieces per thread (8)
   __shared__ __attribute__((aligned(16))) char lds[2][2][AB_NB][AB_PITCH];  // buffer, g/u, row
+  // the chunk's token pieces: buffer, token, 16-byte column (padded rows)
+  __shared__ __attribute__((aligned(16))) char xs[2][16 * AB_MAX_TILES][AB_PITCH];
+  constexpr int XPT = 16 * AB_MAX_TILES * (AB_ROWB / 16) / (AB_WAVES * WAVE);  // token pieces per thread (8)
   const int t = threadIdx.x, lane = t & (WAVE - 1), w = t / WAVE, grp = lane / 16;
   const int n0 = blockIdx.x * AB_NB;
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes), xr = make_rsrc(a.x, a.x_bytes);
@@ -90,21 +92,29 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
       *(uint4*)&lds[buf][proj][row][col * 16] = r[i];
     }
   };
-  // token fragments: tile ti = w + 4j, token 16 ti + lane % 16
-  uint32_t t_off[TPW];
+  // the chunk's token pieces, whole 256-byte row pieces per 16 lanes like
+  // the weights (a fragment load straight from memory would touch 16 token
+  // rows per instruction): piece p -> token p / 16, 16-byte column p % 16
+  uint32_t x_off[XPT];  // byte offset at reduction index 0, or OOB
 #pragma unroll
-  for (int j = 0; j < TPW; ++j) {
-    const int tok = (w + AB_WAVES * j) * 16 + (lane & 15);
-    t_off[j] = tok < a.n ? (uint32_t)tok * dbytes : BUF_OOB;
+  for (int i = 0; i < XPT; ++i) {
+    const int pc = t + AB_WAVES * WAVE * i, tok = pc / (AB_ROWB / 16);
+    x_off[i] = tok < a.n ? (uint32_t)tok * dbytes : BUF_OOB;
   }
-  auto load_tokens = [&](int c, uint4 (&b)[SPC][TPW]) {
+  auto load_xchunk = [&](int c, uint4* r) {
 #pragma unroll
-    for (int s = 0; s < SPC; ++s) {
-      const int k = c * KC + s * KS + grp * V;
+    for (int i = 0; i < XPT; ++i) {
+      const int pc = t + AB_WAVES * WAVE * i;
+      const int k = c * KC + (pc % (AB_ROWB / 16)) * V;
+      r[i] = buf_load16(xr, (x_off[i] != BUF_OOB && k < a.d) ? x_off[i] + (uint32_t)k * ESZ
+                                                             : BUF_OOB, 0);
+    }
+  };
+  auto store_xchunk = [&](int buf, const uint4* r) {
 #pragma unroll
-      for (int j = 0; j < TPW; ++j)
-        b[s][j] = buf_load16(xr, (t_off[j] != BUF_OOB && k < a.d) ? t_off[j] + (uint32_t)k * ESZ
-                                                                 : BUF_OOB, 0);
+    for (int i = 0; i < XPT; ++i) {
+      const int pc = t + AB_WAVES * WAVE * i;
+      *(uint4*)&xs[buf][pc / (AB_ROWB / 16)][(pc % (AB_ROWB / 16)) * 16] = r[i];
     }
   };
   f32x4 accg[MT][TPW], accu[MT][TPW];
@@ -115,20 +125,24 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
 #pragma unroll
       for (int r = 0; r < 4; ++r) accg[m][j][r] = accu[m][j][r] = 0.f;
 
-  uint4 pre[PPT];
-  uint4 bcur[SPC][TPW], bnext[SPC][TPW];
+  uint4 pre[PPT], prex[XPT];
   load_chunk(0, pre);
-  load_tokens(0, bcur);
+  load_xchunk(0, prex);
   store_chunk(0, pre);
+  store_xchunk(0, prex);
   __syncthreads();
   for (int c = 0; c < chunks; ++c) {
     const int buf = c & 1;
     if (c + 1 < chunks) {  // the next chunk is in flight during this one's products
       load_chunk(c + 1, pre);
-      load_tokens(c + 1, bnext);
+      load_xchunk(c + 1, prex);
     }
 #pragma unroll
     for (int s = 0; s < SPC; ++s) {
+      uint4 b[TPW];  // token tile w + 4j: token 16 (w + 4j) + lane % 16
+#pragma unroll
+      for (int j = 0; j < TPW; ++j)
+        b[j] = *(const uint4*)&xs[buf][(w + AB_WAVES * j) * 16 + (lane & 15)][s * 64 + grp * 16];
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
         const int row = 16 * m + (lane & 15);
@@ -136,17 +150,14 @@ __global__ __launch_bounds__(AB_WAVES * WAVE) void act_batch_kernel(ActBatchArgs
         const uint4 au = *(const uint4*)&lds[buf][1][row][s * 64 + grp * 16];
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
-          accg[m][j] = mfma_step<T>(ag, bcur[s][j], accg[m][j]);
-          accu[m][j] = mfma_step<T>(au, bcur[s][j], accu[m][j]);
+          accg[m][j] = mfma_step<T>(ag, b[j], accg[m][j]);
+          accu[m][j] = mfma_step<T>(au, b[j], accu[m][j]);
         }
       }
     }
     if (c + 1 < chunks) {
       store_chunk(buf ^ 1, pre);
-#pragma unroll
-      for (int s = 0; s < SPC; ++s)
-#pragma unroll
-        for (int j = 0; j < TPW; ++j) bcur[s][j] = bnext[s][j];
+      store_xchunk(buf ^ 1, prex);
     }
     __syncthreads();  // the other buffer is complete; this one may be overwritten next
   }
