@@ -355,8 +355,8 @@ class DecodePipeline:
         t0 = time.perf_counter()
         t_call = 0.0
         # with overlap, staging runs on the side stream one layer group at a
-        # time and each group's MLPs are enqueued right after its staging
-        # call, so they run while the host packs the next groups
+        # time and each group's MLPs are enqueued once its staging call has
+        # returned, so they run while the host packs the next groups
         groups = self.chunks if self.overlap else [(0, L)]
         if self.delay_side is not None:
             self.delay_side(self.side)
@@ -371,9 +371,9 @@ class DecodePipeline:
         def enqueue_group(lb, le):
             for l in range(lb, le):
                 # one wait per group, on its last layer's event: a group's
-                # layers land in one or two rounds, and each wait costs the
-                # main stream several microseconds (7B: 460 against 405
-                # tokens/s with a wait per layer)
+                # layers land with one or two staging pieces, and each wait
+                # costs the main stream several microseconds (7B: 460 against
+                # 405 tokens/s with a wait per layer)
                 if self.overlap and l == lb:
                     main.wait_event(self.layer_ready[le - 1])
                 if l == 0 and mlp_block_events is not None:
