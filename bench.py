@@ -477,9 +477,10 @@ def pinned_host_run(cfg, host_storage, steps: int, tokens: int, t0: int = 0,
     records packed into pinned staging and sent with hipMemcpyAsync, then
     scattered) and the sparse MLPs, per token, for the step with staging on a
     side stream in layer groups (each group's MLPs run while the next group
-    is staged) and on the main stream; then the mapped-memory gather of the
-    same tier (np_stage_gather, the GPU reading pinned memory over the host
-    link).  Reports tokens/s of each, the staging rate of np_stage_rows alone
+    is staged; every fourth group is gathered by the GPU from the pinned tier
+    instead of packed) and on the main stream; then the mapped-memory gather
+    of the same tier (np_stage_gather, the GPU reading pinned memory over the
+    host link) for every group.  Reports tokens/s of each, the staging rate of np_stage_rows alone
     against a 1 GiB pinned hipMemcpyAsync of the same run, and the host's
     share (packing and enqueueing).  Each pipeline starts cold and runs 4 +
     `fill` untimed tokens first (with fill, the resident buffer is full and

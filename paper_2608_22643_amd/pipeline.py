@@ -190,6 +190,11 @@ class DecodePipeline:
         self.ws = torch.zeros(B.np_workspace_size(self.shape), dtype=torch.uint8, device=dev)
         self.main = torch.cuda.Stream(device=dev)
         self.side = torch.cuda.Stream(device=dev) if overlap else self.main
+        # host staging with overlap: every gather_every-th layer group
+        # (starting with the second) is gathered by the GPU from the pinned
+        # storage tier on a second side stream, the others packed by the host
+        self.gather_every = 4 if (overlap and tier == "host" and staging == "memcpy") else 0
+        self.side2 = torch.cuda.Stream(device=dev) if self.gather_every else None
         self.ev_delta = torch.cuda.Event()
         self.layer_ready = [torch.cuda.Event() for _ in range(L)] if overlap else None
         # staging chunks of the overlapped gather path: [0,1), [1,3), [3,L)
@@ -198,6 +203,7 @@ class DecodePipeline:
         # group's MLPs run while the next group is staged
         cuts = sorted({0, min(1, L), min(3, L), L} | set(range(3, L, 4)))
         self.chunks = list(zip(cuts[:-1], cuts[1:]))
+        self.gather_ready = [torch.cuda.Event() for _ in self.chunks] if self.gather_every else None
         if staging in ("memcpy", "file"):
             self.plan_host = torch.empty(self.plan_dev.numel(), dtype=torch.int32,
                                          pin_memory=True)
@@ -368,20 +374,43 @@ class DecodePipeline:
         helper = self.overlap and self.stage_log is None and self.mlp_thread
         futs = []
 
-        def enqueue_group(lb, le):
+        def enqueue_group(lb, le, ev=None):
             for l in range(lb, le):
                 # one wait per group, on its last layer's event: a group's
                 # layers land with one or two staging pieces, and each wait
                 # costs the main stream several microseconds (7B: 460 against
                 # 405 tokens/s with a wait per layer)
                 if self.overlap and l == lb:
-                    main.wait_event(self.layer_ready[le - 1])
+                    main.wait_event(ev if ev is not None else self.layer_ready[le - 1])
                 if l == 0 and mlp_block_events is not None:
                     mlp_block_events[0].record(main)
                 mlp(l)
 
+        # the GPU-gathered groups go first, on their own stream: the GPU reads
+        # their records over the link while the host packs the other groups
+        # (7B: 773-777 against 711-715 tokens/s with every group packed; 13B:
+        # 472 against 445-448; every second group gathered is slower)
+        gathered = set()
+        if self.gather_every and self.stage_log is None:
+            gathered = {gi for gi in range(len(groups)) if gi % self.gather_every == 1}
+            if gathered:
+                self.side2.wait_event(self.ev_plan)  # after the delta and the previous MLPs
+                if self.delay_side is not None:
+                    self.delay_side(self.side2)
+                for gi in sorted(gathered):
+                    lb, le = groups[gi]
+                    B.np_stage_gather(s, self.out, lb, le, self.storage, self.resident, self.ws,
+                                      self.side2)
+                    self.gather_ready[gi].record(self.side2)
         try:
             for gi, (lb, le) in enumerate(groups):
+                if gi in gathered:
+                    if helper:
+                        futs.append(_mlp_pool().submit(enqueue_group, lb, le,
+                                                       self.gather_ready[gi]))
+                    else:
+                        enqueue_group(lb, le, self.gather_ready[gi])
+                    continue
                 wait = self.ev_plan if (self.overlap and gi == 0) else None
                 tc = time.perf_counter()
                 if self.staging == "file":
