@@ -45,11 +45,11 @@ HBM_PEAK_GBPS = 8000.0
 MLP_COUNTERS = {
     "config": "7b",
     "sources": ("paper_2608_22643_amd/csrc/np_mlp.hip", "paper_2608_22643_amd/csrc/np_device.hpp"),
-    "sha256": "1a66cf3d0105bd0d9c4855f481fee9c9a79f3c6ca78b6985abbe9af97c537ec4"
+    "sha256": "f4501ceab414e882c8e7347a81de167eef7b38ae8efc2dfd73e1f7495d4605cf"
               "9e0e1f0b7a61ef93b9be1fc993a31341e591454ab40b4db720567ea646fc39f8",
-    "fetch_kib": {"rows": 19929.9, "reduce": 1681.5},
-    "write_kib": {"rows": 3374.6, "reduce": 8.0},
-    "copy_fetch_kib": 131087.9, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
+    "fetch_kib": {"rows": 19930.0, "reduce": 1681.5},
+    "write_kib": {"rows": 3373.6, "reduce": 8.0},
+    "copy_fetch_kib": 131088.2, "copy_write_kib": 262144.0, "copy_kib": 262144.0,
 }
 
 
