@@ -501,6 +501,10 @@ def pinned_host_run(cfg, host_storage, steps: int, tokens: int, t0: int = 0,
         torch.cuda.synchronize()
         wall, _ = timed_steps(p, t0 + 4 + fill, steps, with_mlp_events=False)
         rec = {"tok_s": round(steps / wall, 2), "ms_per_token": round(wall * 1e3 / steps, 3)}
+        if p.gather_every:
+            rec["gpu_gathered_groups"] = (f"every {p.gather_every}th layer group from the "
+                                          f"second on, {p.gather_every - 1} in {p.gather_every} "
+                                          f"packed by the host (staging alone: every group packed)")
         if staging == "memcpy":
             rec.update(staging_rates(p, t0 + 4 + fill + steps, max(3, steps // 2)))
             if best is None or rec["tok_s"] > out[best]["tok_s"]:
