@@ -129,11 +129,12 @@ static PackPool* pack_pool() {
 }
 
 // State of one pinned staging buffer (keyed by device and base address):
-// an event per staging piece (its copy has finished reading the piece) and
-// the scatter stream with its events.  Copies run on the caller's side
-// stream back to back; each landed piece's scatter runs on the buffer's own
-// scatter stream (default priority) once its copy is done (ev_copied), so the
-// copy engine never waits for a kernel between two copies.  ev_scattered
+// an event per staging piece (its copy has finished: the piece may be
+// packed again, and its scatter may start) and the scatter stream with its
+// last event.  Copies run on the caller's side stream back to back; each
+// landed piece's scatter runs on the buffer's own scatter stream (default
+// priority) once the piece's event has fired, so the copy engine never waits
+// for a kernel between two copies.  ev_scattered
 // marks the last scatter: the side stream waits on it before copies reuse
 // the landing area and at the end of each call, so work the caller puts on
 // `side` later follows the scatters.
@@ -146,7 +147,7 @@ struct StageCtx {
   bool pending[MAX_PIECES] = {};
   int next_piece = 0;  // the piece ring continues across calls
   hipStream_t scat = nullptr;
-  hipEvent_t ev_copied = nullptr, ev_scattered = nullptr;
+  hipEvent_t ev_scattered = nullptr;
   bool scattered = false;  // ev_scattered has been recorded
   // the landing area is a ring of landed pieces (byte positions, each piece
   // at a 16-byte boundary) that continues across calls; the copies wait for
@@ -250,11 +251,10 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
       e = hipEventCreateWithFlags(&cx->ev[i], hipEventDisableTiming);
       if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
     }
-  for (hipEvent_t* ev : {&cx->ev_copied, &cx->ev_scattered})
-    if (!*ev) {
-      e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
-      if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
-    }
+  if (!cx->ev_scattered) {
+    e = hipEventCreateWithFlags(&cx->ev_scattered, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+  }
   if (!cx->scat) {
     e = hipStreamCreateWithFlags(&cx->scat, hipStreamNonBlocking);
     if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags (scatter stream)");
@@ -296,9 +296,16 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
   // piece_limit records; group_n: records sent since the last layer_ready
   // event
   size_t n_piece = 0, group_n = 0, pos = cx->land_pos, piece_limit = 1;
-  // the first piece is small (2 MiB) so that the copy engine starts early,
-  // unless it is still busy with the previous call's pieces
-  size_t cur_cap = std::min(piece_cap, std::max<size_t>(1, ((size_t)2 << 20) / rec));
+  // the first piece is small (NP_STAGE_FIRST_KIB, default 2 MiB) so that the
+  // copy engine starts early, unless it is still busy with the previous
+  // call's pieces; each later piece is NP_STAGE_GROWTH_PCT percent of the
+  // one before (default 200), up to the piece capacity
+  size_t first_bytes = (size_t)2 << 20, growth_pct = 200;
+  if (const char* v = getenv("NP_STAGE_FIRST_KIB"))
+    if (atoi(v) > 0) first_bytes = (size_t)atoi(v) << 10;
+  if (const char* v = getenv("NP_STAGE_GROWTH_PCT"))
+    if (atoi(v) >= 100) growth_pct = (size_t)atoi(v);
+  size_t cur_cap = std::min(piece_cap, std::max<size_t>(1, first_bytes / rec));
   {
     const int ph = (h + n_pieces - 1) % n_pieces;
     if (cx->pending[ph] && hipEventQuery(cx->ev[ph]) == hipErrorNotReady) cur_cap = piece_cap;
@@ -369,9 +376,10 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
     ee = hipEventRecord(cx->ev[h], side);
     if (ee != hipSuccess) return hip_fail(ee, "hipEventRecord");
     cx->pending[h] = true;
-    // the piece's scatter, after its copy, on the scatter stream
-    ee = hipEventRecord(cx->ev_copied, side);
-    if (ee == hipSuccess) ee = hipStreamWaitEvent(cx->scat, cx->ev_copied, 0);
+    // the piece's scatter, after its copy (the same event: each event
+    // recorded behind a copy costs the side stream ~5 us), on the scatter
+    // stream
+    ee = hipStreamWaitEvent(cx->scat, cx->ev[h], 0);
     if (ee != hipSuccess) return hip_fail(ee, "scatter stream ordering");
     ee = launch_stage_scatter(*s, landing + pos, (const int32_t*)(landing + pos + rec_bytes),
                               (int)n_piece, dev_resident, cx->scat);
@@ -386,7 +394,7 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
     cx->land_pos = pos;
     group_n += n_piece;
     n_piece = 0;
-    cur_cap = std::min(piece_cap, 2 * cur_cap);
+    cur_cap = std::min(piece_cap, std::max(cur_cap + 1, cur_cap * growth_pct / 100));
     return NP_OK;
   };
   // before a piece is packed: its size (the current piece size, at most
