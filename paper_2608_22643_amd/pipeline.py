@@ -244,10 +244,16 @@ class DecodePipeline:
         B.np_state_reset(self.shape, self.state, self.ws, self.main, self.resident)
         self.main.synchronize()
 
+    def _check_token(self, t: int) -> None:
+        if not 0 <= t < self.T:
+            raise IndexError(f"token {t} outside the {self.T} tokens this pipeline holds")
+
     def x_ptr(self, t: int) -> int:
+        self._check_token(t)
         return self.h.data_ptr() + t * self.row_bytes
 
     def f_ptr(self, t: int) -> int:
+        self._check_token(t)
         return self.feat.data_ptr() + t * self.feat_bytes
 
     def step(self, t: int, mlp_block_events=None) -> None:
@@ -283,6 +289,7 @@ class DecodePipeline:
         after a cold start)."""
         if t != self.graph_t:
             raise ValueError(f"graph tokens run in order from 0: expected {self.graph_t}, got {t}")
+        self._check_token(t)  # the graph reads row t of the hidden states
         with torch.cuda.stream(self.main):
             self.graph.replay()
         self.graph_t += 1

@@ -413,6 +413,11 @@ def test_lockstep_tiny(tier, staging, overlap):
         for l in range(L):
             _, ref64 = orc.sparse_mlp(cfg, l, h[t], store, ids[l], want_f64=True)
             assert np.all(np.abs(y[l] - ref64) <= mlp_tolerance("f32", ref64))
+    # a token past the pipeline's hidden states is refused before anything
+    # is enqueued (its row of h does not exist)
+    for bad in (T, -1):
+        with pytest.raises(IndexError):
+            pipe.step(bad)
     assert pipe.device_error() == 0
 
 
@@ -450,4 +455,6 @@ def test_graph_replay_matches_eager(name, overlap):
         compare_delta(el, ref, L)
         occupied = torch.from_numpy(np.repeat(st.neuron_of.reshape(-1) >= 0, cfg.record_bytes))
         assert torch.equal(graph.resident.cpu()[occupied], eager.resident.cpu()[occupied]), t
+    with pytest.raises(IndexError):  # the pipeline holds T rows of h: one more would read past them
+        graph.step_graph(T)
     assert graph.device_error() == 0 and eager.device_error() == 0
