@@ -299,7 +299,8 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
   // the first piece is small (NP_STAGE_FIRST_KIB, default 2 MiB) so that the
   // copy engine starts early, unless it is still busy with the previous
   // call's pieces; each later piece is NP_STAGE_GROWTH_PCT percent of the
-  // one before (default 200), up to the piece capacity
+  // one before (default 200; 100 keeps every piece at the first size), up
+  // to the piece capacity
   size_t first_bytes = (size_t)2 << 20, growth_pct = 200;
   if (const char* v = getenv("NP_STAGE_FIRST_KIB"))
     if (atoi(v) > 0) first_bytes = (size_t)atoi(v) << 10;
@@ -394,7 +395,8 @@ static np_status stage_common(const char* fn, const np_shape* s, const np_stage_
     cx->land_pos = pos;
     group_n += n_piece;
     n_piece = 0;
-    cur_cap = std::min(piece_cap, std::max(cur_cap + 1, cur_cap * growth_pct / 100));
+    if (growth_pct > 100)  // at least one record more, so that small pieces grow too
+      cur_cap = std::min(piece_cap, std::max(cur_cap + 1, cur_cap * growth_pct / 100));
     return NP_OK;
   };
   // before a piece is packed: its size (the current piece size, at most

@@ -252,6 +252,17 @@ def test_stage_chunk_invariance(records, mode):
     stage_and_check(cfg, mode, staging_records=records)
 
 
+@pytest.mark.parametrize("first_kib,growth", [(1, 100), (1, 150), (64, 100), (8192, 300)])
+def test_stage_piece_schedule_invariance(first_kib, growth, monkeypatch):
+    """The placed bytes do not depend on how the staging pieces are sized:
+    one-record pieces throughout, pieces growing from one record, a fixed
+    small size, and a first piece larger than the piece capacity."""
+    monkeypatch.setenv("NP_STAGE_FIRST_KIB", str(first_kib))
+    monkeypatch.setenv("NP_STAGE_GROWTH_PCT", str(growth))
+    say(f"[stage pieces] first {first_kib} KiB, growth {growth}%")
+    stage_and_check(SHAPES["ragged_f16"], "memcpy", staging_records=1000)
+
+
 def test_stage_rows_rejects_small_staging():
     cfg = SHAPES["tiny"]
     bufs = Bufs(cfg)
