@@ -444,30 +444,51 @@ def h2d_peak_gbps(nbytes: int = 1 << 30) -> float:
 
 def staging_rates(pipe, t0: int, steps: int) -> dict:
     """np_stage_rows alone (memcpy tier): staged bytes over the time from the
-    call (host packing included) to the end of its copies and scatters, next
-    to a 1 GiB pinned hipMemcpyAsync measured in the same run; and the host
-    side alone: the time until the call returns, when every record has been
-    packed into pinned staging and every chunk's copy enqueued (a chunk waits
-    for a staging half to drain when one token's records fill more than
-    one)."""
-    pipe.stage_log = []
-    trace_marker()  # a kernel trace shows this window's copies between two markers
-    for i in range(steps):
-        pipe.step(t0 + i)
+    plan's arrival on the host (host packing included) to the end of its
+    copies and scatters as the host sees it, next to a 1 GiB pinned
+    hipMemcpyAsync measured in the same run; the same span on the device (the
+    event after the plan's copy to the event after the last scatter, both
+    timing-enabled for this window), which leaves out how long the host takes
+    to wake from its waits; and the host side alone: the time until the
+    calls return, when every record has been packed into pinned staging and
+    every piece's copy enqueued."""
     import torch
 
-    torch.cuda.synchronize()
+    L = pipe.cfg.layers
+    plan_ev, last_ev = pipe.ev_plan, pipe.layer_ready[L - 1] if pipe.layer_ready else None
+    timed = last_ev is not None
+    if timed:  # the pipeline's own events, swapped for timing-enabled ones
+        pipe.ev_plan = torch.cuda.Event(enable_timing=True)
+        pipe.layer_ready[L - 1] = torch.cuda.Event(enable_timing=True)
+        pipe.layer_ready[L - 1].record(pipe.side)
+    dev_s = 0.0
+    pipe.stage_log = []
+    trace_marker()  # a kernel trace shows this window's copies between two markers
+    try:
+        for i in range(steps):
+            pipe.step(t0 + i)  # waits for the token's staging before it returns
+            if timed:
+                dev_s += pipe.ev_plan.elapsed_time(pipe.layer_ready[L - 1]) * 1e-3
+        torch.cuda.synchronize()
+    finally:
+        if timed:
+            torch.cuda.synchronize()
+            pipe.ev_plan, pipe.layer_ready[L - 1] = plan_ev, last_ev
     trace_marker()
     nb = sum(e[0] for e in pipe.stage_log)
     sec = sum(e[1] for e in pipe.stage_log)
     call = sum(e[2] for e in pipe.stage_log)
     pipe.stage_log = None
-    return {"staging_h2d_GBps": round(nb / sec / 1e9, 2),
-            "staged_MB_per_token": round(nb / steps / 1e6, 2), "tokens": steps,
-            "staged_bytes": int(nb),
-            "staging_ms_per_token": round(sec * 1e3 / steps, 3),
-            "host_call_ms_per_token": round(call * 1e3 / steps, 3),
-            "h2d_peak_GBps": round(h2d_peak_gbps(), 2)}
+    out = {"staging_h2d_GBps": round(nb / sec / 1e9, 2),
+           "staged_MB_per_token": round(nb / steps / 1e6, 2), "tokens": steps,
+           "staged_bytes": int(nb),
+           "staging_ms_per_token": round(sec * 1e3 / steps, 3),
+           "host_call_ms_per_token": round(call * 1e3 / steps, 3)}
+    if timed:
+        out["device_staging_GBps"] = round(nb / dev_s / 1e9, 2)
+        out["device_staging_ms_per_token"] = round(dev_s * 1e3 / steps, 3)
+    out["h2d_peak_GBps"] = round(h2d_peak_gbps(), 2)
+    return out
 
 
 def pinned_host_run(cfg, host_storage, steps: int, tokens: int, t0: int = 0,
@@ -516,6 +537,8 @@ def pinned_host_run(cfg, host_storage, steps: int, tokens: int, t0: int = 0,
         torch.cuda.empty_cache()
     out["tok_s"] = out[best]["tok_s"]
     out["staging_GBps"] = out[best]["staging_h2d_GBps"]
+    if "device_staging_GBps" in out[best]:
+        out["device_staging_GBps"] = out[best]["device_staging_GBps"]
     out["h2d_peak_GBps"] = out[best]["h2d_peak_GBps"]
     out["mode"] = best
     return out
@@ -1187,7 +1210,8 @@ def pinned_host_summary(main_name, host, big, extra) -> dict | None:
     host memory and np_stage_rows staging (the step's stated tier for 13B and
     70B, where only part of the rows fits the resident buffer), per
     configuration: tokens/s of the faster np_stage_rows mode, its staging
-    rate and the same run's pinned-copy peak.  PCIe-inclusive; the headline
+    rate (as the host sees it, and between device events) and the same run's
+    pinned-copy peak.  PCIe-inclusive; the headline
     `value` keeps the storage tier in HBM."""
     rows = {}
     for name, h in [(main_name, host)] + [(n, (v or {}).get("host_tier"))
@@ -1195,7 +1219,7 @@ def pinned_host_summary(main_name, host, big, extra) -> dict | None:
         if h:
             rows[name] = {"tok_s": h["tok_s"], "staging_GBps": h["staging_GBps"],
                           "h2d_peak_GBps": h["h2d_peak_GBps"], "mode": h["mode"]}
-            for key in ("layers", "ms_per_layer", "note"):
+            for key in ("device_staging_GBps", "layers", "ms_per_layer", "note"):
                 if key in h:
                     rows[name][key] = h[key]
     return rows or None
