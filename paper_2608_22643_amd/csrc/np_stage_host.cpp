@@ -191,9 +191,9 @@ struct StageSource {
 // records into their slots (layer * C + slot).  With layer_ready, at a layer
 // boundary once the layers since the last event hold enough bytes, the open
 // piece is sent and the events of those layers are recorded behind its
-// scatter.  Pieces start small and double (2 MiB, 4, 8, ...) so the first
-// copy starts after little packing; packing piece i + 1 overlaps the copy of
-// piece i.
+// scatter.  Pieces start small and grow (by default 2 MiB, then doubling)
+// so the first copy starts after little packing; packing piece i + 1
+// overlaps the copy of piece i.
 static np_status stage_common(const char* fn, const np_shape* s, const np_stage_plan* plan,
                               int32_t lb, int32_t le, const StageSource& src, void* dev_resident,
                               void* host_staging, size_t staging_bytes, void* dev_landing,
