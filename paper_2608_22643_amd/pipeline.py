@@ -11,10 +11,12 @@ Staging modes:
             tier is device memory ("device" tier) or mapped pinned host memory
             ("host" tier, read over the host link by the kernel).  No host
             synchronisation anywhere in the step.
-  "memcpy"  np_stage_rows: the incoming lists are copied to pinned host
-            memory, the host packs coalesced records into pinned staging and
-            each chunk goes over with hipMemcpyAsync on a side stream, then a
-            scatter kernel places the records.  Needs the "host" tier.
+  "memcpy"  np_stage_rows: the delta's plan (counts, incoming ids and slots)
+            is copied to pinned host memory, the host packs coalesced records
+            into pinned staging pieces and each piece (records and their
+            destination rows) goes over with one hipMemcpyAsync on a side
+            stream, then a scatter kernel places its records.  Needs the
+            "host" tier.
   "file"    np_stage_file: as "memcpy", but the coalesced records are read
             from the storage tier in a file (tier "file"; O_DIRECT when the
             record size allows) through io_uring, up to 256 reads in flight
@@ -35,8 +37,11 @@ four layers at a time) on a side stream, each group followed by events, and
 layer l's MLP waits only for the group holding layer l: staging later layers
 overlaps the MLPs of earlier ones.  Gather staging puts the first group on the
 main stream; host staging (memcpy, file) calls np_stage_rows / np_stage_file
-once per group and enqueues that group's MLPs right after the call, so they
-run while the host packs the next group.  The side stream waits for np_delta
+once per group and hands that group's MLPs to a helper thread right after
+the call, so they run while the host packs the next group; with memcpy
+staging every gather_every-th group (the second, the sixth, ...) is instead
+copied by np_stage_gather from the pinned tier on a second side stream, the
+GPU reading it over the host link while the host packs.  The side stream waits for np_delta
 of the same token, which itself follows the previous token's MLP on the main
 stream, so a victim slot is never overwritten while the previous token still
 reads it.
@@ -197,7 +202,6 @@ class DecodePipeline:
         self.side2 = torch.cuda.Stream(device=dev) if self.gather_every else None
         self.ev_delta = torch.cuda.Event()
         self.layer_ready = [torch.cuda.Event() for _ in range(L)] if overlap else None
-        # staging chunks of the overlapped gather path: [0,1), [1,3), [3,L)
         # staging groups of the overlapped paths: layer 0, layers 1-2, then
         # four layers at a time, so the first MLPs start early and each later
         # group's MLPs run while the next group is staged
@@ -215,7 +219,7 @@ class DecodePipeline:
             self.staging_buf = torch.empty(int(staging_mib * (1 << 20)), dtype=torch.uint8,
                                            pin_memory=True)
             # file reads land in ordinary host memory (a direct read cannot
-            # target pinned memory), one staging half at a time
+            # target pinned memory), one staging piece at a time
             self.io_buf = (B.HostBuffer(int(staging_mib * (1 << 20)) // 2) if staging == "file"
                            else None)
             self.landing = torch.empty(int(landing_mib * (1 << 20)), dtype=torch.uint8, device=dev)
@@ -232,8 +236,9 @@ class DecodePipeline:
         # host staging with overlap: MLP groups enqueued by a helper thread
         self.mlp_thread = True
         # memcpy staging: when a list, each step appends (bytes staged, seconds
-        # from the call to the end of its copies, seconds until the call
-        # returned) and waits for the staging
+        # from the plan's arrival on the host to the end of the copies and
+        # scatters, seconds spent in the staging calls) and waits for the
+        # staging before it enqueues the MLPs
         self.stage_log = None
         self.reset()
 
