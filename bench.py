@@ -564,8 +564,9 @@ def file_tier_run(cfg, host_storage, steps: int) -> dict:
 
     T = 1 + 3 + 2 * steps + 4
     t = time.perf_counter()
-    # staging halves (and the read buffer) of 128 MiB: a token's delta is
-    # read as one batch, the paper's token-level submission
+    # staging pieces of 64 MiB and a read buffer of 128 MiB: each layer
+    # group's records are read as one batch of requests (the paper's
+    # token-level submission, per group)
     pipe = DecodePipeline(cfg, tier="file", staging="file", overlap=True, tokens=T,
                           host_storage=host_storage, staging_mib=256, landing_mib=128)
     write_s = time.perf_counter() - t

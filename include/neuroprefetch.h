@@ -329,8 +329,9 @@ np_status np_stage_rows(const np_shape* shape, const np_stage_plan* plan,
  * so a direct-I/O descriptor needs io_buffer.  fd: a readable descriptor
  * owned by the caller; opened with O_DIRECT, the reads bypass the page cache
  * and the record size, file_offset and the read target must be multiples of
- * 512 bytes.  A failed or short read (end of file) returns NP_ERR_IO; chunks
- * already enqueued stay enqueued.  Everything else as np_stage_rows. */
+ * 512 bytes.  A failed or short read (end of file) returns NP_ERR_IO; the
+ * pieces copied before it are still scattered.  Everything else as
+ * np_stage_rows. */
 np_status np_stage_file(const np_shape* shape, const np_stage_plan* plan,
                         int32_t layer_begin, int32_t layer_end, int32_t fd,
                         int64_t file_offset, void* dev_resident, void* host_staging,
