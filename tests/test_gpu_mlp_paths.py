@@ -7,7 +7,9 @@ NP_MLP_COLSPLIT=1).  Row counts from 0 to the path's
 maximum (fewer rows than workgroups, one row per workgroup, ragged), device
 counts, SwiGLU with eq. 1 thresholds, a slot outside the buffer, and bit-for-
 bit repeatability of each path; workgroups of 4 to 10 waves of one-vector
-slices (d 512 to 5120) and of 8 waves of two-vector slices (d 8192)."""
+slices (d 512 to 5120) and of 8 waves of two-vector slices (d 8192); and
+dyadic records on every shape and path, where y must equal the oracle's
+exactly."""
 import numpy as np
 import pytest
 import torch
@@ -84,6 +86,48 @@ def test_mlp_paths_row_counts(name, path, monkeypatch):
                                       want_f64=True)
             got = decode_y(orc, cfg.adtype, y.cpu().numpy())
             assert np.all(np.abs(got - ref64) <= mlp_tolerance(cfg.adtype, ref64)), (n, l)
+    assert B.np_device_error(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("path", list(PATHS))
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_mlp_paths_dyadic_bit_exact(name, path, monkeypatch):
+    """Dyadic records (m 2^-6, |m| <= 1) and x in {-1, 0, 1}: g and u are
+    multiples of 2^-6, a of 2^-12 below 2^12 and every partial sum of y a
+    multiple of 2^-18 below 2^6, so every sum is exact in fp32 in any order
+    and y is the exact value rounded once to nearest even -- on every launch
+    shape of the rows kernel (4 to 10 waves of one-vector slices, 8 waves of
+    two-vector slices in 4-row rounds), every reduction path and every row
+    count, the GPU's y equals the oracle's value for value (the sign of a
+    zero aside)."""
+    for k_, v_ in PATHS[path].items():
+        monkeypatch.setenv(k_, v_)
+    cfg = SHAPES[name].with_(dyadic=True, dyadic_w_range=1, dyadic_h_range=1)
+    d, k, C = cfg.d_model, cfg.k, cfg.capacity
+    bands = d // 16
+    say(f"[mlp path dyadic] {name} {path}")
+    bufs, rng, store, res, neuron, h = setup(cfg, 24)
+    x = to_dev(h)
+    xv = orc.decode(cfg.adtype, h)
+    assert set(np.unique(xv)) <= {-1.0, 0.0, 1.0}
+    esz = W.ITEMSIZE[cfg.adtype]
+    y = torch.zeros(d * esz, dtype=torch.uint8, device=DEV)
+    slots = rng.permutation(C)[:k].astype(np.int32)  # any order of slots
+    sl = to_dev(slots)
+    for l in range(cfg.layers):
+        rec = orc.decode(cfg.wdtype, store[l][neuron[l][slots]])
+        assert np.all(np.abs(rec) * 64 <= 1) and np.all(rec * 64 == np.round(rec * 64))
+        g, u = rec[:, :d] @ xv, rec[:, d:2 * d] @ xv
+        a = np.maximum(g, 0) * u
+        assert np.max(np.abs(a)) < 2.0 ** 12
+        assert np.max(np.abs(a) @ np.abs(rec[:, 2 * d:])) < 2.0 ** 6
+    for n in sorted({0, 1, 7, bands - 1, bands, bands + 1, k // 2 + 3, k}):
+        for l in range(cfg.layers):
+            B.np_sparse_mlp(bufs.shape, l, x, res, sl, n, y, bufs.ws)
+            torch.cuda.synchronize()
+            ref = orc.sparse_mlp(cfg, l, h, store, neuron[l][slots[:n]].astype(np.int32))
+            got = decode_y(orc, cfg.adtype, y.cpu().numpy())
+            assert np.array_equal(got, decode_y(orc, cfg.adtype, ref)), (n, l)
     assert B.np_device_error(bufs.ws) == 0
 
 
