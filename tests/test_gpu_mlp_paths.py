@@ -128,6 +128,23 @@ def test_mlp_paths_dyadic_bit_exact(name, path, monkeypatch):
             ref = orc.sparse_mlp(cfg, l, h, store, neuron[l][slots[:n]].astype(np.int32))
             got = decode_y(orc, cfg.adtype, y.cpu().numpy())
             assert np.array_equal(got, decode_y(orc, cfg.adtype, ref)), (n, l)
+    # eq. 1 on exact activations: a threshold equal to one row's |a| keeps
+    # that row (only a magnitude below the threshold is zeroed), one just
+    # above it drops the row
+    for l in range(cfg.layers):
+        rec = orc.decode(cfg.wdtype, store[l][neuron[l][slots]])
+        a = np.maximum(rec[:, :d] @ xv, 0) * (rec[:, d:2 * d] @ xv)
+        mags = np.unique(np.abs(a[a != 0]))
+        t0 = np.float32(mags[len(mags) // 2])
+        assert float(t0) == mags[len(mags) // 2]  # exact in fp32
+        for thr in (t0, np.nextafter(t0, np.float32(np.inf))):
+            T = to_dev(np.full(cfg.layers, thr, np.float32))
+            B.np_sparse_mlp_t(bufs.shape, l, x, res, sl, k, None, T, y, bufs.ws)
+            torch.cuda.synchronize()
+            ref = orc.sparse_mlp(cfg, l, h, store, neuron[l][slots].astype(np.int32),
+                                 threshold=float(thr))
+            got = decode_y(orc, cfg.adtype, y.cpu().numpy())
+            assert np.array_equal(got, decode_y(orc, cfg.adtype, ref)), (l, float(thr))
     assert B.np_device_error(bufs.ws) == 0
 
 
