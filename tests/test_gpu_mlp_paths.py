@@ -42,6 +42,14 @@ SHAPES = {
 }
 PATHS = {"colsplit": {"NP_MLP_COLSPLIT": "1"}, "two_kernel": {},
          "fused": {"NP_MLP_FUSED": "1"}}
+# further launch rules at the 7B width, checked with dyadic records: two
+# rounds of 8 rows (k above 8 x 256), and a small set in 4-row rounds on
+# twice the workgroups (fewer than 128 workgroups of 8 rows)
+DYADIC_SHAPES = {**SHAPES,
+                 "d4096_f16_k3302": cfg_small("d4096_f16_k3302", 1, 4096, 6000, 16, 3302, 4000,
+                                              "f16"),
+                 "d4096_f16_k550": cfg_small("d4096_f16_k550", 1, 4096, 6000, 16, 550, 4000,
+                                             "f16")}
 
 
 def resident_of(cfg, store, rng):
@@ -90,19 +98,20 @@ def test_mlp_paths_row_counts(name, path, monkeypatch):
 
 
 @pytest.mark.parametrize("path", list(PATHS))
-@pytest.mark.parametrize("name", list(SHAPES))
+@pytest.mark.parametrize("name", list(DYADIC_SHAPES))
 def test_mlp_paths_dyadic_bit_exact(name, path, monkeypatch):
     """Dyadic records (m 2^-6, |m| <= 1) and x in {-1, 0, 1}: g and u are
     multiples of 2^-6, a of 2^-12 below 2^12 and every partial sum of y a
     multiple of 2^-18 below 2^6, so every sum is exact in fp32 in any order
     and y is the exact value rounded once to nearest even -- on every launch
     shape of the rows kernel (4 to 10 waves of one-vector slices, 8 waves of
-    two-vector slices in 4-row rounds), every reduction path and every row
+    two-vector slices in 4-row rounds, two rounds of 8 rows, a small set in
+    4-row rounds), every reduction path and every row
     count, the GPU's y equals the oracle's value for value (the sign of a
     zero aside)."""
     for k_, v_ in PATHS[path].items():
         monkeypatch.setenv(k_, v_)
-    cfg = SHAPES[name].with_(dyadic=True, dyadic_w_range=1, dyadic_h_range=1)
+    cfg = DYADIC_SHAPES[name].with_(dyadic=True, dyadic_w_range=1, dyadic_h_range=1)
     d, k, C = cfg.d_model, cfg.k, cfg.capacity
     bands = d // 16
     say(f"[mlp path dyadic] {name} {path}")
