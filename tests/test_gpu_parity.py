@@ -70,6 +70,41 @@ def test_predict(name, mfma, monkeypatch):
         assert np.all(np.abs(got - ref) <= tol), np.max(np.abs(got - ref) / tol)
 
 
+# the widths and ranks of the 7B, 13B and 70B predictors (fewer rows of B),
+# and the largest 16-bit shape the check accepts
+PREDICT_DYADIC = {
+    "w7b": cfg_small("w7b", 2, 4096, 3000, 416, 300, 600, "f16"),
+    "w13b": cfg_small("w13b", 2, 5120, 3000, 512, 300, 600, "f16"),
+    "w70b": cfg_small("w70b", 2, 8192, 3000, 768, 300, 600, "bf16"),
+    "d_max_f16": SHAPES["d_max_f16"],
+}
+
+
+@pytest.mark.parametrize("mfma", ["0", "1"])
+@pytest.mark.parametrize("name", list(PREDICT_DYADIC))
+def test_predict_dyadic_bit_exact(name, mfma, monkeypatch):
+    """Dyadic factors (entries m 2^-3, |m| <= 1) and h in {-1, 0, 1}: z is a
+    multiple of 2^-3 below d 2^-3 and every partial sum of a score a
+    multiple of 2^-6 below r d 2^-6 <= 2^18, so both predictor paths (the
+    matrix-core one splitting z into 16-bit parts) compute every score
+    exactly, and the GPU's scores equal O1's bit for bit."""
+    monkeypatch.setenv("NP_PREDICT_MFMA", mfma)
+    cfg = PREDICT_DYADIC[name].with_(dyadic=True, dyadic_h_range=1)
+    assert cfg.rank * cfg.d_model <= 2 ** 24
+    say(f"[predict dyadic] {name} mfma={mfma} d={cfg.d_model} r={cfg.rank}")
+    bufs = Bufs(cfg)
+    A, Bm = W.predictor(cfg)
+    h = W.hidden(cfg, 2)
+    assert set(np.unique(orc.decode(cfg.adtype, h))) <= {-1.0, 0.0, 1.0}
+    dA, dB = to_dev(A), to_dev(Bm)
+    for t in range(2):
+        B.np_predict(bufs.shape, to_dev(h[t]), dA, dB, bufs.scores, bufs.ws)
+        torch.cuda.synchronize()
+        got = from_dev(bufs.scores, np.float32, (cfg.layers, cfg.d_ffn))
+        ref = orc.predict(cfg, h[t], A, Bm).reshape(cfg.layers, cfg.d_ffn)
+        assert np.array_equal(got, ref), (t, int(np.sum(got != ref)))
+
+
 @pytest.mark.parametrize("scale", [3e2, 1e-4])
 @pytest.mark.parametrize("name", ["ragged_f16", "ragged_bf16", "wide_f16"])
 def test_predict_mfma_z_range(name, scale, monkeypatch):
