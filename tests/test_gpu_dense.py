@@ -37,6 +37,33 @@ def test_dense_mlp(name):
     assert B.np_device_error(bufs.ws) == 0
 
 
+def test_dense_mlp_dyadic_7b_width():
+    """A whole 7B-sized dense layer (d 4096, F 11008: the rows kernel in
+    several rounds) on dyadic records (m 2^-6, |m| <= 1) and x in {-1, 0, 1}:
+    every sum exact while max|a| < 2^12 and every column's sum of |a_n D_nj|
+    stays below 2^6 (checked), so y equals O6's value for value."""
+    cfg = W.Config("dense_dyadic", 1, 4096, 11008, 16, 0.15, 0.5, "f16", "f16", 2,
+                   rho_given=0.5, dyadic=True, dyadic_w_range=1, dyadic_h_range=1)
+    d = cfg.d_model
+    say("[dense dyadic] d=4096 F=11008")
+    bufs = Bufs(cfg)
+    store = W.storage(cfg)
+    h = W.hidden(cfg, 2)
+    rec = orc.decode(cfg.wdtype, store[0])
+    w = to_dev(store[0])
+    y = torch.zeros(d * 2, dtype=torch.uint8, device=DEV)
+    for t in range(2):
+        xv = orc.decode(cfg.adtype, h[t])
+        a = np.maximum(rec[:, :d] @ xv, 0) * (rec[:, d:2 * d] @ xv)
+        assert np.max(np.abs(a)) < 2.0 ** 12 and np.max(np.abs(a) @ np.abs(rec[:, 2 * d:])) < 2.0 ** 6
+        B.np_dense_mlp(bufs.shape, w, to_dev(h[t]), y, bufs.ws)
+        torch.cuda.synchronize()
+        ref = orc.dense_mlp(cfg, 0, h[t], store)
+        assert np.array_equal(decode_y(orc, cfg.adtype, y.cpu().numpy()),
+                              decode_y(orc, cfg.adtype, ref)), t
+    assert B.np_device_error(bufs.ws) == 0
+
+
 @pytest.mark.parametrize("tier,staging,overlap", [("device", "gather", False),
                                                   ("host", "memcpy", True),
                                                   ("file", "file", True)])

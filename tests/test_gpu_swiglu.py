@@ -178,6 +178,32 @@ def test_act_batch(name, n, act):
     assert not np.isnan(got).any()  # every output written
 
 
+@pytest.mark.parametrize("d,F,wdt,n", [(4096, 2000, "f16", 1), (4096, 2000, "f16", 128),
+                                       (4096, 2000, "f16", 129), (5120, 1000, "f16", 77),
+                                       (8192, 1000, "bf16", 64)])
+def test_act_batch_dyadic_bit_exact(d, F, wdt, n):
+    """The matrix-core batch activations on dyadic records (m 2^-6, |m| <= 1)
+    and tokens in {-1, 0, 1}, ReLU-gated: g and u are multiples of 2^-6 below
+    d 2^-6 and a = max(g, 0) u a multiple of 2^-12 below 2^12, all exact in
+    fp32, so every activation equals O9's: the 7B, 13B and 70B widths, a
+    ragged tile of neurons (F not a multiple of 64), one token, a full
+    launch of 128 and one token past it."""
+    cfg = W.Config("act_dyadic", 1, d, F, 16, 0.1, 0.5, wdt, wdt, n, rho_given=0.5,
+                   dyadic=True, dyadic_w_range=1, dyadic_h_range=1)
+    say(f"[act batch dyadic] d={d} F={F} {wdt} n={n}")
+    shape = B.make_shape(1, d, F, cfg.rank, cfg.k, cfg.capacity, wdt, wdt, "relu")
+    store = W.storage(cfg, 0, 1)
+    X = W.hidden(cfg, n)
+    assert set(np.unique(orc.decode(wdt, X))) <= {-1.0, 0.0, 1.0}
+    acts = torch.full((n * F,), float("nan"), dtype=torch.float32, device=DEV)
+    B.np_act_batch(shape, to_dev(store[0]), to_dev(X), n, acts)
+    torch.cuda.synchronize()
+    got = acts.cpu().numpy().reshape(n, F).astype(np.float64)
+    ref = orc.act_batch(cfg, store[0], X, n)
+    assert np.max(np.abs(ref)) < 2.0 ** 12
+    assert np.array_equal(got, ref), int(np.sum(got != ref))
+
+
 # ---------------- O10: percentile -------------------------------------------------
 
 @pytest.mark.parametrize("n", [1, 5, 1000, 1001, 32768, 32769, 65536 + 3, 200000, (1 << 20) + 2])
