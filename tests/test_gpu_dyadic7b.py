@@ -1,8 +1,9 @@
 """The dyadic variant of the 7B shape end to end, bit for bit, with no
 lockstep: 31 downstream layers, d 4096, F 11008, r 416, k 1651, C 5504,
 fp16, 8 tokens, in the configuration bench.py times (storage tier in HBM,
-gather staging, eager launches on one stream) and with the storage tier in
-pinned host memory (np_stage_rows in side-stream layer groups).  MLP weights are m 2^-6
+gather staging, eager launches on one stream), with the storage tier in
+pinned host memory (np_stage_rows in side-stream layer groups) and in a file
+(np_stage_file).  MLP weights are m 2^-6
 (|m| <= 3), predictor entries m 2^-3 (|m| <= 1) and h in {-1, 0, 1}, so every
 sum on the path is exact in fp32 in any order provided |a| < 2^12 for every
 active row and sum_n |a_n D_nj| < 2^6 for every column j (then every partial
@@ -97,17 +98,25 @@ def dyadic_7b():
 # the step bench.py times (storage tier in HBM, gather staging, one stream)
 # and the step with the storage tier in pinned host memory (np_stage_rows in
 # side-stream layer groups, every fourth group gathered by the GPU, MLPs
-# enqueued by the helper thread)
+# enqueued by the helper thread), and in a file read with io_uring
 @pytest.mark.parametrize("tier,staging,overlap", [("device", "gather", False),
-                                                  ("host", "memcpy", True)])
+                                                  ("host", "memcpy", True),
+                                                  ("file", "file", True)])
 def test_dyadic_7b_end_to_end_bit_exact(dyadic_7b, tier, staging, overlap):
     from paper_2608_22643_amd.pipeline import DecodePipeline
 
     cfg, host, store = dyadic_7b
-    L, d, F, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.k, cfg.capacity
     say(f"[dyadic7b] tier={tier} staging={staging} overlap={overlap}")
     pipe = DecodePipeline(cfg, tier=tier, staging=staging, overlap=overlap, tokens=T,
                           host_storage=host)
+    try:
+        run_and_check(pipe, cfg, store)
+    finally:
+        pipe.close()  # the file tier's storage file is removed
+
+
+def run_and_check(pipe, cfg, store):
+    L, d, F, k, C = cfg.layers, cfg.d_model, cfg.d_ffn, cfg.k, cfg.capacity
     h = W.hidden(cfg, T)
     A, Bm = W.predictor(cfg)
     st = orc.State(L, F, C)
