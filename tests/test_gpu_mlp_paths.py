@@ -137,6 +137,22 @@ def test_mlp_paths_dyadic_bit_exact(name, path, monkeypatch):
             ref = orc.sparse_mlp(cfg, l, h, store, neuron[l][slots[:n]].astype(np.int32))
             got = decode_y(orc, cfg.adtype, y.cpu().numpy())
             assert np.array_equal(got, decode_y(orc, cfg.adtype, ref)), (n, l)
+    if path == "two_kernel":
+        # the device-count form and the allocation-free entry point run the
+        # same kernels: the same exact values
+        err = torch.zeros(1, dtype=torch.int32, device=DEV)
+        for n in sorted({1, k // 3, k}):
+            cnt = torch.full((cfg.layers,), n, dtype=torch.int32, device=DEV)
+            for l in range(cfg.layers):
+                ref = decode_y(orc, cfg.adtype,
+                               orc.sparse_mlp(cfg, l, h, store, neuron[l][slots[:n]].astype(np.int32)))
+                B.np_sparse_mlp_n(bufs.shape, l, x, res, sl, cnt, y, bufs.ws)
+                torch.cuda.synchronize()
+                assert np.array_equal(decode_y(orc, cfg.adtype, y.cpu().numpy()), ref), ("n", n, l)
+                B.np_sparse_mlp_noalloc(bufs.shape, l, x, res, sl, n, y, err)
+                torch.cuda.synchronize()
+                assert np.array_equal(decode_y(orc, cfg.adtype, y.cpu().numpy()), ref), ("na", n, l)
+        assert int(err.item()) == 0
     # eq. 1 on exact activations: a threshold equal to one row's |a| keeps
     # that row (only a magnitude below the threshold is zeroed), one just
     # above it drops the row
